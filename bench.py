@@ -1,0 +1,258 @@
+#!/usr/bin/env python3
+"""Benchmark of the BSR product Y = X W^T + b on one MI355X.
+
+Default workload: a BERT-base attention layer -- four 768x768 projections (Q, K, V, O), each
+pruned to 32x1 blocks at 10% block density, applied to one batch of 1 x 128 tokens.  One step
+is the four bsr_spmm calls.  Inputs are seeded synthetic tensors (see
+paper_2106_08846_amd/workloads.py), already resident in device memory when timing starts.
+
+Prints one JSON line: effective GFLOP/s (2 * nnz * tokens per call, summed over the step),
+the roofline position of the product kernel (per-launch duration from HIP events on the launch
+stream), the same-shape dense fp32 GEMM, and the CPU oracle timed on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 (matrix / packed)
+BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 matrix
+METRIC = "BSR SpMM effective GFLOP/s (2*nnz*tokens)"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="bert_base_attn",
+                    help="bert_base_attn | single_768 | sweep:RxC | "
+                         "fused_qkv:RxC:density[:bf16] | bert_large:RxC")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU time spent timing the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    return ap.parse_args()
+
+
+def build_workload(spec: str):
+    from paper_2106_08846_amd import workloads as G
+    parts = spec.split(":")
+    kind = parts[0]
+    if kind == "bert_base_attn":
+        return G.bert_base_attention()
+    if kind == "single_768":
+        return G.single_768()
+    R, C = (int(v) for v in parts[1].split("x")) if len(parts) > 1 else (32, 1)
+    if kind == "sweep":
+        return G.block_sweep(R, C)
+    if kind == "fused_qkv":
+        return G.fused_qkv(R, C, float(parts[2]), bf16=len(parts) > 3 and parts[3] == "bf16")
+    if kind == "bert_large":
+        return G.bert_large_zipf(R, C)
+    raise SystemExit(f"unknown workload {spec}")
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path, so run it with --gpus 1.", file=sys.stderr, flush=True)
+        return 2
+
+    import torch
+    from paper_2106_08846_amd import bsr as B
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    wl = build_workload(args.workload)
+    bf16 = wl.bf16
+    print(f"# workload {wl.name}: {len(wl.projections)} projections", file=sys.stderr,
+          flush=True)
+
+    # Inputs to the device; prune every weight on the GPU.
+    X32 = [torch.from_numpy(x).to(dev) for x in wl.X]
+    Xs = [B.bsr_cast_f32_bf16(x) for x in X32] if bf16 else X32
+    calls = []
+    for p in wl.projections:
+        N, K = p.W.shape
+        k = p.k if p.k is not None else B.bsr_prune_count(N, K, p.R, p.C, p.density)
+        Wd = torch.from_numpy(p.W).to(dev)
+        M = B.bsr_prune_from_dense(Wd, p.R, p.C, k=k)
+        if bf16:
+            M = M.to_bf16()
+        bias = torch.from_numpy(p.bias).to(dev)
+        T = wl.X[p.x_index].shape[0]
+        Y = torch.empty((T, N), dtype=torch.float32, device=dev)
+        calls.append(dict(X=Xs[p.x_index], M=M, bias=bias, Y=Y, Wd=Wd, T=T, N=N, K=K, R=p.R,
+                          C=p.C, k=k))
+    torch.cuda.synchronize()
+
+    def step():
+        for c in calls:
+            B.bsr_spmm(c["X"], c["M"], c["bias"], Y=c["Y"])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / args.steps
+
+    flops_step = sum(2.0 * c["k"] * c["R"] * c["C"] * c["T"] for c in calls)
+    value = flops_step / (ms_per_step * 1e-3) / 1e9
+
+    # Roofline of the product kernel: average duration of one launch, from HIP events recorded
+    # on the launch stream around each launch.
+    sx = 2 if bf16 else 4
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(len(calls) * args.steps)]
+    i = 0
+    for _ in range(args.steps):
+        for c in calls:
+            ev[i][0].record()
+            B.bsr_spmm(c["X"], c["M"], c["bias"], Y=c["Y"])
+            ev[i][1].record()
+            i += 1
+    torch.cuda.synchronize()
+    launch_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    def launch_bytes(c):
+        nb_rows = c["N"] // c["R"]
+        return (c["T"] * c["K"] * sx + c["k"] * c["R"] * c["C"] * sx + 4 * c["k"]
+                + 4 * (nb_rows + 1) + 4 * c["N"] + 4 * c["T"] * c["N"])
+
+    bytes_launch = float(np.mean([launch_bytes(c) for c in calls]))
+    flops_launch = flops_step / len(calls)
+    peak_flops = (BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS) * 1e12
+    ai = flops_launch / bytes_launch
+    if ai > peak_flops / (HBM_PEAK_GBS * 1e9):
+        achieved = flops_launch / (launch_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak_flops / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / (peak_flops / 1e12)}
+    else:
+        achieved = bytes_launch / (launch_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+    roof.update({"traffic": None, "kernel": "bsr_spmm", "launch_us": launch_ms * 1e3,
+                 "algorithmic_bytes_per_launch": bytes_launch,
+                 "flops_per_launch": flops_launch, "arithmetic_intensity": ai})
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "GFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "calls_per_step": len(calls),
+                   "tokens": calls[0]["T"], "N": calls[0]["N"], "K": calls[0]["K"],
+                   "block": f"{calls[0]['R']}x{calls[0]['C']}",
+                   "density": wl.projections[0].density,
+                   "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in calls][:8]},
+        "roofline": roof,
+    }
+
+    if not args.no_dense:
+        Wds = [c["Wd"].to(torch.bfloat16) if bf16 else c["Wd"] for c in calls]
+        Xd = [c["X"] for c in calls]
+
+        def dense_step():
+            for c, W, X in zip(calls, Wds, Xd):
+                if bf16:
+                    c["Y"].copy_(torch.matmul(X, W.t()).float() + c["bias"])
+                else:
+                    torch.addmm(c["bias"], X, W.t(), out=c["Y"])
+
+        for _ in range(args.warmup):
+            dense_step()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            dense_step()
+        end.record()
+        torch.cuda.synchronize()
+        out["dense_gemm_ms_per_step"] = start.elapsed_time(end) / args.steps
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, calls, args.cpu_seconds)
+
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def cpu_baseline(wl, calls, seconds: float) -> dict:
+    """The C oracle (fp64 naive BSR loop, OpenMP over tokens) on this host's cores.
+
+    The sample is the whole step when it fits the time budget, otherwise the first projections'
+    calls on a leading slice of tokens; the rate is scaled to GFLOP/s of the same metric.
+    """
+    import torch
+    from oracle import bsr_oracle as O
+    from oracle import cpu_oracle
+    cores = len(os.sched_getaffinity(0))
+    cpu_oracle.set_num_threads(cores)
+    host = []
+    for c, p in zip(calls, wl.projections):
+        ip = c["M"].indptr.cpu().numpy()
+        ix = c["M"].indices.cpu().numpy()[:c["k"]]
+        d = c["M"].data[:c["k"]]
+        if d.dtype != torch.float32:
+            dt = O.bf16_to_f32(d.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+        else:
+            dt = d.cpu().numpy()
+        X = wl.X[p.x_index]
+        if wl.bf16:
+            X = O.bf16_roundtrip(X)
+        host.append((X, ip, ix, dt.reshape(c["k"], c["R"], c["C"]), c["N"], p.bias, c))
+    # Calibrate on the first call with a few tokens, then size the sample to ~`seconds`.
+    X, ip, ix, dt, N, b, c = host[0]
+    t_probe = min(16, X.shape[0])
+    t0 = time.perf_counter()
+    cpu_oracle.spmm(X[:t_probe], ip, ix, dt, N, b)
+    per_token = (time.perf_counter() - t0) / t_probe
+    step_tokens = sum(h[0].shape[0] for h in host)
+    budget_tokens = max(1, int(seconds / max(per_token, 1e-9)))
+    flops = 0.0
+    t0 = time.perf_counter()
+    if budget_tokens >= step_tokens:
+        reps = max(1, budget_tokens // step_tokens)
+        for _ in range(reps):
+            for X, ip, ix, dt, N, b, c in host:
+                cpu_oracle.spmm(X, ip, ix, dt, N, b)
+                flops += 2.0 * c["k"] * c["R"] * c["C"] * X.shape[0]
+        sample = f"{reps} x the full step ({len(host)} calls x {host[0][0].shape[0]} tokens)"
+    else:
+        left = budget_tokens
+        used = 0
+        for X, ip, ix, dt, N, b, c in host:
+            if left <= 0:
+                break
+            tt = min(left, X.shape[0])
+            cpu_oracle.spmm(X[:tt], ip, ix, dt, N, b)
+            flops += 2.0 * c["k"] * c["R"] * c["C"] * tt
+            left -= tt
+            used += 1
+        sample = f"{budget_tokens} tokens over the first {used} calls of the step"
+    el = time.perf_counter() - t0
+    return {"value": flops / el / 1e9, "unit": "GFLOP/s", "cores": cpu_oracle.num_threads(),
+            "kind": "oracle", "sample": sample, "seconds": el,
+            "cpu": platform.processor() or platform.machine()}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

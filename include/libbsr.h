@@ -1,0 +1,160 @@
+/*
+ * libbsr -- block-sparse-row (BSR) weights times dense activations on AMD MI355X (gfx950).
+ *
+ * The operations are those of "Algorithm to Compilation Co-design: An Integrated View of Neural
+ * Network Sparsity" (Guo & Huang, 2021):
+ *   - block-magnitude pruning of a dense weight (Sec. 2.1, Eq. 2 and Eq. 3): partition W into
+ *     R x C blocks, score each block by its l2 norm, keep the k blocks with the largest norm;
+ *   - the BSR storage of the pruned weight as data, indices and indptr in SciPy's layout
+ *     (Sec. 2.2, second bullet);
+ *   - the sparse-weight x dense-input product that touches only stored blocks (Sec. 2.2, first and
+ *     second bullets), applied to the BERT attention projections (Sec. 2.3): Y = X W^T + b.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Shapes.  W is N x K, row-major, laid out [out][in] like a linear layer's weight.  A block shape
+ *   R x C means R output rows by C input columns; R must divide N and C must divide K.  Then
+ *   Nb = N / R block-rows, Kb = K / C block-columns, nb = Nb * Kb blocks.  Block (i, j) covers
+ *   W[iR:(i+1)R, jC:(j+1)C] and has the row-major id i * Kb + j.
+ * BSR layout.  indptr int32[Nb + 1] with indptr[0] = 0, non-decreasing, indptr[Nb] = nnzb;
+ *   indices int32[nnzb], strictly ascending inside each block-row, each < Kb;
+ *   data [nnzb][R][C] row-major (fp32, or bf16 as raw uint16 bit patterns).
+ * Activations.  X is T x K row-major with row pitch ldx >= K elements (T = batch * sequence);
+ *   Y is T x N fp32 row-major with row pitch ldy >= N.  Bias is fp32[N] or NULL (adds +0).
+ * Memory.  Every data pointer is a device pointer (hipMalloc or torch memory) owned by the
+ *   caller.  The library never allocates, frees or synchronises; it only enqueues kernels.
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = the null stream).  All work is
+ *   stream-ordered; results are visible after the caller synchronises that stream.
+ * Errors.  Arguments are validated on the host before anything is enqueued; on error nothing is
+ *   launched and outputs are untouched.  A launch failure reported by the HIP runtime returns
+ *   BSR_ERR_HIP.  Device contents (indptr, indices) cannot be checked without a synchronisation,
+ *   so they are trusted; kernels clamp every index they read to the declared array bounds, so a
+ *   malformed matrix yields wrong values but no out-of-bounds access.
+ * Concurrency.  A bsr_matrix_t is read-only to the library and may be used on several streams at
+ *   once.  X, Y, W and workspaces must not overlap each other.
+ */
+#ifndef LIBBSR_H
+#define LIBBSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define LIBBSR_API __attribute__((visibility("default")))
+#else
+#define LIBBSR_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BSR_OK = 0,
+    BSR_ERR_NULL = 1,       /* a required pointer is NULL                                      */
+    BSR_ERR_SHAPE = 2,      /* R does not divide N, C does not divide K, ld < width, T < 0      */
+    BSR_ERR_ARG = 3,        /* density NaN or outside [0, 1]; k outside [0, nb]; bad dtype enum */
+    BSR_ERR_DTYPE = 4,      /* X dtype differs from the BSR data dtype                          */
+    BSR_ERR_CAPACITY = 5,   /* output arrays too small for k blocks                             */
+    BSR_ERR_WORKSPACE = 6,  /* workspace NULL or smaller than bsr_prune_workspace_bytes()       */
+    BSR_ERR_HIP = 7,        /* the HIP runtime reported an error                                */
+    BSR_ERR_ARCH = 8,       /* the current device is not gfx950                                 */
+    BSR_ERR_UNSUPPORTED = 9 /* valid arguments outside what the library implements (e.g. sizes
+                               beyond int32 element offsets)                                    */
+} bsr_status;
+
+typedef enum { BSR_F32 = 0, BSR_BF16 = 1 } bsr_dtype;
+
+/* A BSR matrix in device memory (all pointers device pointers, owned by the caller). */
+typedef struct {
+    int64_t n_rows;          /* N: dense output rows                                    */
+    int64_t n_cols;          /* K: dense input columns                                  */
+    int32_t R, C;            /* block shape; R | N, C | K                               */
+    int64_t nnzb;            /* number of stored blocks                                 */
+    const int32_t *indptr;   /* [N/R + 1]                                               */
+    const int32_t *indices;  /* [nnzb]                                                  */
+    const void *data;        /* [nnzb][R][C] row-major, of type `dtype`                 */
+    bsr_dtype dtype;         /* BSR_F32 (float) or BSR_BF16 (uint16 bf16 bit patterns)  */
+} bsr_matrix_t;
+
+/*
+ * Number of blocks kept at a block density (Sec. 2.1, Eq. 2: the bound tau on the number of
+ * nonzero groups): k = floor(density * nb + 0.5) computed in double, clamped to [0, nb].
+ * Host only; touches no device.  Errors: BSR_ERR_NULL (k), BSR_ERR_SHAPE (sizes <= 0 or not
+ * tiled by R x C), BSR_ERR_ARG (density NaN or outside [0, 1]).
+ */
+LIBBSR_API bsr_status bsr_prune_count(int64_t N, int64_t K, int32_t R, int32_t C, double density,
+                           int64_t *k);
+
+/* Device workspace bytes that bsr_prune_from_dense needs for an N x K weight with R x C blocks
+ * (0 if the shape is invalid).  Host only. */
+LIBBSR_API size_t bsr_prune_workspace_bytes(int64_t N, int64_t K, int32_t R, int32_t C);
+
+/*
+ * Block-magnitude pruning, dense fp32 W -> BSR keeping exactly k blocks (Sec. 2.1, Eq. 2 and
+ * Eq. 3, with the l2 norm as the per-block norm; Sec. 2.2 for the BSR layout).
+ *   key(i, j) = sum of w^2 over the block, in fp64, summed row r outer, column c inner, from
+ *   +0.0 (a NaN key ranks above +inf).  The kept blocks are the first k in the order
+ *   (key descending, block id ascending), so the result is unique and equal, bit for bit, to a
+ *   CPU computation of the same definition.
+ * W: device fp32, N x K with row pitch ldw >= K.
+ * k: number of blocks to keep, 0 <= k <= nb (see bsr_prune_count).
+ * Outputs (device, caller-allocated): indptr int32[N/R + 1]; indices int32[capacity_blocks];
+ *   data float[capacity_blocks * R * C].  The first k entries of indices/data are written; data
+ *   holds exact bit copies of W's elements.
+ * workspace: device memory of at least bsr_prune_workspace_bytes(N, K, R, C) bytes; its
+ *   contents on entry do not matter.  It is in use until the enqueued work completes.
+ * Errors: BSR_ERR_NULL, BSR_ERR_SHAPE, BSR_ERR_ARG (k out of range), BSR_ERR_CAPACITY
+ *   (capacity_blocks < k), BSR_ERR_WORKSPACE, BSR_ERR_UNSUPPORTED (nb >= 2^31 or
+ *   N * ldw >= 2^53), BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_prune_from_dense(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R,
+                                int32_t C, int64_t k, int32_t *indptr, int32_t *indices,
+                                float *data, int64_t capacity_blocks, void *workspace,
+                                size_t ws_bytes, void *stream);
+
+/*
+ * The BSR product (Sec. 2.2; BERT attention projections, Sec. 2.3):
+ *   Y[t][n] = bias[n] + sum over stored blocks p of block-row i = floor(n / R), sum over c < C of
+ *             X[t][indices[p] * C + c] * data[p][n - iR][c].
+ * Arithmetic is fp32 with fp32 accumulation and fp32 output (bf16 x bf16 products are exact in
+ * fp32); the summation order is the kernel's and fixed for a given launch configuration, so
+ * repeated calls are bitwise reproducible.  A block-row with no stored blocks gives Y = bias.
+ * X: device, T x K (K = W->n_cols) with row pitch ldx, of type x_dtype (BSR_BF16 = uint16 bf16
+ *   bit patterns); x_dtype must equal W->dtype.
+ * W: host pointer to a bsr_matrix_t describing device arrays.
+ * bias: device fp32[N] or NULL.  Y: device fp32, T x N with row pitch ldy.
+ * T = 0 is a no-op.  Errors: BSR_ERR_NULL, BSR_ERR_SHAPE, BSR_ERR_ARG, BSR_ERR_DTYPE,
+ *   BSR_ERR_UNSUPPORTED, BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_spmm(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
+                    const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
+                    void *stream);
+
+/*
+ * Expand an fp32 BSR matrix to dense (Sec. 2.2 layout): out[n][k] = the stored element covering
+ * (n, k), or +0.0 where no block is stored.  out: device fp32, N x K with row pitch ldo >= K.
+ * Errors: BSR_ERR_NULL, BSR_ERR_SHAPE, BSR_ERR_DTYPE (bf16 data), BSR_ERR_UNSUPPORTED,
+ *   BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *stream);
+
+/*
+ * fp32 -> bf16, round to nearest with ties to even; NaN stays a quiet NaN (its upper 16 bits
+ * with the quiet bit set); overflow rounds to infinity.  Used to feed the bf16 product with
+ * bf16 activations and BSR data.  src, dst: device arrays of n elements (dst as uint16).
+ * Errors: BSR_ERR_NULL, BSR_ERR_SHAPE (n < 0), BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_cast_f32_bf16(const float *src, uint16_t *dst, int64_t n, void *stream);
+
+/* Static, human-readable name of a status code. */
+LIBBSR_API const char *bsr_status_str(bsr_status s);
+
+/* Text of the last HIP error seen by this thread's libbsr calls ("" if none). */
+LIBBSR_API const char *bsr_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBBSR_H */

@@ -1,0 +1,231 @@
+"""Thin Python binding of libbsr's C ABI (ctypes).
+
+Argument marshalling only: torch tensors supply device memory and the current HIP stream; every
+computation runs in libbsr's kernels.  The functions carry the C entry points' names.  Loading
+fails loudly when libbsr.so has not been built -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY = os.path.join(_HERE, "libbsr.so")
+
+BSR_F32, BSR_BF16 = 0, 1
+STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
+          4: "BSR_ERR_DTYPE", 5: "BSR_ERR_CAPACITY", 6: "BSR_ERR_WORKSPACE", 7: "BSR_ERR_HIP",
+          8: "BSR_ERR_ARCH", 9: "BSR_ERR_UNSUPPORTED"}
+
+# The C ABI's exported entry points (the tests check this list against include/libbsr.h).
+EXPORTS = ["bsr_prune_count", "bsr_prune_workspace_bytes", "bsr_prune_from_dense", "bsr_spmm",
+           "bsr_to_dense", "bsr_cast_f32_bf16", "bsr_status_str", "bsr_last_hip_error"]
+
+
+class BSRError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str = ""):
+        self.status = status
+        name = STATUS.get(status, str(status))
+        msg = f"{where}: {name} ({_lib().bsr_status_str(status).decode()})"
+        if detail:
+            msg += f": {detail}"
+        super().__init__(msg)
+
+
+class bsr_matrix_t(ctypes.Structure):
+    _fields_ = [("n_rows", ctypes.c_int64), ("n_cols", ctypes.c_int64),
+                ("R", ctypes.c_int32), ("C", ctypes.c_int32), ("nnzb", ctypes.c_int64),
+                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p),
+                ("data", ctypes.c_void_p), ("dtype", ctypes.c_int)]
+
+
+_LIB = None
+
+
+def _lib() -> ctypes.CDLL:
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIBRARY):
+            raise RuntimeError(f"libbsr is not built ({LIBRARY} missing); "
+                               "run paper_2106_08846_amd/build.py")
+        lib = ctypes.CDLL(LIBRARY)
+        i64, i32, p, sz = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+        st = ctypes.c_int
+        lib.bsr_prune_count.argtypes = [i64, i64, i32, i32, ctypes.c_double,
+                                        ctypes.POINTER(i64)]
+        lib.bsr_prune_count.restype = st
+        lib.bsr_prune_workspace_bytes.argtypes = [i64, i64, i32, i32]
+        lib.bsr_prune_workspace_bytes.restype = sz
+        lib.bsr_prune_from_dense.argtypes = [p, i64, i64, i64, i32, i32, i64, p, p, p, i64, p,
+                                             sz, p]
+        lib.bsr_prune_from_dense.restype = st
+        lib.bsr_spmm.argtypes = [p, ctypes.c_int, i64, i64, ctypes.POINTER(bsr_matrix_t), p, p,
+                                 i64, p]
+        lib.bsr_spmm.restype = st
+        lib.bsr_to_dense.argtypes = [ctypes.POINTER(bsr_matrix_t), p, i64, p]
+        lib.bsr_to_dense.restype = st
+        lib.bsr_cast_f32_bf16.argtypes = [p, p, i64, p]
+        lib.bsr_cast_f32_bf16.restype = st
+        lib.bsr_status_str.argtypes = [ctypes.c_int]
+        lib.bsr_status_str.restype = ctypes.c_char_p
+        lib.bsr_last_hip_error.argtypes = []
+        lib.bsr_last_hip_error.restype = ctypes.c_char_p
+        _LIB = lib
+    return _LIB
+
+
+def library() -> ctypes.CDLL:
+    """The loaded libbsr (raises if it has not been built)."""
+    return _lib()
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        detail = _lib().bsr_last_hip_error().decode() if status == 7 else ""
+        raise BSRError(status, where, detail)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _require_cuda(t: torch.Tensor, name: str, dtype=None) -> None:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _pitch(t: torch.Tensor, name: str) -> int:
+    """Row pitch (elements) of a 2-D tensor whose rows are contiguous."""
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name} must be 2-D with unit column stride")
+    return t.stride(0) if t.shape[0] > 1 else max(t.shape[1], 1)
+
+
+@dataclass
+class BSRMatrix:
+    """A BSR matrix whose arrays live in torch device tensors (Sec. 2.2 layout)."""
+    n_rows: int
+    n_cols: int
+    R: int
+    C: int
+    indptr: torch.Tensor      # int32 [N/R + 1]
+    indices: torch.Tensor     # int32 [>= nnzb]
+    data: torch.Tensor        # float32 or bfloat16 [>= nnzb, R, C]
+    nnzb: int
+
+    @property
+    def dtype(self) -> int:
+        return BSR_BF16 if self.data.dtype == torch.bfloat16 else BSR_F32
+
+    def struct(self) -> bsr_matrix_t:
+        return bsr_matrix_t(self.n_rows, self.n_cols, self.R, self.C, self.nnzb,
+                            _ptr(self.indptr), _ptr(self.indices), _ptr(self.data), self.dtype)
+
+    def to_bf16(self, stream=None) -> "BSRMatrix":
+        """Copy with data rounded to bf16 by bsr_cast_f32_bf16 (indices shared)."""
+        data = bsr_cast_f32_bf16(self.data[: self.nnzb], stream=stream)
+        return BSRMatrix(self.n_rows, self.n_cols, self.R, self.C, self.indptr, self.indices,
+                         data, self.nnzb)
+
+
+def bsr_prune_count(N: int, K: int, R: int, C: int, density: float) -> int:
+    k = ctypes.c_int64(0)
+    _check(_lib().bsr_prune_count(N, K, R, C, float(density), ctypes.byref(k)),
+           "bsr_prune_count")
+    return k.value
+
+
+def bsr_prune_workspace_bytes(N: int, K: int, R: int, C: int) -> int:
+    return int(_lib().bsr_prune_workspace_bytes(N, K, R, C))
+
+
+def bsr_prune_from_dense(W: torch.Tensor, R: int, C: int, k: int | None = None,
+                         density: float | None = None, workspace: torch.Tensor | None = None,
+                         stream=None) -> BSRMatrix:
+    """Prune dense fp32 W (device, [N, K]) to BSR with R x C blocks, keeping k blocks."""
+    _require_cuda(W, "W", torch.float32)
+    N, K = W.shape
+    ldw = _pitch(W, "W")
+    if (k is None) == (density is None):
+        raise ValueError("give exactly one of k and density")
+    if k is None:
+        k = bsr_prune_count(N, K, R, C, density)
+    dev = W.device
+    Nb = N // R if R > 0 and N % R == 0 else 0
+    indptr = torch.empty(Nb + 1, dtype=torch.int32, device=dev)
+    indices = torch.empty(max(k, 1), dtype=torch.int32, device=dev)
+    data = torch.empty((max(k, 1), R, C), dtype=torch.float32, device=dev)
+    ws_bytes = bsr_prune_workspace_bytes(N, K, R, C)
+    if workspace is None:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    _check(_lib().bsr_prune_from_dense(_ptr(W), N, K, ldw, R, C, k, _ptr(indptr),
+                                       _ptr(indices), _ptr(data), max(k, 1), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(),
+                                       _stream(stream)),
+           "bsr_prune_from_dense")
+    return BSRMatrix(N, K, R, C, indptr, indices, data, k)
+
+
+def bsr_spmm(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
+             Y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Y = X W^T + bias with W in BSR (fp32 or bf16 inputs; fp32 accumulate and output)."""
+    _require_cuda(X, "X")
+    if X.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("X must be float32 or bfloat16")
+    x_dtype = BSR_BF16 if X.dtype == torch.bfloat16 else BSR_F32
+    T = X.shape[0]
+    ldx = _pitch(X, "X")
+    if bias is not None:
+        _require_cuda(bias, "bias", torch.float32)
+        if bias.dim() != 1 or bias.numel() != W.n_rows or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous [N] float32 tensor")
+    if Y is None:
+        Y = torch.empty((T, W.n_rows), dtype=torch.float32, device=X.device)
+    _require_cuda(Y, "Y", torch.float32)
+    if Y.shape[0] != T:
+        raise ValueError("Y must have T rows")
+    ldy = _pitch(Y, "Y")
+    m = W.struct()
+    _check(_lib().bsr_spmm(_ptr(X), x_dtype, T, ldx, ctypes.byref(m), _ptr(bias), _ptr(Y), ldy,
+                           _stream(stream)), "bsr_spmm")
+    return Y
+
+
+def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Dense fp32 [N, K] expansion of an fp32 BSR matrix."""
+    if out is None:
+        out = torch.empty((W.n_rows, W.n_cols), dtype=torch.float32, device=W.indptr.device)
+    _require_cuda(out, "out", torch.float32)
+    m = W.struct()
+    _check(_lib().bsr_to_dense(ctypes.byref(m), _ptr(out), _pitch(out, "out"), _stream(stream)),
+           "bsr_to_dense")
+    return out
+
+
+def bsr_cast_f32_bf16(src: torch.Tensor, dst: torch.Tensor | None = None,
+                      stream=None) -> torch.Tensor:
+    """Round a contiguous fp32 tensor to bf16 (nearest, ties to even); returns a bf16 tensor."""
+    _require_cuda(src, "src", torch.float32)
+    if not src.is_contiguous():
+        raise ValueError("src must be contiguous")
+    if dst is None:
+        dst = torch.empty(src.shape, dtype=torch.bfloat16, device=src.device)
+    _require_cuda(dst, "dst", torch.bfloat16)
+    if dst.numel() != src.numel() or not dst.is_contiguous():
+        raise ValueError("dst must be contiguous with src's element count")
+    _check(_lib().bsr_cast_f32_bf16(_ptr(src), _ptr(dst), src.numel(), _stream(stream)),
+           "bsr_cast_f32_bf16")
+    return dst

@@ -1,0 +1,46 @@
+// Internal declarations shared by libbsr's translation units (not part of the C ABI).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/libbsr.h"
+
+namespace bsr {
+
+// Workspace layout of the pruning pipeline: fp64 key bits per block, then the source block id
+// of every kept block.  Each region starts on a 256-byte boundary.
+struct PruneWorkspace {
+    size_t key_offset, key_bytes;
+    size_t src_offset, src_bytes;
+    size_t total;
+};
+PruneWorkspace prune_workspace_layout(int64_t nb);
+
+// Host-side argument checks; pure C++ (no HIP), so they also run where no GPU exists.
+bsr_status check_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,
+                       int64_t k, const int32_t *indptr, const int32_t *indices,
+                       const float *data, int64_t capacity_blocks, const void *workspace,
+                       size_t ws_bytes);
+bsr_status check_matrix(const bsr_matrix_t *W);
+bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const bsr_matrix_t *W,
+                      const float *Y, int64_t ldy);
+bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo);
+bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
+
+// Device-side entry points (implemented in the .hip files).  Arguments are already validated.
+bsr_status ensure_device();  // current device is gfx950; caches its properties
+int device_cu_count();
+size_t device_lds_per_block();
+
+bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,
+                        int64_t k, int32_t *indptr, int32_t *indices, float *data,
+                        void *workspace, void *stream);
+bsr_status launch_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *stream);
+bsr_status launch_cast(const float *src, uint16_t *dst, int64_t n, void *stream);
+bsr_status launch_spmm_generic(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W,
+                               const float *bias, float *Y, int64_t ldy, void *stream);
+
+void set_last_hip_error(const char *msg);
+
+}  // namespace bsr

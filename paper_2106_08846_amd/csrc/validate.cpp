@@ -1,0 +1,139 @@
+// Host-side validation for libbsr's C ABI: pure C++ with no HIP dependency.
+//
+// Every check here runs before anything is enqueued, so a rejected call launches nothing and
+// leaves its outputs untouched.
+#include <cmath>
+#include <cstring>
+
+#include "bsr_internal.h"
+
+namespace {
+
+constexpr int64_t kMaxBlocks = (int64_t(1) << 31) - 1;   // block ids and indptr are int32
+constexpr int64_t kMaxElems = int64_t(1) << 53;          // element offsets stay exact
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool tiles(int64_t N, int64_t K, int32_t R, int32_t C) {
+    return N > 0 && K > 0 && R > 0 && C > 0 && N % R == 0 && K % C == 0;
+}
+
+}  // namespace
+
+namespace bsr {
+
+PruneWorkspace prune_workspace_layout(int64_t nb) {
+    PruneWorkspace w{};
+    w.key_offset = 0;
+    w.key_bytes = size_t(nb) * sizeof(uint64_t);
+    w.src_offset = align256(w.key_bytes);
+    w.src_bytes = size_t(nb) * sizeof(int32_t);
+    w.total = align256(w.src_offset + w.src_bytes);
+    return w;
+}
+
+bsr_status check_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,
+                       int64_t k, const int32_t *indptr, const int32_t *indices,
+                       const float *data, int64_t capacity_blocks, const void *workspace,
+                       size_t ws_bytes) {
+    if (!W || !indptr) return BSR_ERR_NULL;
+    if (!tiles(N, K, R, C) || ldw < K) return BSR_ERR_SHAPE;
+    const int64_t Nb = N / R, Kb = K / C;
+    if (Nb > kMaxBlocks / Kb) return BSR_ERR_UNSUPPORTED;
+    const int64_t nb = Nb * Kb;
+    if (N > kMaxElems / ldw) return BSR_ERR_UNSUPPORTED;
+    if (k < 0 || k > nb) return BSR_ERR_ARG;
+    if (k > 0 && (!indices || !data)) return BSR_ERR_NULL;
+    if (capacity_blocks < k) return BSR_ERR_CAPACITY;
+    if (!workspace || ws_bytes < prune_workspace_layout(nb).total) return BSR_ERR_WORKSPACE;
+    return BSR_OK;
+}
+
+bsr_status check_matrix(const bsr_matrix_t *W) {
+    if (!W) return BSR_ERR_NULL;
+    if (W->dtype != BSR_F32 && W->dtype != BSR_BF16) return BSR_ERR_ARG;
+    if (!tiles(W->n_rows, W->n_cols, W->R, W->C)) return BSR_ERR_SHAPE;
+    const int64_t Nb = W->n_rows / W->R, Kb = W->n_cols / W->C;
+    if (Nb > kMaxBlocks / Kb) return BSR_ERR_UNSUPPORTED;
+    if (W->nnzb < 0 || W->nnzb > Nb * Kb) return BSR_ERR_ARG;
+    if (int64_t(W->R) * W->C > kMaxElems / (W->nnzb > 0 ? W->nnzb : 1))
+        return BSR_ERR_UNSUPPORTED;
+    if (!W->indptr) return BSR_ERR_NULL;
+    if (W->nnzb > 0 && (!W->indices || !W->data)) return BSR_ERR_NULL;
+    return BSR_OK;
+}
+
+bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const bsr_matrix_t *W,
+                      const float *Y, int64_t ldy) {
+    if (!W) return BSR_ERR_NULL;
+    bsr_status s = check_matrix(W);
+    if (s != BSR_OK) return s;
+    if (x_dtype != BSR_F32 && x_dtype != BSR_BF16) return BSR_ERR_ARG;
+    if (x_dtype != int(W->dtype)) return BSR_ERR_DTYPE;
+    if (T < 0 || ldx < W->n_cols || ldy < W->n_rows) return BSR_ERR_SHAPE;
+    if (T > 0 && (!X || !Y)) return BSR_ERR_NULL;
+    if (T > kMaxElems / ldx || T > kMaxElems / ldy) return BSR_ERR_UNSUPPORTED;
+    return BSR_OK;
+}
+
+bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo) {
+    if (!W || !out) return BSR_ERR_NULL;
+    bsr_status s = check_matrix(W);
+    if (s != BSR_OK) return s;
+    if (W->dtype != BSR_F32) return BSR_ERR_DTYPE;
+    if (ldo < W->n_cols) return BSR_ERR_SHAPE;
+    if (W->n_rows > kMaxElems / ldo) return BSR_ERR_UNSUPPORTED;
+    return BSR_OK;
+}
+
+bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n) {
+    if (n < 0) return BSR_ERR_SHAPE;
+    if (n > 0 && (!src || !dst)) return BSR_ERR_NULL;
+    if (n > kMaxElems) return BSR_ERR_UNSUPPORTED;
+    return BSR_OK;
+}
+
+}  // namespace bsr
+
+extern "C" {
+
+bsr_status bsr_prune_count(int64_t N, int64_t K, int32_t R, int32_t C, double density,
+                           int64_t *k) {
+    if (!k) return BSR_ERR_NULL;
+    if (!tiles(N, K, R, C)) return BSR_ERR_SHAPE;
+    if (!(density >= 0.0 && density <= 1.0)) return BSR_ERR_ARG;  // rejects NaN too
+    const int64_t Nb = N / R, Kb = K / C;
+    if (Nb > kMaxBlocks / Kb) return BSR_ERR_UNSUPPORTED;
+    const int64_t nb = Nb * Kb;
+    double v = std::floor(density * double(nb) + 0.5);
+    int64_t kk = int64_t(v);
+    if (kk < 0) kk = 0;
+    if (kk > nb) kk = nb;
+    *k = kk;
+    return BSR_OK;
+}
+
+size_t bsr_prune_workspace_bytes(int64_t N, int64_t K, int32_t R, int32_t C) {
+    if (!tiles(N, K, R, C)) return 0;
+    const int64_t Nb = N / R, Kb = K / C;
+    if (Nb > kMaxBlocks / Kb) return 0;
+    return bsr::prune_workspace_layout(Nb * Kb).total;
+}
+
+const char *bsr_status_str(bsr_status s) {
+    switch (s) {
+        case BSR_OK: return "ok";
+        case BSR_ERR_NULL: return "null pointer argument";
+        case BSR_ERR_SHAPE: return "invalid shape or leading dimension";
+        case BSR_ERR_ARG: return "invalid argument value";
+        case BSR_ERR_DTYPE: return "dtype mismatch";
+        case BSR_ERR_CAPACITY: return "output capacity too small";
+        case BSR_ERR_WORKSPACE: return "workspace missing or too small";
+        case BSR_ERR_HIP: return "HIP runtime error";
+        case BSR_ERR_ARCH: return "device is not gfx950";
+        case BSR_ERR_UNSUPPORTED: return "unsupported size";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,157 @@
+"""C-ABI checks that need no GPU: exports, host-only entry points and every validation error.
+
+Each error case is built so that validation rejects it before any HIP call, so these run on a
+machine without a GPU.  (Fake device pointers are never dereferenced.)
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import bsr_oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "libbsr.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2106_08846_amd import bsr as libbsr
+    return libbsr.library()
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2106_08846_amd import bsr as libbsr
+    return libbsr
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return re.findall(r"LIBBSR_API\s+[\w\s\*]+?\b(bsr_\w+)\s*\(", text)
+
+
+def test_header_declares_the_binding_exports(L):
+    assert sorted(declared_symbols()) == sorted(L.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    names = declared_symbols()
+    assert names
+    for name in names:
+        assert getattr(lib, name) is not None
+
+
+def test_only_the_abi_is_exported():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only",
+                          os.path.join(ROOT, "paper_2106_08846_amd", "libbsr.so")],
+                         capture_output=True, text=True, check=True).stdout
+    text_syms = sorted(l.split()[-1] for l in out.splitlines() if " T " in l)
+    assert text_syms == sorted(declared_symbols())
+
+
+def test_status_strings(lib):
+    for s in range(10):
+        assert lib.bsr_status_str(s)
+    assert lib.bsr_status_str(0) == b"ok"
+    assert lib.bsr_status_str(123) == b"unknown status"
+
+
+@pytest.mark.parametrize("N,K,R,C,d", [(768, 768, 32, 1, 0.2), (768, 768, 1, 1, 0.1),
+                                       (2304, 768, 16, 16, 0.05), (1024, 1024, 32, 32, 0.1),
+                                       (64, 64, 16, 16, 0.5 / 16), (64, 64, 8, 8, 0.0),
+                                       (64, 64, 8, 8, 1.0), (96, 40, 3, 5, 0.37)])
+def test_prune_count_matches_oracle(L, N, K, R, C, d):
+    assert L.bsr_prune_count(N, K, R, C, d) == O.prune_count(N, K, R, C, d)
+
+
+@pytest.mark.parametrize("args,status", [((768, 768, 7, 1, 0.1), 2), ((768, 768, 32, 5, 0.1), 2),
+                                         ((0, 768, 32, 1, 0.1), 2), ((64, 64, 8, 8, -0.1), 3),
+                                         ((64, 64, 8, 8, 1.5), 3),
+                                         ((64, 64, 8, 8, float("nan")), 3)])
+def test_prune_count_errors(lib, args, status):
+    k = ctypes.c_int64(-1)
+    assert lib.bsr_prune_count(*args, ctypes.byref(k)) == status
+    assert k.value == -1
+    assert lib.bsr_prune_count(64, 64, 8, 8, ctypes.c_double(0.5), None) == 1
+
+
+def test_prune_workspace_bytes(lib):
+    nb = 18432
+    expect = ((nb * 8 + 255) // 256 * 256 + nb * 4 + 255) // 256 * 256
+    assert lib.bsr_prune_workspace_bytes(768, 768, 32, 1) == expect
+    assert lib.bsr_prune_workspace_bytes(768, 768, 7, 1) == 0
+
+
+FAKE = 0x10000  # never dereferenced: every call below fails validation first
+
+
+def _prune(lib, W=FAKE, N=64, K=64, ldw=64, R=8, C=8, k=6, indptr=FAKE, indices=FAKE,
+           data=FAKE, cap=6, ws=FAKE, ws_bytes=1 << 20):
+    return lib.bsr_prune_from_dense(W, N, K, ldw, R, C, k, indptr, indices, data, cap, ws,
+                                    ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"W": None}, 1), ({"indptr": None}, 1), ({"indices": None}, 1), ({"data": None}, 1),
+    ({"R": 7}, 2), ({"C": 3}, 2), ({"ldw": 63}, 2), ({"N": 0}, 2),
+    ({"k": -1}, 3), ({"k": 65}, 3),
+    ({"cap": 5}, 5),
+    ({"ws": None}, 6), ({"ws_bytes": 100}, 6),
+])
+def test_prune_errors(lib, kw, status):
+    assert _prune(lib, **kw) == status
+
+
+def _matrix(L, N=64, K=64, R=8, C=8, nnzb=6, indptr=FAKE, indices=FAKE, data=FAKE, dtype=0):
+    return L.bsr_matrix_t(N, K, R, C, nnzb, indptr, indices, data, dtype)
+
+
+def _spmm(L, lib, m=None, X=FAKE, x_dtype=0, T=4, ldx=64, Y=FAKE, ldy=64):
+    m = m if m is not None else _matrix(L)
+    return lib.bsr_spmm(X, x_dtype, T, ldx, ctypes.byref(m), None, Y, ldy, None)
+
+
+@pytest.mark.parametrize("kw,mkw,status", [
+    ({"X": None}, {}, 1), ({"Y": None}, {}, 1),
+    ({}, {"indptr": None}, 1), ({}, {"indices": None}, 1), ({}, {"data": None}, 1),
+    ({}, {"R": 7}, 2), ({}, {"C": 3}, 2), ({"ldx": 63}, {}, 2), ({"ldy": 63}, {}, 2),
+    ({"T": -1}, {}, 2),
+    ({}, {"nnzb": -1}, 3), ({}, {"nnzb": 65}, 3), ({"x_dtype": 2}, {}, 3), ({}, {"dtype": 5}, 3),
+    ({"x_dtype": 1}, {}, 4), ({}, {"dtype": 1}, 4),
+])
+def test_spmm_errors(L, lib, kw, mkw, status):
+    assert _spmm(L, lib, m=_matrix(L, **mkw), **kw) == status
+
+
+def test_spmm_null_matrix(lib):
+    assert lib.bsr_spmm(FAKE, 0, 4, 64, None, None, FAKE, 64, None) == 1
+
+
+def test_spmm_zero_tokens_is_a_noop(L, lib):
+    # T = 0 returns before touching the device, even with NULL X and Y.
+    assert _spmm(L, lib, X=None, Y=None, T=0) == 0
+
+
+@pytest.mark.parametrize("mkw,ldo,out,status", [
+    ({}, 64, None, 1), ({"dtype": 1}, 64, FAKE, 4), ({}, 63, FAKE, 2), ({"R": 5}, 64, FAKE, 2),
+])
+def test_to_dense_errors(L, lib, mkw, ldo, out, status):
+    m = _matrix(L, **mkw)
+    assert lib.bsr_to_dense(ctypes.byref(m), out, ldo, None) == status
+
+
+def test_cast_errors(lib):
+    assert lib.bsr_cast_f32_bf16(FAKE, FAKE, -1, None) == 2
+    assert lib.bsr_cast_f32_bf16(None, FAKE, 4, None) == 1
+    assert lib.bsr_cast_f32_bf16(FAKE, None, 4, None) == 1
+    assert lib.bsr_cast_f32_bf16(None, None, 0, None) == 0
+
+
+def test_python_binding_rejects_cpu_tensors(L):
+    import torch
+    with pytest.raises(TypeError):
+        L.bsr_cast_f32_bf16(torch.zeros(4))

@@ -1,0 +1,267 @@
+"""GPU parity: libbsr (through its C ABI) against the CPU oracle on the same seeded inputs.
+
+Pruning, to_dense and the bf16 cast must match bit for bit; products must satisfy
+|Y - Y64| <= 1e-5 * sum|x||w| + 1e-6 per element (bf16: against the oracle on bf16-rounded
+inputs), and be bit-exact on integer-valued inputs where every summation order is exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bsr_oracle as O
+from paper_2106_08846_amd import bsr as B
+from paper_2106_08846_amd import workloads as G
+
+from .gpu_common import (bf16_tensor, check_prune, check_spmm, dev, host, log, oracle_bsr,
+                         prune_on_gpu)
+
+pytestmark = pytest.mark.gpu
+
+
+def rng(seed):
+    return np.random.Generator(np.random.PCG64(seed))
+
+
+# ----------------------------------------------------------------------------- the workloads
+
+
+def test_single_768_32x1(device):
+    w = G.single_768()
+    p = w.projections[0]
+    k = B.bsr_prune_count(768, 768, p.R, p.C, p.density)
+    log(f"single_768: k={k}")
+    M = prune_on_gpu(p.W, p.R, p.C, k)
+    check_prune(p.W, p.R, p.C, M, k)
+    Y = B.bsr_spmm(dev(w.X[0]), M, dev(p.bias))
+    torch.cuda.synchronize()
+    check_spmm(w.X[0], M, p.bias, Y)
+
+
+def test_bert_base_qkvo(device):
+    w = G.bert_base_attention()
+    X = dev(w.X[0])
+    for p in w.projections:
+        k = B.bsr_prune_count(768, 768, p.R, p.C, p.density)
+        log(f"bert_base {p.name}: k={k}")
+        M = prune_on_gpu(p.W, p.R, p.C, k)
+        check_prune(p.W, p.R, p.C, M, k)
+        Y = B.bsr_spmm(X, M, dev(p.bias))
+        torch.cuda.synchronize()
+        check_spmm(w.X[0], M, p.bias, Y)
+
+
+@pytest.mark.parametrize("R,C", G.SHAPES_SWEEP)
+def test_block_sweep(device, R, C):
+    w = G.block_sweep(R, C)
+    p = w.projections[0]
+    k = B.bsr_prune_count(768, 768, R, C, p.density)
+    log(f"sweep {R}x{C}: k={k}")
+    M = prune_on_gpu(p.W, R, C, k)
+    check_prune(p.W, R, C, M, k)
+    D = B.bsr_to_dense(M)
+    Y = B.bsr_spmm(dev(w.X[0]), M, dev(p.bias))
+    torch.cuda.synchronize()
+    ip, ix, dt = O.prune(p.W, R, C, k=k)
+    assert np.array_equal(host(D).view(np.uint32),
+                          O.to_dense(ip, ix, dt, 768, 768).view(np.uint32))
+    check_spmm(w.X[0], M, p.bias, Y)
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("R,C", [(32, 1), (16, 16)])
+@pytest.mark.parametrize("density", G.QKV_DENSITIES)
+def test_fused_qkv(device, R, C, density, bf16):
+    w = G.fused_qkv(R, C, density, bf16=bf16)
+    p = w.projections[0]
+    k = B.bsr_prune_count(2304, 768, R, C, density)
+    log(f"fused_qkv {R}x{C} d={density} bf16={bf16}: k={k}")
+    M = prune_on_gpu(p.W, R, C, k)
+    check_prune(p.W, R, C, M, k)
+    if bf16:
+        M = M.to_bf16()
+        X = bf16_tensor(w.X[0])
+    else:
+        X = dev(w.X[0])
+    Y = B.bsr_spmm(X, M, dev(p.bias))
+    torch.cuda.synchronize()
+    check_spmm(w.X[0], M, p.bias, Y, bf16=bf16)
+
+
+@pytest.mark.parametrize("R,C", [(32, 1), (32, 32)])
+def test_bert_large_zipf(device, R, C):
+    """All 96 projections on the GPU; the oracle checks 8 of them fully pruned and every
+    product on a sample of 48 token rows."""
+    w = G.bert_large_zipf(R, C)
+    Xs = [dev(x) for x in w.X]
+    sample = rng(5).choice(w.tokens, size=48, replace=False)
+    sample.sort()
+    for n, p in enumerate(w.projections):
+        M = prune_on_gpu(p.W, R, C, p.k)
+        if n % 12 == 0:
+            log(f"bert_large {R}x{C} {p.name}: checking prune, k={p.k}")
+            check_prune(p.W, R, C, M, p.k)
+            counts = np.diff(host(M.indptr))
+            assert sorted(counts.tolist(), reverse=True) == w.notes["row_counts_by_rank"]
+        Y = B.bsr_spmm(Xs[p.x_index], M, dev(p.bias))
+        torch.cuda.synchronize()
+        check_spmm(w.X[p.x_index], M, p.bias, Y, rows=sample)
+
+
+# ----------------------------------------------------------------------------- edge cases
+
+
+def test_k_zero_gives_bias(device):
+    W = rng(1).standard_normal((64, 96)).astype(np.float32)
+    M = prune_on_gpu(W, 32, 1, 0)
+    assert host(M.indptr).tolist() == [0, 0, 0]
+    X = rng(2).standard_normal((5, 96)).astype(np.float32)
+    b = rng(3).standard_normal(64).astype(np.float32)
+    Y = B.bsr_spmm(dev(X), M, dev(b))
+    assert np.array_equal(host(Y), np.broadcast_to(b, (5, 64)))
+    Y0 = B.bsr_spmm(dev(X), M, None)
+    assert not host(Y0).any()
+
+
+def test_density_one_equals_dense(device):
+    g = rng(4)
+    W = g.standard_normal((128, 64)).astype(np.float32)
+    X = g.standard_normal((33, 64)).astype(np.float32)
+    b = g.standard_normal(128).astype(np.float32)
+    for R, C in [(32, 1), (16, 16), (1, 1)]:
+        M = prune_on_gpu(W, R, C, (128 // R) * (64 // C))
+        assert np.array_equal(host(B.bsr_to_dense(M)), W)
+        Y = B.bsr_spmm(dev(X), M, dev(b))
+        torch.cuda.synchronize()
+        check_spmm(X, M, b, Y)
+
+
+@pytest.mark.parametrize("T", [1, 2, 15, 17, 31, 33, 63, 65, 127, 129, 200])
+@pytest.mark.parametrize("R,C", [(32, 1), (16, 1), (32, 32), (16, 16), (8, 8), (1, 1), (1, 32),
+                                 (4, 4)])
+def test_ragged_token_counts(device, T, R, C):
+    g = rng(T * 100 + R + C)
+    W = g.standard_normal((256, 128)).astype(np.float32)
+    X = g.standard_normal((T, 128)).astype(np.float32)
+    b = g.standard_normal(256).astype(np.float32)
+    k = B.bsr_prune_count(256, 128, R, C, 0.3)
+    M = prune_on_gpu(W, R, C, k)
+    Y = B.bsr_spmm(dev(X), M, dev(b))
+    torch.cuda.synchronize()
+    check_spmm(X, M, b, Y)
+
+
+def test_leading_dimensions(device):
+    g = rng(6)
+    Wbig = g.standard_normal((96, 80)).astype(np.float32)
+    W = Wbig[:, :64]
+    Xbig = g.standard_normal((21, 100)).astype(np.float32)
+    X = Xbig[:, :64]
+    Wd = dev(Wbig)[:, :64]
+    M = B.bsr_prune_from_dense(Wd, 32, 1, k=40)
+    check_prune(np.ascontiguousarray(W), 32, 1, M, 40)
+    Ybig = torch.full((21, 130), 7.0, device="cuda:0")
+    Y = Ybig[:, :96]
+    B.bsr_spmm(dev(Xbig)[:, :64], M, None, Y=Y)
+    torch.cuda.synchronize()
+    check_spmm(np.ascontiguousarray(X), M, None, Y)
+    assert np.all(host(Ybig)[:, 96:] == 7.0)
+
+
+def test_single_block_row_and_full_row(device):
+    g = rng(7)
+    W = g.standard_normal((32, 256)).astype(np.float32)   # R = N: one block-row
+    X = g.standard_normal((50, 256)).astype(np.float32)
+    M = prune_on_gpu(W, 32, 1, 256)                      # every block of the row kept
+    Y = B.bsr_spmm(dev(X), M, None)
+    torch.cuda.synchronize()
+    check_spmm(X, M, None, Y)
+    M = prune_on_gpu(W, 32, 32, 3)
+    Y = B.bsr_spmm(dev(X), M, None)
+    torch.cuda.synchronize()
+    check_spmm(X, M, None, Y)
+
+
+@pytest.mark.parametrize("R,C", [(32, 1), (16, 16), (32, 32), (1, 1), (8, 1), (4, 4)])
+def test_integer_inputs_bit_exact(device, R, C):
+    """|x|, |w| <= 8 integers: every partial sum is an integer below 2^24, so any summation
+    order gives the exact result; fp32 and bf16 paths must match the exact product."""
+    g = rng(8 + R * C)
+    W = g.integers(-8, 9, size=(256, 192)).astype(np.float32)
+    X = g.integers(-8, 9, size=(70, 192)).astype(np.float32)
+    b = g.integers(-8, 9, size=256).astype(np.float32)
+    k = B.bsr_prune_count(256, 192, R, C, 0.4)
+    M = prune_on_gpu(W, R, C, k)
+    ip, ix, dt = O.prune(W, R, C, k=k)
+    exact = (X.astype(np.int64) @ O.to_dense(ip, ix, dt, 256, 192).astype(np.int64).T
+             + b.astype(np.int64)).astype(np.float32)
+    Y = B.bsr_spmm(dev(X), M, dev(b))
+    assert np.array_equal(host(Y), exact)
+    Yb = B.bsr_spmm(bf16_tensor(X), M.to_bf16(), dev(b))
+    assert np.array_equal(host(Yb), exact)
+
+
+def test_ties_and_zero_blocks(device):
+    W = np.zeros((64, 64), dtype=np.float32)
+    W[0:16, 16:32] = 1.0
+    W[16:32, 48:64] = -1.0          # same key as the block above
+    W[32:48, 0:16] = 0.5
+    for k in [1, 2, 3, 5, 16]:
+        M = prune_on_gpu(W, 16, 16, k)
+        check_prune(W, 16, 16, M, k)
+    W = np.zeros((32, 32), dtype=np.float32)   # all keys zero: lowest ids first
+    M = prune_on_gpu(W, 1, 1, 100)
+    check_prune(W, 1, 1, M, 100)
+
+
+def test_nonfinite_weights_prune(device):
+    W = rng(9).standard_normal((64, 64)).astype(np.float32)
+    W[3, 5] = np.inf
+    W[40, 7] = np.nan
+    W[10, 60] = -np.inf
+    for R, C in [(32, 1), (8, 8), (1, 1)]:
+        k = B.bsr_prune_count(64, 64, R, C, 0.1)
+        M = prune_on_gpu(W, R, C, k)
+        ip, ix, dt = O.prune(W, R, C, k=k)
+        assert np.array_equal(host(M.indptr), ip)
+        assert np.array_equal(host(M.indices)[:k], ix)
+        assert np.array_equal(host(M.data)[:k].view(np.uint32), dt.view(np.uint32))
+
+
+def test_cast_bit_exact(device):
+    g = rng(10)
+    u = g.integers(0, 1 << 32, size=1 << 20, dtype=np.uint64).astype(np.uint32)
+    special = np.array([0, 0x80000000, 0x7F800000, 0xFF800000, 0x7F7FFFFF, 0x7F7F8000,
+                        0x7F7F7FFF, 0x3F808000, 0x3F818000, 0x3F808001, 0x00000001, 0x00018000,
+                        0x7FC00000, 0x7F800001, 0xFFFFFFFF], dtype=np.uint32)
+    u = np.concatenate([special, u])
+    x = u.view(np.float32)
+    got = host(B.bsr_cast_f32_bf16(dev(x)).view(torch.int16)).view(np.uint16)
+    ref = O.bf16_round(x)
+    nan = np.isnan(x)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.all(np.isnan(O.bf16_to_f32(got[nan])))
+    assert np.array_equal(got[nan], ref[nan])
+
+
+def test_deterministic(device):
+    w = G.fused_qkv(32, 1, 0.2)
+    p = w.projections[0]
+    M = prune_on_gpu(p.W, 32, 1, B.bsr_prune_count(2304, 768, 32, 1, 0.2))
+    X = dev(w.X[0])
+    Y1 = B.bsr_spmm(X, M, dev(p.bias))
+    Y2 = B.bsr_spmm(X, M, dev(p.bias))
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
+
+
+def test_stream_ordering(device):
+    """Work enqueued on a side stream is ordered on that stream."""
+    w = G.single_768()
+    p = w.projections[0]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        Wd, Xd, bd = dev(p.W), dev(w.X[0]), dev(p.bias)
+        M = B.bsr_prune_from_dense(Wd, 32, 1, density=0.2, stream=s)
+        Y = B.bsr_spmm(Xd, M, bd, stream=s)
+    s.synchronize()
+    check_spmm(w.X[0], M, p.bias, Y)
