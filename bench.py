@@ -198,8 +198,8 @@ def main() -> int:
 def cpu_baseline(wl, calls, seconds: float) -> dict:
     """The C oracle (fp64 naive BSR loop, OpenMP over tokens) on this host's cores.
 
-    The sample is the whole step when it fits the time budget, otherwise the first projections'
-    calls on a leading slice of tokens; the rate is scaled to GFLOP/s of the same metric.
+    The sample is the whole step, repeated until about `seconds` of wall time have passed; the
+    rate is in GFLOP/s of the same metric (2 * nnz * tokens per call).
     """
     import torch
     from oracle import bsr_oracle as O
@@ -219,39 +219,34 @@ def cpu_baseline(wl, calls, seconds: float) -> dict:
         if wl.bf16:
             X = O.bf16_roundtrip(X)
         host.append((X, ip, ix, dt.reshape(c["k"], c["R"], c["C"]), c["N"], p.bias, c))
-    # Calibrate on the first call with a few tokens, then size the sample to ~`seconds`.
-    X, ip, ix, dt, N, b, c = host[0]
-    t_probe = min(16, X.shape[0])
-    t0 = time.perf_counter()
-    cpu_oracle.spmm(X[:t_probe], ip, ix, dt, N, b)
-    per_token = (time.perf_counter() - t0) / t_probe
+    # Run whole steps until the time budget is spent (at least one step).
     step_tokens = sum(h[0].shape[0] for h in host)
-    budget_tokens = max(1, int(seconds / max(per_token, 1e-9)))
     flops = 0.0
+    reps = 0
     t0 = time.perf_counter()
-    if budget_tokens >= step_tokens:
-        reps = max(1, budget_tokens // step_tokens)
-        for _ in range(reps):
-            for X, ip, ix, dt, N, b, c in host:
-                cpu_oracle.spmm(X, ip, ix, dt, N, b)
-                flops += 2.0 * c["k"] * c["R"] * c["C"] * X.shape[0]
-        sample = f"{reps} x the full step ({len(host)} calls x {host[0][0].shape[0]} tokens)"
-    else:
-        left = budget_tokens
-        used = 0
+    while True:
         for X, ip, ix, dt, N, b, c in host:
-            if left <= 0:
-                break
-            tt = min(left, X.shape[0])
-            cpu_oracle.spmm(X[:tt], ip, ix, dt, N, b)
-            flops += 2.0 * c["k"] * c["R"] * c["C"] * tt
-            left -= tt
-            used += 1
-        sample = f"{budget_tokens} tokens over the first {used} calls of the step"
+            cpu_oracle.spmm(X, ip, ix, dt, N, b)
+            flops += 2.0 * c["k"] * c["R"] * c["C"] * X.shape[0]
+        reps += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    sample = (f"{reps} x the full step ({len(host)} calls, {step_tokens} token-rows in all)")
     el = time.perf_counter() - t0
     return {"value": flops / el / 1e9, "unit": "GFLOP/s", "cores": cpu_oracle.num_threads(),
             "kind": "oracle", "sample": sample, "seconds": el,
-            "cpu": platform.processor() or platform.machine()}
+            "cpu": cpu_model()}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.machine()
 
 
 if __name__ == "__main__":

@@ -131,6 +131,30 @@ LIBBSR_API bsr_status bsr_spmm(const void *X, bsr_dtype x_dtype, int64_t T, int6
                     const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
                     void *stream);
 
+/* Kernel choice for bsr_spmm_ex (bsr_spmm uses BSR_KERNEL_AUTO). */
+typedef enum {
+    BSR_KERNEL_AUTO = 0,     /* the library picks                                           */
+    BSR_KERNEL_GENERIC = 1,  /* one thread per output element; every block shape and dtype   */
+    BSR_KERNEL_TILED = 2     /* LDS-staged token tiles on matrix cores; 32x1, 16x1, 32x32,
+                                16x16 blocks (BSR_ERR_UNSUPPORTED for other shapes)          */
+} bsr_kernel;
+
+typedef struct {
+    int32_t kernel;   /* a bsr_kernel value                                                  */
+    int32_t slices;   /* tiled kernel: block-row slices per 32-token tile; 0 = automatic     */
+} bsr_spmm_options_t;
+
+/*
+ * bsr_spmm with an explicit kernel choice and launch shape (for tests and tuning).  Same
+ * arguments, result and errors as bsr_spmm; opts may be NULL (automatic).  Different launch
+ * shapes may sum in different orders; each shape is bitwise reproducible.  Extra errors:
+ * BSR_ERR_ARG (unknown kernel, slices < 0), BSR_ERR_UNSUPPORTED (the forced kernel does not
+ * handle this shape, dtype or size).
+ */
+LIBBSR_API bsr_status bsr_spmm_ex(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
+                                  const bsr_matrix_t *W, const float *bias, float *Y,
+                                  int64_t ldy, const bsr_spmm_options_t *opts, void *stream);
+
 /*
  * Expand an fp32 BSR matrix to dense (Sec. 2.2 layout): out[n][k] = the stored element covering
  * (n, k), or +0.0 where no block is stored.  out: device fp32, N x K with row pitch ldo >= K.

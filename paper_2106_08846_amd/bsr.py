@@ -22,7 +22,9 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 
 # The C ABI's exported entry points (the tests check this list against include/libbsr.h).
 EXPORTS = ["bsr_prune_count", "bsr_prune_workspace_bytes", "bsr_prune_from_dense", "bsr_spmm",
-           "bsr_to_dense", "bsr_cast_f32_bf16", "bsr_status_str", "bsr_last_hip_error"]
+           "bsr_spmm_ex", "bsr_to_dense", "bsr_cast_f32_bf16", "bsr_status_str",
+           "bsr_last_hip_error"]
+KERNEL_AUTO, KERNEL_GENERIC, KERNEL_TILED = 0, 1, 2
 
 
 class BSRError(RuntimeError):
@@ -33,6 +35,10 @@ class BSRError(RuntimeError):
         if detail:
             msg += f": {detail}"
         super().__init__(msg)
+
+
+class bsr_spmm_options_t(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("slices", ctypes.c_int32)]
 
 
 class bsr_matrix_t(ctypes.Structure):
@@ -65,6 +71,9 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_spmm.argtypes = [p, ctypes.c_int, i64, i64, ctypes.POINTER(bsr_matrix_t), p, p,
                                  i64, p]
         lib.bsr_spmm.restype = st
+        lib.bsr_spmm_ex.argtypes = [p, ctypes.c_int, i64, i64, ctypes.POINTER(bsr_matrix_t), p,
+                                    p, i64, ctypes.POINTER(bsr_spmm_options_t), p]
+        lib.bsr_spmm_ex.restype = st
         lib.bsr_to_dense.argtypes = [ctypes.POINTER(bsr_matrix_t), p, i64, p]
         lib.bsr_to_dense.restype = st
         lib.bsr_cast_f32_bf16.argtypes = [p, p, i64, p]
@@ -182,6 +191,13 @@ def bsr_prune_from_dense(W: torch.Tensor, R: int, C: int, k: int | None = None,
 def bsr_spmm(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
              Y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Y = X W^T + bias with W in BSR (fp32 or bf16 inputs; fp32 accumulate and output)."""
+    return bsr_spmm_ex(X, W, bias, Y, None, None, stream)
+
+
+def bsr_spmm_ex(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
+                Y: torch.Tensor | None = None, kernel: int | None = None,
+                slices: int | None = None, stream=None) -> torch.Tensor:
+    """bsr_spmm with an explicit kernel (KERNEL_*) and slice count; None = automatic."""
     _require_cuda(X, "X")
     if X.dtype not in (torch.float32, torch.bfloat16):
         raise TypeError("X must be float32 or bfloat16")
@@ -199,8 +215,14 @@ def bsr_spmm(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
         raise ValueError("Y must have T rows")
     ldy = _pitch(Y, "Y")
     m = W.struct()
-    _check(_lib().bsr_spmm(_ptr(X), x_dtype, T, ldx, ctypes.byref(m), _ptr(bias), _ptr(Y), ldy,
-                           _stream(stream)), "bsr_spmm")
+    if kernel is None and slices is None:
+        _check(_lib().bsr_spmm(_ptr(X), x_dtype, T, ldx, ctypes.byref(m), _ptr(bias), _ptr(Y),
+                               ldy, _stream(stream)), "bsr_spmm")
+    else:
+        opts = bsr_spmm_options_t(kernel or 0, slices or 0)
+        _check(_lib().bsr_spmm_ex(_ptr(X), x_dtype, T, ldx, ctypes.byref(m), _ptr(bias),
+                                  _ptr(Y), ldy, ctypes.byref(opts), _stream(stream)),
+               "bsr_spmm_ex")
     return Y
 
 

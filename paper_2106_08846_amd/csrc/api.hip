@@ -7,6 +7,7 @@
 #include <mutex>
 
 #include "bsr_internal.h"
+#include "spmm_tiled.h"
 
 namespace bsr {
 
@@ -63,6 +64,17 @@ bsr_status ensure_device() {
     return ok ? BSR_OK : BSR_ERR_ARCH;
 }
 
+int auto_slices(int64_t T, const bsr_matrix_t *W, int cu_count) {
+    // Enough workgroups to give every CU one: token tiles times slices >= CUs, with at least
+    // one block-row per slice.
+    const int64_t tiles = (T + 31) / 32;
+    const int64_t Nb = W->n_rows / W->R;
+    int64_t S = (cu_count > 0 ? cu_count : 256) / (tiles > 0 ? tiles : 1);
+    if (S < 1) S = 1;
+    if (S > Nb) S = Nb;
+    return int(S);
+}
+
 int device_cu_count() {
     int dev = current_device();
     return (dev >= 0 && dev < kMaxDevices) ? g_devices[dev].cu_count : 0;
@@ -90,14 +102,30 @@ bsr_status bsr_prune_from_dense(const float *W, int64_t N, int64_t K, int64_t ld
     return bsr::launch_prune(W, N, K, ldw, R, C, k, indptr, indices, data, workspace, stream);
 }
 
+bsr_status bsr_spmm_ex(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
+                       const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
+                       const bsr_spmm_options_t *opts, void *stream) {
+    bsr_status s = bsr::check_spmm(X, int(x_dtype), T, ldx, W, Y, ldy);
+    if (s != BSR_OK) return s;
+    const int kernel = opts ? opts->kernel : BSR_KERNEL_AUTO;
+    const int slices = opts ? opts->slices : 0;
+    if (kernel < BSR_KERNEL_AUTO || kernel > BSR_KERNEL_TILED || slices < 0) return BSR_ERR_ARG;
+    if (T == 0) return BSR_OK;
+    if ((s = bsr::ensure_device()) != BSR_OK) return s;
+    if (kernel != BSR_KERNEL_GENERIC && bsr::tiled_supported(W->R, W->C, W->dtype)) {
+        const int S = slices > 0 ? slices : bsr::auto_slices(T, W, bsr::device_cu_count());
+        bsr::TiledPlan plan =
+            bsr::plan_tiled(X, T, ldx, W, S, bsr::device_lds_per_block());
+        if (plan.ok) return bsr::launch_spmm_tiled(plan, X, T, ldx, W, bias, Y, ldy, stream);
+    }
+    if (kernel == BSR_KERNEL_TILED) return BSR_ERR_UNSUPPORTED;
+    return bsr::launch_spmm_generic(X, T, ldx, W, bias, Y, ldy, stream);
+}
+
 bsr_status bsr_spmm(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
                     const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
                     void *stream) {
-    bsr_status s = bsr::check_spmm(X, int(x_dtype), T, ldx, W, Y, ldy);
-    if (s != BSR_OK) return s;
-    if (T == 0) return BSR_OK;
-    if ((s = bsr::ensure_device()) != BSR_OK) return s;
-    return bsr::launch_spmm_generic(X, T, ldx, W, bias, Y, ldy, stream);
+    return bsr_spmm_ex(X, x_dtype, T, ldx, W, bias, Y, ldy, nullptr, stream);
 }
 
 bsr_status bsr_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *stream) {

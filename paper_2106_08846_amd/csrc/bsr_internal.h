@@ -31,6 +31,7 @@ bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
 // Device-side entry points (implemented in the .hip files).  Arguments are already validated.
 bsr_status ensure_device();  // current device is gfx950; caches its properties
 int device_cu_count();
+int auto_slices(int64_t T, const bsr_matrix_t *W, int cu_count);
 size_t device_lds_per_block();
 
 bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,

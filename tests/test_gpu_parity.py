@@ -265,3 +265,121 @@ def test_stream_ordering(device):
         Y = B.bsr_spmm(Xd, M, bd, stream=s)
     s.synchronize()
     check_spmm(w.X[0], M, p.bias, Y)
+
+
+# ------------------------------------------------------------------ kernel choice and shapes
+
+TILED_SHAPES = [(32, 1), (16, 1), (32, 32), (16, 16)]
+
+
+def _skewed_weight(g, N, K, R, C, k):
+    """W whose nonzero blocks follow a Zipf-like row skew with k blocks in all."""
+    Nb, Kb = N // R, K // C
+    counts = G.zipf_counts(Nb, Kb, k)
+    mask = G.zipf_block_mask(counts, Kb, int(g.integers(1 << 30)))
+    return G.apply_block_mask(g.standard_normal((N, K)).astype(np.float32), R, C, mask)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+@pytest.mark.parametrize("slices", [1, 2, 3, 7, 0])
+def test_tiled_kernel_slices(device, R, C, slices):
+    g = rng(1000 + R * 10 + C + slices)
+    N, K, T = 256, 384, 100
+    W = g.standard_normal((N, K)).astype(np.float32)
+    X = g.standard_normal((T, K)).astype(np.float32)
+    b = g.standard_normal(N).astype(np.float32)
+    for density in [0.0, 0.05, 0.3, 1.0]:
+        k = B.bsr_prune_count(N, K, R, C, density)
+        M = prune_on_gpu(W, R, C, k)
+        Y = B.bsr_spmm_ex(dev(X), M, dev(b), kernel=B.KERNEL_TILED, slices=slices)
+        torch.cuda.synchronize()
+        check_spmm(X, M, b, Y)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+def test_tiled_kernel_skewed_rows(device, R, C):
+    g = rng(2000 + R + C)
+    N, K = 512, 512
+    Nb, Kb = N // R, K // C
+    k = max(1, (Nb * Kb) // 8)
+    W = _skewed_weight(g, N, K, R, C, k)
+    X = g.standard_normal((77, K)).astype(np.float32)
+    M = prune_on_gpu(W, R, C, k)
+    for slices in [1, 2, 5]:
+        Y = B.bsr_spmm_ex(dev(X), M, None, kernel=B.KERNEL_TILED, slices=slices)
+        torch.cuda.synchronize()
+        check_spmm(X, M, None, Y)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+def test_tiled_unaligned_and_pitched(device, R, C):
+    """Odd row pitches (no float4 staging) and offsets into larger buffers."""
+    g = rng(3000 + R + C)
+    N, K, T = 128, 256, 45
+    W = g.standard_normal((N, K)).astype(np.float32)
+    Xbig = g.standard_normal((T, K + 3)).astype(np.float32)
+    k = B.bsr_prune_count(N, K, R, C, 0.25)
+    M = prune_on_gpu(W, R, C, k)
+    Xd = dev(Xbig)[:, 1:K + 1]          # ldx = K + 3, base not 16-byte aligned
+    Ybig = torch.zeros((T, N + 5), device="cuda:0")
+    Y = Ybig[:, 2:N + 2]
+    B.bsr_spmm_ex(Xd, M, None, Y=Y, kernel=B.KERNEL_TILED)
+    torch.cuda.synchronize()
+    check_spmm(np.ascontiguousarray(Xbig[:, 1:K + 1]), M, None, Y)
+    assert not host(Ybig)[:, :2].any() and not host(Ybig)[:, N + 2:].any()
+
+
+def test_tiled_odd_width_r_by_1(device):
+    """K not a multiple of 4 for R x 1 blocks (scalar staging path)."""
+    g = rng(4000)
+    N, K, T = 96, 770, 40
+    W = g.standard_normal((N, K)).astype(np.float32)
+    X = g.standard_normal((T, K)).astype(np.float32)
+    for R in (32, 16):
+        M = prune_on_gpu(W, R, 1, B.bsr_prune_count(N, K, R, 1, 0.2))
+        Y = B.bsr_spmm_ex(dev(X), M, None, kernel=B.KERNEL_TILED)
+        torch.cuda.synchronize()
+        check_spmm(X, M, None, Y)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+def test_kernels_agree_bitwise_on_integers(device, R, C):
+    g = rng(5000 + R + C)
+    W = g.integers(-8, 9, size=(256, 256)).astype(np.float32)
+    X = g.integers(-8, 9, size=(67, 256)).astype(np.float32)
+    b = g.integers(-8, 9, size=256).astype(np.float32)
+    M = prune_on_gpu(W, R, C, B.bsr_prune_count(256, 256, R, C, 0.35))
+    Yg = B.bsr_spmm_ex(dev(X), M, dev(b), kernel=B.KERNEL_GENERIC)
+    Yt = B.bsr_spmm_ex(dev(X), M, dev(b), kernel=B.KERNEL_TILED, slices=3)
+    torch.cuda.synchronize()
+    assert torch.equal(Yg, Yt)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+def test_generic_kernel_on_tiled_shapes(device, R, C):
+    w = G.block_sweep(R, C)
+    p = w.projections[0]
+    M = prune_on_gpu(p.W, R, C, B.bsr_prune_count(768, 768, R, C, p.density))
+    Y = B.bsr_spmm_ex(dev(w.X[0]), M, dev(p.bias), kernel=B.KERNEL_GENERIC)
+    torch.cuda.synchronize()
+    check_spmm(w.X[0], M, p.bias, Y)
+
+
+def test_forced_tiled_unsupported_shape(device):
+    W = rng(6000).standard_normal((64, 64)).astype(np.float32)
+    M = prune_on_gpu(W, 8, 8, 10)
+    X = dev(rng(6001).standard_normal((4, 64)).astype(np.float32))
+    with pytest.raises(B.BSRError) as e:
+        B.bsr_spmm_ex(X, M, kernel=B.KERNEL_TILED)
+    assert e.value.status == 9
+
+
+def test_tiled_deterministic_and_repeatable(device):
+    w = G.bert_large_zipf(32, 1, layers=1)
+    p = w.projections[0]
+    M = prune_on_gpu(p.W, 32, 1, p.k)
+    X = dev(w.X[0])
+    Y1 = B.bsr_spmm(X, M, dev(p.bias))
+    Y2 = B.bsr_spmm(X, M, dev(p.bias))
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
