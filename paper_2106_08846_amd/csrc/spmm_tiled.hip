@@ -58,241 +58,240 @@ __device__ __forceinline__ int wave_lower_bound(const int *s_indptr, int n, int6
     return n;
 }
 
-// ---------------------------------------------------------------------------------- engines
-// Each engine knows its accumulator tile, how to add blocks [pa, pb) of one block-row into it,
-// how to store it to Y (with bias), and how to spill / add it through LDS.
+// ------------------------------------------------------------------------------------ units
+// A wave walks its stored blocks as a stream of fixed-size "units" of four MFMA steps: 8 blocks
+// for 32x1 (2 per v_mfma_f32_32x32x2_f32), 16 for 16x1 (4 per v_mfma_f32_16x16x4_f32, for each
+// 16-token half), one block for square shapes.  A unit policy loads a unit's operands into
+// registers, issues its MFMAs (all lanes, or only the blocks in an offset range [lo, hi) of the
+// unit when it crosses a row end), and stores a finished row tile to Y.
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Raw buffer resource over [base, base + bytes): loads past the end return 0.  Word 3 is the
+// default raw-buffer configuration for gfx9-family chips.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int64_t bytes) {
+    const int n = bytes > 0x7FFFFFFF ? 0x7FFFFFFF : int(bytes < 0 ? 0 : bytes);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, n, 0x00020000);
+}
+
+// Clamp a block column read from memory into [0, Kb) (unsigned compare also catches negatives).
+__device__ __forceinline__ int clamp_col(int j, int Kb) {
+    return int(min(unsigned(j), unsigned(Kb - 1)));
+}
 
 template <int R, int C>
-struct Engine;
+struct Unit;
 
-// 32x1 blocks, v_mfma_f32_32x32x2_f32.  acc[v] of lane l holds
-// Y[t0 + 8*(v/4) + 4*(l/32) + v%4][n0 + l%32].
-template <>
-struct Engine<32, 1> {
-    using Acc = floatx16;
-    static constexpr int kRegs = 16;
+// R x 1 blocks.  For R = 32, lane l supplies block l/32 of a step (A: token l%32 of the X tile;
+// B: feature l%32 of the block), acc[v] holds Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].
+// For R = 16, lane l supplies block l/16 of a step for both token halves, acc.h[h][v] holds
+// Y[t0 + 16h + 4(l/16) + v][n0 + l%16].
+template <int R>
+struct LinearUnit {
+    static constexpr int kPer = 64 / R;     // blocks per MFMA step
+    static constexpr int kSteps = 4;
+    static constexpr int kAhead = (R == 32) ? 2 : 3;   // units loaded ahead of use
+    static constexpr int KB = kPer * kSteps;
     static constexpr int kPad = 1;
-    __device__ static void zero(Acc &a) {
+    struct Ops {
+        int j[kSteps];
+        float b[kSteps];
+    };
+    __device__ static int offset_in_step() { return (threadIdx.x & 63) / R; }
+    __device__ static int feature() { return (threadIdx.x & 63) % R; }
+    // Loads every lane's operands for the unit at p through raw buffer loads based at the
+    // unit: one code path for every unit, no per-lane address arithmetic, and lanes past the
+    // end of the arrays (nnzb blocks) read 0.  Lanes past the unit's row segment read the next
+    // row's blocks; mask() zeroes them before the MFMAs.
+    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
+                                const float *__restrict__ data) {
+        const int o = offset_in_step(), f = feature();
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, int64_t(nnzb - p) * 4);
+        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data + int64_t(p) * R, int64_t(nnzb - p) * R * 4);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) a[v] = 0.0f;
-    }
-    __device__ static void accumulate(Acc &acc, int pa, int pb, const int *__restrict__ indices,
-                                      const float *__restrict__ data, const float *Xs, int XP,
-                                      int Kb) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const float *xrow = Xs + tl * XP;
-        int p = pa;
-        for (; p + 8 <= pb; p += 8) {
-            int j[4];
-            float b[4], a[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int q = p + 2 * u + kh;
-                j[u] = clampi(indices[q], 0, Kb - 1);
-                b[u] = data[int64_t(q) * 32 + tl];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) a[u] = xrow[j[u]];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) acc = mfma32(a[u], b[u], acc);
-        }
-        for (; p < pb; p += 2) {
-            const int q = p + kh;
-            float a = 0.0f, b = 0.0f;
-            if (q < pb) {
-                a = xrow[clampi(indices[q], 0, Kb - 1)];
-                b = data[int64_t(q) * 32 + tl];
-            }
-            acc = mfma32(a, b, acc);
+        for (int m = 0; m < kSteps; ++m) {
+            ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
+            ops.b[m] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rd, (o * R + f) * 4, m * kPer * R * 4, 0));
         }
     }
-    __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
-                                 int64_t T, int64_t n0, const float *__restrict__ bias) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const float bv = bias ? bias[n0 + tl] : 0.0f;
+    // Zero the operands of lanes whose block offset in the unit is >= nvalid (partial units).
+    __device__ static void mask(Ops &ops, int nvalid) {
+        const int o = offset_in_step();
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int64_t t = t0 + 8 * (v >> 2) + 4 * kh + (v & 3);
-            if (t < T) Y[t * ldy + n0 + tl] = acc[v] + bv;
+        for (int m = 0; m < kSteps; ++m) {
+            const bool in = m * kPer + o < nvalid;
+            ops.j[m] = in ? ops.j[m] : -1;
+            ops.b[m] = in ? ops.b[m] : 0.0f;
         }
     }
 };
 
-// 16x1 blocks, v_mfma_f32_16x16x4_f32 on two 16-token halves.  acc[h][v] of lane l holds
-// Y[t0 + 16h + 4*(l/16) + v][n0 + l%16].
 template <>
-struct Engine<16, 1> {
+struct Unit<32, 1> : LinearUnit<32> {
+    static constexpr int kRegs = 16;
+    using Acc = floatx16;
+    __device__ static void zero(Acc &acc) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+    }
+    // MFMAs of one unit.  Column indices are clamped to [0, Kb]; column Kb of the X tile is
+    // the zero pad column that masked lanes point at.
+    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
+        const float *xrow = Xs + feature() * XP;
+        float a[kSteps];
+#pragma unroll
+        for (int m = 0; m < kSteps; ++m) a[m] = xrow[clamp_col(ops.j[m], Kb + 1)];
+#pragma unroll
+        for (int m = 0; m < kSteps; ++m) acc = mfma32(a[m], ops.b[m], acc);
+    }
+    __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
+                                 int64_t T, int64_t n0, const float *__restrict__ bias) {
+        // Y is written once and never read here: nontemporal stores keep it out of the caches.
+        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
+        const float bv = bias ? bias[n0 + tl] : 0.0f;
+        const int64_t tq = t0 + 4 * kh;
+        float *yl = Y + tq * ldy + n0 + tl;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int r = 8 * (v >> 2) + (v & 3);
+            if (tq + r < T) __builtin_nontemporal_store(acc[v] + bv, yl + r * ldy);
+        }
+    }
+    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
+    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
+};
+
+template <>
+struct Unit<16, 1> : LinearUnit<16> {
+    static constexpr int kRegs = 8;
     struct Acc {
         floatx4 h[2];
     };
-    static constexpr int kRegs = 8;
-    static constexpr int kPad = 1;
-    __device__ static void zero(Acc &a) {
+    __device__ static void zero(Acc &acc) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) a.h[0][v] = a.h[1][v] = 0.0f;
+        for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = 0.0f;
     }
-    __device__ static void accumulate(Acc &acc, int pa, int pb, const int *__restrict__ indices,
-                                      const float *__restrict__ data, const float *Xs, int XP,
-                                      int Kb) {
-        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const float *x0 = Xs + tl * XP;
-        const float *x1 = Xs + (16 + tl) * XP;
-        int p = pa;
-        for (; p + 16 <= pb; p += 16) {
-            int j[4];
-            float b[4];
+    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
+        const float *x0 = Xs + feature() * XP;
+        const float *x1 = x0 + 16 * XP;
+        float a0[kSteps], a1[kSteps];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int q = p + 4 * u + kq;
-                j[u] = clampi(indices[q], 0, Kb - 1);
-                b[u] = data[int64_t(q) * 16 + tl];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const float a0 = x0[j[u]], a1 = x1[j[u]];
-                acc.h[0] = mfma16(a0, b[u], acc.h[0]);
-                acc.h[1] = mfma16(a1, b[u], acc.h[1]);
-            }
+        for (int m = 0; m < kSteps; ++m) {
+            const int j = clamp_col(ops.j[m], Kb + 1);
+            a0[m] = x0[j];
+            a1[m] = x1[j];
         }
-        for (; p < pb; p += 4) {
-            const int q = p + kq;
-            float a0 = 0.0f, a1 = 0.0f, b = 0.0f;
-            if (q < pb) {
-                const int jj = clampi(indices[q], 0, Kb - 1);
-                a0 = x0[jj];
-                a1 = x1[jj];
-                b = data[int64_t(q) * 16 + tl];
-            }
-            acc.h[0] = mfma16(a0, b, acc.h[0]);
-            acc.h[1] = mfma16(a1, b, acc.h[1]);
+#pragma unroll
+        for (int m = 0; m < kSteps; ++m) {
+            acc.h[0] = mfma16(a0[m], ops.b[m], acc.h[0]);
+            acc.h[1] = mfma16(a1[m], ops.b[m], acc.h[1]);
         }
     }
     __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
                                  int64_t T, int64_t n0, const float *__restrict__ bias) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
         const float bv = bias ? bias[n0 + tl] : 0.0f;
+        const int64_t tq = t0 + 4 * kq;
+        float *yl = Y + tq * ldy + n0 + tl;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int64_t t = t0 + 16 * h + 4 * kq + v;
-                if (t < T) Y[t * ldy + n0 + tl] = acc.h[h][v] + bv;
+                const int r = 16 * h + v;
+                if (tq + r < T) __builtin_nontemporal_store(acc.h[h][v] + bv, yl + r * ldy);
             }
         }
     }
+    __device__ static float get(const Acc &acc, int v) { return acc.h[v >> 2][v & 3]; }
+    __device__ static void add(Acc &acc, int v, float x) { acc.h[v >> 2][v & 3] += x; }
 };
 
-// 32x32 blocks, v_mfma_f32_32x32x2_f32.  For block-column step u (8 columns) and e in 0..3,
-// lane l's k-slot l/32 stands for c = 8u + 4*(l/32) + e in both operands.
+// 32x32 blocks, v_mfma_f32_32x32x2_f32.  Lane l loads columns 8u + 4(l/32) .. +3 of block row
+// l%32 (u = 0..3); for step (u, e) its k-slot l/32 stands for c = 8u + 4(l/32) + e in both
+// operands.
 template <>
-struct Engine<32, 32> {
-    using Acc = floatx16;
-    static constexpr int kRegs = 16;
+struct Unit<32, 32> {
+    static constexpr int KB = 1;
+    static constexpr int kAhead = 1;
     static constexpr int kPad = 4;
-    __device__ static void zero(Acc &a) { Engine<32, 1>::zero(a); }
-    __device__ static void load_block(floatx4 (&d)[4], const float *__restrict__ data, int p,
-                                      int tl, int kh) {
+    static constexpr int kRegs = 16;
+    using Acc = floatx16;
+    struct Ops {
+        int j;
+        floatx4 d[4];
+    };
+    __device__ static void zero(Acc &acc) { Unit<32, 1>::zero(acc); }
+    __device__ static void mask(Ops &, int) {}
+    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+                                const float *__restrict__ data) {
+        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
+        ops.j = uniform(indices[p]);
         const floatx4 *blk = reinterpret_cast<const floatx4 *>(data + int64_t(p) * 1024);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) d[u] = blk[tl * 8 + 2 * u + kh];
+        for (int u = 0; u < 4; ++u) ops.d[u] = blk[tl * 8 + 2 * u + kh];
     }
-    __device__ static void accumulate(Acc &acc, int pa, int pb, const int *__restrict__ indices,
-                                      const float *__restrict__ data, const float *Xs, int XP,
-                                      int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const float *xrow = Xs + tl * XP + 4 * kh;
-        if (pa >= pb) return;
-        floatx4 d[4], dn[4];
-        int j = clampi(indices[pa], 0, Kb - 1);
-        load_block(d, data, pa, tl, kh);
-        for (int p = pa; p < pb; ++p) {
-            int jn = j;
-            if (p + 1 < pb) {
-                jn = clampi(indices[p + 1], 0, Kb - 1);
-                load_block(dn, data, p + 1, tl, kh);
-            }
-            const float *xb = xrow + j * 32;
+        const float *xb = Xs + tl * XP + 4 * kh + clamp_col(ops.j, Kb) * 32;
+        floatx4 a[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const floatx4 a = *reinterpret_cast<const floatx4 *>(xb + 8 * u);
+        for (int u = 0; u < 4; ++u) a[u] = *reinterpret_cast<const floatx4 *>(xb + 8 * u);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc = mfma32(a[e], d[u][e], acc);
-            }
-            if (p + 1 < pb) {
+        for (int u = 0; u < 4; ++u) {
 #pragma unroll
-                for (int u = 0; u < 4; ++u) d[u] = dn[u];
-            }
-            j = jn;
+            for (int e = 0; e < 4; ++e) acc = mfma32(a[u][e], ops.d[u][e], acc);
         }
     }
     __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
                                  int64_t T, int64_t n0, const float *__restrict__ bias) {
-        Engine<32, 1>::store(acc, Y, ldy, t0, T, n0, bias);
+        Unit<32, 1>::store(acc, Y, ldy, t0, T, n0, bias);
     }
+    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
+    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
 };
 
-// 16x16 blocks, v_mfma_f32_16x16x4_f32 on two 16-token halves.  Lane l loads row l%16,
-// columns 4*(l/16)..+3 of the block (the whole block in one instruction); k-slot l/16 of step
-// e stands for c = 4*(l/16) + e.
+// 16x16 blocks, v_mfma_f32_16x16x4_f32 on two 16-token halves.  Lane l loads row l%16, columns
+// 4(l/16)..+3 of the block (the whole block in one instruction); k-slot l/16 of step e stands
+// for c = 4(l/16) + e.
 template <>
-struct Engine<16, 16> {
-    using Acc = Engine<16, 1>::Acc;
-    static constexpr int kRegs = 8;
+struct Unit<16, 16> {
+    static constexpr int KB = 1;
+    static constexpr int kAhead = 3;
     static constexpr int kPad = 4;
-    __device__ static void zero(Acc &a) { Engine<16, 1>::zero(a); }
-    __device__ static void accumulate(Acc &acc, int pa, int pb, const int *__restrict__ indices,
-                                      const float *__restrict__ data, const float *Xs, int XP,
-                                      int Kb) {
+    static constexpr int kRegs = 8;
+    using Acc = Unit<16, 1>::Acc;
+    struct Ops {
+        int j;
+        floatx4 d;
+    };
+    __device__ static void zero(Acc &acc) { Unit<16, 1>::zero(acc); }
+    __device__ static void mask(Ops &, int) {}
+    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+                                const float *__restrict__ data) {
+        const int lane = threadIdx.x & 63;
+        ops.j = uniform(indices[p]);
+        ops.d = reinterpret_cast<const floatx4 *>(data + int64_t(p) * 256)[(lane & 15) * 4 +
+                                                                           (lane >> 4)];
+    }
+    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const float *x0 = Xs + tl * XP + 4 * kq;
-        const float *x1 = Xs + (16 + tl) * XP + 4 * kq;
-        int p = pa;
-        for (; p + 2 <= pb; p += 2) {
-            int j[2];
-            floatx4 d[2];
+        const float *xb = Xs + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
+        const floatx4 a0 = *reinterpret_cast<const floatx4 *>(xb);
+        const floatx4 a1 = *reinterpret_cast<const floatx4 *>(xb + 16 * XP);
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                j[u] = clampi(indices[p + u], 0, Kb - 1);
-                d[u] = reinterpret_cast<const floatx4 *>(data + int64_t(p + u) * 256)[tl * 4 + kq];
-            }
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const floatx4 a0 = *reinterpret_cast<const floatx4 *>(x0 + j[u] * 16);
-                const floatx4 a1 = *reinterpret_cast<const floatx4 *>(x1 + j[u] * 16);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    acc.h[0] = mfma16(a0[e], d[u][e], acc.h[0]);
-                    acc.h[1] = mfma16(a1[e], d[u][e], acc.h[1]);
-                }
-            }
-        }
-        if (p < pb) {
-            const int jj = clampi(indices[p], 0, Kb - 1);
-            const floatx4 d = reinterpret_cast<const floatx4 *>(data + int64_t(p) * 256)[tl * 4 + kq];
-            const floatx4 a0 = *reinterpret_cast<const floatx4 *>(x0 + jj * 16);
-            const floatx4 a1 = *reinterpret_cast<const floatx4 *>(x1 + jj * 16);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                acc.h[0] = mfma16(a0[e], d[e], acc.h[0]);
-                acc.h[1] = mfma16(a1[e], d[e], acc.h[1]);
-            }
+        for (int e = 0; e < 4; ++e) {
+            acc.h[0] = mfma16(a0[e], ops.d[e], acc.h[0]);
+            acc.h[1] = mfma16(a1[e], ops.d[e], acc.h[1]);
         }
     }
     __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
                                  int64_t T, int64_t n0, const float *__restrict__ bias) {
-        Engine<16, 1>::store(acc, Y, ldy, t0, T, n0, bias);
+        Unit<16, 1>::store(acc, Y, ldy, t0, T, n0, bias);
     }
+    __device__ static float get(const Acc &acc, int v) { return Unit<16, 1>::get(acc, v); }
+    __device__ static void add(Acc &acc, int v, float x) { Unit<16, 1>::add(acc, v, x); }
 };
-
-// Register v of an accumulator tile (the tile is a 16-wide vector or two 4-wide vectors).
-__device__ __forceinline__ float acc_get(const floatx16 &a, int v) { return a[v]; }
-__device__ __forceinline__ void acc_add(floatx16 &a, int v, float x) { a[v] += x; }
-__device__ __forceinline__ float acc_get(const Engine<16, 1>::Acc &a, int v) {
-    return a.h[v >> 2][v & 3];
-}
-__device__ __forceinline__ void acc_add(Engine<16, 1>::Acc &a, int v, float x) {
-    a.h[v >> 2][v & 3] += x;
-}
 
 // -------------------------------------------------------------------------------- the kernel
 
@@ -302,12 +301,14 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(
     const int32_t *__restrict__ indices, const float *__restrict__ data, int nnzb, int Nb, int Kb,
     const float *__restrict__ bias, float *__restrict__ Y, int64_t ldy, int num_tiles,
     int slices, int XP, int indptr_words, int x_vec4) {
-    using E = Engine<R, C>;
+    using U = Unit<R, C>;
     extern __shared__ float smem[];
     int *s_indptr = reinterpret_cast<int *>(smem);
     float *Xs = smem + indptr_words;
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // The wave index is uniform across a wave; readfirstlane tells the compiler so, which
+    // keeps all loop and row bookkeeping in scalar registers with scalar branches.
+    const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
     constexpr int kThreads = NW * 64;
 
     // Workgroup -> (token tile, slice).  Workgroups are dealt to the 8 XCDs round robin, so
@@ -319,22 +320,44 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(
 
     for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
 
-    // Stage X[t0 : t0 + 32][0 : K] into LDS (row pitch XP); rows past T are zero.
+    // Stage X[t0 : t0 + 32][0 : K] into LDS (row pitch XP); rows past T are zero, and so is
+    // the pad column K of the R x 1 layout.  Each thread issues all its loads before its LDS
+    // stores (up to kStageVec float4 per thread), advancing (t, c4) without divisions.
     if (x_vec4) {
-        const int K4 = K >> 2;
-        for (int f = threadIdx.x; f < kTT * K4; f += kThreads) {
-            const int t = f / K4, c4 = f - t * K4;
-            floatx4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-            if (t0 + t < T)
-                v = *reinterpret_cast<const floatx4 *>(X + (t0 + t) * ldx + 4 * c4);
-            float *dst = Xs + t * XP + 4 * c4;
-            if constexpr (E::kPad == 4) {
-                *reinterpret_cast<floatx4 *>(dst) = v;
-            } else {
-                dst[0] = v[0];
-                dst[1] = v[1];
-                dst[2] = v[2];
-                dst[3] = v[3];
+        constexpr int kStageVec = 12;
+        const int K4 = K >> 2, total = kTT * K4;
+        const int dt = kThreads / K4, dc = kThreads - dt * K4;
+        int t = threadIdx.x / K4, c4 = threadIdx.x - t * K4;
+        for (int f0 = threadIdx.x; f0 < total; f0 += kStageVec * kThreads) {
+            floatx4 v[kStageVec];
+            int off[kStageVec];
+#pragma unroll
+            for (int u = 0; u < kStageVec; ++u) {
+                off[u] = t * XP + 4 * c4;
+                v[u] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+                if (f0 + u * kThreads < total && t0 + t < T)
+                    v[u] = __builtin_nontemporal_load(
+                        reinterpret_cast<const floatx4 *>(X + (t0 + t) * ldx + 4 * c4));
+                c4 += dc;
+                t += dt;
+                if (c4 >= K4) {
+                    c4 -= K4;
+                    ++t;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kStageVec; ++u) {
+                if (f0 + u * kThreads < total) {
+                    float *dst = Xs + off[u];
+                    if constexpr (U::kPad == 4) {
+                        *reinterpret_cast<floatx4 *>(dst) = v[u];
+                    } else {
+                        dst[0] = v[u][0];
+                        dst[1] = v[u][1];
+                        dst[2] = v[u][2];
+                        dst[3] = v[u][3];
+                    }
+                }
             }
         }
     } else {
@@ -343,48 +366,138 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(
             Xs[t * XP + c] = (t0 + t < T) ? X[(t0 + t) * ldx + c] : 0.0f;
         }
     }
+    if constexpr (U::kPad == 1) {
+        if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
+    }
     __syncthreads();
 
     // This slice's block-rows and stored-block range.
-    const int64_t k = s_indptr[Nb];
-    const int row_lo = (s == 0) ? 0 : wave_lower_bound(s_indptr, Nb, int64_t(s) * k / slices);
+    const int64_t k = uniform(s_indptr[Nb]);
+    const int row_lo =
+        (s == 0) ? 0 : uniform(wave_lower_bound(s_indptr, Nb, int64_t(s) * k / slices));
     const int row_hi = (s == slices - 1)
                            ? Nb
-                           : wave_lower_bound(s_indptr, Nb, int64_t(s + 1) * k / slices);
-    const int64_t Q0 = s_indptr[row_lo], Q1 = s_indptr[row_hi];
+                           : uniform(wave_lower_bound(s_indptr, Nb, int64_t(s + 1) * k / slices));
+    const int64_t Q0 = uniform(s_indptr[row_lo]), Q1 = uniform(s_indptr[row_hi]);
     const int64_t span = Q1 > Q0 ? Q1 - Q0 : 0;
-    auto wave_start = [&](int w) -> int64_t { return Q0 + span * w / NW; };
-    const int64_t Pw = wave_start(wave), Pw1 = wave_start(wave + 1);
+    auto wave_start = [&](int w) -> int { return int(Q0 + span * w / NW); };
+    const int Pw = uniform(wave_start(wave)), Pw1 = uniform(wave_start(wave + 1));
 
     // Rows owned by this wave: those whose first block lies in [Pw, Pw1) (last wave: all rows
     // up to the slice end, including trailing empty rows).
-    int rlo = (wave == 0) ? row_lo : wave_lower_bound(s_indptr, Nb, Pw);
+    int rlo = (wave == 0) ? row_lo : uniform(wave_lower_bound(s_indptr, Nb, Pw));
     rlo = rlo < row_lo ? row_lo : (rlo > row_hi ? row_hi : rlo);
-    int rhi = (wave == NW - 1) ? row_hi : wave_lower_bound(s_indptr, Nb, Pw1);
+    int rhi = (wave == NW - 1) ? row_hi : uniform(wave_lower_bound(s_indptr, Nb, Pw1));
     rhi = rhi < rlo ? rlo : (rhi > row_hi ? row_hi : rhi);
 
-    // Head: blocks of [Pw, Pw1) that belong to the row started by an earlier wave.
-    int64_t head_end = (rlo < rhi) ? int64_t(s_indptr[rlo]) : Pw1;
+    // Head: blocks of [Pw, Pw1) that belong to row rlo - 1, started by an earlier wave.
+    int head_end = (rlo < rhi) ? uniform(s_indptr[rlo]) : Pw1;
     head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
     const bool has_head = head_end > Pw;
-    typename E::Acc head;
-    E::zero(head);
-    if (has_head)
-        E::accumulate(head, int(Pw), int(head_end), indices, data, Xs, XP, Kb);
+    const int r_first = has_head ? rlo - 1 : rlo;
 
-    typename E::Acc acc;
-    int tail_row = -1;
-    for (int i = rlo; i < rhi; ++i) {
-        const int pa = s_indptr[i];
-        const int pe = s_indptr[i + 1];
-        const int pb = pe < Pw1 ? pe : int(Pw1);
-        E::zero(acc);
-        E::accumulate(acc, pa, pb, indices, data, Xs, XP, Kb);
-        if (pe > Pw1) {
-            tail_row = i;
-            break;
+    // Empty owned rows: Y = bias.  (The stream below visits only segments with blocks.)
+    for (int r = rlo; r < rhi; ++r) {
+        if (uniform(s_indptr[r + 1]) == uniform(s_indptr[r])) {
+            typename U::Acc z;
+            U::zero(z);
+            U::store(z, Y, ldy, t0, T, int64_t(r) * R, bias);
         }
-        E::store(acc, Y, ldy, t0, T, int64_t(i) * R, bias);
+    }
+
+    // The wave's block range [Pw, Pw1) is cut into row segments: the head segment
+    // [Pw, head_end) of row rlo - 1 (if any), then each owned row with blocks, clipped to Pw1.
+    // Each segment is a counted loop over units of KB blocks from its start (the last one may
+    // be partial, masked branch-free).  Operands are double-buffered in A/B: every unit's
+    // MFMAs are issued after the loads of the following unit, which for a segment's last unit
+    // is the first unit of the next segment.  Row bookkeeping (stores, zeroing) stays outside
+    // the inner loop so the accumulator is updated in place.
+    constexpr int KB = U::KB;
+    typename U::Acc acc, head;
+    U::zero(acc);
+    U::zero(head);
+    int tail_row = -1;
+
+    // First row after r with blocks (rhi if none); returns its start and clipped end.
+    auto next_row = [&](int r, int &start, int &end) -> int {
+        for (++r; r < rhi; ++r) {
+            start = uniform(s_indptr[r]);
+            const int e = uniform(s_indptr[r + 1]);
+            if (start < e) {
+                end = e < Pw1 ? e : Pw1;
+                return r;
+            }
+        }
+        start = end = 0;
+        return rhi;
+    };
+    int row, p, end;
+    if (has_head) {
+        row = rlo - 1;
+        p = Pw;
+        end = head_end;
+    } else {
+        row = next_row(rlo - 1, p, end);
+    }
+    if (row < rhi) {
+        typename U::Ops A, B;
+        U::load(A, p, nnzb, indices, data);
+        while (true) {
+            int np, nend;
+            const int nrow = next_row(row, np, nend);
+            const bool more = nrow < rhi;
+            // After the segment's last unit, prefetch the next segment's first unit (or, at
+            // the very end, reload the current unit: a harmless in-bounds load).
+            const int fp = more ? np : p;
+            const int nu = (end - p + KB - 1) / KB;
+            bool next_in_b;
+            int u = 0;
+            // sched_barrier keeps the compiler from sinking each prefetch next to its use,
+            // which would leave no load in flight while the MFMAs run.  A partial last unit
+            // has its operand registers masked (never the accumulator, which stays in place).
+            while (true) {
+                const int q = p + u * KB;
+                const bool last = u + 1 == nu;
+                U::load(B, last ? fp : q + KB, nnzb, indices, data);
+                __builtin_amdgcn_sched_barrier(0);
+                if (q + KB > end) U::mask(A, end - q);
+                U::mma(acc, A, Xs, XP, Kb);
+                __builtin_amdgcn_sched_barrier(0);
+                if (last) {
+                    next_in_b = true;
+                    break;
+                }
+                ++u;
+                const int q2 = p + u * KB;
+                const bool last2 = u + 1 == nu;
+                U::load(A, last2 ? fp : q2 + KB, nnzb, indices, data);
+                __builtin_amdgcn_sched_barrier(0);
+                if (q2 + KB > end) U::mask(B, end - q2);
+                U::mma(acc, B, Xs, XP, Kb);
+                __builtin_amdgcn_sched_barrier(0);
+                if (last2) {
+                    next_in_b = false;
+                    break;
+                }
+                ++u;
+            }
+            // Finish the segment: head -> `head`, complete row -> Y, a row continuing past
+            // Pw1 (necessarily the last segment) -> tail, left in `acc`.
+            if (row == rlo - 1) {
+                head = acc;
+                U::zero(acc);
+            } else if (uniform(s_indptr[row + 1]) <= Pw1) {
+                U::store(acc, Y, ldy, t0, T, int64_t(row) * R, bias);
+                U::zero(acc);
+            } else {
+                tail_row = row;
+            }
+            if (!more) break;
+            if (next_in_b) A = B;
+            row = nrow;
+            p = np;
+            end = nend;
+        }
     }
 
     // Combine rows cut by wave boundaries.  The X tile is dead now; reuse its LDS.
@@ -392,21 +505,20 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(
     float *H = Xs;
     if (has_head) {
 #pragma unroll
-        for (int v = 0; v < E::kRegs; ++v)
-            H[(wave * E::kRegs + v) * 64 + lane] = acc_get(head, v);
+        for (int v = 0; v < U::kRegs; ++v) H[(wave * U::kRegs + v) * 64 + lane] = U::get(head, v);
     }
     __syncthreads();
     if (tail_row >= 0) {
         // Every later wave whose range starts inside this row holds a head partial of it,
         // except waves with an empty range, which wrote nothing.
-        const int64_t end = s_indptr[tail_row + 1];
+        const int end = uniform(s_indptr[tail_row + 1]);
         for (int w2 = wave + 1; w2 < NW && wave_start(w2) < end; ++w2) {
             if (wave_start(w2 + 1) == wave_start(w2)) continue;
 #pragma unroll
-            for (int v = 0; v < E::kRegs; ++v)
-                acc_add(acc, v, H[(w2 * E::kRegs + v) * 64 + lane]);
+            for (int v = 0; v < U::kRegs; ++v)
+                U::add(acc, v, H[(w2 * U::kRegs + v) * 64 + lane]);
         }
-        E::store(acc, Y, ldy, t0, T, int64_t(tail_row) * R, bias);
+        U::store(acc, Y, ldy, t0, T, int64_t(tail_row) * R, bias);
     }
 }
 
@@ -432,7 +544,9 @@ bool tiled_supported(int R, int C, int dtype) {
            (R == 16 && C == 16);
 }
 
-int tiled_waves(int R, int C) { return (R == 32 && C == 32) ? 8 : 16; }
+// Waves per workgroup, chosen so that each variant's registers fit without spilling
+// (512 VGPRs per SIMD lane shared by the waves on that SIMD).
+int tiled_waves(int R, int C) { return 16; }
 
 TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int slices,
                      size_t lds_limit) {
@@ -440,7 +554,7 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     const int R = W->R, C = W->C;
     if (!tiled_supported(R, C, W->dtype)) return p;
     const int64_t K = W->n_cols, Nb = W->n_rows / R;
-    const int pad = (C == 1) ? 1 : 4;
+    const int pad = (C == 1) ? 1 : 4;   // Unit<R, C>::kPad
     const int regs = (R == 32) ? 16 : 8;
     const int NW = tiled_waves(R, C);
     p.x_pitch = int(K + pad);
@@ -472,7 +586,7 @@ bsr_status launch_spmm_tiled(const TiledPlan &plan, const void *X, int64_t T, in
     if (W->R == 16 && W->C == 1)
         return launch_variant<16, 1, 16>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
     if (W->R == 32 && W->C == 32)
-        return launch_variant<32, 32, 8>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
+        return launch_variant<32, 32, 16>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
     if (W->R == 16 && W->C == 16)
         return launch_variant<16, 16, 16>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
     return BSR_ERR_UNSUPPORTED;
