@@ -3,19 +3,25 @@
 
 Default workload: a BERT-base attention layer -- four 768x768 projections (Q, K, V, O), each
 pruned to 32x1 blocks at 10% block density, applied to one batch of 1 x 128 tokens.  One step
-is the four bsr_spmm calls.  Inputs are seeded synthetic tensors (see
-paper_2106_08846_amd/workloads.py), already resident in device memory when timing starts.
+is the four bsr_spmm calls.  Inputs are seeded synthetic tensors (paper_2106_08846_amd/
+workloads.py), pruned on the GPU by bsr_prune_from_dense, and resident in device memory when
+timing starts.
 
-Prints one JSON line: effective GFLOP/s (2 * nnz * tokens per call, summed over the step),
-the roofline position of the product kernel (per-launch duration from HIP events on the launch
-stream), the same-shape dense fp32 GEMM, and the CPU oracle timed on this host's cores.
+The step is timed as a HIP graph of its calls, replayed --steps times (the way a fixed inference
+step is issued in production; --eager times the same calls launched one by one from Python).
+Prints one JSON line: effective GFLOP/s (2 * nnz * tokens per call, summed over the step), the
+roofline position of the product kernel (average launch duration from HIP events recorded on
+the launch stream), the same-shape dense fp32/bf16 GEMM, and the CPU oracle on this host.
 """
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
 import platform
+import re
 import sys
 import time
 
@@ -25,9 +31,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
-FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 (matrix / packed)
-BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 matrix
+FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 matrix (dense)
+BF16_PEAK_TFLOPS = 2516.6      # MI355X bf16 matrix (dense)
 METRIC = "BSR SpMM effective GFLOP/s (2*nnz*tokens)"
+KERNEL_SOURCES = "paper_2106_08846_amd/csrc"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm.md")
 
 
 def parse():
@@ -38,10 +46,17 @@ def parse():
     ap.add_argument("--workload", default="bert_base_attn",
                     help="bert_base_attn | single_768 | sweep:RxC | "
                          "fused_qkv:RxC:density[:bf16] | bert_large:RxC")
+    ap.add_argument("--slices", type=int, default=0,
+                    help="block-row slices per token tile (0: the library's choice)")
+    ap.add_argument("--eager", action="store_true",
+                    help="time the calls launched one by one instead of a graph replay")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB --steps times (the reference "
+                         "kernel for scaling HBM byte counters) and exit")
     return ap.parse_args()
 
 
@@ -63,6 +78,46 @@ def build_workload(spec: str):
     raise SystemExit(f"unknown workload {spec}")
 
 
+def kernel_source_hash() -> str:
+    """sha256 over libbsr's kernel and launch sources (counters go stale when it changes)."""
+    h = hashlib.sha256()
+    for path in sorted(glob.glob(os.path.join(ROOT, KERNEL_SOURCES, "*"))):
+        if os.path.isfile(path) and path.endswith((".hip", ".h", ".cpp")):
+            h.update(os.path.basename(path).encode())
+            with open(path, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str) -> dict | None:
+    """HBM bytes per launch from the committed counter summary, if it is for this source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    table = json.loads(m.group(1))
+    if table.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return table.get("workloads", {}).get(workload)
+
+
+def calibrate_copy(args) -> int:
+    import torch
+    n = args.calibrate_copy * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(args.steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes_read": 4 * n, "calibrate_copy_bytes_written": 4 * n,
+                      "launches": args.steps}), flush=True)
+    return 0
+
+
 def main() -> int:
     args = parse()
     if args.gpus != 1:
@@ -76,6 +131,8 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
+    if args.calibrate_copy:
+        return calibrate_copy(args)
     dev = torch.device("cuda:0")
     wl = build_workload(args.workload)
     bf16 = wl.bf16
@@ -96,41 +153,71 @@ def main() -> int:
         bias = torch.from_numpy(p.bias).to(dev)
         T = wl.X[p.x_index].shape[0]
         Y = torch.empty((T, N), dtype=torch.float32, device=dev)
+        run = B.SpmmCall(Xs[p.x_index], M, bias, Y, slices=args.slices or None)
         calls.append(dict(X=Xs[p.x_index], M=M, bias=bias, Y=Y, Wd=Wd, T=T, N=N, K=K, R=p.R,
-                          C=p.C, k=k))
+                          C=p.C, k=k, run=run))
     torch.cuda.synchronize()
 
     def step():
         for c in calls:
-            B.bsr_spmm(c["X"], c["M"], c["bias"], Y=c["Y"])
+            c["run"]()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(args.steps):
-        step()
-    end.record()
-    torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(end) / args.steps
+
+    def time_steps(fn, n):
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(n):
+            fn()
+        end.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / n
+
+    eager_ms = time_steps(step, args.steps)
+    graph_ms = None
+    if not args.eager:
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(args.warmup):
+            g.replay()
+        graph_ms = time_steps(g.replay, args.steps)
+    ms_per_step = eager_ms if args.eager else graph_ms
 
     flops_step = sum(2.0 * c["k"] * c["R"] * c["C"] * c["T"] for c in calls)
     value = flops_step / (ms_per_step * 1e-3) / 1e9
 
     # Roofline of the product kernel: average duration of one launch, from HIP events recorded
-    # on the launch stream around each launch.
+    # on the launch stream (torch's current stream, which the calls use) around each launch.
+    # A large device fill is queued first so that the host runs ahead of the device and the
+    # event pairs bracket device execution rather than host launch gaps.
     sx = 2 if bf16 else 4
+    n_ev = max(1, min(args.steps, 400 // len(calls) + 1))
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(len(calls) * args.steps)]
+          for _ in range(len(calls) * n_ev)]
+    pad = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    for _ in range(24):
+        pad.fill_(1.0)
     i = 0
-    for _ in range(args.steps):
+    for _ in range(n_ev):
         for c in calls:
             ev[i][0].record()
-            B.bsr_spmm(c["X"], c["M"], c["bias"], Y=c["Y"])
+            c["run"]()
             ev[i][1].record()
             i += 1
     torch.cuda.synchronize()
+    del pad
     launch_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
 
     def launch_bytes(c):
@@ -142,17 +229,20 @@ def main() -> int:
     flops_launch = flops_step / len(calls)
     peak_flops = (BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS) * 1e12
     ai = flops_launch / bytes_launch
+    gbs = bytes_launch / (launch_ms * 1e-3) / 1e9
+    tfs = flops_launch / (launch_ms * 1e-3) / 1e12
     if ai > peak_flops / (HBM_PEAK_GBS * 1e9):
-        achieved = flops_launch / (launch_ms * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": peak_flops / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / (peak_flops / 1e12)}
+        roof = {"bound": "mfma", "achieved": tfs, "peak": peak_flops / 1e12,
+                "unit": "TFLOP/s", "frac": tfs / (peak_flops / 1e12)}
     else:
-        achieved = bytes_launch / (launch_ms * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS}
-    roof.update({"traffic": None, "kernel": "bsr_spmm", "launch_us": launch_ms * 1e3,
+        roof = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": gbs / HBM_PEAK_GBS}
+    tr = measured_traffic(wl.name)
+    roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
+                 "kernel": tiled_kernel_name(calls[0]), "launch_us": launch_ms * 1e3,
                  "algorithmic_bytes_per_launch": bytes_launch,
-                 "flops_per_launch": flops_launch, "arithmetic_intensity": ai})
+                 "flops_per_launch": flops_launch, "arithmetic_intensity": ai,
+                 "achieved_gbs": gbs, "achieved_tflops": tfs})
 
     out = {
         "metric": METRIC, "value": value, "unit": "GFLOP/s", "n_gpus": 1,
@@ -163,7 +253,11 @@ def main() -> int:
                    "tokens": calls[0]["T"], "N": calls[0]["N"], "K": calls[0]["K"],
                    "block": f"{calls[0]['R']}x{calls[0]['C']}",
                    "density": wl.projections[0].density,
-                   "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in calls][:8]},
+                   "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in calls][:8],
+                   "timing": "eager" if args.eager else "hip_graph_replay",
+                   "slices": args.slices or "auto"},
+        "eager_ms_per_step": eager_ms,
+        "graph_ms_per_step": graph_ms,
         "roofline": roof,
     }
 
@@ -180,19 +274,17 @@ def main() -> int:
 
         for _ in range(args.warmup):
             dense_step()
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(args.steps):
-            dense_step()
-        end.record()
-        torch.cuda.synchronize()
-        out["dense_gemm_ms_per_step"] = start.elapsed_time(end) / args.steps
+        out["dense_gemm_ms_per_step"] = time_steps(dense_step, args.steps)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, calls, args.cpu_seconds)
 
     print(json.dumps(out), flush=True)
     return 0
+
+
+def tiled_kernel_name(c) -> str:
+    return f"bsr_spmm ({c['R']}x{c['C']} blocks)"
 
 
 def cpu_baseline(wl, calls, seconds: float) -> dict:

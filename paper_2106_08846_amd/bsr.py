@@ -226,6 +226,42 @@ def bsr_spmm_ex(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
     return Y
 
 
+class SpmmCall:
+    """A bsr_spmm / bsr_spmm_ex call with its arguments marshalled once.
+
+    Calling it re-issues the same C call (same tensors, same options) on the given stream, or
+    on torch's current stream, which is what a serving loop or a HIP graph capture needs: the
+    per-call host cost is one foreign call.  The tensors stay referenced by the object.
+    """
+
+    def __init__(self, X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None,
+                 Y: torch.Tensor, kernel: int | None = None, slices: int | None = None):
+        _require_cuda(X, "X")
+        if X.dtype not in (torch.float32, torch.bfloat16):
+            raise TypeError("X must be float32 or bfloat16")
+        if bias is not None:
+            _require_cuda(bias, "bias", torch.float32)
+            if bias.dim() != 1 or bias.numel() != W.n_rows or not bias.is_contiguous():
+                raise ValueError("bias must be a contiguous [N] float32 tensor")
+        _require_cuda(Y, "Y", torch.float32)
+        if Y.shape[0] != X.shape[0]:
+            raise ValueError("Y must have T rows")
+        self._keep = (X, W, bias, Y)
+        self._m = W.struct()
+        self._opts = bsr_spmm_options_t(kernel or 0, slices or 0)
+        x_dtype = BSR_BF16 if X.dtype == torch.bfloat16 else BSR_F32
+        self._args = (_ptr(X), x_dtype, X.shape[0], _pitch(X, "X"), ctypes.byref(self._m),
+                      _ptr(bias), _ptr(Y), _pitch(Y, "Y"), ctypes.byref(self._opts))
+        self._fn = _lib().bsr_spmm_ex
+        self.Y = Y
+
+    def __call__(self, stream=None) -> torch.Tensor:
+        st = self._fn(*self._args, _stream(stream))
+        if st != 0:
+            _check(st, "bsr_spmm_ex")
+        return self.Y
+
+
 def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Dense fp32 [N, K] expansion of an fp32 BSR matrix."""
     if out is None:

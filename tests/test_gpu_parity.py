@@ -383,3 +383,65 @@ def test_tiled_deterministic_and_repeatable(device):
     Y2 = B.bsr_spmm(X, M, dev(p.bias))
     torch.cuda.synchronize()
     assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
+
+
+# ------------------------------------------------------------------ prepared calls and graphs
+
+
+@pytest.mark.parametrize("R,C,kernel,bf16", [(32, 1, B.KERNEL_AUTO, False),
+                                             (16, 16, B.KERNEL_AUTO, False),
+                                             (8, 8, B.KERNEL_AUTO, False),
+                                             (32, 1, B.KERNEL_GENERIC, True)])
+def test_graph_replay_matches_eager(device, R, C, kernel, bf16):
+    """A captured step replays bit-identically to the eager call, replay after replay."""
+    log(f"graph replay R={R} C={C} kernel={kernel} bf16={bf16}")
+    w = G.bert_base_attention(R, C, 0.1, tokens=96)
+    calls, eager = [], []
+    Xd = dev(w.X[0])
+    Xin = B.bsr_cast_f32_bf16(Xd) if bf16 else Xd
+    for p in w.projections:
+        k = B.bsr_prune_count(768, 768, R, C, p.density)
+        M = prune_on_gpu(p.W, R, C, k)
+        if bf16:
+            M = M.to_bf16()
+        Y = torch.empty((96, 768), dtype=torch.float32, device=device)
+        run = B.SpmmCall(Xin, M, dev(p.bias), Y, kernel=kernel)
+        eager.append(run().clone())
+        calls.append(run)
+    torch.cuda.synchronize()
+    check_spmm(w.X[0], calls[0]._keep[1], w.projections[0].bias, eager[0], bf16=bf16)
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for run in calls:
+            run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for run in calls:
+            run()
+    for rep in range(3):
+        for run in calls:
+            run.Y.fill_(float("nan"))     # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for run, ref in zip(calls, eager):
+            assert torch.equal(run.Y.view(torch.int32), ref.view(torch.int32)), f"replay {rep}"
+
+
+def test_prepared_call_matches_bsr_spmm(device):
+    w = G.single_768()
+    p = w.projections[0]
+    k = B.bsr_prune_count(768, 768, 32, 1, p.density)
+    M = prune_on_gpu(p.W, 32, 1, k)
+    X, b = dev(w.X[0]), dev(p.bias)
+    Y = torch.empty((128, 768), dtype=torch.float32, device=device)
+    run = B.SpmmCall(X, M, b, Y, slices=5)
+    Yp = run().clone()
+    Ys = B.bsr_spmm_ex(X, M, b, slices=5)
+    torch.cuda.synchronize()
+    assert torch.equal(Yp.view(torch.int32), Ys.view(torch.int32))
+    with pytest.raises(ValueError):
+        B.SpmmCall(X, M, b, torch.empty((127, 768), dtype=torch.float32, device=device))
