@@ -3,12 +3,14 @@
 
 Default workload: a BERT-base attention layer -- four 768x768 projections (Q, K, V, O), each
 pruned to 32x1 blocks at 10% block density, applied to one batch of 1 x 128 tokens.  One step
-is the four bsr_spmm calls.  Inputs are seeded synthetic tensors (paper_2106_08846_amd/
-workloads.py), pruned on the GPU by bsr_prune_from_dense, and resident in device memory when
-timing starts.
+computes the four products, issued as one bsr_spmm_batched call (one kernel launch; workloads
+with more products use one call per 8).  Inputs are seeded synthetic tensors
+(paper_2106_08846_amd/workloads.py), pruned on the GPU by bsr_prune_from_dense, and resident in
+device memory when timing starts.
 
-The step is timed as a HIP graph of its calls, replayed --steps times (the way a fixed inference
-step is issued in production; --eager times the same calls launched one by one from Python).
+The step is timed as --steps direct issues of its prepared calls (arguments marshalled once,
+one foreign call per launch); --graph times HIP graph replays of the same calls instead, and
+both figures are reported.
 Prints one JSON line: effective GFLOP/s (2 * nnz * tokens per call, summed over the step), the
 roofline position of the product kernel (average launch duration from HIP events recorded on
 the launch stream), the same-shape dense fp32/bf16 GEMM, and the CPU oracle on this host.
@@ -48,8 +50,10 @@ def parse():
                          "fused_qkv:RxC:density[:bf16] | bert_large:RxC")
     ap.add_argument("--slices", type=int, default=0,
                     help="block-row slices per token tile (0: the library's choice)")
-    ap.add_argument("--eager", action="store_true",
-                    help="time the calls launched one by one instead of a graph replay")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the step as HIP graph replays instead of direct calls")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the graph-replay figure (e.g. under counter collection)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent timing the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -153,14 +157,18 @@ def main() -> int:
         bias = torch.from_numpy(p.bias).to(dev)
         T = wl.X[p.x_index].shape[0]
         Y = torch.empty((T, N), dtype=torch.float32, device=dev)
-        run = B.SpmmCall(Xs[p.x_index], M, bias, Y, slices=args.slices or None)
         calls.append(dict(X=Xs[p.x_index], M=M, bias=bias, Y=Y, Wd=Wd, T=T, N=N, K=K, R=p.R,
-                          C=p.C, k=k, run=run))
+                          C=p.C, k=k))
+    # The step's products go to bsr_spmm_batched in groups of up to 8 (one kernel launch each:
+    # Q, K, V and O of a layer share one launch).
+    groups = [calls[i:i + 8] for i in range(0, len(calls), 8)]
+    runs = [B.SpmmBatchCall([(c["X"], c["M"], c["bias"], c["Y"]) for c in grp],
+                            slices=args.slices or None) for grp in groups]
     torch.cuda.synchronize()
 
     def step():
-        for c in calls:
-            c["run"]()
+        for run in runs:
+            run()
 
     for _ in range(args.warmup):
         step()
@@ -179,7 +187,7 @@ def main() -> int:
 
     eager_ms = time_steps(step, args.steps)
     graph_ms = None
-    if not args.eager:
+    if args.graph or not args.no_graph:
         g = torch.cuda.CUDAGraph()
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
@@ -192,32 +200,28 @@ def main() -> int:
         for _ in range(args.warmup):
             g.replay()
         graph_ms = time_steps(g.replay, args.steps)
-    ms_per_step = eager_ms if args.eager else graph_ms
+    ms_per_step = graph_ms if args.graph else eager_ms
 
     flops_step = sum(2.0 * c["k"] * c["R"] * c["C"] * c["T"] for c in calls)
     value = flops_step / (ms_per_step * 1e-3) / 1e9
 
-    # Roofline of the product kernel: average duration of one launch, from HIP events recorded
-    # on the launch stream (torch's current stream, which the calls use) around each launch.
-    # A large device fill is queued first so that the host runs ahead of the device and the
-    # event pairs bracket device execution rather than host launch gaps.
+    # Roofline of the product kernel: average device duration of one launch.  Each launch gets a
+    # pair of HIP events that the library records at the kernel's own start and end on the
+    # launch stream (hipExtLaunchKernel), so host gaps and dispatch overhead are excluded.
     sx = 2 if bf16 else 4
-    n_ev = max(1, min(args.steps, 400 // len(calls) + 1))
+    n_ev = max(1, min(args.steps, 400 // len(runs) + 1))
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(len(calls) * n_ev)]
-    pad = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+          for _ in range(len(runs) * n_ev)]
+    for a, b in ev:
+        a.record()
+        b.record()
     torch.cuda.synchronize()
-    for _ in range(24):
-        pad.fill_(1.0)
     i = 0
     for _ in range(n_ev):
-        for c in calls:
-            ev[i][0].record()
-            c["run"]()
-            ev[i][1].record()
+        for run in runs:
+            run.timed(*ev[i])
             i += 1
     torch.cuda.synchronize()
-    del pad
     launch_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
 
     def launch_bytes(c):
@@ -225,8 +229,8 @@ def main() -> int:
         return (c["T"] * c["K"] * sx + c["k"] * c["R"] * c["C"] * sx + 4 * c["k"]
                 + 4 * (nb_rows + 1) + 4 * c["N"] + 4 * c["T"] * c["N"])
 
-    bytes_launch = float(np.mean([launch_bytes(c) for c in calls]))
-    flops_launch = flops_step / len(calls)
+    bytes_launch = sum(launch_bytes(c) for c in calls) / len(runs)
+    flops_launch = flops_step / len(runs)
     peak_flops = (BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS) * 1e12
     ai = flops_launch / bytes_launch
     gbs = bytes_launch / (launch_ms * 1e-3) / 1e9
@@ -249,12 +253,13 @@ def main() -> int:
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
-        "config": {"workload": wl.name, "calls_per_step": len(calls),
+        "config": {"workload": wl.name, "products_per_step": len(calls),
+                   "launches_per_step": len(runs),
                    "tokens": calls[0]["T"], "N": calls[0]["N"], "K": calls[0]["K"],
                    "block": f"{calls[0]['R']}x{calls[0]['C']}",
                    "density": wl.projections[0].density,
                    "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in calls][:8],
-                   "timing": "eager" if args.eager else "hip_graph_replay",
+                   "timing": "hip_graph_replay" if args.graph else "direct_calls",
                    "slices": args.slices or "auto"},
         "eager_ms_per_step": eager_ms,
         "graph_ms_per_step": graph_ms,
@@ -284,7 +289,11 @@ def main() -> int:
 
 
 def tiled_kernel_name(c) -> str:
-    return f"bsr_spmm ({c['R']}x{c['C']} blocks)"
+    """The kernel libbsr launches for this product (its tiled variants are fp32 only)."""
+    tiled = c["M"].dtype == 0 and (c["R"], c["C"]) in ((32, 1), (16, 1), (32, 32), (16, 16))
+    if tiled:
+        return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16> via bsr_spmm_batched"
+    return "spmm_generic_kernel via bsr_spmm_batched"
 
 
 def cpu_baseline(wl, calls, seconds: float) -> dict:

@@ -140,20 +140,56 @@ typedef enum {
 } bsr_kernel;
 
 typedef struct {
-    int32_t kernel;   /* a bsr_kernel value                                                  */
-    int32_t slices;   /* tiled kernel: block-row slices per 32-token tile; 0 = automatic     */
+    int32_t kernel;     /* a bsr_kernel value                                                */
+    int32_t slices;     /* tiled kernel: block-row slices per 32-token tile; 0 = automatic   */
+    void *start_event;  /* hipEvent_t or NULL: recorded when the product kernel starts       */
+    void *stop_event;   /* hipEvent_t or NULL: recorded when it ends (both or neither)       */
 } bsr_spmm_options_t;
 
 /*
  * bsr_spmm with an explicit kernel choice and launch shape (for tests and tuning).  Same
  * arguments, result and errors as bsr_spmm; opts may be NULL (automatic).  Different launch
- * shapes may sum in different orders; each shape is bitwise reproducible.  Extra errors:
- * BSR_ERR_ARG (unknown kernel, slices < 0), BSR_ERR_UNSUPPORTED (the forced kernel does not
- * handle this shape, dtype or size).
+ * shapes may sum in different orders; each shape is bitwise reproducible.  With an event
+ * pair (caller-created hipEvents with timing enabled), the kernel is launched through
+ * hipExtLaunchKernel so that hipEventElapsedTime(start, stop) is the kernel's own device time
+ * (no event is recorded when T = 0, as nothing is launched).  Extra errors: BSR_ERR_ARG
+ * (unknown kernel, slices < 0, only one event given), BSR_ERR_UNSUPPORTED (the forced kernel
+ * does not handle this shape, dtype or size).
  */
 LIBBSR_API bsr_status bsr_spmm_ex(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
                                   const bsr_matrix_t *W, const float *bias, float *Y,
                                   int64_t ldy, const bsr_spmm_options_t *opts, void *stream);
+
+/* One product of a batched call: the arguments of one bsr_spmm call. */
+typedef struct {
+    const void *X;          /* device, T x K, row pitch ldx, of type x_dtype                 */
+    bsr_dtype x_dtype;      /* must equal W->dtype                                           */
+    int64_t T;              /* tokens (rows of X and Y); 0 = nothing to do for this product  */
+    int64_t ldx;            /* row pitch of X in elements, >= K                              */
+    const bsr_matrix_t *W;  /* host pointer to the matrix descriptor                         */
+    const float *bias;      /* device fp32[N] or NULL                                        */
+    float *Y;               /* device fp32, T x N, row pitch ldy                             */
+    int64_t ldy;            /* row pitch of Y in elements, >= N                              */
+} bsr_spmm_item_t;
+
+/*
+ * Several BSR products in as few kernel launches as possible: the projections of one attention
+ * layer (Sec. 2.3: Q, K, V and O of BERT), or any set of independent products.  The paper's
+ * compiler reuses work across tasks that share a sparse structure (Sec. 2.2, third bullet); here
+ * independent products of one block shape share a single launch, up to 8 per launch, which
+ * removes the per-launch fixed cost that dominates small token counts.
+ * Result: each items[i].Y is what bsr_spmm_ex(items[i], opts) computes with the same kernel and
+ * slice count.  With opts->slices = 0 the automatic slice count considers the token tiles of
+ * every product in the launch, so it can differ from a single call's choice (the results then
+ * differ only in fp32 summation order).  Products are independent and may run in any order or
+ * concurrently: no Y may overlap another product's X, W arrays, bias or Y.  With an event pair
+ * in opts, the start event is recorded at the start of the first kernel and the stop event at
+ * the end of the last one.  n_items = 0 (or all T = 0) is a no-op.
+ * Errors: as bsr_spmm_ex for the first invalid item (nothing is launched if any item is
+ *   invalid); BSR_ERR_ARG for n_items < 0; BSR_ERR_NULL for items = NULL with n_items > 0.
+ */
+LIBBSR_API bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
+                                       const bsr_spmm_options_t *opts, void *stream);
 
 /*
  * Expand an fp32 BSR matrix to dense (Sec. 2.2 layout): out[n][k] = the stored element covering

@@ -22,8 +22,8 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 
 # The C ABI's exported entry points (the tests check this list against include/libbsr.h).
 EXPORTS = ["bsr_prune_count", "bsr_prune_workspace_bytes", "bsr_prune_from_dense", "bsr_spmm",
-           "bsr_spmm_ex", "bsr_to_dense", "bsr_cast_f32_bf16", "bsr_status_str",
-           "bsr_last_hip_error"]
+           "bsr_spmm_ex", "bsr_spmm_batched", "bsr_to_dense", "bsr_cast_f32_bf16",
+           "bsr_status_str", "bsr_last_hip_error"]
 KERNEL_AUTO, KERNEL_GENERIC, KERNEL_TILED = 0, 1, 2
 
 
@@ -38,7 +38,8 @@ class BSRError(RuntimeError):
 
 
 class bsr_spmm_options_t(ctypes.Structure):
-    _fields_ = [("kernel", ctypes.c_int32), ("slices", ctypes.c_int32)]
+    _fields_ = [("kernel", ctypes.c_int32), ("slices", ctypes.c_int32),
+                ("start_event", ctypes.c_void_p), ("stop_event", ctypes.c_void_p)]
 
 
 class bsr_matrix_t(ctypes.Structure):
@@ -46,6 +47,12 @@ class bsr_matrix_t(ctypes.Structure):
                 ("R", ctypes.c_int32), ("C", ctypes.c_int32), ("nnzb", ctypes.c_int64),
                 ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p),
                 ("data", ctypes.c_void_p), ("dtype", ctypes.c_int)]
+
+
+class bsr_spmm_item_t(ctypes.Structure):
+    _fields_ = [("X", ctypes.c_void_p), ("x_dtype", ctypes.c_int), ("T", ctypes.c_int64),
+                ("ldx", ctypes.c_int64), ("W", ctypes.POINTER(bsr_matrix_t)),
+                ("bias", ctypes.c_void_p), ("Y", ctypes.c_void_p), ("ldy", ctypes.c_int64)]
 
 
 _LIB = None
@@ -74,6 +81,9 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_spmm_ex.argtypes = [p, ctypes.c_int, i64, i64, ctypes.POINTER(bsr_matrix_t), p,
                                     p, i64, ctypes.POINTER(bsr_spmm_options_t), p]
         lib.bsr_spmm_ex.restype = st
+        lib.bsr_spmm_batched.argtypes = [ctypes.POINTER(bsr_spmm_item_t), i32,
+                                         ctypes.POINTER(bsr_spmm_options_t), p]
+        lib.bsr_spmm_batched.restype = st
         lib.bsr_to_dense.argtypes = [ctypes.POINTER(bsr_matrix_t), p, i64, p]
         lib.bsr_to_dense.restype = st
         lib.bsr_cast_f32_bf16.argtypes = [p, p, i64, p]
@@ -118,6 +128,8 @@ def _require_cuda(t: torch.Tensor, name: str, dtype=None) -> None:
 
 def _pitch(t: torch.Tensor, name: str) -> int:
     """Row pitch (elements) of a 2-D tensor whose rows are contiguous."""
+    if t.dim() == 2 and t.numel() == 0:
+        return max(t.shape[1], 1)          # an empty tensor's strides carry no layout
     if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
         raise ValueError(f"{name} must be 2-D with unit column stride")
     return t.stride(0) if t.shape[0] > 1 else max(t.shape[1], 1)
@@ -219,47 +231,108 @@ def bsr_spmm_ex(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
         _check(_lib().bsr_spmm(_ptr(X), x_dtype, T, ldx, ctypes.byref(m), _ptr(bias), _ptr(Y),
                                ldy, _stream(stream)), "bsr_spmm")
     else:
-        opts = bsr_spmm_options_t(kernel or 0, slices or 0)
+        opts = bsr_spmm_options_t(kernel or 0, slices or 0, None, None)
         _check(_lib().bsr_spmm_ex(_ptr(X), x_dtype, T, ldx, ctypes.byref(m), _ptr(bias),
                                   _ptr(Y), ldy, ctypes.byref(opts), _stream(stream)),
                "bsr_spmm_ex")
     return Y
 
 
-class SpmmCall:
-    """A bsr_spmm / bsr_spmm_ex call with its arguments marshalled once.
+def _check_call(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None,
+                Y: torch.Tensor) -> None:
+    _require_cuda(X, "X")
+    if X.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("X must be float32 or bfloat16")
+    if bias is not None:
+        _require_cuda(bias, "bias", torch.float32)
+        if bias.dim() != 1 or bias.numel() != W.n_rows or not bias.is_contiguous():
+            raise ValueError("bias must be a contiguous [N] float32 tensor")
+    _require_cuda(Y, "Y", torch.float32)
+    if Y.shape[0] != X.shape[0]:
+        raise ValueError("Y must have T rows")
 
-    Calling it re-issues the same C call (same tensors, same options) on the given stream, or
-    on torch's current stream, which is what a serving loop or a HIP graph capture needs: the
-    per-call host cost is one foreign call.  The tensors stay referenced by the object.
+
+class SpmmBatchCall:
+    """A bsr_spmm_batched call with its arguments marshalled once.
+
+    `products` is a list of (X, W, bias, Y) tuples.  Calling the object re-issues the same C
+    call on the given stream, or on torch's current stream, which is what a serving loop or a
+    HIP graph capture needs: the per-call host cost is one foreign call.  The tensors stay
+    referenced by the object.
     """
+
+    def __init__(self, products, kernel: int | None = None, slices: int | None = None):
+        self._keep = list(products)
+        self._mats = []
+        items = (bsr_spmm_item_t * max(len(products), 1))()
+        for i, (X, W, bias, Y) in enumerate(products):
+            _check_call(X, W, bias, Y)
+            m = W.struct()
+            self._mats.append(m)
+            items[i] = bsr_spmm_item_t(_ptr(X), BSR_BF16 if X.dtype == torch.bfloat16 else BSR_F32,
+                                       X.shape[0], _pitch(X, "X"), ctypes.pointer(m), _ptr(bias),
+                                       _ptr(Y), _pitch(Y, "Y"))
+        self._items = items
+        self._opts = bsr_spmm_options_t(kernel or 0, slices or 0, None, None)
+        self._timed_opts = bsr_spmm_options_t(kernel or 0, slices or 0, None, None)
+        self._fn = _lib().bsr_spmm_batched
+        self._n = len(products)
+        self.Y = [p[3] for p in products]
+
+    def __call__(self, stream=None):
+        st = self._fn(self._items, self._n, ctypes.byref(self._opts), _stream(stream))
+        if st != 0:
+            _check(st, "bsr_spmm_batched")
+        return self.Y
+
+    def timed(self, start: torch.cuda.Event, stop: torch.cuda.Event, stream=None):
+        """Issue the call with `start`/`stop` recorded at the start of its first kernel and the
+        end of its last one.
+
+        Both events must be timing events that have been recorded once (torch creates the
+        underlying HIP event lazily); afterwards start.elapsed_time(stop) is the device time of
+        the call's kernels in ms.
+        """
+        if not start.cuda_event or not stop.cuda_event:
+            raise ValueError("record both events once before passing them")
+        self._timed_opts.start_event = start.cuda_event
+        self._timed_opts.stop_event = stop.cuda_event
+        st = self._fn(self._items, self._n, ctypes.byref(self._timed_opts), _stream(stream))
+        if st != 0:
+            _check(st, "bsr_spmm_batched")
+        return self.Y
+
+
+class SpmmCall(SpmmBatchCall):
+    """A single prepared product (a batch of one): bsr_spmm_ex with arguments marshalled once."""
 
     def __init__(self, X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None,
                  Y: torch.Tensor, kernel: int | None = None, slices: int | None = None):
-        _require_cuda(X, "X")
-        if X.dtype not in (torch.float32, torch.bfloat16):
-            raise TypeError("X must be float32 or bfloat16")
-        if bias is not None:
-            _require_cuda(bias, "bias", torch.float32)
-            if bias.dim() != 1 or bias.numel() != W.n_rows or not bias.is_contiguous():
-                raise ValueError("bias must be a contiguous [N] float32 tensor")
-        _require_cuda(Y, "Y", torch.float32)
-        if Y.shape[0] != X.shape[0]:
-            raise ValueError("Y must have T rows")
-        self._keep = (X, W, bias, Y)
-        self._m = W.struct()
-        self._opts = bsr_spmm_options_t(kernel or 0, slices or 0)
-        x_dtype = BSR_BF16 if X.dtype == torch.bfloat16 else BSR_F32
-        self._args = (_ptr(X), x_dtype, X.shape[0], _pitch(X, "X"), ctypes.byref(self._m),
-                      _ptr(bias), _ptr(Y), _pitch(Y, "Y"), ctypes.byref(self._opts))
-        self._fn = _lib().bsr_spmm_ex
+        super().__init__([(X, W, bias, Y)], kernel, slices)
         self.Y = Y
 
     def __call__(self, stream=None) -> torch.Tensor:
-        st = self._fn(*self._args, _stream(stream))
-        if st != 0:
-            _check(st, "bsr_spmm_ex")
+        super().__call__(stream)
         return self.Y
+
+    def timed(self, start, stop, stream=None) -> torch.Tensor:
+        super().timed(start, stop, stream)
+        return self.Y
+
+
+def bsr_spmm_batched(products, kernel: int | None = None, slices: int | None = None,
+                     stream=None) -> list:
+    """Several products Y_i = X_i W_i^T + bias_i in as few launches as possible.
+
+    `products` is a list of (X, W, bias, Y) with Y allocated by the caller (Y may be None to
+    allocate it).  Returns the list of Y tensors.
+    """
+    full = []
+    for X, W, bias, Y in products:
+        if Y is None:
+            Y = torch.empty((X.shape[0], W.n_rows), dtype=torch.float32, device=X.device)
+        full.append((X, W, bias, Y))
+    return SpmmBatchCall(full, kernel, slices)(stream)
 
 
 def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

@@ -5,6 +5,7 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
+#include <vector>
 
 #include "bsr_internal.h"
 #include "spmm_tiled.h"
@@ -64,12 +65,10 @@ bsr_status ensure_device() {
     return ok ? BSR_OK : BSR_ERR_ARCH;
 }
 
-int auto_slices(int64_t T, const bsr_matrix_t *W, int cu_count) {
-    // Enough workgroups to give every CU one: token tiles times slices >= CUs, with at least
-    // one block-row per slice.
-    const int64_t tiles = (T + 31) / 32;
-    const int64_t Nb = W->n_rows / W->R;
-    int64_t S = (cu_count > 0 ? cu_count : 256) / (tiles > 0 ? tiles : 1);
+int auto_slices(int64_t total_tiles, int64_t Nb, int cu_count) {
+    // Enough workgroups to give every CU one: token tiles (over every product of the launch)
+    // times slices >= CUs, with at least one block-row per slice.
+    int64_t S = (cu_count > 0 ? cu_count : 256) / (total_tiles > 0 ? total_tiles : 1);
     if (S < 1) S = 1;
     if (S > Nb) S = Nb;
     return int(S);
@@ -105,21 +104,109 @@ bsr_status bsr_prune_from_dense(const float *W, int64_t N, int64_t K, int64_t ld
 bsr_status bsr_spmm_ex(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
                        const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
                        const bsr_spmm_options_t *opts, void *stream) {
-    bsr_status s = bsr::check_spmm(X, int(x_dtype), T, ldx, W, Y, ldy);
-    if (s != BSR_OK) return s;
+    bsr_spmm_item_t item{X, x_dtype, T, ldx, W, bias, Y, ldy};
+    return bsr_spmm_batched(&item, 1, opts, stream);
+}
+
+bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
+                            const bsr_spmm_options_t *opts, void *stream) {
+    if (n_items < 0) return BSR_ERR_ARG;
+    if (n_items > 0 && !items) return BSR_ERR_NULL;
+    for (int32_t i = 0; i < n_items; ++i) {
+        const bsr_spmm_item_t &it = items[i];
+        bsr_status s = bsr::check_spmm(it.X, int(it.x_dtype), it.T, it.ldx, it.W, it.Y, it.ldy);
+        if (s != BSR_OK) return s;
+    }
     const int kernel = opts ? opts->kernel : BSR_KERNEL_AUTO;
     const int slices = opts ? opts->slices : 0;
-    if (kernel < BSR_KERNEL_AUTO || kernel > BSR_KERNEL_TILED || slices < 0) return BSR_ERR_ARG;
-    if (T == 0) return BSR_OK;
-    if ((s = bsr::ensure_device()) != BSR_OK) return s;
-    if (kernel != BSR_KERNEL_GENERIC && bsr::tiled_supported(W->R, W->C, W->dtype)) {
-        const int S = slices > 0 ? slices : bsr::auto_slices(T, W, bsr::device_cu_count());
-        bsr::TiledPlan plan =
-            bsr::plan_tiled(X, T, ldx, W, S, bsr::device_lds_per_block());
-        if (plan.ok) return bsr::launch_spmm_tiled(plan, X, T, ldx, W, bias, Y, ldy, stream);
+    bsr::LaunchEvents ev;
+    if (opts) {
+        ev.start = opts->start_event;
+        ev.stop = opts->stop_event;
     }
-    if (kernel == BSR_KERNEL_TILED) return BSR_ERR_UNSUPPORTED;
-    return bsr::launch_spmm_generic(X, T, ldx, W, bias, Y, ldy, stream);
+    if (kernel < BSR_KERNEL_AUTO || kernel > BSR_KERNEL_TILED || slices < 0) return BSR_ERR_ARG;
+    if ((ev.start == nullptr) != (ev.stop == nullptr)) return BSR_ERR_ARG;
+
+    // Plan: every non-empty product goes to the tiled kernel when it supports the shape (and
+    // the kernel is not forced to generic), else to the generic kernel.
+    std::vector<int> work;
+    for (int32_t i = 0; i < n_items; ++i)
+        if (items[i].T > 0) work.push_back(i);
+    if (work.empty()) return BSR_OK;
+    bsr_status s = bsr::ensure_device();
+    if (s != BSR_OK) return s;
+    const int cus = bsr::device_cu_count();
+    const size_t lds_limit = bsr::device_lds_per_block();
+    std::vector<bsr::TiledWork> tiled(work.size());
+    std::vector<char> is_tiled(work.size(), 0);
+    int64_t total_tiles = 0;
+    for (size_t w = 0; w < work.size(); ++w) {
+        const bsr_spmm_item_t &it = items[work[w]];
+        if (kernel != BSR_KERNEL_GENERIC && bsr::tiled_supported(it.W->R, it.W->C, it.W->dtype)) {
+            // A trial plan with one slice decides whether the shape fits.
+            if (bsr::plan_tiled(it.X, it.T, it.ldx, it.W, 1, lds_limit).ok) {
+                is_tiled[w] = 1;
+                total_tiles += (it.T + 31) / 32;
+            }
+        }
+        if (!is_tiled[w] && kernel == BSR_KERNEL_TILED) return BSR_ERR_UNSUPPORTED;
+    }
+    for (size_t w = 0; w < work.size(); ++w) {
+        if (!is_tiled[w]) continue;
+        const bsr_spmm_item_t &it = items[work[w]];
+        const int S = slices > 0
+                          ? slices
+                          : bsr::auto_slices(total_tiles, it.W->n_rows / it.W->R, cus);
+        tiled[w] = bsr::TiledWork{bsr::plan_tiled(it.X, it.T, it.ldx, it.W, S, lds_limit), it.X,
+                                  it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
+    }
+
+    // Launch order: tiled products grouped by block shape, up to kMaxItems per launch, then
+    // generic products one by one.  With an event pair, the start event goes with the first
+    // launch and the stop event with the last.
+    struct Launch {
+        bool tiled;
+        std::vector<int> members;  // indices into `work`
+    };
+    std::vector<Launch> launches;
+    std::vector<char> done(work.size(), 0);
+    for (size_t w = 0; w < work.size(); ++w) {
+        if (!is_tiled[w] || done[w]) continue;
+        Launch l{true, {}};
+        for (size_t v = w; v < work.size(); ++v) {
+            if (!is_tiled[v] || done[v]) continue;
+            if (items[work[v]].W->R != items[work[w]].W->R ||
+                items[work[v]].W->C != items[work[w]].W->C)
+                continue;
+            l.members.push_back(int(v));
+            done[v] = 1;
+            if (int(l.members.size()) == bsr::kMaxItems) {
+                launches.push_back(l);
+                l.members.clear();
+            }
+        }
+        if (!l.members.empty()) launches.push_back(l);
+    }
+    for (size_t w = 0; w < work.size(); ++w)
+        if (!is_tiled[w]) launches.push_back(Launch{false, {int(w)}});
+
+    for (size_t li = 0; li < launches.size(); ++li) {
+        bsr::LaunchEvents lev;
+        if (li == 0) lev.start = ev.start;
+        if (li + 1 == launches.size()) lev.stop = ev.stop;
+        const Launch &l = launches[li];
+        if (l.tiled) {
+            bsr::TiledWork batch[bsr::kMaxItems];
+            for (size_t m = 0; m < l.members.size(); ++m) batch[m] = tiled[l.members[m]];
+            s = bsr::launch_spmm_tiled(batch, int(l.members.size()), stream, lev);
+        } else {
+            const bsr_spmm_item_t &it = items[work[l.members[0]]];
+            s = bsr::launch_spmm_generic(it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy, stream,
+                                         lev);
+        }
+        if (s != BSR_OK) return s;
+    }
+    return BSR_OK;
 }
 
 bsr_status bsr_spmm(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,

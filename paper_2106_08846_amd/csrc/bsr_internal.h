@@ -31,7 +31,7 @@ bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
 // Device-side entry points (implemented in the .hip files).  Arguments are already validated.
 bsr_status ensure_device();  // current device is gfx950; caches its properties
 int device_cu_count();
-int auto_slices(int64_t T, const bsr_matrix_t *W, int cu_count);
+int auto_slices(int64_t total_tiles, int64_t Nb, int cu_count);
 size_t device_lds_per_block();
 
 bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,
@@ -39,8 +39,15 @@ bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32
                         void *workspace, void *stream);
 bsr_status launch_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *stream);
 bsr_status launch_cast(const float *src, uint16_t *dst, int64_t n, void *stream);
+// Optional event pair recorded at a product kernel's start and end (hipExtLaunchKernel).
+struct LaunchEvents {
+    void *start = nullptr;
+    void *stop = nullptr;
+};
+
 bsr_status launch_spmm_generic(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W,
-                               const float *bias, float *Y, int64_t ldy, void *stream);
+                               const float *bias, float *Y, int64_t ldy, void *stream,
+                               const LaunchEvents &ev);
 
 void set_last_hip_error(const char *msg);
 

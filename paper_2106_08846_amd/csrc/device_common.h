@@ -1,6 +1,7 @@
 // Small device/host helpers shared by libbsr's kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "bsr_internal.h"
@@ -15,6 +16,20 @@ inline bsr_status launch_status() {
     if (e == hipSuccess) return BSR_OK;
     set_last_hip_error(hipGetErrorString(e));
     return BSR_ERR_HIP;
+}
+
+// Launch `kernel`, through hipExtLaunchKernel when an event pair is given so that the events
+// mark the kernel's own start and end on the device.
+template <typename... Params, typename... Args>
+inline void launch_kernel(void (*kernel)(Params...), dim3 grid, dim3 block, size_t lds,
+                          hipStream_t st, const LaunchEvents &ev, Args... args) {
+    if (ev.start != nullptr || ev.stop != nullptr)
+        hipExtLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(lds), st,
+                              static_cast<hipEvent_t>(ev.start),
+                              static_cast<hipEvent_t>(ev.stop), 0u, static_cast<Params>(args)...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(lds), st,
+                           static_cast<Params>(args)...);
 }
 
 __device__ __forceinline__ int64_t clamp64(int64_t v, int64_t lo, int64_t hi) {

@@ -48,18 +48,13 @@ __global__ __launch_bounds__(256) void spmm_generic_kernel(
 }  // namespace
 
 bsr_status launch_spmm_generic(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W,
-                               const float *bias, float *Y, int64_t ldy, void *stream) {
+                               const float *bias, float *Y, int64_t ldy, void *stream,
+                               const LaunchEvents &ev) {
     const int64_t N = W->n_rows, Kb = W->n_cols / W->C;
     const dim3 grid(grid_for(T * N, 256)), block(256);
-    if (W->dtype == BSR_BF16) {
-        hipLaunchKernelGGL(spmm_generic_kernel<true>, grid, block, 0, as_stream(stream), X, T,
-                           ldx, W->indptr, W->indices, W->data, W->nnzb, W->R, W->C, N, Kb,
-                           bias, Y, ldy);
-    } else {
-        hipLaunchKernelGGL(spmm_generic_kernel<false>, grid, block, 0, as_stream(stream), X, T,
-                           ldx, W->indptr, W->indices, W->data, W->nnzb, W->R, W->C, N, Kb,
-                           bias, Y, ldy);
-    }
+    auto kernel = (W->dtype == BSR_BF16) ? spmm_generic_kernel<true> : spmm_generic_kernel<false>;
+    launch_kernel(kernel, grid, block, 0, as_stream(stream), ev, X, T, ldx, W->indptr,
+                  W->indices, W->data, W->nnzb, W->R, W->C, N, Kb, bias, Y, ldy);
     return launch_status();
 }
 

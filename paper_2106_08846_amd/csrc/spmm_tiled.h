@@ -27,8 +27,41 @@ int tiled_waves(int R, int C);  // waves per workgroup
 TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int slices,
                      size_t lds_limit);
 
-bsr_status launch_spmm_tiled(const TiledPlan &plan, const void *X, int64_t T, int64_t ldx,
-                             const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
-                             void *stream);
+// Most products one tiled launch takes (all with the same block shape).
+constexpr int kMaxItems = 8;
+
+// One product of a tiled launch, as planned on the host.
+struct TiledWork {
+    TiledPlan plan;
+    const void *X;
+    int64_t T, ldx;
+    const bsr_matrix_t *W;
+    const float *bias;
+    float *Y;
+    int64_t ldy;
+};
+
+// The device-side view of one product, passed by value in the kernel arguments.
+struct TiledItem {
+    const float *X;
+    int64_t T, ldx;
+    const int32_t *indptr;
+    const int32_t *indices;
+    const float *data;
+    const float *bias;
+    float *Y;
+    int64_t ldy;
+    int K, nnzb, Nb, Kb;
+    int num_tiles, slices, XP, indptr_words, x_vec4;
+    int wg_begin;  // first workgroup id of this product (a multiple of 8)
+};
+
+struct TiledBatch {
+    int n;
+    TiledItem item[kMaxItems];
+};
+
+// Launch 1..kMaxItems planned products of one block shape as a single kernel.
+bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream, const LaunchEvents &ev);
 
 }  // namespace bsr

@@ -296,26 +296,44 @@ struct Unit<16, 16> {
 // -------------------------------------------------------------------------------- the kernel
 
 template <int R, int C, int NW>
-__global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(
-    const float *__restrict__ X, int64_t T, int64_t ldx, int K, const int32_t *__restrict__ indptr,
-    const int32_t *__restrict__ indices, const float *__restrict__ data, int nnzb, int Nb, int Kb,
-    const float *__restrict__ bias, float *__restrict__ Y, int64_t ldy, int num_tiles,
-    int slices, int XP, int indptr_words, int x_vec4) {
+__global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch batch) {
     using U = Unit<R, C>;
     extern __shared__ float smem[];
-    int *s_indptr = reinterpret_cast<int *>(smem);
-    float *Xs = smem + indptr_words;
 
     // The wave index is uniform across a wave; readfirstlane tells the compiler so, which
     // keeps all loop and row bookkeeping in scalar registers with scalar branches.
     const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
     constexpr int kThreads = NW * 64;
 
+    // This workgroup's product: the last item whose first workgroup id is <= blockIdx.x.
+    const int g = blockIdx.x;
+    int it = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxItems; ++i)
+        if (i < batch.n && g >= batch.item[i].wg_begin) it = i;
+    const TiledItem &I = batch.item[it];
+    const float *__restrict__ X = I.X;
+    const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
+    const int32_t *__restrict__ indptr = I.indptr;
+    const int32_t *__restrict__ indices = I.indices;
+    const float *__restrict__ data = I.data;
+    const float *__restrict__ bias = I.bias;
+    float *__restrict__ Y = I.Y;
+    const int K = I.K, nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
+              slices = I.slices, XP = I.XP, x_vec4 = I.x_vec4;
+    int *s_indptr = reinterpret_cast<int *>(smem);
+    float *Xs = smem + I.indptr_words;
+
     // Workgroup -> (token tile, slice).  Workgroups are dealt to the 8 XCDs round robin, so
-    // ids with equal (id mod 8) share an XCD; all slices of a tile get the same residue.
-    const int g = blockIdx.x, xcd = g & 7, local = g >> 3;
-    const int tile = (local / slices) * 8 + xcd, s = local % slices;
-    if (tile >= num_tiles) return;
+    // ids with equal (id mod 8) share an XCD (each item's first id is a multiple of 8).  The
+    // item's (tile, slice) pairs, in tile-major order, are cut into 8 contiguous ranges, one
+    // per XCD: every XCD gets work, and the slices of a tile stay on as few XCDs (L2s) as
+    // possible.
+    const int gl = g - I.wg_begin, xcd = gl & 7, rank = gl >> 3;
+    const int pairs = num_tiles * slices, per_xcd = (pairs + 7) >> 3;
+    const int q = xcd * per_xcd + rank;
+    if (rank >= per_xcd || q >= pairs) return;
+    const int tile = q / slices, s = q - tile * slices;
     const int64_t t0 = int64_t(tile) * kTT;
 
     for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
@@ -500,39 +518,41 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(
         }
     }
 
-    // Combine rows cut by wave boundaries.  The X tile is dead now; reuse its LDS.
+    // Combine rows cut by wave boundaries.  The X tile is dead now; reuse its LDS.  A head
+    // partial is kept as [register group of 4][lane][4] so it moves in 16-byte LDS accesses.
     __syncthreads();
-    float *H = Xs;
+    floatx4 *H = reinterpret_cast<floatx4 *>(Xs);
+    constexpr int kGroups = U::kRegs / 4;
     if (has_head) {
 #pragma unroll
-        for (int v = 0; v < U::kRegs; ++v) H[(wave * U::kRegs + v) * 64 + lane] = U::get(head, v);
+        for (int q = 0; q < kGroups; ++q)
+            H[(wave * kGroups + q) * 64 + lane] =
+                floatx4{U::get(head, 4 * q), U::get(head, 4 * q + 1), U::get(head, 4 * q + 2),
+                        U::get(head, 4 * q + 3)};
     }
     __syncthreads();
     if (tail_row >= 0) {
         // Every later wave whose range starts inside this row holds a head partial of it,
-        // except waves with an empty range, which wrote nothing.
+        // except waves with an empty range, which wrote nothing.  They are added in wave order.
         const int end = uniform(s_indptr[tail_row + 1]);
         for (int w2 = wave + 1; w2 < NW && wave_start(w2) < end; ++w2) {
             if (wave_start(w2 + 1) == wave_start(w2)) continue;
+            floatx4 h[kGroups];
 #pragma unroll
-            for (int v = 0; v < U::kRegs; ++v)
-                U::add(acc, v, H[(w2 * U::kRegs + v) * 64 + lane]);
+            for (int q = 0; q < kGroups; ++q) h[q] = H[(w2 * kGroups + q) * 64 + lane];
+#pragma unroll
+            for (int q = 0; q < kGroups; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) U::add(acc, 4 * q + e, h[q][e]);
         }
         U::store(acc, Y, ldy, t0, T, int64_t(tail_row) * R, bias);
     }
 }
 
 template <int R, int C, int NW>
-bsr_status launch_variant(const TiledPlan &plan, const float *X, int64_t T, int64_t ldx,
-                          const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
-                          hipStream_t st) {
-    const int K = int(W->n_cols), Nb = int(W->n_rows / R), Kb = int(W->n_cols / C);
-    const int grid = ((plan.num_tiles + 7) / 8) * 8 * plan.slices;
-    hipLaunchKernelGGL((spmm_tiled_kernel<R, C, NW>), dim3(grid), dim3(NW * 64), plan.lds_bytes,
-                       st, X, T, ldx, K, W->indptr, W->indices,
-                       static_cast<const float *>(W->data), int(W->nnzb), Nb, Kb, bias, Y, ldy,
-                       plan.num_tiles, plan.slices, plan.x_pitch, plan.indptr_words,
-                       plan.x_vec4);
+bsr_status launch_variant(const TiledBatch &batch, int grid, size_t lds, hipStream_t st,
+                          const LaunchEvents &ev) {
+    launch_kernel(spmm_tiled_kernel<R, C, NW>, dim3(grid), dim3(NW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
@@ -576,19 +596,45 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     return p;
 }
 
-bsr_status launch_spmm_tiled(const TiledPlan &plan, const void *X, int64_t T, int64_t ldx,
-                             const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
-                             void *stream) {
+bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
+                             const LaunchEvents &ev) {
+    if (n < 1 || n > kMaxItems) return BSR_ERR_ARG;
+    const int R = work[0].W->R, C = work[0].W->C;
+    TiledBatch batch{};
+    batch.n = n;
+    int grid = 0;
+    size_t lds = 0;
+    for (int i = 0; i < n; ++i) {
+        const TiledWork &w = work[i];
+        if (w.W->R != R || w.W->C != C) return BSR_ERR_ARG;
+        TiledItem &it = batch.item[i];
+        it.X = static_cast<const float *>(w.X);
+        it.T = w.T;
+        it.ldx = w.ldx;
+        it.indptr = w.W->indptr;
+        it.indices = w.W->indices;
+        it.data = static_cast<const float *>(w.W->data);
+        it.bias = w.bias;
+        it.Y = w.Y;
+        it.ldy = w.ldy;
+        it.K = int(w.W->n_cols);
+        it.nnzb = int(w.W->nnzb);
+        it.Nb = int(w.W->n_rows / R);
+        it.Kb = int(w.W->n_cols / C);
+        it.num_tiles = w.plan.num_tiles;
+        it.slices = w.plan.slices;
+        it.XP = w.plan.x_pitch;
+        it.indptr_words = w.plan.indptr_words;
+        it.x_vec4 = w.plan.x_vec4;
+        it.wg_begin = grid;
+        grid += ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
+        if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
+    }
     hipStream_t st = as_stream(stream);
-    const float *Xf = static_cast<const float *>(X);
-    if (W->R == 32 && W->C == 1)
-        return launch_variant<32, 1, 16>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
-    if (W->R == 16 && W->C == 1)
-        return launch_variant<16, 1, 16>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
-    if (W->R == 32 && W->C == 32)
-        return launch_variant<32, 32, 16>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
-    if (W->R == 16 && W->C == 16)
-        return launch_variant<16, 16, 16>(plan, Xf, T, ldx, W, bias, Y, ldy, st);
+    if (R == 32 && C == 1) return launch_variant<32, 1, 16>(batch, grid, lds, st, ev);
+    if (R == 16 && C == 1) return launch_variant<16, 1, 16>(batch, grid, lds, st, ev);
+    if (R == 32 && C == 32) return launch_variant<32, 32, 16>(batch, grid, lds, st, ev);
+    if (R == 16 && C == 16) return launch_variant<16, 16, 16>(batch, grid, lds, st, ev);
     return BSR_ERR_UNSUPPORTED;
 }
 

@@ -155,3 +155,33 @@ def test_python_binding_rejects_cpu_tensors(L):
     import torch
     with pytest.raises(TypeError):
         L.bsr_cast_f32_bf16(torch.zeros(4))
+
+
+@pytest.mark.parametrize("kernel,slices,start,stop", [
+    (3, 0, None, None), (-1, 0, None, None), (0, -1, None, None),
+    (0, 0, FAKE, None), (0, 0, None, FAKE),
+])
+def test_spmm_ex_option_errors(L, lib, kernel, slices, start, stop):
+    m = _matrix(L)
+    opts = L.bsr_spmm_options_t(kernel, slices, start, stop)
+    assert lib.bsr_spmm_ex(FAKE, 0, 4, 64, ctypes.byref(m), None, FAKE, 64, ctypes.byref(opts),
+                           None) == 3
+
+
+
+def _item(L, m, X=FAKE, x_dtype=0, T=4, ldx=64, Y=FAKE, ldy=64):
+    return L.bsr_spmm_item_t(X, x_dtype, T, ldx, ctypes.pointer(m), None, Y, ldy)
+
+
+def test_spmm_batched_errors(L, lib):
+    m = _matrix(L)
+    bad = _matrix(L, R=7)
+    items = (L.bsr_spmm_item_t * 3)(_item(L, m), _item(L, bad), _item(L, m))
+    assert lib.bsr_spmm_batched(items, 3, None, None) == 2      # second item: R does not divide N
+    assert lib.bsr_spmm_batched(items, -1, None, None) == 3
+    assert lib.bsr_spmm_batched(None, 2, None, None) == 1
+    assert lib.bsr_spmm_batched(None, 0, None, None) == 0
+    empty = (L.bsr_spmm_item_t * 2)(_item(L, m, X=None, Y=None, T=0), _item(L, m, T=0))
+    assert lib.bsr_spmm_batched(empty, 2, None, None) == 0     # nothing to launch
+    one_event = L.bsr_spmm_options_t(0, 0, FAKE, None)
+    assert lib.bsr_spmm_batched(empty, 2, ctypes.byref(one_event), None) == 3

@@ -409,7 +409,7 @@ def test_graph_replay_matches_eager(device, R, C, kernel, bf16):
         eager.append(run().clone())
         calls.append(run)
     torch.cuda.synchronize()
-    check_spmm(w.X[0], calls[0]._keep[1], w.projections[0].bias, eager[0], bf16=bf16)
+    check_spmm(w.X[0], calls[0]._keep[0][1], w.projections[0].bias, eager[0], bf16=bf16)
     g = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
@@ -445,3 +445,96 @@ def test_prepared_call_matches_bsr_spmm(device):
     assert torch.equal(Yp.view(torch.int32), Ys.view(torch.int32))
     with pytest.raises(ValueError):
         B.SpmmCall(X, M, b, torch.empty((127, 768), dtype=torch.float32, device=device))
+
+
+@pytest.mark.parametrize("kernel", [B.KERNEL_TILED, B.KERNEL_GENERIC])
+def test_timed_call_records_kernel_events(device, kernel):
+    w = G.single_768()
+    p = w.projections[0]
+    k = B.bsr_prune_count(768, 768, 32, 1, p.density)
+    M = prune_on_gpu(p.W, 32, 1, k)
+    X, b = dev(w.X[0]), dev(p.bias)
+    run = B.SpmmCall(X, M, b, torch.empty((128, 768), dtype=torch.float32, device=device),
+                     kernel=kernel)
+    ref = run().clone()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    e1.record()
+    run.Y.fill_(float("nan"))
+    run.timed(e0, e1)
+    torch.cuda.synchronize()
+    assert torch.equal(run.Y.view(torch.int32), ref.view(torch.int32))
+    ms = e0.elapsed_time(e1)
+    assert 0.0 < ms < 100.0
+
+
+
+# --------------------------------------------------------------------------- batched products
+
+
+def test_batched_equals_single_calls(device):
+    """One launch for Q, K, V, O gives each product bit for bit what a single call gives."""
+    w = G.bert_base_attention()
+    X = dev(w.X[0])
+    prods, singles = [], []
+    for p in w.projections:
+        k = B.bsr_prune_count(768, 768, 32, 1, p.density)
+        M = prune_on_gpu(p.W, 32, 1, k)
+        b = dev(p.bias)
+        prods.append((X, M, b, None))
+        singles.append(B.bsr_spmm_ex(X, M, b, slices=6))
+    Ys = B.bsr_spmm_batched(prods, slices=6)
+    torch.cuda.synchronize()
+    for (X_, M, b, _), Y, Y1, p in zip(prods, Ys, singles, w.projections):
+        assert torch.equal(Y.view(torch.int32), Y1.view(torch.int32))
+        check_spmm(w.X[0], M, p.bias, Y)
+
+
+def test_batched_auto_slices_mixed_shapes(device):
+    """A batch mixing tiled shapes, a generic shape, bf16, empty products and more than one
+    launch's worth of products; every product checked against the oracle."""
+    g = rng(7001)
+    cases = []
+    for i, (R, C, T, bf16) in enumerate([(32, 1, 200, False), (16, 16, 64, False),
+                                          (8, 8, 33, False), (32, 1, 0, False),
+                                          (32, 32, 96, False), (16, 1, 40, False),
+                                          (32, 1, 128, True)] + [(32, 1, 7 + 9 * j, False)
+                                                                 for j in range(9)]):
+        N, K = 256, 192
+        W = (g.standard_normal((N, K)) * 0.02).astype(np.float32)
+        X = g.standard_normal((T, K)).astype(np.float32)
+        b = (g.standard_normal(N) * 0.02).astype(np.float32)
+        k = B.bsr_prune_count(N, K, R, C, 0.3)
+        M = prune_on_gpu(W, R, C, k)
+        Xd = dev(X)
+        if bf16:
+            M = M.to_bf16()
+            Xd = B.bsr_cast_f32_bf16(Xd)
+        cases.append((X, M, b, bf16, (Xd, M, dev(b), None)))
+    log(f"batched mixed: {len(cases)} products")
+    Ys = B.bsr_spmm_batched([c[4] for c in cases])
+    torch.cuda.synchronize()
+    for (X, M, b, bf16, _), Y in zip(cases, Ys):
+        if X.shape[0]:
+            check_spmm(X, M, b, Y, bf16=bf16)
+        else:
+            assert Y.shape[0] == 0
+
+
+def test_batched_timed_events(device):
+    w = G.bert_base_attention()
+    X = dev(w.X[0])
+    prods = []
+    for p in w.projections:
+        M = prune_on_gpu(p.W, 32, 1, B.bsr_prune_count(768, 768, 32, 1, p.density))
+        prods.append((X, M, dev(p.bias), torch.empty((128, 768), device=device)))
+    run = B.SpmmBatchCall(prods)
+    ref = [y.clone() for y in run()]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    e1.record()
+    run.timed(e0, e1)
+    torch.cuda.synchronize()
+    for y, r in zip(run.Y, ref):
+        assert torch.equal(y.view(torch.int32), r.view(torch.int32))
+    assert 0.0 < e0.elapsed_time(e1) < 100.0
