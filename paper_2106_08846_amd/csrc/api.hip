@@ -144,7 +144,7 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         const bsr_spmm_item_t &it = items[work[w]];
         if (kernel != BSR_KERNEL_GENERIC && bsr::tiled_supported(it.W->R, it.W->C, it.W->dtype)) {
             // A trial plan with one slice decides whether the shape fits.
-            if (bsr::plan_tiled(it.X, it.T, it.ldx, it.W, 1, lds_limit).ok) {
+            if (bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok) {
                 is_tiled[w] = 1;
                 total_tiles += (it.T + 31) / 32;
             }
@@ -157,7 +157,7 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         const int S = slices > 0
                           ? slices
                           : bsr::auto_slices(total_tiles, it.W->n_rows / it.W->R, cus);
-        tiled[w] = bsr::TiledWork{bsr::plan_tiled(it.X, it.T, it.ldx, it.W, S, lds_limit), it.X,
+        tiled[w] = bsr::TiledWork{bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit), it.X,
                                   it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
     }
 

@@ -14,7 +14,7 @@ struct TiledPlan {
     int slices = 1;         // block-row slices per token tile
     int x_pitch = 0;        // LDS row pitch of the X tile, in floats
     int indptr_words = 0;   // LDS words reserved for indptr
-    int x_vec4 = 0;         // X rows can be read as float4
+    int bias_words = 0;     // LDS words reserved for the bias
     size_t lds_bytes = 0;   // dynamic LDS per workgroup
 };
 
@@ -24,8 +24,8 @@ int tiled_waves(int R, int C);  // waves per workgroup
 
 // Plan a tiled launch; plan.ok is false when the shape does not fit (LDS, alignment, sizes).
 // slices <= 0 leaves the slice count at 1; the caller picks it.
-TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int slices,
-                     size_t lds_limit);
+TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int64_t ldy,
+                     int slices, size_t lds_limit);
 
 // Most products one tiled launch takes (all with the same block shape).
 constexpr int kMaxItems = 8;
@@ -52,7 +52,7 @@ struct TiledItem {
     float *Y;
     int64_t ldy;
     int K, nnzb, Nb, Kb;
-    int num_tiles, slices, XP, indptr_words, x_vec4;
+    int num_tiles, slices, XP, indptr_words, bias_words;
     int wg_begin;  // first workgroup id of this product (a multiple of 8)
 };
 

@@ -18,8 +18,10 @@
 //     does not see.  A comes from the LDS X tile with 16-byte reads.
 //
 // Work decomposition (one workgroup = 32 tokens x one slice of block-rows):
-//   * the X tile [32 tokens][K] is staged once into LDS, row pitch K+1 (R x 1: conflict-free
-//     4-byte gathers of one column for 32 tokens) or K+4 (square blocks: 16-byte aligned rows);
+//   * the X tile [32 tokens][K] is staged once into LDS by direct global->LDS loads (no
+//     registers, no address arithmetic), row pitch K+1 (R x 1: conflict-free 4-byte gathers of
+//     one column for 32 tokens) or K+4 (square blocks: 16-byte aligned rows); the bias is
+//     staged beside it and is the initial value of every row the workgroup finishes;
 //   * slices hold whole block-rows, balanced by stored-block count;
 //   * inside a slice the stored blocks are split evenly over the waves (so skewed rows are
 //     spread over several waves); a block-row cut by a wave boundary is summed by the wave where
@@ -37,7 +39,8 @@ namespace {
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kTT = 32;  // tokens per workgroup
+constexpr int kTT = 32;           // tokens per workgroup
+constexpr int kStageChunks = 12;  // 64-column chunks of an X row in flight per wave
 
 __device__ __forceinline__ floatx16 mfma32(float a, float b, floatx16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
@@ -67,12 +70,28 @@ __device__ __forceinline__ int wave_lower_bound(const int *s_indptr, int n, int6
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-// Raw buffer resource over [base, base + bytes): loads past the end return 0.  Word 3 is the
-// default raw-buffer configuration for gfx9-family chips.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int64_t bytes) {
-    const int n = bytes > 0x7FFFFFFF ? 0x7FFFFFFF : int(bytes < 0 ? 0 : bytes);
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, n, 0x00020000);
+// Raw buffer resource over [base, base + bytes): loads past the end return 0 and stores past
+// it are dropped.  Word 3 is the default raw-buffer configuration for gfx9-family chips.  The
+// plan keeps every range below 2^31 bytes.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, unsigned bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, int(bytes), 0x00020000);
 }
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Cache policy of the Y stores: nontemporal (Y is written once and not read here).
+constexpr int kStoreNT = 2;
+
+// Destination of one 32-token tile of Y.  Full tiles store through a buffer resource with the
+// row offset in a scalar register (no per-store address arithmetic); the last, partial tile of
+// a product stores lane by lane with a bound check.
+struct TileOut {
+    __amdgpu_buffer_rsrc_t rsrc;  // over the tile's 32 rows of Y (full tiles only)
+    float *Y;                     // row t0 of Y
+    int64_t ldy;
+    int ldy4;                     // ldy * 4 bytes (full tiles)
+    int rows;                     // valid token rows in the tile, 1..32
+};
 
 // Clamp a block column read from memory into [0, Kb) (unsigned compare also catches negatives).
 __device__ __forceinline__ int clamp_col(int j, int Kb) {
@@ -106,8 +125,9 @@ struct LinearUnit {
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const float *__restrict__ data) {
         const int o = offset_in_step(), f = feature();
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, int64_t(nnzb - p) * 4);
-        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data + int64_t(p) * R, int64_t(nnzb - p) * R * 4);
+        const unsigned left = unsigned(nnzb - p);
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
+        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data + int64_t(p) * R, left * (R * 4u));
 #pragma unroll
         for (int m = 0; m < kSteps; ++m) {
             ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
@@ -135,6 +155,12 @@ struct Unit<32, 1> : LinearUnit<32> {
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
     }
+    // Every element of the tile starts at its column's bias (s_bias: the bias staged in LDS).
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        const float b = s_bias[n0 + (threadIdx.x & 31)];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[v] = b;
+    }
     // MFMAs of one unit.  Column indices are clamped to [0, Kb]; column Kb of the X tile is
     // the zero pad column that masked lanes point at.
     __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
@@ -145,17 +171,24 @@ struct Unit<32, 1> : LinearUnit<32> {
 #pragma unroll
         for (int m = 0; m < kSteps; ++m) acc = mfma32(a[m], ops.b[m], acc);
     }
-    __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
-                                 int64_t T, int64_t n0, const float *__restrict__ bias) {
-        // Y is written once and never read here: nontemporal stores keep it out of the caches.
+    // Element v of lane l is Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const float bv = bias ? bias[n0 + tl] : 0.0f;
-        const int64_t tq = t0 + 4 * kh;
-        float *yl = Y + tq * ldy + n0 + tl;
+        if (o.rows == 32) {
+            const int vo = 4 * kh * o.ldy4 + tl * 4;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int r = 8 * (v >> 2) + (v & 3);
-            if (tq + r < T) __builtin_nontemporal_store(acc[v] + bv, yl + r * ldy);
+            for (int v = 0; v < 16; ++v) {
+                const int r = 8 * (v >> 2) + (v & 3);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), o.rsrc,
+                                                      vo, n0 * 4 + r * o.ldy4, kStoreNT);
+            }
+        } else {
+            float *yl = o.Y + int64_t(4 * kh) * o.ldy + n0 + tl;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int r = 8 * (v >> 2) + (v & 3);
+                if (4 * kh + r < o.rows) __builtin_nontemporal_store(acc[v], yl + r * o.ldy);
+            }
         }
     }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
@@ -171,6 +204,11 @@ struct Unit<16, 1> : LinearUnit<16> {
     __device__ static void zero(Acc &acc) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = 0.0f;
+    }
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        const float b = s_bias[n0 + (threadIdx.x & 15)];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = b;
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
         const float *x0 = Xs + feature() * XP;
@@ -188,19 +226,27 @@ struct Unit<16, 1> : LinearUnit<16> {
             acc.h[1] = mfma16(a1[m], ops.b[m], acc.h[1]);
         }
     }
-    __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
-                                 int64_t T, int64_t n0, const float *__restrict__ bias) {
+    // Element (h, v) of lane l is Y[t0 + 16h + 4(l/16) + v][n0 + l%16].
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const float bv = bias ? bias[n0 + tl] : 0.0f;
-        const int64_t tq = t0 + 4 * kq;
-        float *yl = Y + tq * ldy + n0 + tl;
+        if (o.rows == 32) {
+            const int vo = 4 * kq * o.ldy4 + tl * 4;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int r = 16 * h + v;
-                if (tq + r < T) __builtin_nontemporal_store(acc.h[h][v] + bv, yl + r * ldy);
-            }
+                for (int v = 0; v < 4; ++v)
+                    __builtin_amdgcn_raw_buffer_store_b32(
+                        __float_as_uint(acc.h[h][v]), o.rsrc, vo,
+                        n0 * 4 + (16 * h + v) * o.ldy4, kStoreNT);
+        } else {
+            float *yl = o.Y + int64_t(4 * kq) * o.ldy + n0 + tl;
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int r = 16 * h + v;
+                    if (4 * kq + r < o.rows) __builtin_nontemporal_store(acc.h[h][v], yl + r * o.ldy);
+                }
         }
     }
     __device__ static float get(const Acc &acc, int v) { return acc.h[v >> 2][v & 3]; }
@@ -222,6 +268,9 @@ struct Unit<32, 32> {
         floatx4 d[4];
     };
     __device__ static void zero(Acc &acc) { Unit<32, 1>::zero(acc); }
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        Unit<32, 1>::init(acc, s_bias, n0);
+    }
     __device__ static void mask(Ops &, int) {}
     __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
                                 const float *__restrict__ data) {
@@ -243,9 +292,8 @@ struct Unit<32, 32> {
             for (int e = 0; e < 4; ++e) acc = mfma32(a[u][e], ops.d[u][e], acc);
         }
     }
-    __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
-                                 int64_t T, int64_t n0, const float *__restrict__ bias) {
-        Unit<32, 1>::store(acc, Y, ldy, t0, T, n0, bias);
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
+        Unit<32, 1>::store(acc, o, n0);
     }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
@@ -266,6 +314,9 @@ struct Unit<16, 16> {
         floatx4 d;
     };
     __device__ static void zero(Acc &acc) { Unit<16, 1>::zero(acc); }
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        Unit<16, 1>::init(acc, s_bias, n0);
+    }
     __device__ static void mask(Ops &, int) {}
     __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
                                 const float *__restrict__ data) {
@@ -285,9 +336,8 @@ struct Unit<16, 16> {
             acc.h[1] = mfma16(a1[e], ops.d[e], acc.h[1]);
         }
     }
-    __device__ static void store(const Acc &acc, float *__restrict__ Y, int64_t ldy, int64_t t0,
-                                 int64_t T, int64_t n0, const float *__restrict__ bias) {
-        Unit<16, 1>::store(acc, Y, ldy, t0, T, n0, bias);
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
+        Unit<16, 1>::store(acc, o, n0);
     }
     __device__ static float get(const Acc &acc, int v) { return Unit<16, 1>::get(acc, v); }
     __device__ static void add(Acc &acc, int v, float x) { Unit<16, 1>::add(acc, v, x); }
@@ -320,9 +370,11 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     const float *__restrict__ bias = I.bias;
     float *__restrict__ Y = I.Y;
     const int K = I.K, nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
-              slices = I.slices, XP = I.XP, x_vec4 = I.x_vec4;
+              slices = I.slices, XP = I.XP;
+    // LDS: indptr, bias (N floats), then the X tile (reused for partial tiles at the end).
     int *s_indptr = reinterpret_cast<int *>(smem);
-    float *Xs = smem + I.indptr_words;
+    float *s_bias = smem + I.indptr_words;
+    float *Xs = s_bias + I.bias_words;
 
     // Workgroup -> (token tile, slice).  Workgroups are dealt to the 8 XCDs round robin, so
     // ids with equal (id mod 8) share an XCD (each item's first id is a multiple of 8).  The
@@ -336,58 +388,48 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     const int tile = q / slices, s = q - tile * slices;
     const int64_t t0 = int64_t(tile) * kTT;
 
-    for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
-
-    // Stage X[t0 : t0 + 32][0 : K] into LDS (row pitch XP); rows past T are zero, and so is
-    // the pad column K of the R x 1 layout.  Each thread issues all its loads before its LDS
-    // stores (up to kStageVec float4 per thread), advancing (t, c4) without divisions.
-    if (x_vec4) {
-        constexpr int kStageVec = 12;
-        const int K4 = K >> 2, total = kTT * K4;
-        const int dt = kThreads / K4, dc = kThreads - dt * K4;
-        int t = threadIdx.x / K4, c4 = threadIdx.x - t * K4;
-        for (int f0 = threadIdx.x; f0 < total; f0 += kStageVec * kThreads) {
-            floatx4 v[kStageVec];
-            int off[kStageVec];
+    // Stage X[t0 : t0 + 32][0 : K] into LDS (row pitch XP).  Each wave moves whole rows: per
+    // 64 columns one coalesced dword load (lane = column; constant offsets go in the
+    // instruction) and one conflict-free dword LDS store.  A row's loads are all issued before
+    // its stores.  Rows past T are zero, and so is the pad column K of the R x 1 layout.
+    const int rows = int(T - t0 < kTT ? T - t0 : kTT);
 #pragma unroll
-            for (int u = 0; u < kStageVec; ++u) {
-                off[u] = t * XP + 4 * c4;
-                v[u] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-                if (f0 + u * kThreads < total && t0 + t < T)
-                    v[u] = __builtin_nontemporal_load(
-                        reinterpret_cast<const floatx4 *>(X + (t0 + t) * ldx + 4 * c4));
-                c4 += dc;
-                t += dt;
-                if (c4 >= K4) {
-                    c4 -= K4;
-                    ++t;
+    for (int t = wave; t < kTT; t += NW) {
+        float *dst = Xs + t * XP + lane;
+        if (t < rows) {
+            const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(X + (t0 + t) * ldx, unsigned(K) * 4u);
+            for (int c0 = 0; c0 < K; c0 += 64 * kStageChunks) {
+                float v[kStageChunks];
+#pragma unroll
+                for (int m = 0; m < kStageChunks; ++m) {
+                    if (c0 + 64 * m < K)
+                        v[m] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                             rx, (c0 + lane) * 4 + 256 * m, 0, 0));
+                }
+#pragma unroll
+                for (int m = 0; m < kStageChunks; ++m) {
+                    const int c = c0 + 64 * m;
+                    if (c + 64 <= K || (c < K && c + lane < K)) dst[c] = v[m];
                 }
             }
-#pragma unroll
-            for (int u = 0; u < kStageVec; ++u) {
-                if (f0 + u * kThreads < total) {
-                    float *dst = Xs + off[u];
-                    if constexpr (U::kPad == 4) {
-                        *reinterpret_cast<floatx4 *>(dst) = v[u];
-                    } else {
-                        dst[0] = v[u][0];
-                        dst[1] = v[u][1];
-                        dst[2] = v[u][2];
-                        dst[3] = v[u][3];
-                    }
-                }
-            }
-        }
-    } else {
-        for (int f = threadIdx.x; f < kTT * K; f += kThreads) {
-            const int t = f / K, c = f - t * K;
-            Xs[t * XP + c] = (t0 + t < T) ? X[(t0 + t) * ldx + c] : 0.0f;
+        } else {
+            for (int c = 0; c < K; c += 64)
+                if (c + lane < K) dst[c] = 0.0f;
         }
     }
     if constexpr (U::kPad == 1) {
         if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
     }
+    for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
+    for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
     __syncthreads();
+
+    TileOut out;
+    out.Y = Y + t0 * ldy;
+    out.ldy = ldy;
+    out.ldy4 = int(ldy) * 4;
+    out.rows = rows;
+    out.rsrc = buffer_rsrc(out.Y, rows == kTT ? unsigned(kTT * ldy * 4) : 0u);
 
     // This slice's block-rows and stored-block range.
     const int64_t k = uniform(s_indptr[Nb]);
@@ -418,8 +460,8 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     for (int r = rlo; r < rhi; ++r) {
         if (uniform(s_indptr[r + 1]) == uniform(s_indptr[r])) {
             typename U::Acc z;
-            U::zero(z);
-            U::store(z, Y, ldy, t0, T, int64_t(r) * R, bias);
+            U::init(z, s_bias, r * R);
+            U::store(z, out, r * R);
         }
     }
 
@@ -429,10 +471,10 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     // be partial, masked branch-free).  Operands are double-buffered in A/B: every unit's
     // MFMAs are issued after the loads of the following unit, which for a segment's last unit
     // is the first unit of the next segment.  Row bookkeeping (stores, zeroing) stays outside
-    // the inner loop so the accumulator is updated in place.
+    // the inner loop so the accumulator is updated in place.  An owned row's accumulator starts
+    // at the bias; a head (a row another wave finishes) starts at zero.
     constexpr int KB = U::KB;
     typename U::Acc acc, head;
-    U::zero(acc);
     U::zero(head);
     int tail_row = -1;
 
@@ -454,8 +496,11 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
         row = rlo - 1;
         p = Pw;
         end = head_end;
+        U::zero(acc);
     } else {
         row = next_row(rlo - 1, p, end);
+        if (row < rhi) U::init(acc, s_bias, row * R);
+        else U::zero(acc);
     }
     if (row < rhi) {
         typename U::Ops A, B;
@@ -500,17 +545,17 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
                 ++u;
             }
             // Finish the segment: head -> `head`, complete row -> Y, a row continuing past
-            // Pw1 (necessarily the last segment) -> tail, left in `acc`.
+            // Pw1 (necessarily the last segment) -> tail, left in `acc`.  The next segment is
+            // an owned row.
             if (row == rlo - 1) {
                 head = acc;
-                U::zero(acc);
             } else if (uniform(s_indptr[row + 1]) <= Pw1) {
-                U::store(acc, Y, ldy, t0, T, int64_t(row) * R, bias);
-                U::zero(acc);
+                U::store(acc, out, row * R);
             } else {
                 tail_row = row;
             }
             if (!more) break;
+            U::init(acc, s_bias, nrow * R);
             if (next_in_b) A = B;
             row = nrow;
             p = np;
@@ -545,7 +590,7 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
 #pragma unroll
                 for (int e = 0; e < 4; ++e) U::add(acc, 4 * q + e, h[q][e]);
         }
-        U::store(acc, Y, ldy, t0, T, int64_t(tail_row) * R, bias);
+        U::store(acc, out, tail_row * R);
     }
 }
 
@@ -568,8 +613,8 @@ bool tiled_supported(int R, int C, int dtype) {
 // (512 VGPRs per SIMD lane shared by the waves on that SIMD).
 int tiled_waves(int R, int C) { return 16; }
 
-TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int slices,
-                     size_t lds_limit) {
+TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int64_t ldy,
+                     int slices, size_t lds_limit) {
     TiledPlan p{};
     const int R = W->R, C = W->C;
     if (!tiled_supported(R, C, W->dtype)) return p;
@@ -579,16 +624,19 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     const int NW = tiled_waves(R, C);
     p.x_pitch = int(K + pad);
     p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3));
+    p.bias_words = int((W->n_rows + 3) & ~int64_t(3));
     const size_t tile_bytes = size_t(kTT) * size_t(p.x_pitch) * 4;
     const size_t h_bytes = size_t(NW) * regs * 64 * 4;
-    p.lds_bytes = size_t(p.indptr_words) * 4 + (tile_bytes > h_bytes ? tile_bytes : h_bytes);
+    p.lds_bytes = size_t(p.indptr_words + p.bias_words) * 4 +
+                  (tile_bytes > h_bytes ? tile_bytes : h_bytes);
     if (p.lds_bytes > lds_limit) return TiledPlan{};
-    if (W->nnzb >= (int64_t(1) << 31) / (R * C)) return TiledPlan{};
-    // Square kernels read 16-byte vectors from data; both kernels read X in float4 when the
-    // rows allow it.
+    // Buffer ranges are 32-bit: the block data, one X row and a 32-row tile of Y stay below
+    // 2^31 bytes.
+    if (W->nnzb * R * C >= (int64_t(1) << 29)) return TiledPlan{};
+    if (ldy >= (int64_t(1) << 24) || K >= (int64_t(1) << 24)) return TiledPlan{};
+    // Square kernels read 16-byte vectors from data.
     const bool data_al = (reinterpret_cast<uintptr_t>(W->data) & 15) == 0;
     if (C > 1 && !data_al) return TiledPlan{};
-    p.x_vec4 = ((reinterpret_cast<uintptr_t>(X) & 15) == 0 && K % 4 == 0 && ldx % 4 == 0) ? 1 : 0;
     p.num_tiles = int((T + kTT - 1) / kTT);
     p.slices = slices > 0 ? slices : 1;
     if (p.slices > Nb) p.slices = int(Nb);
@@ -625,7 +673,7 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
         it.slices = w.plan.slices;
         it.XP = w.plan.x_pitch;
         it.indptr_words = w.plan.indptr_words;
-        it.x_vec4 = w.plan.x_vec4;
+        it.bias_words = w.plan.bias_words;
         it.wg_begin = grid;
         grid += ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
