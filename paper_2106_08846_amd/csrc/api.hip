@@ -161,8 +161,8 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
                                   it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
     }
 
-    // Launch order: tiled products grouped by block shape, up to kMaxItems per launch, then
-    // generic products one by one.  With an event pair, the start event goes with the first
+    // Launch order: tiled products grouped by block shape and dtype, up to kMaxItems per launch,
+    // then generic products one by one.  With an event pair, the start event goes with the first
     // launch and the stop event with the last.
     struct Launch {
         bool tiled;
@@ -176,7 +176,8 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         for (size_t v = w; v < work.size(); ++v) {
             if (!is_tiled[v] || done[v]) continue;
             if (items[work[v]].W->R != items[work[w]].W->R ||
-                items[work[v]].W->C != items[work[w]].W->C)
+                items[work[v]].W->C != items[work[w]].W->C ||
+                items[work[v]].W->dtype != items[work[w]].W->dtype)
                 continue;
             l.members.push_back(int(v));
             done[v] = 1;

@@ -27,7 +27,7 @@ int tiled_waves(int R, int C);  // waves per workgroup
 TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int64_t ldy,
                      int slices, size_t lds_limit);
 
-// Most products one tiled launch takes (all with the same block shape).
+// Most products one tiled launch takes (all with the same block shape and dtype).
 constexpr int kMaxItems = 8;
 
 // One product of a tiled launch, as planned on the host.
@@ -43,11 +43,11 @@ struct TiledWork {
 
 // The device-side view of one product, passed by value in the kernel arguments.
 struct TiledItem {
-    const float *X;
+    const void *X;
     int64_t T, ldx;
     const int32_t *indptr;
     const int32_t *indices;
-    const float *data;
+    const void *data;   // fp32 or bf16 blocks
     const float *bias;
     float *Y;
     int64_t ldy;

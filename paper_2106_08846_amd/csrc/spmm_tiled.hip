@@ -38,6 +38,11 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
+typedef unsigned uintx2 __attribute__((ext_vector_type(2)));
+typedef unsigned short bf16_t;  // a bf16 value as its bit pattern
 
 constexpr int kTT = 32;           // tokens per workgroup
 constexpr int kStageChunks = 12;  // 64-column chunks of an X row in flight per wave
@@ -98,20 +103,22 @@ __device__ __forceinline__ int clamp_col(int j, int Kb) {
     return int(min(unsigned(j), unsigned(Kb - 1)));
 }
 
-template <int R, int C>
+template <int R, int C, bool BF>
 struct Unit;
 
 // R x 1 blocks.  For R = 32, lane l supplies block l/32 of a step (A: token l%32 of the X tile;
 // B: feature l%32 of the block), acc[v] holds Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].
 // For R = 16, lane l supplies block l/16 of a step for both token halves, acc.h[h][v] holds
 // Y[t0 + 16h + 4(l/16) + v][n0 + l%16].
-template <int R>
+// With bf16 data the operands are widened to fp32 as they are loaded (exact) and the same fp32
+// MFMAs run; the X tile is staged widened to fp32 as well.
+template <int R, bool BF>
 struct LinearUnit {
     static constexpr int kPer = 64 / R;     // blocks per MFMA step
     static constexpr int kSteps = 4;
-    static constexpr int kAhead = (R == 32) ? 2 : 3;   // units loaded ahead of use
     static constexpr int KB = kPer * kSteps;
     static constexpr int kPad = 1;
+    static constexpr bool kTileBF16 = false;
     struct Ops {
         int j[kSteps];
         float b[kSteps];
@@ -123,16 +130,29 @@ struct LinearUnit {
     // end of the arrays (nnzb blocks) read 0.  Lanes past the unit's row segment read the next
     // row's blocks; mask() zeroes them before the MFMAs.
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const float *__restrict__ data) {
+                                const void *__restrict__ data) {
         const int o = offset_in_step(), f = feature();
         const unsigned left = unsigned(nnzb - p);
         const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data + int64_t(p) * R, left * (R * 4u));
+        if constexpr (BF) {
+            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
+                static_cast<const bf16_t *>(data) + int64_t(p) * R, left * (R * 2u));
 #pragma unroll
-        for (int m = 0; m < kSteps; ++m) {
-            ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
-            ops.b[m] = __builtin_bit_cast(
-                float, __builtin_amdgcn_raw_buffer_load_b32(rd, (o * R + f) * 4, m * kPer * R * 4, 0));
+            for (int m = 0; m < kSteps; ++m) {
+                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
+                ops.b[m] = __uint_as_float(unsigned(__builtin_amdgcn_raw_buffer_load_b16(
+                                               rd, (o * R + f) * 2, m * kPer * R * 2, 0))
+                                           << 16);
+            }
+        } else {
+            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
+                static_cast<const float *>(data) + int64_t(p) * R, left * (R * 4u));
+#pragma unroll
+            for (int m = 0; m < kSteps; ++m) {
+                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
+                ops.b[m] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                         rd, (o * R + f) * 4, m * kPer * R * 4, 0));
+            }
         }
     }
     // Zero the operands of lanes whose block offset in the unit is >= nvalid (partial units).
@@ -147,8 +167,10 @@ struct LinearUnit {
     }
 };
 
-template <>
-struct Unit<32, 1> : LinearUnit<32> {
+template <bool BF>
+struct Unit<32, 1, BF> : LinearUnit<32, BF> {
+    using Ops = typename LinearUnit<32, BF>::Ops;
+    using LinearUnit<32, BF>::feature;
     static constexpr int kRegs = 16;
     using Acc = floatx16;
     __device__ static void zero(Acc &acc) {
@@ -163,8 +185,9 @@ struct Unit<32, 1> : LinearUnit<32> {
     }
     // MFMAs of one unit.  Column indices are clamped to [0, Kb]; column Kb of the X tile is
     // the zero pad column that masked lanes point at.
-    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
-        const float *xrow = Xs + feature() * XP;
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+        constexpr int kSteps = LinearUnit<32, BF>::kSteps;
+        const float *xrow = static_cast<const float *>(Xs) + feature() * XP;
         float a[kSteps];
 #pragma unroll
         for (int m = 0; m < kSteps; ++m) a[m] = xrow[clamp_col(ops.j[m], Kb + 1)];
@@ -195,8 +218,10 @@ struct Unit<32, 1> : LinearUnit<32> {
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
 };
 
-template <>
-struct Unit<16, 1> : LinearUnit<16> {
+template <bool BF>
+struct Unit<16, 1, BF> : LinearUnit<16, BF> {
+    using Ops = typename LinearUnit<16, BF>::Ops;
+    using LinearUnit<16, BF>::feature;
     static constexpr int kRegs = 8;
     struct Acc {
         floatx4 h[2];
@@ -210,8 +235,9 @@ struct Unit<16, 1> : LinearUnit<16> {
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = b;
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
-        const float *x0 = Xs + feature() * XP;
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+        constexpr int kSteps = LinearUnit<16, BF>::kSteps;
+        const float *x0 = static_cast<const float *>(Xs) + feature() * XP;
         const float *x1 = x0 + 16 * XP;
         float a0[kSteps], a1[kSteps];
 #pragma unroll
@@ -253,36 +279,43 @@ struct Unit<16, 1> : LinearUnit<16> {
     __device__ static void add(Acc &acc, int v, float x) { acc.h[v >> 2][v & 3] += x; }
 };
 
-// 32x32 blocks, v_mfma_f32_32x32x2_f32.  Lane l loads columns 8u + 4(l/32) .. +3 of block row
-// l%32 (u = 0..3); for step (u, e) its k-slot l/32 stands for c = 8u + 4(l/32) + e in both
+// Accumulator, bias and store plumbing shared by the square units (the output layouts of the
+// 32x32 and 16x16 MFMAs do not depend on the input type).
+template <int R>
+using LinearBase = Unit<R, 1, false>;
+
+// 32x32 fp32 blocks, v_mfma_f32_32x32x2_f32.  Lane l loads columns 8u + 4(l/32) .. +3 of block
+// row l%32 (u = 0..3); for step (u, e) its k-slot l/32 stands for c = 8u + 4(l/32) + e in both
 // operands.
 template <>
-struct Unit<32, 32> {
+struct Unit<32, 32, false> {
     static constexpr int KB = 1;
-    static constexpr int kAhead = 1;
     static constexpr int kPad = 4;
+    static constexpr bool kTileBF16 = false;
     static constexpr int kRegs = 16;
     using Acc = floatx16;
     struct Ops {
         int j;
         floatx4 d[4];
     };
-    __device__ static void zero(Acc &acc) { Unit<32, 1>::zero(acc); }
+    __device__ static void zero(Acc &acc) { LinearBase<32>::zero(acc); }
     __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        Unit<32, 1>::init(acc, s_bias, n0);
+        LinearBase<32>::init(acc, s_bias, n0);
     }
     __device__ static void mask(Ops &, int) {}
     __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
-                                const float *__restrict__ data) {
+                                const void *__restrict__ data) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
         ops.j = uniform(indices[p]);
-        const floatx4 *blk = reinterpret_cast<const floatx4 *>(data + int64_t(p) * 1024);
+        const floatx4 *blk =
+            reinterpret_cast<const floatx4 *>(static_cast<const float *>(data) + int64_t(p) * 1024);
 #pragma unroll
         for (int u = 0; u < 4; ++u) ops.d[u] = blk[tl * 8 + 2 * u + kh];
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const float *xb = Xs + tl * XP + 4 * kh + clamp_col(ops.j, Kb) * 32;
+        const float *xb =
+            static_cast<const float *>(Xs) + tl * XP + 4 * kh + clamp_col(ops.j, Kb) * 32;
         floatx4 a[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) a[u] = *reinterpret_cast<const floatx4 *>(xb + 8 * u);
@@ -293,41 +326,90 @@ struct Unit<32, 32> {
         }
     }
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        Unit<32, 1>::store(acc, o, n0);
+        LinearBase<32>::store(acc, o, n0);
     }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
 };
 
-// 16x16 blocks, v_mfma_f32_16x16x4_f32 on two 16-token halves.  Lane l loads row l%16, columns
-// 4(l/16)..+3 of the block (the whole block in one instruction); k-slot l/16 of step e stands
-// for c = 4(l/16) + e.
+// 32x32 bf16 blocks, v_mfma_f32_32x32x16_bf16, two instructions per block.  For half u of the
+// block's columns, lane l supplies k-slots 8(l/32) .. +7, standing for c = 16u + 8(l/32) + e:
+// 16 contiguous bytes of token l%32's X row (from the bf16 LDS tile) and of block row l%32.
 template <>
-struct Unit<16, 16> {
+struct Unit<32, 32, true> {
     static constexpr int KB = 1;
-    static constexpr int kAhead = 3;
+    static constexpr int kPad = 8;
+    static constexpr bool kTileBF16 = true;
+    static constexpr int kRegs = 16;
+    using Acc = floatx16;
+    struct Ops {
+        int j;
+        uintx4 d[2];
+    };
+    __device__ static void zero(Acc &acc) { LinearBase<32>::zero(acc); }
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        LinearBase<32>::init(acc, s_bias, n0);
+    }
+    __device__ static void mask(Ops &, int) {}
+    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+                                const void *__restrict__ data) {
+        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
+        ops.j = uniform(indices[p]);
+        const uintx4 *blk = reinterpret_cast<const uintx4 *>(static_cast<const bf16_t *>(data) +
+                                                             int64_t(p) * 1024);
+#pragma unroll
+        for (int u = 0; u < 2; ++u) ops.d[u] = blk[tl * 4 + 2 * u + kh];
+    }
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
+        const bf16_t *xb =
+            static_cast<const bf16_t *>(Xs) + tl * XP + 8 * kh + clamp_col(ops.j, Kb) * 32;
+        uintx4 a[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) a[u] = *reinterpret_cast<const uintx4 *>(xb + 16 * u);
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[u]),
+                                                         __builtin_bit_cast(bf16x8, ops.d[u]),
+                                                         acc, 0, 0, 0);
+    }
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
+        LinearBase<32>::store(acc, o, n0);
+    }
+    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
+    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
+};
+
+// 16x16 fp32 blocks, v_mfma_f32_16x16x4_f32 on two 16-token halves.  Lane l loads row l%16,
+// columns 4(l/16)..+3 of the block (the whole block in one instruction); k-slot l/16 of step e
+// stands for c = 4(l/16) + e.
+template <>
+struct Unit<16, 16, false> {
+    static constexpr int KB = 1;
     static constexpr int kPad = 4;
+    static constexpr bool kTileBF16 = false;
     static constexpr int kRegs = 8;
-    using Acc = Unit<16, 1>::Acc;
+    using Acc = typename LinearBase<16>::Acc;
     struct Ops {
         int j;
         floatx4 d;
     };
-    __device__ static void zero(Acc &acc) { Unit<16, 1>::zero(acc); }
+    __device__ static void zero(Acc &acc) { LinearBase<16>::zero(acc); }
     __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        Unit<16, 1>::init(acc, s_bias, n0);
+        LinearBase<16>::init(acc, s_bias, n0);
     }
     __device__ static void mask(Ops &, int) {}
     __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
-                                const float *__restrict__ data) {
+                                const void *__restrict__ data) {
         const int lane = threadIdx.x & 63;
         ops.j = uniform(indices[p]);
-        ops.d = reinterpret_cast<const floatx4 *>(data + int64_t(p) * 256)[(lane & 15) * 4 +
-                                                                           (lane >> 4)];
+        ops.d = reinterpret_cast<const floatx4 *>(static_cast<const float *>(data) +
+                                                  int64_t(p) * 256)[(lane & 15) * 4 + (lane >> 4)];
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const float *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const float *xb = Xs + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
+        const float *xb =
+            static_cast<const float *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
         const floatx4 a0 = *reinterpret_cast<const floatx4 *>(xb);
         const floatx4 a1 = *reinterpret_cast<const floatx4 *>(xb + 16 * XP);
 #pragma unroll
@@ -337,17 +419,62 @@ struct Unit<16, 16> {
         }
     }
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        Unit<16, 1>::store(acc, o, n0);
+        LinearBase<16>::store(acc, o, n0);
     }
-    __device__ static float get(const Acc &acc, int v) { return Unit<16, 1>::get(acc, v); }
-    __device__ static void add(Acc &acc, int v, float x) { Unit<16, 1>::add(acc, v, x); }
+    __device__ static float get(const Acc &acc, int v) { return LinearBase<16>::get(acc, v); }
+    __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
+};
+
+// 16x16 bf16 blocks, v_mfma_f32_16x16x16_bf16 on two 16-token halves, one instruction per
+// block and half.  Lane l supplies k-slots 4(l/16) .. +3, standing for c = 4(l/16) + e: 8
+// contiguous bytes of token l%16's X row and of block row l%16.
+template <>
+struct Unit<16, 16, true> {
+    static constexpr int KB = 1;
+    static constexpr int kPad = 8;
+    static constexpr bool kTileBF16 = true;
+    static constexpr int kRegs = 8;
+    using Acc = typename LinearBase<16>::Acc;
+    struct Ops {
+        int j;
+        uintx2 d;
+    };
+    __device__ static void zero(Acc &acc) { LinearBase<16>::zero(acc); }
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        LinearBase<16>::init(acc, s_bias, n0);
+    }
+    __device__ static void mask(Ops &, int) {}
+    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+                                const void *__restrict__ data) {
+        const int lane = threadIdx.x & 63;
+        ops.j = uniform(indices[p]);
+        ops.d = reinterpret_cast<const uintx2 *>(static_cast<const bf16_t *>(data) +
+                                                 int64_t(p) * 256)[(lane & 15) * 4 + (lane >> 4)];
+    }
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
+        const bf16_t *xb =
+            static_cast<const bf16_t *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
+        const uintx2 a0 = *reinterpret_cast<const uintx2 *>(xb);
+        const uintx2 a1 = *reinterpret_cast<const uintx2 *>(xb + 16 * XP);
+        const shortx4 b = __builtin_bit_cast(shortx4, ops.d);
+        acc.h[0] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, a0), b,
+                                                            acc.h[0], 0, 0, 0);
+        acc.h[1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, a1), b,
+                                                            acc.h[1], 0, 0, 0);
+    }
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
+        LinearBase<16>::store(acc, o, n0);
+    }
+    __device__ static float get(const Acc &acc, int v) { return LinearBase<16>::get(acc, v); }
+    __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
 };
 
 // -------------------------------------------------------------------------------- the kernel
 
-template <int R, int C, int NW>
+template <int R, int C, int NW, bool BF>
 __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch batch) {
-    using U = Unit<R, C>;
+    using U = Unit<R, C, BF>;
     extern __shared__ float smem[];
 
     // The wave index is uniform across a wave; readfirstlane tells the compiler so, which
@@ -362,16 +489,17 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     for (int i = 1; i < kMaxItems; ++i)
         if (i < batch.n && g >= batch.item[i].wg_begin) it = i;
     const TiledItem &I = batch.item[it];
-    const float *__restrict__ X = I.X;
+    const void *__restrict__ X = I.X;
     const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
     const int32_t *__restrict__ indptr = I.indptr;
     const int32_t *__restrict__ indices = I.indices;
-    const float *__restrict__ data = I.data;
+    const void *__restrict__ data = I.data;
     const float *__restrict__ bias = I.bias;
     float *__restrict__ Y = I.Y;
     const int K = I.K, nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
               slices = I.slices, XP = I.XP;
-    // LDS: indptr, bias (N floats), then the X tile (reused for partial tiles at the end).
+    // LDS: indptr, bias (N floats), then the X tile (fp32, or bf16 for the bf16 square units;
+    // reused for partial tiles at the end).
     int *s_indptr = reinterpret_cast<int *>(smem);
     float *s_bias = smem + I.indptr_words;
     float *Xs = s_bias + I.bias_words;
@@ -388,36 +516,50 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     const int tile = q / slices, s = q - tile * slices;
     const int64_t t0 = int64_t(tile) * kTT;
 
-    // Stage X[t0 : t0 + 32][0 : K] into LDS (row pitch XP).  Each wave moves whole rows: per
-    // 64 columns one coalesced dword load (lane = column; constant offsets go in the
-    // instruction) and one conflict-free dword LDS store.  A row's loads are all issued before
-    // its stores.  Rows past T are zero, and so is the pad column K of the R x 1 layout.
+    // Stage X[t0 : t0 + 32][0 : K] into LDS (row pitch XP elements).  Each wave moves whole
+    // rows: per 64 lanes one coalesced buffer load (constant offsets go in the instruction) and
+    // one conflict-free LDS store of consecutive words.  A row's loads are all issued before
+    // its stores.  fp32 X and the widened bf16 X move one column per lane; a bf16 tile moves
+    // two columns (one dword) per lane.  Rows past T are zero, and so is the pad column K of
+    // the R x 1 layout.
     const int rows = int(T - t0 < kTT ? T - t0 : kTT);
+    constexpr int kXBytes = BF ? 2 : 4;
+    constexpr int kColsPerLane = U::kTileBF16 ? 2 : 1;
+    const int lane_words = (K + kColsPerLane - 1) / kColsPerLane;   // LDS words per row
 #pragma unroll
     for (int t = wave; t < kTT; t += NW) {
-        float *dst = Xs + t * XP + lane;
+        // Row t of the tile as 32-bit words (fp32 columns, or pairs of bf16 columns).
+        unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane) + lane;
         if (t < rows) {
-            const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(X + (t0 + t) * ldx, unsigned(K) * 4u);
-            for (int c0 = 0; c0 < K; c0 += 64 * kStageChunks) {
-                float v[kStageChunks];
+            const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(
+                static_cast<const char *>(X) + (t0 + t) * ldx * kXBytes, unsigned(K) * kXBytes);
+            for (int c0 = 0; c0 < lane_words; c0 += 64 * kStageChunks) {
+                unsigned v[kStageChunks];
 #pragma unroll
                 for (int m = 0; m < kStageChunks; ++m) {
-                    if (c0 + 64 * m < K)
-                        v[m] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                             rx, (c0 + lane) * 4 + 256 * m, 0, 0));
+                    if (c0 + 64 * m < lane_words) {
+                        if constexpr (BF && !U::kTileBF16)
+                            v[m] = unsigned(__builtin_amdgcn_raw_buffer_load_b16(
+                                       rx, (c0 + lane) * 2 + 128 * m, 0, 0))
+                                   << 16;
+                        else
+                            v[m] = __builtin_amdgcn_raw_buffer_load_b32(
+                                rx, (c0 + lane) * 4 + 256 * m, 0, 0);
+                    }
                 }
 #pragma unroll
                 for (int m = 0; m < kStageChunks; ++m) {
                     const int c = c0 + 64 * m;
-                    if (c + 64 <= K || (c < K && c + lane < K)) dst[c] = v[m];
+                    if (c + 64 <= lane_words || (c < lane_words && c + lane < lane_words))
+                        dst[c] = v[m];
                 }
             }
         } else {
-            for (int c = 0; c < K; c += 64)
-                if (c + lane < K) dst[c] = 0.0f;
+            for (int c = 0; c < lane_words; c += 64)
+                if (c + lane < lane_words) dst[c] = 0u;
         }
     }
-    if constexpr (U::kPad == 1) {
+    if constexpr (U::kPad == 1) {   // the fp32 R x 1 tile's zero pad column
         if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
     }
     for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
@@ -594,17 +736,17 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     }
 }
 
-template <int R, int C, int NW>
+template <int R, int C, int NW, bool BF>
 bsr_status launch_variant(const TiledBatch &batch, int grid, size_t lds, hipStream_t st,
                           const LaunchEvents &ev) {
-    launch_kernel(spmm_tiled_kernel<R, C, NW>, dim3(grid), dim3(NW * 64), lds, st, ev, batch);
+    launch_kernel(spmm_tiled_kernel<R, C, NW, BF>, dim3(grid), dim3(NW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
 }  // namespace
 
 bool tiled_supported(int R, int C, int dtype) {
-    if (dtype != BSR_F32) return false;
+    if (dtype != BSR_F32 && dtype != BSR_BF16) return false;
     return (R == 32 && C == 1) || (R == 16 && C == 1) || (R == 32 && C == 32) ||
            (R == 16 && C == 16);
 }
@@ -619,13 +761,15 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     const int R = W->R, C = W->C;
     if (!tiled_supported(R, C, W->dtype)) return p;
     const int64_t K = W->n_cols, Nb = W->n_rows / R;
-    const int pad = (C == 1) ? 1 : 4;   // Unit<R, C>::kPad
+    const bool bf = W->dtype == BSR_BF16;
+    const bool tile_bf16 = bf && C > 1;   // Unit<R, C, BF>::kTileBF16
+    const int pad = (C == 1) ? 1 : (tile_bf16 ? 8 : 4);   // Unit<R, C, BF>::kPad
     const int regs = (R == 32) ? 16 : 8;
     const int NW = tiled_waves(R, C);
     p.x_pitch = int(K + pad);
     p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3));
     p.bias_words = int((W->n_rows + 3) & ~int64_t(3));
-    const size_t tile_bytes = size_t(kTT) * size_t(p.x_pitch) * 4;
+    const size_t tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
     const size_t h_bytes = size_t(NW) * regs * 64 * 4;
     p.lds_bytes = size_t(p.indptr_words + p.bias_words) * 4 +
                   (tile_bytes > h_bytes ? tile_bytes : h_bytes);
@@ -634,9 +778,13 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     // 2^31 bytes.
     if (W->nnzb * R * C >= (int64_t(1) << 29)) return TiledPlan{};
     if (ldy >= (int64_t(1) << 24) || K >= (int64_t(1) << 24)) return TiledPlan{};
-    // Square kernels read 16-byte vectors from data.
+    // Square kernels read 8- or 16-byte vectors from data.
     const bool data_al = (reinterpret_cast<uintptr_t>(W->data) & 15) == 0;
     if (C > 1 && !data_al) return TiledPlan{};
+    // bf16 X rows are read from their byte offset ldx * 2; keep them 4-byte aligned for the
+    // dword loads of the bf16 tile.
+    if (tile_bf16 && ((reinterpret_cast<uintptr_t>(X) & 3) != 0 || (ldx & 1) != 0))
+        return TiledPlan{};
     p.num_tiles = int((T + kTT - 1) / kTT);
     p.slices = slices > 0 ? slices : 1;
     if (p.slices > Nb) p.slices = int(Nb);
@@ -654,14 +802,14 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
     size_t lds = 0;
     for (int i = 0; i < n; ++i) {
         const TiledWork &w = work[i];
-        if (w.W->R != R || w.W->C != C) return BSR_ERR_ARG;
+        if (w.W->R != R || w.W->C != C || w.W->dtype != work[0].W->dtype) return BSR_ERR_ARG;
         TiledItem &it = batch.item[i];
-        it.X = static_cast<const float *>(w.X);
+        it.X = w.X;
         it.T = w.T;
         it.ldx = w.ldx;
         it.indptr = w.W->indptr;
         it.indices = w.W->indices;
-        it.data = static_cast<const float *>(w.W->data);
+        it.data = w.W->data;
         it.bias = w.bias;
         it.Y = w.Y;
         it.ldy = w.ldy;
@@ -679,10 +827,17 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
     }
     hipStream_t st = as_stream(stream);
-    if (R == 32 && C == 1) return launch_variant<32, 1, 16>(batch, grid, lds, st, ev);
-    if (R == 16 && C == 1) return launch_variant<16, 1, 16>(batch, grid, lds, st, ev);
-    if (R == 32 && C == 32) return launch_variant<32, 32, 16>(batch, grid, lds, st, ev);
-    if (R == 16 && C == 16) return launch_variant<16, 16, 16>(batch, grid, lds, st, ev);
+    if (work[0].W->dtype == BSR_BF16) {
+        if (R == 32 && C == 1) return launch_variant<32, 1, 16, true>(batch, grid, lds, st, ev);
+        if (R == 16 && C == 1) return launch_variant<16, 1, 16, true>(batch, grid, lds, st, ev);
+        if (R == 32 && C == 32) return launch_variant<32, 32, 16, true>(batch, grid, lds, st, ev);
+        if (R == 16 && C == 16) return launch_variant<16, 16, 16, true>(batch, grid, lds, st, ev);
+    } else {
+        if (R == 32 && C == 1) return launch_variant<32, 1, 16, false>(batch, grid, lds, st, ev);
+        if (R == 16 && C == 1) return launch_variant<16, 1, 16, false>(batch, grid, lds, st, ev);
+        if (R == 32 && C == 32) return launch_variant<32, 32, 16, false>(batch, grid, lds, st, ev);
+        if (R == 16 && C == 16) return launch_variant<16, 16, 16, false>(batch, grid, lds, st, ev);
+    }
     return BSR_ERR_UNSUPPORTED;
 }
 

@@ -355,6 +355,103 @@ def test_kernels_agree_bitwise_on_integers(device, R, C):
     assert torch.equal(Yg, Yt)
 
 
+def _bf16_bsr(W, R, C, k):
+    return prune_on_gpu(W, R, C, k).to_bf16()
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+@pytest.mark.parametrize("slices", [1, 3, 0])
+def test_tiled_bf16_slices(device, R, C, slices):
+    """bf16 X and blocks on the tiled kernels (native bf16 MFMA for square blocks, widened
+    operands for R x 1), against the oracle on the bf16-rounded inputs."""
+    g = rng(7100 + R * 10 + C + slices)
+    N, K, T = 256, 384, 100
+    W = g.standard_normal((N, K)).astype(np.float32)
+    X = g.standard_normal((T, K)).astype(np.float32)
+    b = g.standard_normal(N).astype(np.float32)
+    Xb = bf16_tensor(X)
+    for density in [0.0, 0.05, 0.3, 1.0]:
+        k = B.bsr_prune_count(N, K, R, C, density)
+        M = _bf16_bsr(W, R, C, k)
+        Y = B.bsr_spmm_ex(Xb, M, dev(b), kernel=B.KERNEL_TILED, slices=slices)
+        torch.cuda.synchronize()
+        check_spmm(X, M, b, Y, bf16=True)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+def test_tiled_bf16_skewed_rows_ragged_tokens(device, R, C):
+    g = rng(7200 + R + C)
+    N, K = 512, 512
+    Nb, Kb = N // R, K // C
+    k = max(1, (Nb * Kb) // 8)
+    W = _skewed_weight(g, N, K, R, C, k)
+    M = _bf16_bsr(W, R, C, k)
+    for T in (1, 31, 33, 77):
+        X = g.standard_normal((T, K)).astype(np.float32)
+        for slices in [1, 5]:
+            Y = B.bsr_spmm_ex(bf16_tensor(X), M, None, kernel=B.KERNEL_TILED, slices=slices)
+            torch.cuda.synchronize()
+            check_spmm(X, M, None, Y, bf16=True)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+def test_tiled_bf16_pitched(device, R, C):
+    """bf16 X with an even row pitch inside a larger buffer; Y pitched."""
+    g = rng(7300 + R + C)
+    N, K, T = 128, 256, 45
+    W = g.standard_normal((N, K)).astype(np.float32)
+    Xbig = g.standard_normal((T, K + 6)).astype(np.float32)
+    M = _bf16_bsr(W, R, C, B.bsr_prune_count(N, K, R, C, 0.25))
+    Xd = bf16_tensor(Xbig)[:, 2:K + 2]          # ldx = K + 6, 4-byte aligned start
+    Ybig = torch.zeros((T, N + 5), device="cuda:0")
+    Y = Ybig[:, 2:N + 2]
+    B.bsr_spmm_ex(Xd, M, None, Y=Y, kernel=B.KERNEL_TILED)
+    torch.cuda.synchronize()
+    check_spmm(np.ascontiguousarray(Xbig[:, 2:K + 2]), M, None, Y, bf16=True)
+    assert not host(Ybig)[:, :2].any() and not host(Ybig)[:, N + 2:].any()
+
+
+def test_tiled_bf16_odd_width_and_odd_pitch(device):
+    """R x 1 bf16 with odd K and odd row pitch runs tiled; a square bf16 product on an odd pitch
+    is refused by the forced tiled kernel and computed by the automatic choice."""
+    g = rng(7400)
+    N, K, T = 96, 771, 40
+    W = g.standard_normal((N, K)).astype(np.float32)
+    X = g.standard_normal((T, K)).astype(np.float32)
+    for R in (32, 16):
+        M = _bf16_bsr(W, R, 1, B.bsr_prune_count(N, K, R, 1, 0.2))
+        Y = B.bsr_spmm_ex(bf16_tensor(X), M, None, kernel=B.KERNEL_TILED)
+        torch.cuda.synchronize()
+        check_spmm(X, M, None, Y, bf16=True)
+    K2 = 256
+    W2 = g.standard_normal((64, K2)).astype(np.float32)
+    Xbig = g.standard_normal((T, K2 + 1)).astype(np.float32)
+    M2 = _bf16_bsr(W2, 16, 16, B.bsr_prune_count(64, K2, 16, 16, 0.3))
+    Xd = bf16_tensor(Xbig)[:, :K2]              # ldx = K2 + 1 (odd)
+    with pytest.raises(B.BSRError) as e:
+        B.bsr_spmm_ex(Xd, M2, None, kernel=B.KERNEL_TILED)
+    assert e.value.status == 9
+    Y = B.bsr_spmm_ex(Xd, M2, None)
+    torch.cuda.synchronize()
+    check_spmm(np.ascontiguousarray(Xbig[:, :K2]), M2, None, Y, bf16=True)
+
+
+@pytest.mark.parametrize("R,C", TILED_SHAPES)
+def test_kernels_agree_bitwise_on_integers_bf16(device, R, C):
+    g = rng(7500 + R + C)
+    W = g.integers(-8, 9, size=(256, 256)).astype(np.float32)
+    X = g.integers(-8, 9, size=(67, 256)).astype(np.float32)
+    b = g.integers(-8, 9, size=256).astype(np.float32)
+    M = _bf16_bsr(W, R, C, B.bsr_prune_count(256, 256, R, C, 0.35))
+    Xb = bf16_tensor(X)
+    Yg = B.bsr_spmm_ex(Xb, M, dev(b), kernel=B.KERNEL_GENERIC)
+    Yt = B.bsr_spmm_ex(Xb, M, dev(b), kernel=B.KERNEL_TILED, slices=3)
+    torch.cuda.synchronize()
+    assert torch.equal(Yg, Yt)
+    Y64 = X.astype(np.float64) @ O.to_dense(*oracle_bsr(M), 256, 256).T.astype(np.float64) + b
+    assert np.array_equal(host(Yt).astype(np.float64), Y64)
+
+
 @pytest.mark.parametrize("R,C", TILED_SHAPES)
 def test_generic_kernel_on_tiled_shapes(device, R, C):
     w = G.block_sweep(R, C)
