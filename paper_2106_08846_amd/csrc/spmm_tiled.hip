@@ -87,15 +87,12 @@ typedef __attribute__((address_space(3))) void lds_void;
 // Cache policy of the Y stores: nontemporal (Y is written once and not read here).
 constexpr int kStoreNT = 2;
 
-// Destination of one 32-token tile of Y.  Full tiles store through a buffer resource with the
-// row offset in a scalar register (no per-store address arithmetic); the last, partial tile of
-// a product stores lane by lane with a bound check.
+// Destination of one 32-token tile of Y: a buffer resource over the tile's valid rows (rows
+// past the last token of the product fall outside it, and the hardware drops those stores).
+// The row offset goes in the range-checked vector offset, the column in the scalar offset.
 struct TileOut {
-    __amdgpu_buffer_rsrc_t rsrc;  // over the tile's 32 rows of Y (full tiles only)
-    float *Y;                     // row t0 of Y
-    int64_t ldy;
-    int ldy4;                     // ldy * 4 bytes (full tiles)
-    int rows;                     // valid token rows in the tile, 1..32
+    __amdgpu_buffer_rsrc_t rsrc;  // Y + t0 * ldy, over rows * ldy * 4 bytes
+    int ldy4;                     // ldy * 4 bytes
 };
 
 // Clamp a block column read from memory into [0, Kb) (unsigned compare also catches negatives).
@@ -197,21 +194,12 @@ struct Unit<32, 1, BF> : LinearUnit<32, BF> {
     // Element v of lane l is Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        if (o.rows == 32) {
-            const int vo = 4 * kh * o.ldy4 + tl * 4;
+        const int vo = 4 * kh * o.ldy4 + tl * 4;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int r = 8 * (v >> 2) + (v & 3);
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), o.rsrc,
-                                                      vo, n0 * 4 + r * o.ldy4, kStoreNT);
-            }
-        } else {
-            float *yl = o.Y + int64_t(4 * kh) * o.ldy + n0 + tl;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int r = 8 * (v >> 2) + (v & 3);
-                if (4 * kh + r < o.rows) __builtin_nontemporal_store(acc[v], yl + r * o.ldy);
-            }
+        for (int v = 0; v < 16; ++v) {
+            const int r = 8 * (v >> 2) + (v & 3);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), o.rsrc,
+                                                  vo + r * o.ldy4, n0 * 4, kStoreNT);
         }
     }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
@@ -255,25 +243,14 @@ struct Unit<16, 1, BF> : LinearUnit<16, BF> {
     // Element (h, v) of lane l is Y[t0 + 16h + 4(l/16) + v][n0 + l%16].
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        if (o.rows == 32) {
-            const int vo = 4 * kq * o.ldy4 + tl * 4;
+        const int vo = 4 * kq * o.ldy4 + tl * 4;
 #pragma unroll
-            for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    __builtin_amdgcn_raw_buffer_store_b32(
-                        __float_as_uint(acc.h[h][v]), o.rsrc, vo,
-                        n0 * 4 + (16 * h + v) * o.ldy4, kStoreNT);
-        } else {
-            float *yl = o.Y + int64_t(4 * kq) * o.ldy + n0 + tl;
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int r = 16 * h + v;
-                    if (4 * kq + r < o.rows) __builtin_nontemporal_store(acc.h[h][v], yl + r * o.ldy);
-                }
-        }
+            for (int v = 0; v < 4; ++v)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc.h[h][v]), o.rsrc,
+                                                      vo + (16 * h + v) * o.ldy4, n0 * 4,
+                                                      kStoreNT);
     }
     __device__ static float get(const Acc &acc, int v) { return acc.h[v >> 2][v & 3]; }
     __device__ static void add(Acc &acc, int v, float x) { acc.h[v >> 2][v & 3] += x; }
@@ -525,53 +502,63 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     const int rows = int(T - t0 < kTT ? T - t0 : kTT);
     constexpr int kXBytes = BF ? 2 : 4;
     constexpr int kColsPerLane = U::kTileBF16 ? 2 : 1;
+    constexpr int kRowsPerWave = kTT / NW;
+    static_assert(kTT % NW == 0, "every wave stages the same number of rows");
     const int lane_words = (K + kColsPerLane - 1) / kColsPerLane;   // LDS words per row
+    unsigned v[kRowsPerWave][kStageChunks];
+    // Loads of chunk group c0 for every row this wave stages.  They need no guard: each row's
+    // buffer range ends at column K, so lanes past it read 0 (and are not written to LDS).
+    auto load_group = [&](int c0) {
 #pragma unroll
-    for (int t = wave; t < kTT; t += NW) {
-        // Row t of the tile as 32-bit words (fp32 columns, or pairs of bf16 columns).
-        unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane) + lane;
-        if (t < rows) {
-            const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(
-                static_cast<const char *>(X) + (t0 + t) * ldx * kXBytes, unsigned(K) * kXBytes);
-            for (int c0 = 0; c0 < lane_words; c0 += 64 * kStageChunks) {
-                unsigned v[kStageChunks];
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            const int tr = t < rows ? t : rows - 1;   // rows past T: any valid row, not stored
+            const __amdgpu_buffer_rsrc_t rx =
+                buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
+                            unsigned(K) * kXBytes);
 #pragma unroll
-                for (int m = 0; m < kStageChunks; ++m) {
-                    if (c0 + 64 * m < lane_words) {
-                        if constexpr (BF && !U::kTileBF16)
-                            v[m] = unsigned(__builtin_amdgcn_raw_buffer_load_b16(
-                                       rx, (c0 + lane) * 2 + 128 * m, 0, 0))
-                                   << 16;
-                        else
-                            v[m] = __builtin_amdgcn_raw_buffer_load_b32(
-                                rx, (c0 + lane) * 4 + 256 * m, 0, 0);
-                    }
-                }
-#pragma unroll
-                for (int m = 0; m < kStageChunks; ++m) {
-                    const int c = c0 + 64 * m;
-                    if (c + 64 <= lane_words || (c < lane_words && c + lane < lane_words))
-                        dst[c] = v[m];
-                }
+            for (int m = 0; m < kStageChunks; ++m) {
+                if constexpr (BF && !U::kTileBF16)
+                    v[r][m] = unsigned(__builtin_amdgcn_raw_buffer_load_b16(
+                                  rx, (c0 + lane) * 2 + 128 * m, 0, 0))
+                              << 16;
+                else
+                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b32(
+                        rx, (c0 + lane) * 4 + 256 * m, 0, 0);
             }
-        } else {
-            for (int c = 0; c < lane_words; c += 64)
-                if (c + lane < lane_words) dst[c] = 0u;
         }
+    };
+    auto store_group = [&](int c0) {
+#pragma unroll
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            // Row t of the tile as 32-bit words (fp32 columns, or pairs of bf16 columns).
+            unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane) + lane;
+#pragma unroll
+            for (int m = 0; m < kStageChunks; ++m) {
+                const int c = c0 + 64 * m;
+                if (c + 64 <= lane_words || (c < lane_words && c + lane < lane_words))
+                    dst[c] = t < rows ? v[r][m] : 0u;
+            }
+        }
+    };
+    load_group(0);
+    // indptr and bias (small) while the tile's first loads are in flight.
+    for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
+    for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
+    store_group(0);
+    for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
+        load_group(c0);
+        store_group(c0);
     }
     if constexpr (U::kPad == 1) {   // the fp32 R x 1 tile's zero pad column
         if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
     }
-    for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
-    for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
     __syncthreads();
 
     TileOut out;
-    out.Y = Y + t0 * ldy;
-    out.ldy = ldy;
     out.ldy4 = int(ldy) * 4;
-    out.rows = rows;
-    out.rsrc = buffer_rsrc(out.Y, rows == kTT ? unsigned(kTT * ldy * 4) : 0u);
+    out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(out.ldy4));
 
     // This slice's block-rows and stored-block range.
     const int64_t k = uniform(s_indptr[Nb]);
