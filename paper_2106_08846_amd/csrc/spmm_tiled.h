@@ -15,6 +15,7 @@ struct TiledPlan {
     int x_pitch = 0;        // LDS row pitch of the X tile, in floats
     int indptr_words = 0;   // LDS words reserved for indptr
     int bias_words = 0;     // LDS words reserved for the bias
+    int wbuf_offset = 0;    // bytes from the X tile to the per-wave block scratch (if any)
     size_t lds_bytes = 0;   // dynamic LDS per workgroup
 };
 
@@ -52,7 +53,7 @@ struct TiledItem {
     float *Y;
     int64_t ldy;
     int K, nnzb, Nb, Kb;
-    int num_tiles, slices, XP, indptr_words, bias_words;
+    int num_tiles, slices, XP, indptr_words, bias_words, wbuf_offset;
     int wg_begin;  // first workgroup id of this product (a multiple of 8)
 };
 

@@ -43,6 +43,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
 typedef unsigned uintx2 __attribute__((ext_vector_type(2)));
 typedef unsigned short bf16_t;  // a bf16 value as its bit pattern
+typedef short shortx8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
 
 constexpr int kTT = 32;           // tokens per workgroup
 constexpr int kStageChunks = 12;  // 64-column chunks of an X row in flight per wave
@@ -116,6 +118,7 @@ struct LinearUnit {
     static constexpr int KB = kPer * kSteps;
     static constexpr int kPad = 1;
     static constexpr bool kTileBF16 = false;
+    static constexpr bool kTransposed = false;
     struct Ops {
         int j[kSteps];
         float b[kSteps];
@@ -182,7 +185,8 @@ struct Unit<32, 1, BF> : LinearUnit<32, BF> {
     }
     // MFMAs of one unit.  Column indices are clamped to [0, Kb]; column Kb of the X tile is
     // the zero pad column that masked lanes point at.
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                                    char *) {
         constexpr int kSteps = LinearUnit<32, BF>::kSteps;
         const float *xrow = static_cast<const float *>(Xs) + feature() * XP;
         float a[kSteps];
@@ -223,7 +227,8 @@ struct Unit<16, 1, BF> : LinearUnit<16, BF> {
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = b;
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                                    char *) {
         constexpr int kSteps = LinearUnit<16, BF>::kSteps;
         const float *x0 = static_cast<const float *>(Xs) + feature() * XP;
         const float *x1 = x0 + 16 * XP;
@@ -256,6 +261,100 @@ struct Unit<16, 1, BF> : LinearUnit<16, BF> {
     __device__ static void add(Acc &acc, int v, float x) { acc.h[v >> 2][v & 3] += x; }
 };
 
+// LDS transpose read (ds_read_b64_tr_b16): within each group of 16 lanes, lane i receives
+// element i % 4 of the 8-byte chunks addressed by lanes 4c + i / 4 of its group, c = 0..3.
+__device__ __forceinline__ shortx4 lds_read_tr16(const char *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_shortx4 *)((__attribute__((address_space(3))) char *)p));
+}
+
+// 32x1 bf16 blocks on v_mfma_f32_32x32x16_bf16: the contraction index is the block, 16 blocks
+// per instruction, two instructions per unit.  Lane l supplies k-slots 8(l/32) .. +7 for token
+// l%32 (A) and feature l%32 (B); both operands are assembled by transpose reads, four chunks
+// (c = 0..3) per read:
+//   * A from the transposed X tile (each column holds the 32 tokens contiguously, 2 bytes each,
+//     column pitch XP bf16): lane 4c + q of group g addresses tokens 16(g%2) + 4q .. +3 of
+//     column indices[16m + 8(g/2) + 4s + c] for read s of instruction m;
+//   * B from a per-wave LDS copy of the unit's blocks ([block][32 features]): the same lane
+//     addresses features 16(g%2) + 4q .. +3 of block 16m + 8(g/2) + 4s + c.
+// Blocks past the segment end read the tile's zero pad column (A) and zero weights (B).
+template <>
+struct Unit<32, 1, true> {
+    static constexpr int KB = 32;
+    static constexpr int kPad = 0;
+    static constexpr bool kTileBF16 = true;
+    static constexpr bool kTransposed = true;
+    static constexpr int kRegs = 16;
+    static constexpr int kSlotBytes = 2048;  // LDS per wave for the unit's blocks
+    using Acc = floatx16;
+    struct Ops {
+        int j[4];     // index for read (m, s) = 2m + s
+        uintx4 w[2];  // instruction m: block 16m + l/4, features 8(l%4) .. +7
+    };
+    __device__ static void zero(Acc &acc) { Unit<32, 1, false>::zero(acc); }
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        Unit<32, 1, false>::init(acc, s_bias, n0);
+    }
+    __device__ static int read_block(int r) {   // block of read r within the unit, this lane
+        const int l = threadIdx.x & 63;
+        return 16 * (r >> 1) + 8 * (l >> 5) + 4 * (r & 1) + ((l & 15) >> 2);
+    }
+    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
+                                const void *__restrict__ data) {
+        const int l = threadIdx.x & 63;
+        const unsigned left = unsigned(nnzb - p);
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
+        const __amdgpu_buffer_rsrc_t rd =
+            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 32, left * 64u);
+        const int io = (8 * (l >> 5) + ((l & 15) >> 2)) * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            ops.j[r] = __builtin_amdgcn_raw_buffer_load_b32(ri, io, (16 * (r >> 1) + 4 * (r & 1)) * 4, 0);
+#pragma unroll
+        for (int m = 0; m < 2; ++m) ops.w[m] = __builtin_amdgcn_raw_buffer_load_b128(rd, l * 16, m * 1024, 0);
+    }
+    __device__ static void mask(Ops &ops, int nvalid) {
+        const int l = threadIdx.x & 63;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ops.j[r] = read_block(r) < nvalid ? ops.j[r] : -1;
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            const bool in = 16 * m + (l >> 2) < nvalid;
+            ops.w[m] = in ? ops.w[m] : uintx4{0u, 0u, 0u, 0u};
+        }
+    }
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                               char *wslot) {
+        const int l = threadIdx.x & 63, g = l >> 4, c = (l & 15) >> 2, q = l & 3;
+        uintx4 *ws = reinterpret_cast<uintx4 *>(wslot);
+        ws[l] = ops.w[0];
+        ws[64 + l] = ops.w[1];
+        const char *xt = static_cast<const char *>(Xs);
+        const int tok = (16 * (g & 1) + 4 * q) * 2;            // byte offset within a column
+        const int boff = (8 * (g >> 1) + c) * 64 + tok;        // byte offset within the slot
+        shortx4 a[4], b[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            a[r] = lds_read_tr16(xt + clamp_col(ops.j[r], Kb + 1) * (2 * XP) + tok);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            b[r] = lds_read_tr16(wslot + (r >> 1) * 1024 + (r & 1) * 256 + boff);
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            const shortx8 av = __builtin_shufflevector(a[2 * m], a[2 * m + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+            const shortx8 bv = __builtin_shufflevector(b[2 * m], b[2 * m + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
+                                                         __builtin_bit_cast(bf16x8, bv), acc,
+                                                         0, 0, 0);
+        }
+    }
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
+        Unit<32, 1, false>::store(acc, o, n0);
+    }
+    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
+    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
+};
+
 // Accumulator, bias and store plumbing shared by the square units (the output layouts of the
 // 32x32 and 16x16 MFMAs do not depend on the input type).
 template <int R>
@@ -269,6 +368,7 @@ struct Unit<32, 32, false> {
     static constexpr int KB = 1;
     static constexpr int kPad = 4;
     static constexpr bool kTileBF16 = false;
+    static constexpr bool kTransposed = false;
     static constexpr int kRegs = 16;
     using Acc = floatx16;
     struct Ops {
@@ -289,7 +389,8 @@ struct Unit<32, 32, false> {
 #pragma unroll
         for (int u = 0; u < 4; ++u) ops.d[u] = blk[tl * 8 + 2 * u + kh];
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                                    char *) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
         const float *xb =
             static_cast<const float *>(Xs) + tl * XP + 4 * kh + clamp_col(ops.j, Kb) * 32;
@@ -317,6 +418,7 @@ struct Unit<32, 32, true> {
     static constexpr int KB = 1;
     static constexpr int kPad = 8;
     static constexpr bool kTileBF16 = true;
+    static constexpr bool kTransposed = false;
     static constexpr int kRegs = 16;
     using Acc = floatx16;
     struct Ops {
@@ -337,7 +439,8 @@ struct Unit<32, 32, true> {
 #pragma unroll
         for (int u = 0; u < 2; ++u) ops.d[u] = blk[tl * 4 + 2 * u + kh];
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                                    char *) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
         const bf16_t *xb =
             static_cast<const bf16_t *>(Xs) + tl * XP + 8 * kh + clamp_col(ops.j, Kb) * 32;
@@ -365,6 +468,7 @@ struct Unit<16, 16, false> {
     static constexpr int KB = 1;
     static constexpr int kPad = 4;
     static constexpr bool kTileBF16 = false;
+    static constexpr bool kTransposed = false;
     static constexpr int kRegs = 8;
     using Acc = typename LinearBase<16>::Acc;
     struct Ops {
@@ -383,7 +487,8 @@ struct Unit<16, 16, false> {
         ops.d = reinterpret_cast<const floatx4 *>(static_cast<const float *>(data) +
                                                   int64_t(p) * 256)[(lane & 15) * 4 + (lane >> 4)];
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                                    char *) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
         const float *xb =
             static_cast<const float *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
@@ -410,6 +515,7 @@ struct Unit<16, 16, true> {
     static constexpr int KB = 1;
     static constexpr int kPad = 8;
     static constexpr bool kTileBF16 = true;
+    static constexpr bool kTransposed = false;
     static constexpr int kRegs = 8;
     using Acc = typename LinearBase<16>::Acc;
     struct Ops {
@@ -428,7 +534,8 @@ struct Unit<16, 16, true> {
         ops.d = reinterpret_cast<const uintx2 *>(static_cast<const bf16_t *>(data) +
                                                  int64_t(p) * 256)[(lane & 15) * 4 + (lane >> 4)];
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb) {
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                                    char *) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
         const bf16_t *xb =
             static_cast<const bf16_t *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
@@ -504,58 +611,97 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     constexpr int kColsPerLane = U::kTileBF16 ? 2 : 1;
     constexpr int kRowsPerWave = kTT / NW;
     static_assert(kTT % NW == 0, "every wave stages the same number of rows");
-    const int lane_words = (K + kColsPerLane - 1) / kColsPerLane;   // LDS words per row
-    unsigned v[kRowsPerWave][kStageChunks];
-    // Loads of chunk group c0 for every row this wave stages.  They need no guard: each row's
-    // buffer range ends at column K, so lanes past it read 0 (and are not written to LDS).
-    auto load_group = [&](int c0) {
+    if constexpr (U::kTransposed) {
+        // bf16 tile stored transposed: column c holds tokens 0..31 contiguously (pitch XP
+        // bf16).  A wave moves its rows 64 columns (one bf16 per lane) per load; column K is
+        // the zero pad column.
+        bf16_t *xt = reinterpret_cast<bf16_t *>(Xs);
+        for (int c0 = 0; c0 < K; c0 += 64 * kStageChunks) {
+            unsigned short v[kRowsPerWave][kStageChunks];
 #pragma unroll
-        for (int r = 0; r < kRowsPerWave; ++r) {
-            const int t = wave + NW * r;
-            const int tr = t < rows ? t : rows - 1;   // rows past T: any valid row, not stored
-            const __amdgpu_buffer_rsrc_t rx =
-                buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
-                            unsigned(K) * kXBytes);
+            for (int r = 0; r < kRowsPerWave; ++r) {
+                const int t = wave + NW * r;
+                const int tr = t < rows ? t : rows - 1;
+                const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(
+                    static_cast<const bf16_t *>(X) + (t0 + tr) * ldx, unsigned(K) * 2u);
 #pragma unroll
-            for (int m = 0; m < kStageChunks; ++m) {
-                if constexpr (BF && !U::kTileBF16)
-                    v[r][m] = unsigned(__builtin_amdgcn_raw_buffer_load_b16(
-                                  rx, (c0 + lane) * 2 + 128 * m, 0, 0))
-                              << 16;
-                else
-                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b32(
-                        rx, (c0 + lane) * 4 + 256 * m, 0, 0);
+                for (int m = 0; m < kStageChunks; ++m)
+                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b16(rx, (c0 + lane) * 2 + 128 * m,
+                                                                   0, 0);
+            }
+            if (c0 == 0) {
+                for (int i = threadIdx.x; i <= Nb; i += kThreads)
+                    s_indptr[i] = clampi(indptr[i], 0, nnzb);
+                for (int i = threadIdx.x; i < Nb * R; i += kThreads)
+                    s_bias[i] = bias ? bias[i] : 0.0f;
+            }
+#pragma unroll
+            for (int r = 0; r < kRowsPerWave; ++r) {
+                const int t = wave + NW * r;
+#pragma unroll
+                for (int m = 0; m < kStageChunks; ++m) {
+                    const int c = c0 + 64 * m + lane;
+                    if (c < K) xt[c * XP + t] = t < rows ? v[r][m] : bf16_t(0);
+                }
             }
         }
-    };
-    auto store_group = [&](int c0) {
-#pragma unroll
-        for (int r = 0; r < kRowsPerWave; ++r) {
-            const int t = wave + NW * r;
-            // Row t of the tile as 32-bit words (fp32 columns, or pairs of bf16 columns).
-            unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane) + lane;
-#pragma unroll
-            for (int m = 0; m < kStageChunks; ++m) {
-                const int c = c0 + 64 * m;
-                if (c + 64 <= lane_words || (c < lane_words && c + lane < lane_words))
-                    dst[c] = t < rows ? v[r][m] : 0u;
+        if (threadIdx.x < kTT) xt[K * XP + threadIdx.x] = 0;
+    } else {
+        const int lane_words = (K + kColsPerLane - 1) / kColsPerLane;   // LDS words per row
+        unsigned v[kRowsPerWave][kStageChunks];
+        // Loads of chunk group c0 for every row this wave stages.  They need no guard: each row's
+        // buffer range ends at column K, so lanes past it read 0 (and are not written to LDS).
+        auto load_group = [&](int c0) {
+    #pragma unroll
+            for (int r = 0; r < kRowsPerWave; ++r) {
+                const int t = wave + NW * r;
+                const int tr = t < rows ? t : rows - 1;   // rows past T: any valid row, not stored
+                const __amdgpu_buffer_rsrc_t rx =
+                    buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
+                                unsigned(K) * kXBytes);
+    #pragma unroll
+                for (int m = 0; m < kStageChunks; ++m) {
+                    if constexpr (BF && !U::kTileBF16)
+                        v[r][m] = unsigned(__builtin_amdgcn_raw_buffer_load_b16(
+                                      rx, (c0 + lane) * 2 + 128 * m, 0, 0))
+                                  << 16;
+                    else
+                        v[r][m] = __builtin_amdgcn_raw_buffer_load_b32(
+                            rx, (c0 + lane) * 4 + 256 * m, 0, 0);
+                }
             }
+        };
+        auto store_group = [&](int c0) {
+    #pragma unroll
+            for (int r = 0; r < kRowsPerWave; ++r) {
+                const int t = wave + NW * r;
+                // Row t of the tile as 32-bit words (fp32 columns, or pairs of bf16 columns).
+                unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane) + lane;
+    #pragma unroll
+                for (int m = 0; m < kStageChunks; ++m) {
+                    const int c = c0 + 64 * m;
+                    if (c + 64 <= lane_words || (c < lane_words && c + lane < lane_words))
+                        dst[c] = t < rows ? v[r][m] : 0u;
+                }
+            }
+        };
+        load_group(0);
+        // indptr and bias (small) while the tile's first loads are in flight.
+        for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
+        for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
+        store_group(0);
+        for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
+            load_group(c0);
+            store_group(c0);
         }
-    };
-    load_group(0);
-    // indptr and bias (small) while the tile's first loads are in flight.
-    for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
-    for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
-    store_group(0);
-    for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
-        load_group(c0);
-        store_group(c0);
     }
     if constexpr (U::kPad == 1) {   // the fp32 R x 1 tile's zero pad column
         if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
     }
     __syncthreads();
 
+    // Per-wave LDS scratch of units that stage their blocks (transposed bf16 32x1).
+    char *wslot = reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048;
     TileOut out;
     out.ldy4 = int(ldy) * 4;
     out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(out.ldy4));
@@ -653,7 +799,7 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
                 U::load(B, last ? fp : q + KB, nnzb, indices, data);
                 __builtin_amdgcn_sched_barrier(0);
                 if (q + KB > end) U::mask(A, end - q);
-                U::mma(acc, A, Xs, XP, Kb);
+                U::mma(acc, A, Xs, XP, Kb, wslot);
                 __builtin_amdgcn_sched_barrier(0);
                 if (last) {
                     next_in_b = true;
@@ -665,7 +811,7 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
                 U::load(A, last2 ? fp : q2 + KB, nnzb, indices, data);
                 __builtin_amdgcn_sched_barrier(0);
                 if (q2 + KB > end) U::mask(B, end - q2);
-                U::mma(acc, B, Xs, XP, Kb);
+                U::mma(acc, B, Xs, XP, Kb, wslot);
                 __builtin_amdgcn_sched_barrier(0);
                 if (last2) {
                     next_in_b = false;
@@ -749,14 +895,25 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     if (!tiled_supported(R, C, W->dtype)) return p;
     const int64_t K = W->n_cols, Nb = W->n_rows / R;
     const bool bf = W->dtype == BSR_BF16;
-    const bool tile_bf16 = bf && C > 1;   // Unit<R, C, BF>::kTileBF16
+    const bool transposed = bf && R == 32 && C == 1;   // Unit<32, 1, true>::kTransposed
+    const bool tile_bf16 = bf && (C > 1 || transposed);   // Unit<R, C, BF>::kTileBF16
     const int pad = (C == 1) ? 1 : (tile_bf16 ? 8 : 4);   // Unit<R, C, BF>::kPad
     const int regs = (R == 32) ? 16 : 8;
     const int NW = tiled_waves(R, C);
-    p.x_pitch = int(K + pad);
     p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3));
     p.bias_words = int((W->n_rows + 3) & ~int64_t(3));
-    const size_t tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
+    size_t tile_bytes;
+    if (transposed) {
+        // K + 1 columns (the last is the zero pad) of 32 tokens, pitch 36 bf16 (72 bytes,
+        // 8-byte aligned for the transpose reads), then 2 KB of block scratch per wave.
+        p.x_pitch = 36;
+        p.wbuf_offset = int(((K + 1) * 72 + 255) & ~int64_t(255));
+        tile_bytes = size_t(p.wbuf_offset) + size_t(NW) * 2048;
+    } else {
+        p.x_pitch = int(K + pad);
+        p.wbuf_offset = 0;
+        tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
+    }
     const size_t h_bytes = size_t(NW) * regs * 64 * 4;
     p.lds_bytes = size_t(p.indptr_words + p.bias_words) * 4 +
                   (tile_bytes > h_bytes ? tile_bytes : h_bytes);
@@ -770,7 +927,7 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     if (C > 1 && !data_al) return TiledPlan{};
     // bf16 X rows are read from their byte offset ldx * 2; keep them 4-byte aligned for the
     // dword loads of the bf16 tile.
-    if (tile_bf16 && ((reinterpret_cast<uintptr_t>(X) & 3) != 0 || (ldx & 1) != 0))
+    if (bf && C > 1 && ((reinterpret_cast<uintptr_t>(X) & 3) != 0 || (ldx & 1) != 0))
         return TiledPlan{};
     p.num_tiles = int((T + kTT - 1) / kTT);
     p.slices = slices > 0 ? slices : 1;
@@ -809,6 +966,7 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
         it.XP = w.plan.x_pitch;
         it.indptr_words = w.plan.indptr_words;
         it.bias_words = w.plan.bias_words;
+        it.wbuf_offset = w.plan.wbuf_offset;
         it.wg_begin = grid;
         grid += ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
