@@ -608,103 +608,104 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     // the R x 1 layout.
     const int rows = int(T - t0 < kTT ? T - t0 : kTT);
     constexpr int kXBytes = BF ? 2 : 4;
-    constexpr int kColsPerLane = U::kTileBF16 ? 2 : 1;
+    constexpr int kColsPerLane = U::kTileBF16 && !U::kTransposed ? 2 : 1;
     constexpr int kRowsPerWave = kTT / NW;
     static_assert(kTT % NW == 0, "every wave stages the same number of rows");
-    if constexpr (U::kTransposed) {
-        // bf16 tile stored transposed: column c holds tokens 0..31 contiguously (pitch XP
-        // bf16).  A wave moves its rows 64 columns (one bf16 per lane) per load; column K is
-        // the zero pad column.
-        bf16_t *xt = reinterpret_cast<bf16_t *>(Xs);
-        for (int c0 = 0; c0 < K; c0 += 64 * kStageChunks) {
-            unsigned short v[kRowsPerWave][kStageChunks];
+
+    // The prologue overlaps three latencies: (1) indptr and bias are loaded into registers
+    // first, (2) then every X-tile load this wave issues, (3) indptr and bias go to LDS and a
+    // light barrier (waiting on LDS only) lets every wave compute its share of the slice and
+    // issue its first unit's loads while the X tile is still in flight; (4) the tile is then
+    // written to LDS and a full barrier ends the prologue.
+    constexpr int kIpPer = 2, kBiasPer = 4;   // entries per thread handled in registers
+    int ipv[kIpPer];
+    float bv[kBiasPer];
+    {
+        const __amdgpu_buffer_rsrc_t rip = buffer_rsrc(indptr, unsigned(Nb + 1) * 4u);
+        const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(bias, bias ? unsigned(Nb * R) * 4u : 0u);
 #pragma unroll
-            for (int r = 0; r < kRowsPerWave; ++r) {
-                const int t = wave + NW * r;
-                const int tr = t < rows ? t : rows - 1;
-                const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(
-                    static_cast<const bf16_t *>(X) + (t0 + tr) * ldx, unsigned(K) * 2u);
+        for (int u = 0; u < kIpPer; ++u)
+            ipv[u] = __builtin_amdgcn_raw_buffer_load_b32(rip, (threadIdx.x + u * kThreads) * 4, 0, 0);
 #pragma unroll
-                for (int m = 0; m < kStageChunks; ++m)
+        for (int u = 0; u < kBiasPer; ++u)
+            bv[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                  rb, (threadIdx.x + u * kThreads) * 4, 0, 0));
+    }
+
+    // X tile staging, split into loads (into v) and LDS stores so that other work fits in
+    // between.  Row-major layout (pitch XP elements): per 64 lanes one coalesced load of one
+    // 32-bit word (fp32, widened bf16, or a pair of bf16 columns) and one conflict-free LDS
+    // store.  Transposed layout (bf16 32x1): one bf16 per lane, stored to column c at token t.
+    const int lane_words = (K + kColsPerLane - 1) / kColsPerLane;   // LDS words per row
+    unsigned v[kRowsPerWave][kStageChunks];
+    auto x_load = [&](int c0) {
+#pragma unroll
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            const int tr = t < rows ? t : rows - 1;   // rows past T: any valid row, not stored
+            const __amdgpu_buffer_rsrc_t rx =
+                buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
+                            unsigned(K) * kXBytes);
+#pragma unroll
+            for (int m = 0; m < kStageChunks; ++m) {
+                // No guard needed: each row's buffer range ends at column K, so lanes past it
+                // read 0 (and are not stored).
+                if constexpr (BF && (U::kTransposed || !U::kTileBF16))
                     v[r][m] = __builtin_amdgcn_raw_buffer_load_b16(rx, (c0 + lane) * 2 + 128 * m,
                                                                    0, 0);
+                else
+                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b32(rx, (c0 + lane) * 4 + 256 * m,
+                                                                   0, 0);
             }
-            if (c0 == 0) {
-                for (int i = threadIdx.x; i <= Nb; i += kThreads)
-                    s_indptr[i] = clampi(indptr[i], 0, nnzb);
-                for (int i = threadIdx.x; i < Nb * R; i += kThreads)
-                    s_bias[i] = bias ? bias[i] : 0.0f;
-            }
+        }
+    };
+    auto x_store = [&](int c0) {
 #pragma unroll
-            for (int r = 0; r < kRowsPerWave; ++r) {
-                const int t = wave + NW * r;
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            if constexpr (U::kTransposed) {
+                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs);
 #pragma unroll
                 for (int m = 0; m < kStageChunks; ++m) {
                     const int c = c0 + 64 * m + lane;
-                    if (c < K) xt[c * XP + t] = t < rows ? v[r][m] : bf16_t(0);
+                    if (c < K) xt[c * XP + t] = t < rows ? bf16_t(v[r][m]) : bf16_t(0);
                 }
-            }
-        }
-        if (threadIdx.x < kTT) xt[K * XP + threadIdx.x] = 0;
-    } else {
-        const int lane_words = (K + kColsPerLane - 1) / kColsPerLane;   // LDS words per row
-        unsigned v[kRowsPerWave][kStageChunks];
-        // Loads of chunk group c0 for every row this wave stages.  They need no guard: each row's
-        // buffer range ends at column K, so lanes past it read 0 (and are not written to LDS).
-        auto load_group = [&](int c0) {
-    #pragma unroll
-            for (int r = 0; r < kRowsPerWave; ++r) {
-                const int t = wave + NW * r;
-                const int tr = t < rows ? t : rows - 1;   // rows past T: any valid row, not stored
-                const __amdgpu_buffer_rsrc_t rx =
-                    buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
-                                unsigned(K) * kXBytes);
-    #pragma unroll
-                for (int m = 0; m < kStageChunks; ++m) {
-                    if constexpr (BF && !U::kTileBF16)
-                        v[r][m] = unsigned(__builtin_amdgcn_raw_buffer_load_b16(
-                                      rx, (c0 + lane) * 2 + 128 * m, 0, 0))
-                                  << 16;
-                    else
-                        v[r][m] = __builtin_amdgcn_raw_buffer_load_b32(
-                            rx, (c0 + lane) * 4 + 256 * m, 0, 0);
-                }
-            }
-        };
-        auto store_group = [&](int c0) {
-    #pragma unroll
-            for (int r = 0; r < kRowsPerWave; ++r) {
-                const int t = wave + NW * r;
+            } else {
                 // Row t of the tile as 32-bit words (fp32 columns, or pairs of bf16 columns).
                 unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane) + lane;
-    #pragma unroll
+#pragma unroll
                 for (int m = 0; m < kStageChunks; ++m) {
                     const int c = c0 + 64 * m;
+                    unsigned w = v[r][m];
+                    if constexpr (BF && !U::kTileBF16) w <<= 16;   // bf16 -> fp32, exact
                     if (c + 64 <= lane_words || (c < lane_words && c + lane < lane_words))
-                        dst[c] = t < rows ? v[r][m] : 0u;
+                        dst[c] = t < rows ? w : 0u;
                 }
             }
-        };
-        load_group(0);
-        // indptr and bias (small) while the tile's first loads are in flight.
-        for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
-        for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
-        store_group(0);
-        for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
-            load_group(c0);
-            store_group(c0);
         }
-    }
-    if constexpr (U::kPad == 1) {   // the fp32 R x 1 tile's zero pad column
-        if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
-    }
-    __syncthreads();
+    };
+    x_load(0);
 
-    // Per-wave LDS scratch of units that stage their blocks (transposed bf16 32x1).
-    char *wslot = reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048;
-    TileOut out;
-    out.ldy4 = int(ldy) * 4;
-    out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(out.ldy4));
+    // Unconditional stores (threads past the arrays write a spare word at the end of the
+    // indptr region), so that no load above is sunk below the tile's loads.
+    int *s_spare = s_indptr + I.indptr_words - 1;
+#pragma unroll
+    for (int u = 0; u < kIpPer; ++u) {
+        const int i = threadIdx.x + u * kThreads;
+        *(i <= Nb ? s_indptr + i : s_spare) = clampi(ipv[u], 0, nnzb);
+    }
+#pragma unroll
+    for (int u = 0; u < kBiasPer; ++u) {
+        const int i = threadIdx.x + u * kThreads;
+        *(i < Nb * R ? reinterpret_cast<int *>(s_bias) + i : s_spare) = __float_as_int(bv[u]);
+    }
+    for (int i = threadIdx.x + kIpPer * kThreads; i <= Nb; i += kThreads)
+        s_indptr[i] = clampi(indptr[i], 0, nnzb);
+    for (int i = threadIdx.x + kBiasPer * kThreads; i < Nb * R; i += kThreads)
+        s_bias[i] = bias ? bias[i] : 0.0f;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 
     // This slice's block-rows and stored-block range.
     const int64_t k = uniform(s_indptr[Nb]);
@@ -729,7 +730,50 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     int head_end = (rlo < rhi) ? uniform(s_indptr[rlo]) : Pw1;
     head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
     const bool has_head = head_end > Pw;
-    const int r_first = has_head ? rlo - 1 : rlo;
+
+    // First row after r with blocks (rhi if none); returns its start and clipped end.
+    auto next_row = [&](int r, int &start, int &end) -> int {
+        for (++r; r < rhi; ++r) {
+            start = uniform(s_indptr[r]);
+            const int e = uniform(s_indptr[r + 1]);
+            if (start < e) {
+                end = e < Pw1 ? e : Pw1;
+                return r;
+            }
+        }
+        start = end = 0;
+        return rhi;
+    };
+    // The wave's first segment, and its first unit's loads (in flight during the tile stores).
+    int row, p, end;
+    if (has_head) {
+        row = rlo - 1;
+        p = Pw;
+        end = head_end;
+    } else {
+        row = next_row(rlo - 1, p, end);
+    }
+    typename U::Ops A, B;
+    if (row < rhi) U::load(A, p, nnzb, indices, data);
+
+    x_store(0);
+    for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
+        x_load(c0);
+        x_store(c0);
+    }
+    if constexpr (U::kPad == 1) {   // the fp32 R x 1 tile's zero pad column
+        if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
+    }
+    if constexpr (U::kTransposed) {   // the transposed tile's zero pad column K
+        if (threadIdx.x < kTT) reinterpret_cast<bf16_t *>(Xs)[K * XP + threadIdx.x] = 0;
+    }
+    __syncthreads();
+
+    // Per-wave LDS scratch of units that stage their blocks (transposed bf16 32x1).
+    char *wslot = reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048;
+    TileOut out;
+    out.ldy4 = int(ldy) * 4;
+    out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(out.ldy4));
 
     // Empty owned rows: Y = bias.  (The stream below visits only segments with blocks.)
     for (int r = rlo; r < rhi; ++r) {
@@ -753,33 +797,13 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     U::zero(head);
     int tail_row = -1;
 
-    // First row after r with blocks (rhi if none); returns its start and clipped end.
-    auto next_row = [&](int r, int &start, int &end) -> int {
-        for (++r; r < rhi; ++r) {
-            start = uniform(s_indptr[r]);
-            const int e = uniform(s_indptr[r + 1]);
-            if (start < e) {
-                end = e < Pw1 ? e : Pw1;
-                return r;
-            }
-        }
-        start = end = 0;
-        return rhi;
-    };
-    int row, p, end;
     if (has_head) {
-        row = rlo - 1;
-        p = Pw;
-        end = head_end;
         U::zero(acc);
     } else {
-        row = next_row(rlo - 1, p, end);
         if (row < rhi) U::init(acc, s_bias, row * R);
         else U::zero(acc);
     }
     if (row < rhi) {
-        typename U::Ops A, B;
-        U::load(A, p, nnzb, indices, data);
         while (true) {
             int np, nend;
             const int nrow = next_row(row, np, nend);
@@ -900,7 +924,7 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     const int pad = (C == 1) ? 1 : (tile_bf16 ? 8 : 4);   // Unit<R, C, BF>::kPad
     const int regs = (R == 32) ? 16 : 8;
     const int NW = tiled_waves(R, C);
-    p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3));
+    p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3)) + 4;   // + a spare word, 16-byte multiple
     p.bias_words = int((W->n_rows + 3) & ~int64_t(3));
     size_t tile_bytes;
     if (transposed) {
