@@ -54,7 +54,6 @@ struct TiledItem {
     int64_t ldy;
     int K, nnzb, Nb, Kb;
     int num_tiles, slices, XP, indptr_words, bias_words, wbuf_offset;
-    int wg_begin;  // first workgroup id of this product (a multiple of 8)
 };
 
 struct TiledBatch {

@@ -380,14 +380,20 @@ struct Unit<32, 32, false> {
         LinearBase<32>::init(acc, s_bias, n0);
     }
     __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+    // Range-checked loads based at the unit, as for the R x 1 units: a position at or past
+    // nnzb reads 0 and touches no memory.
+    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        ops.j = uniform(indices[p]);
-        const floatx4 *blk =
-            reinterpret_cast<const floatx4 *>(static_cast<const float *>(data) + int64_t(p) * 1024);
+        const unsigned left = unsigned(nnzb - p);
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
+        const __amdgpu_buffer_rsrc_t rd =
+            buffer_rsrc(static_cast<const float *>(data) + int64_t(p) * 1024, left * 4096u);
+        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
 #pragma unroll
-        for (int u = 0; u < 4; ++u) ops.d[u] = blk[tl * 8 + 2 * u + kh];
+        for (int u = 0; u < 4; ++u)
+            ops.d[u] = __builtin_bit_cast(
+                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rd, (tl * 8 + kh) * 16, 32 * u, 0));
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                     char *) {
@@ -430,14 +436,17 @@ struct Unit<32, 32, true> {
         LinearBase<32>::init(acc, s_bias, n0);
     }
     __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        ops.j = uniform(indices[p]);
-        const uintx4 *blk = reinterpret_cast<const uintx4 *>(static_cast<const bf16_t *>(data) +
-                                                             int64_t(p) * 1024);
+        const unsigned left = unsigned(nnzb - p);
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
+        const __amdgpu_buffer_rsrc_t rd =
+            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 1024, left * 2048u);
+        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
 #pragma unroll
-        for (int u = 0; u < 2; ++u) ops.d[u] = blk[tl * 4 + 2 * u + kh];
+        for (int u = 0; u < 2; ++u)
+            ops.d[u] = __builtin_amdgcn_raw_buffer_load_b128(rd, (tl * 4 + kh) * 16, 32 * u, 0);
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                     char *) {
@@ -480,12 +489,16 @@ struct Unit<16, 16, false> {
         LinearBase<16>::init(acc, s_bias, n0);
     }
     __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63;
-        ops.j = uniform(indices[p]);
-        ops.d = reinterpret_cast<const floatx4 *>(static_cast<const float *>(data) +
-                                                  int64_t(p) * 256)[(lane & 15) * 4 + (lane >> 4)];
+        const unsigned left = unsigned(nnzb - p);
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
+        const __amdgpu_buffer_rsrc_t rd =
+            buffer_rsrc(static_cast<const float *>(data) + int64_t(p) * 256, left * 1024u);
+        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
+        ops.d = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                rd, ((lane & 15) * 4 + (lane >> 4)) * 16, 0, 0));
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                     char *) {
@@ -527,12 +540,15 @@ struct Unit<16, 16, true> {
         LinearBase<16>::init(acc, s_bias, n0);
     }
     __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int, const int *__restrict__ indices,
+    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63;
-        ops.j = uniform(indices[p]);
-        ops.d = reinterpret_cast<const uintx2 *>(static_cast<const bf16_t *>(data) +
-                                                 int64_t(p) * 256)[(lane & 15) * 4 + (lane >> 4)];
+        const unsigned left = unsigned(nnzb - p);
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
+        const __amdgpu_buffer_rsrc_t rd =
+            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 256, left * 512u);
+        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
+        ops.d = __builtin_amdgcn_raw_buffer_load_b64(rd, ((lane & 15) * 4 + (lane >> 4)) * 8, 0, 0);
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                     char *) {
@@ -566,13 +582,10 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
     constexpr int kThreads = NW * 64;
 
-    // This workgroup's product: the last item whose first workgroup id is <= blockIdx.x.
+    // This workgroup's product is blockIdx.y, so its descriptor's address is known without a
+    // lookup and every field arrives in one round of scalar loads.
     const int g = blockIdx.x;
-    int it = 0;
-#pragma unroll
-    for (int i = 1; i < kMaxItems; ++i)
-        if (i < batch.n && g >= batch.item[i].wg_begin) it = i;
-    const TiledItem &I = batch.item[it];
+    const TiledItem &I = batch.item[blockIdx.y];
     const void *__restrict__ X = I.X;
     const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
     const int32_t *__restrict__ indptr = I.indptr;
@@ -588,12 +601,19 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     float *s_bias = smem + I.indptr_words;
     float *Xs = s_bias + I.bias_words;
 
-    // Workgroup -> (token tile, slice).  Workgroups are dealt to the 8 XCDs round robin, so
-    // ids with equal (id mod 8) share an XCD (each item's first id is a multiple of 8).  The
-    // item's (tile, slice) pairs, in tile-major order, are cut into 8 contiguous ranges, one
-    // per XCD: every XCD gets work, and the slices of a tile stay on as few XCDs (L2s) as
-    // possible.
-    const int gl = g - I.wg_begin, xcd = gl & 7, rank = gl >> 3;
+    // The descriptor's fields are pinned here, ahead of the early exit below; otherwise the
+    // compiler sinks their loads past it and the X-tile loads wait for a second round.
+    asm volatile("" ::"s"(X), "s"(T), "s"(ldx), "s"(ldy), "s"(indptr), "s"(indices), "s"(data),
+                 "s"(bias), "s"(Y));
+    asm volatile("" ::"s"(K), "s"(nnzb), "s"(Nb), "s"(Kb), "s"(num_tiles), "s"(slices), "s"(XP),
+                 "s"(I.indptr_words), "s"(I.bias_words), "s"(I.wbuf_offset));
+
+    // Workgroup -> (token tile, slice).  Workgroups are dealt to the 8 XCDs round robin in
+    // dispatch order (x fastest, and the grid's x extent is a multiple of 8), so ids with equal
+    // blockIdx.x mod 8 share an XCD.  The item's (tile, slice) pairs, in tile-major order, are
+    // cut into 8 contiguous ranges, one per XCD: every XCD gets work, and the slices of a tile
+    // stay on as few XCDs (L2s) as possible.
+    const int xcd = g & 7, rank = g >> 3;
     const int pairs = num_tiles * slices, per_xcd = (pairs + 7) >> 3;
     const int q = xcd * per_xcd + rank;
     if (rank >= per_xcd || q >= pairs) return;
@@ -612,20 +632,25 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     constexpr int kRowsPerWave = kTT / NW;
     static_assert(kTT % NW == 0, "every wave stages the same number of rows");
 
-    // The prologue overlaps three latencies: (1) indptr and bias are loaded into registers
-    // first, (2) then every X-tile load this wave issues, (3) indptr and bias go to LDS and a
-    // light barrier (waiting on LDS only) lets every wave compute its share of the slice and
-    // issue its first unit's loads while the X tile is still in flight; (4) the tile is then
-    // written to LDS and a full barrier ends the prologue.
-    constexpr int kIpPer = 2, kBiasPer = 4;   // entries per thread handled in registers
-    int ipv[kIpPer];
+    // The prologue overlaps the latencies of indptr, the X tile and the first unit:
+    //   (1) every wave loads indptr into registers, the bias, and then its X-tile rows;
+    //   (2) as soon as indptr arrives, the wave computes its share of the slice from registers
+    //       (ballots and lane reads; no LDS, no barrier) and issues its first unit's loads;
+    //   (3) indptr, bias and the X tile are written to LDS and one barrier ends the prologue.
+    // A product with 256 or more block-rows copies indptr to LDS first and searches it there.
+    constexpr int kIpChunks = 4;   // indptr entries per wave in registers: 64 per chunk
+    constexpr int kBiasPer = 4;    // bias entries per thread staged through registers
+    const bool reg_part = Nb < 64 * kIpChunks;
+    int ip[kIpChunks];   // indptr[64 j + lane]
     float bv[kBiasPer];
     {
         const __amdgpu_buffer_rsrc_t rip = buffer_rsrc(indptr, unsigned(Nb + 1) * 4u);
         const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(bias, bias ? unsigned(Nb * R) * 4u : 0u);
+        // Large products skip these loads: an offset past the range reads 0 without a fetch.
+        const unsigned off = reg_part ? unsigned(lane) * 4u : 0x7ffff000u;
 #pragma unroll
-        for (int u = 0; u < kIpPer; ++u)
-            ipv[u] = __builtin_amdgcn_raw_buffer_load_b32(rip, (threadIdx.x + u * kThreads) * 4, 0, 0);
+        for (int j = 0; j < kIpChunks; ++j)
+            ip[j] = __builtin_amdgcn_raw_buffer_load_b32(rip, off + 256 * j, 0, 0);
 #pragma unroll
         for (int u = 0; u < kBiasPer; ++u)
             bv[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
@@ -686,75 +711,153 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     };
     x_load(0);
 
-    // Unconditional stores (threads past the arrays write a spare word at the end of the
-    // indptr region), so that no load above is sunk below the tile's loads.
-    int *s_spare = s_indptr + I.indptr_words - 1;
+    // The wave's share of the slice.  Slices hold whole block-rows, balanced by stored-block
+    // count: slice s covers rows [row_lo, row_hi) where row_lo is the first row whose start
+    // is >= floor(s k / slices).  The slice's blocks [Q0, Q1) are split evenly over the waves
+    // (wave w: [Pw, Pw1)).  A wave owns the rows whose first block lies in its range (the last
+    // wave also owns trailing empty rows); blocks at the front of its range that belong to
+    // row rlo - 1 are a head, summed into that row by the wave that owns it.
+    int64_t k, Q0, Q1;
+    int row_lo, row_hi, Pw, Pw1, rlo, rhi, head_end, row, p, end;
+    auto wave_start = [&](int w) -> int { return int(Q0 + (Q1 - Q0) * w / NW); };
+    auto share = [&](auto lower_bound) {
+        Pw = uniform(wave_start(wave));
+        Pw1 = uniform(wave_start(wave + 1));
+        rlo = (wave == 0) ? row_lo : lower_bound(int64_t(Pw));
+        rlo = rlo < row_lo ? row_lo : (rlo > row_hi ? row_hi : rlo);
+        rhi = (wave == NW - 1) ? row_hi : lower_bound(int64_t(Pw1));
+        rhi = rhi < rlo ? rlo : (rhi > row_hi ? row_hi : rhi);
+    };
+    if (reg_part) {
 #pragma unroll
-    for (int u = 0; u < kIpPer; ++u) {
-        const int i = threadIdx.x + u * kThreads;
-        *(i <= Nb ? s_indptr + i : s_spare) = clampi(ipv[u], 0, nnzb);
+        for (int j = 0; j < kIpChunks; ++j) ip[j] = clampi(ip[j], 0, nnzb);
+        // Entry i (uniform, <= Nb) of a register-resident array: one lane read per chunk and a
+        // scalar select (a dynamic register index would send the array to scratch memory).
+        auto lane_read = [&](const int(&a)[kIpChunks], int i) -> int {
+            const int l = i & 63, c = i >> 6;
+            int v = __builtin_amdgcn_readlane(a[0], l);
+#pragma unroll
+            for (int j = 1; j < kIpChunks; ++j) {
+                const int x = __builtin_amdgcn_readlane(a[j], l);
+                v = c == j ? x : v;
+            }
+            return v;
+        };
+        // Number of rows i < Nb meeting a per-entry predicate; for a monotone predicate on
+        // the non-decreasing indptr this is a lower bound.
+        auto count_rows = [&](auto pred) -> int {
+            int c = 0;
+#pragma unroll
+            for (int j = 0; j < kIpChunks; ++j)
+                c += __popcll(__ballot(64 * j + lane < Nb && pred(ip[j])));
+            return uniform(c);
+        };
+        k = lane_read(ip, Nb);
+        // indptr[i] < floor(s k / slices)  <=>  (indptr[i] + 1) slices <= s k.
+        auto slice_start = [&](int s2) -> int {
+            const uint64_t sk = uint64_t(s2) * uint64_t(k);
+            return count_rows([&](int x) { return uint64_t(x + 1) * uint64_t(slices) <= sk; });
+        };
+        row_lo = (s == 0) ? 0 : slice_start(s);
+        row_hi = (s == slices - 1) ? Nb : slice_start(s + 1);
+        Q0 = lane_read(ip, row_lo);
+        Q1 = lane_read(ip, row_hi);
+        if (Q1 < Q0) Q1 = Q0;
+        share([&](int64_t v) { return count_rows([&](int x) { return x < v; }); });
+        head_end = (rlo < rhi) ? lane_read(ip, rlo) : Pw1;
+        head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
+        if (head_end > Pw) {
+            row = rlo - 1;
+            p = Pw;
+            end = head_end;
+        } else {
+            // First owned row with blocks.  Rows rlo, rlo + 1, ... that start where rlo starts
+            // are empty except the last of them, which is the last row i with indptr[i] <= v
+            // (a prefix of the non-decreasing indptr); it has blocks if its end exceeds v.
+            row = rhi;
+            p = end = 0;
+            if (rlo < rhi) {
+                const int v = lane_read(ip, rlo);
+                const int c = count_rows([&](int x) { return x <= v; });
+                const int e = lane_read(ip, c);
+                if (c - 1 >= rlo && c - 1 < rhi && e > v) {
+                    row = c - 1;
+                    p = v;
+                    end = e < Pw1 ? e : Pw1;
+                }
+            }
+        }
+    } else {
+        for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        k = uniform(s_indptr[Nb]);
+        row_lo = (s == 0) ? 0 : uniform(wave_lower_bound(s_indptr, Nb, int64_t(s) * k / slices));
+        row_hi = (s == slices - 1)
+                     ? Nb
+                     : uniform(wave_lower_bound(s_indptr, Nb, int64_t(s + 1) * k / slices));
+        Q0 = uniform(s_indptr[row_lo]);
+        Q1 = uniform(s_indptr[row_hi]);
+        if (Q1 < Q0) Q1 = Q0;
+        share([&](int64_t v) { return uniform(wave_lower_bound(s_indptr, Nb, v)); });
+        head_end = (rlo < rhi) ? uniform(s_indptr[rlo]) : Pw1;
+        head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
+        row = rlo - 1;
+        p = Pw;
+        end = head_end;
+        if (head_end <= Pw) {
+            for (row = rlo; row < rhi; ++row) {
+                p = uniform(s_indptr[row]);
+                const int e = uniform(s_indptr[row + 1]);
+                if (p < e) {
+                    end = e < Pw1 ? e : Pw1;
+                    break;
+                }
+            }
+            if (row >= rhi) p = end = 0;
+        }
+    }
+    const bool has_head = head_end > Pw;
+
+    // First row after r with blocks (rhi if none); returns its start and clipped end.  Reads
+    // the LDS copy of indptr (complete after the prologue's barrier).
+    auto next_row = [&](int r, int &start, int &end_) -> int {
+        for (++r; r < rhi; ++r) {
+            start = uniform(s_indptr[r]);
+            const int e = uniform(s_indptr[r + 1]);
+            if (start < e) {
+                end_ = e < Pw1 ? e : Pw1;
+                return r;
+            }
+        }
+        start = end_ = 0;
+        return rhi;
+    };
+    // The first unit's loads (in flight during the tile stores).  Issued on every path, also
+    // for a wave without blocks (an in-range position, never used), so the compiler can count
+    // exactly which loads the tile stores below have to wait for.
+    typename U::Ops A, B;
+    U::load(A, row < rhi ? p : 0, nnzb, indices, data);
+
+    // indptr (register path: wave 0) and bias into LDS.  Unconditional stores (threads past
+    // the arrays write a spare word at the end of the indptr region), so that no load above is
+    // sunk below the tile's loads.
+    int *s_spare = s_indptr + I.indptr_words - 1;
+    if (reg_part && wave == 0) {
+#pragma unroll
+        for (int j = 0; j < kIpChunks; ++j) {
+            const int i = 64 * j + lane;
+            *(i <= Nb ? s_indptr + i : s_spare) = ip[j];
+        }
     }
 #pragma unroll
     for (int u = 0; u < kBiasPer; ++u) {
         const int i = threadIdx.x + u * kThreads;
         *(i < Nb * R ? reinterpret_cast<int *>(s_bias) + i : s_spare) = __float_as_int(bv[u]);
     }
-    for (int i = threadIdx.x + kIpPer * kThreads; i <= Nb; i += kThreads)
-        s_indptr[i] = clampi(indptr[i], 0, nnzb);
     for (int i = threadIdx.x + kBiasPer * kThreads; i < Nb * R; i += kThreads)
         s_bias[i] = bias ? bias[i] : 0.0f;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-
-    // This slice's block-rows and stored-block range.
-    const int64_t k = uniform(s_indptr[Nb]);
-    const int row_lo =
-        (s == 0) ? 0 : uniform(wave_lower_bound(s_indptr, Nb, int64_t(s) * k / slices));
-    const int row_hi = (s == slices - 1)
-                           ? Nb
-                           : uniform(wave_lower_bound(s_indptr, Nb, int64_t(s + 1) * k / slices));
-    const int64_t Q0 = uniform(s_indptr[row_lo]), Q1 = uniform(s_indptr[row_hi]);
-    const int64_t span = Q1 > Q0 ? Q1 - Q0 : 0;
-    auto wave_start = [&](int w) -> int { return int(Q0 + span * w / NW); };
-    const int Pw = uniform(wave_start(wave)), Pw1 = uniform(wave_start(wave + 1));
-
-    // Rows owned by this wave: those whose first block lies in [Pw, Pw1) (last wave: all rows
-    // up to the slice end, including trailing empty rows).
-    int rlo = (wave == 0) ? row_lo : uniform(wave_lower_bound(s_indptr, Nb, Pw));
-    rlo = rlo < row_lo ? row_lo : (rlo > row_hi ? row_hi : rlo);
-    int rhi = (wave == NW - 1) ? row_hi : uniform(wave_lower_bound(s_indptr, Nb, Pw1));
-    rhi = rhi < rlo ? rlo : (rhi > row_hi ? row_hi : rhi);
-
-    // Head: blocks of [Pw, Pw1) that belong to row rlo - 1, started by an earlier wave.
-    int head_end = (rlo < rhi) ? uniform(s_indptr[rlo]) : Pw1;
-    head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
-    const bool has_head = head_end > Pw;
-
-    // First row after r with blocks (rhi if none); returns its start and clipped end.
-    auto next_row = [&](int r, int &start, int &end) -> int {
-        for (++r; r < rhi; ++r) {
-            start = uniform(s_indptr[r]);
-            const int e = uniform(s_indptr[r + 1]);
-            if (start < e) {
-                end = e < Pw1 ? e : Pw1;
-                return r;
-            }
-        }
-        start = end = 0;
-        return rhi;
-    };
-    // The wave's first segment, and its first unit's loads (in flight during the tile stores).
-    int row, p, end;
-    if (has_head) {
-        row = rlo - 1;
-        p = Pw;
-        end = head_end;
-    } else {
-        row = next_row(rlo - 1, p, end);
-    }
-    typename U::Ops A, B;
-    if (row < rhi) U::load(A, p, nnzb, indices, data);
 
     x_store(0);
     for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
@@ -894,9 +997,9 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
 }
 
 template <int R, int C, int NW, bool BF>
-bsr_status launch_variant(const TiledBatch &batch, int grid, size_t lds, hipStream_t st,
+bsr_status launch_variant(const TiledBatch &batch, dim3 grid, size_t lds, hipStream_t st,
                           const LaunchEvents &ev) {
-    launch_kernel(spmm_tiled_kernel<R, C, NW, BF>, dim3(grid), dim3(NW * 64), lds, st, ev, batch);
+    launch_kernel(spmm_tiled_kernel<R, C, NW, BF>, grid, dim3(NW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
@@ -966,7 +1069,7 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
     const int R = work[0].W->R, C = work[0].W->C;
     TiledBatch batch{};
     batch.n = n;
-    int grid = 0;
+    int gx = 0;   // workgroups per product: the largest product's pairs, rounded up to 8
     size_t lds = 0;
     for (int i = 0; i < n; ++i) {
         const TiledWork &w = work[i];
@@ -991,21 +1094,21 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
         it.indptr_words = w.plan.indptr_words;
         it.bias_words = w.plan.bias_words;
         it.wbuf_offset = w.plan.wbuf_offset;
-        it.wg_begin = grid;
-        grid += ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
+        const int wgs = ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
+        if (wgs > gx) gx = wgs;
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
     }
     hipStream_t st = as_stream(stream);
     if (work[0].W->dtype == BSR_BF16) {
-        if (R == 32 && C == 1) return launch_variant<32, 1, 16, true>(batch, grid, lds, st, ev);
-        if (R == 16 && C == 1) return launch_variant<16, 1, 16, true>(batch, grid, lds, st, ev);
-        if (R == 32 && C == 32) return launch_variant<32, 32, 16, true>(batch, grid, lds, st, ev);
-        if (R == 16 && C == 16) return launch_variant<16, 16, 16, true>(batch, grid, lds, st, ev);
+        if (R == 32 && C == 1) return launch_variant<32, 1, 16, true>(batch, dim3(gx, n), lds, st, ev);
+        if (R == 16 && C == 1) return launch_variant<16, 1, 16, true>(batch, dim3(gx, n), lds, st, ev);
+        if (R == 32 && C == 32) return launch_variant<32, 32, 16, true>(batch, dim3(gx, n), lds, st, ev);
+        if (R == 16 && C == 16) return launch_variant<16, 16, 16, true>(batch, dim3(gx, n), lds, st, ev);
     } else {
-        if (R == 32 && C == 1) return launch_variant<32, 1, 16, false>(batch, grid, lds, st, ev);
-        if (R == 16 && C == 1) return launch_variant<16, 1, 16, false>(batch, grid, lds, st, ev);
-        if (R == 32 && C == 32) return launch_variant<32, 32, 16, false>(batch, grid, lds, st, ev);
-        if (R == 16 && C == 16) return launch_variant<16, 16, 16, false>(batch, grid, lds, st, ev);
+        if (R == 32 && C == 1) return launch_variant<32, 1, 16, false>(batch, dim3(gx, n), lds, st, ev);
+        if (R == 16 && C == 1) return launch_variant<16, 1, 16, false>(batch, dim3(gx, n), lds, st, ev);
+        if (R == 32 && C == 32) return launch_variant<32, 32, 16, false>(batch, dim3(gx, n), lds, st, ev);
+        if (R == 16 && C == 16) return launch_variant<16, 16, 16, false>(batch, dim3(gx, n), lds, st, ev);
     }
     return BSR_ERR_UNSUPPORTED;
 }
