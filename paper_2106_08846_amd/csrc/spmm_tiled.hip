@@ -206,6 +206,13 @@ struct Unit<32, 1, BF> : LinearUnit<32, BF> {
                                                   vo + r * o.ldy4, n0 * 4, kStoreNT);
         }
     }
+    // Register v of every lane alone (v uniform).
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
+        const int r = 8 * (v >> 2) + (v & 3);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), o.rsrc,
+                                              (4 * kh + r) * o.ldy4 + tl * 4, n0 * 4, kStoreNT);
+    }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
 };
@@ -256,6 +263,12 @@ struct Unit<16, 1, BF> : LinearUnit<16, BF> {
                 __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc.h[h][v]), o.rsrc,
                                                       vo + (16 * h + v) * o.ldy4, n0 * 4,
                                                       kStoreNT);
+    }
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), o.rsrc,
+                                              (4 * kq + 16 * (v >> 2) + (v & 3)) * o.ldy4 + tl * 4,
+                                              n0 * 4, kStoreNT);
     }
     __device__ static float get(const Acc &acc, int v) { return acc.h[v >> 2][v & 3]; }
     __device__ static void add(Acc &acc, int v, float x) { acc.h[v >> 2][v & 3] += x; }
@@ -351,6 +364,9 @@ struct Unit<32, 1, true> {
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         Unit<32, 1, false>::store(acc, o, n0);
     }
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        Unit<32, 1, false>::store_reg(x, o, n0, v);
+    }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
 };
@@ -412,6 +428,9 @@ struct Unit<32, 32, false> {
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         LinearBase<32>::store(acc, o, n0);
     }
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        LinearBase<32>::store_reg(x, o, n0, v);
+    }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
 };
@@ -465,6 +484,9 @@ struct Unit<32, 32, true> {
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         LinearBase<32>::store(acc, o, n0);
     }
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        LinearBase<32>::store_reg(x, o, n0, v);
+    }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
 };
@@ -516,6 +538,9 @@ struct Unit<16, 16, false> {
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         LinearBase<16>::store(acc, o, n0);
     }
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        LinearBase<16>::store_reg(x, o, n0, v);
+    }
     __device__ static float get(const Acc &acc, int v) { return LinearBase<16>::get(acc, v); }
     __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
 };
@@ -565,6 +590,9 @@ struct Unit<16, 16, true> {
     }
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         LinearBase<16>::store(acc, o, n0);
+    }
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        LinearBase<16>::store_reg(x, o, n0, v);
     }
     __device__ static float get(const Acc &acc, int v) { return LinearBase<16>::get(acc, v); }
     __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
@@ -719,10 +747,14 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     // row rlo - 1 are a head, summed into that row by the wave that owns it.
     int64_t k, Q0, Q1;
     int row_lo, row_hi, Pw, Pw1, rlo, rhi, head_end, row, p, end;
-    auto wave_start = [&](int w) -> int { return int(Q0 + (Q1 - Q0) * w / NW); };
+    // Wave starts, one per lane: ws = start of wave `lane`, wsn = start of wave lane + 1.
+    int ws = 0, wsn = 0;
     auto share = [&](auto lower_bound) {
-        Pw = uniform(wave_start(wave));
-        Pw1 = uniform(wave_start(wave + 1));
+        const int64_t span = Q1 - Q0;
+        ws = int(Q0 + span * lane / NW);
+        wsn = int(Q0 + span * (lane + 1) / NW);
+        Pw = __builtin_amdgcn_readlane(ws, wave);
+        Pw1 = __builtin_amdgcn_readlane(wsn, wave);
         rlo = (wave == 0) ? row_lo : lower_bound(int64_t(Pw));
         rlo = rlo < row_lo ? row_lo : (rlo > row_hi ? row_hi : rlo);
         rhi = (wave == NW - 1) ? row_hi : lower_bound(int64_t(Pw1));
@@ -965,34 +997,69 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
         }
     }
 
-    // Combine rows cut by wave boundaries.  The X tile is dead now; reuse its LDS.  A head
-    // partial is kept as [register group of 4][lane][4] so it moves in 16-byte LDS accesses.
+    // Combine rows cut by wave boundaries, in wave order: the owner's partial (bias and its
+    // blocks), then each later wave's head partial.  The X tile is dead now; its LDS holds the
+    // head partials P[w][v][lane], the partials of wide tails T[w][v][lane] and one word per
+    // wave naming its wide tail row.  A tail with at most kLocalHeads heads is finished by its
+    // owner; a wider one (a long row spread over many waves) is reduced by all waves at once,
+    // wave v summing accumulator register v of every lane.
+    constexpr int kLocalHeads = 2;
+    constexpr int kSlot = U::kRegs * 64;   // floats per partial
     __syncthreads();
-    floatx4 *H = reinterpret_cast<floatx4 *>(Xs);
-    constexpr int kGroups = U::kRegs / 4;
+    float *P = reinterpret_cast<float *>(Xs);
+    float *Tw = P + NW * kSlot;
+    int *s_wide = reinterpret_cast<int *>(Tw + NW * kSlot);   // [NW] rows, then [NW] head masks
+    // The waves holding head partials of the tail row this wave owns (bit w2 set): later waves
+    // whose range starts before the row's end, except waves with an empty range.
+    unsigned tail_heads = 0;
+    if (tail_row >= 0) {
+        const int e = uniform(s_indptr[tail_row + 1]);
+        tail_heads = unsigned(__ballot(lane > wave && lane < NW && ws < e && wsn != ws));
+    }
+    const bool wide = __popc(tail_heads) > kLocalHeads;
     if (has_head) {
 #pragma unroll
-        for (int q = 0; q < kGroups; ++q)
-            H[(wave * kGroups + q) * 64 + lane] =
-                floatx4{U::get(head, 4 * q), U::get(head, 4 * q + 1), U::get(head, 4 * q + 2),
-                        U::get(head, 4 * q + 3)};
+        for (int v = 0; v < U::kRegs; ++v) P[(wave * U::kRegs + v) * 64 + lane] = U::get(head, v);
     }
+    if (wide) {
+#pragma unroll
+        for (int v = 0; v < U::kRegs; ++v) Tw[(wave * U::kRegs + v) * 64 + lane] = U::get(acc, v);
+    }
+    s_wide[wave] = wide ? tail_row : -1;
+    s_wide[NW + wave] = int(tail_heads);
     __syncthreads();
-    if (tail_row >= 0) {
-        // Every later wave whose range starts inside this row holds a head partial of it,
-        // except waves with an empty range, which wrote nothing.  They are added in wave order.
-        const int end = uniform(s_indptr[tail_row + 1]);
-        for (int w2 = wave + 1; w2 < NW && wave_start(w2) < end; ++w2) {
-            if (wave_start(w2 + 1) == wave_start(w2)) continue;
-            floatx4 h[kGroups];
+    if (tail_row >= 0 && !wide) {
+        for (unsigned m = tail_heads; m; m &= m - 1) {
+            const int w2 = __ffs(m) - 1;
+            float h[U::kRegs];
 #pragma unroll
-            for (int q = 0; q < kGroups; ++q) h[q] = H[(w2 * kGroups + q) * 64 + lane];
+            for (int v = 0; v < U::kRegs; ++v) h[v] = P[(w2 * U::kRegs + v) * 64 + lane];
 #pragma unroll
-            for (int q = 0; q < kGroups; ++q)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) U::add(acc, 4 * q + e, h[q][e]);
+            for (int v = 0; v < U::kRegs; ++v) U::add(acc, v, h[v]);
         }
         U::store(acc, out, tail_row * R);
+    }
+    // Wide tails, in owner order.  All reads of a tail are issued before the sums; an absent
+    // head adds -0, which leaves every value (also +0) unchanged.
+    const int wv = lane < NW ? s_wide[lane] : -1;
+    const int whm = lane < NW ? s_wide[NW + lane] : 0;
+    for (unsigned long long m = __ballot(wv >= 0); m; m &= m - 1) {
+        const int w = __ffsll(static_cast<long long>(m)) - 1;
+        const int trow = __builtin_amdgcn_readlane(wv, w);
+        if (wave < U::kRegs) {
+            const unsigned hm = unsigned(__builtin_amdgcn_readlane(whm, w));
+            const int v = wave;
+            float x = Tw[(w * U::kRegs + v) * 64 + lane];
+            float h[NW - 1];
+#pragma unroll
+            for (int i = 0; i < NW - 1; ++i) {
+                const int w2 = i + 1;
+                h[i] = P[(w2 * U::kRegs + v) * 64 + lane];
+            }
+#pragma unroll
+            for (int i = 0; i < NW - 1; ++i) x += (hm >> (i + 1)) & 1u ? h[i] : -0.0f;
+            U::store_reg(x, out, trow * R, v);
+        }
     }
 }
 
@@ -1041,7 +1108,7 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
         p.wbuf_offset = 0;
         tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
     }
-    const size_t h_bytes = size_t(NW) * regs * 64 * 4;
+    const size_t h_bytes = 2 * size_t(NW) * regs * 64 * 4 + size_t(NW) * 8;   // partials, wide tails
     p.lds_bytes = size_t(p.indptr_words + p.bias_words) * 4 +
                   (tile_bytes > h_bytes ? tile_bytes : h_bytes);
     if (p.lds_bytes > lds_limit) return TiledPlan{};
