@@ -29,6 +29,8 @@
 //     The summation order is fixed by the launch shape, so results are bitwise reproducible.
 //   * workgroup ids are mapped so that the slices of one token tile run on the same XCD and
 //     share its L2 for the X tile.
+#include <type_traits>
+
 #include "device_common.h"
 #include "spmm_tiled.h"
 
@@ -695,14 +697,15 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
 #pragma unroll
         for (int r = 0; r < kRowsPerWave; ++r) {
             const int t = wave + NW * r;
-            const int tr = t < rows ? t : rows - 1;   // rows past T: any valid row, not stored
+            // Rows past T get an empty range (every load returns 0); the base is any valid row.
+            const int tr = t < rows ? t : rows - 1;
             const __amdgpu_buffer_rsrc_t rx =
                 buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
-                            unsigned(K) * kXBytes);
+                            t < rows ? unsigned(K) * kXBytes : 0u);
 #pragma unroll
             for (int m = 0; m < kStageChunks; ++m) {
                 // No guard needed: each row's buffer range ends at column K, so lanes past it
-                // read 0 (and are not stored).
+                // read 0.
                 if constexpr (BF && (U::kTransposed || !U::kTileBF16))
                     v[r][m] = __builtin_amdgcn_raw_buffer_load_b16(rx, (c0 + lane) * 2 + 128 * m,
                                                                    0, 0);
@@ -712,31 +715,36 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
             }
         }
     };
-    auto x_store = [&](int c0) {
+    // Branch-free stores (straight-line code keeps the prologue short to fetch: every launch
+    // starts with a cold instruction cache).  With `clamp`, a lane past the end of the row
+    // (it loaded 0: the row's buffer range ends there) stores to the first word after the
+    // row, which is padding that holds 0 anyway; without, every column of the group exists.
+    auto x_store = [&](int c0, auto clamp) {
 #pragma unroll
         for (int r = 0; r < kRowsPerWave; ++r) {
             const int t = wave + NW * r;
             if constexpr (U::kTransposed) {
-                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs);
+                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs) + t;
 #pragma unroll
                 for (int m = 0; m < kStageChunks; ++m) {
                     const int c = c0 + 64 * m + lane;
-                    if (c < K) xt[c * XP + t] = t < rows ? bf16_t(v[r][m]) : bf16_t(0);
+                    xt[(decltype(clamp)::value ? min(c, K) : c) * XP] = bf16_t(v[r][m]);
                 }
             } else {
                 // Row t of the tile as 32-bit words (fp32 columns, or pairs of bf16 columns).
-                unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane) + lane;
+                unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * (XP / kColsPerLane);
 #pragma unroll
                 for (int m = 0; m < kStageChunks; ++m) {
-                    const int c = c0 + 64 * m;
                     unsigned w = v[r][m];
                     if constexpr (BF && !U::kTileBF16) w <<= 16;   // bf16 -> fp32, exact
-                    if (c + 64 <= lane_words || (c < lane_words && c + lane < lane_words))
-                        dst[c] = t < rows ? w : 0u;
+                    const int c = c0 + 64 * m + lane;
+                    dst[decltype(clamp)::value ? min(c, lane_words) : c] = w;
                 }
             }
         }
     };
+    using Clamp = std::true_type;
+    using NoClamp = std::false_type;
     x_load(0);
 
     // The wave's share of the slice.  Slices hold whole block-rows, balanced by stored-block
@@ -760,7 +768,7 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
         rhi = (wave == NW - 1) ? row_hi : lower_bound(int64_t(Pw1));
         rhi = rhi < rlo ? rlo : (rhi > row_hi ? row_hi : rhi);
     };
-    if (reg_part) {
+    if (__builtin_expect(reg_part, 1)) {
 #pragma unroll
         for (int j = 0; j < kIpChunks; ++j) ip[j] = clampi(ip[j], 0, nnzb);
         // Entry i (uniform, <= Nb) of a register-resident array: one lane read per chunk and a
@@ -891,10 +899,13 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     for (int i = threadIdx.x + kBiasPer * kThreads; i < Nb * R; i += kThreads)
         s_bias[i] = bias ? bias[i] : 0.0f;
 
-    x_store(0);
+    if (lane_words >= 64 * kStageChunks)
+        x_store(0, NoClamp{});
+    else
+        x_store(0, Clamp{});
     for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
         x_load(c0);
-        x_store(c0);
+        x_store(c0, Clamp{});
     }
     if constexpr (U::kPad == 1) {   // the fp32 R x 1 tile's zero pad column
         if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
