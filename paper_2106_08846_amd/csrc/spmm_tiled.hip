@@ -758,9 +758,12 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     // Wave starts, one per lane: ws = start of wave `lane`, wsn = start of wave lane + 1.
     int ws = 0, wsn = 0;
     auto share = [&](auto lower_bound) {
-        const int64_t span = Q1 - Q0;
-        ws = int(Q0 + span * lane / NW);
-        wsn = int(Q0 + span * (lane + 1) / NW);
+        // floor(span l / NW) in 32-bit parts (span < 2^29, l <= 64).
+        static_assert(NW == 16, "wave starts use a division by 16");
+        const unsigned span = unsigned(Q1 - Q0), hi = span >> 4, lo = span & 15u;
+        const unsigned l0 = unsigned(lane), l1 = l0 + 1;
+        ws = int(Q0) + int(hi * l0 + ((lo * l0) >> 4));
+        wsn = int(Q0) + int(hi * l1 + ((lo * l1) >> 4));
         Pw = __builtin_amdgcn_readlane(ws, wave);
         Pw1 = __builtin_amdgcn_readlane(wsn, wave);
         rlo = (wave == 0) ? row_lo : lower_bound(int64_t(Pw));
@@ -784,13 +787,16 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
             return v;
         };
         // Number of rows i < Nb meeting a per-entry predicate; for a monotone predicate on
-        // the non-decreasing indptr this is a lower bound.
+        // the non-decreasing indptr this is a lower bound.  (Lane masks of the rows < Nb are
+        // formed once; each count is then one compare, mask and bit count per chunk.)
+        unsigned long long in_rows[kIpChunks];
+#pragma unroll
+        for (int j = 0; j < kIpChunks; ++j) in_rows[j] = __ballot(64 * j + lane < Nb);
         auto count_rows = [&](auto pred) -> int {
             int c = 0;
 #pragma unroll
-            for (int j = 0; j < kIpChunks; ++j)
-                c += __popcll(__ballot(64 * j + lane < Nb && pred(ip[j])));
-            return uniform(c);
+            for (int j = 0; j < kIpChunks; ++j) c += __popcll(__ballot(pred(ip[j])) & in_rows[j]);
+            return c;
         };
         k = lane_read(ip, Nb);
         // indptr[i] < floor(s k / slices)  <=>  (indptr[i] + 1) slices <= s k.
@@ -803,7 +809,7 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
         Q0 = lane_read(ip, row_lo);
         Q1 = lane_read(ip, row_hi);
         if (Q1 < Q0) Q1 = Q0;
-        share([&](int64_t v) { return count_rows([&](int x) { return x < v; }); });
+        share([&](int64_t v) { return count_rows([&](int x) { return x < int(v); }); });
         head_end = (rlo < rhi) ? lane_read(ip, rlo) : Pw1;
         head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
         if (head_end > Pw) {
@@ -818,7 +824,7 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
             p = end = 0;
             if (rlo < rhi) {
                 const int v = lane_read(ip, rlo);
-                const int c = count_rows([&](int x) { return x <= v; });
+                const int c = count_rows([&](int x) { return x < v + 1; });
                 const int e = lane_read(ip, c);
                 if (c - 1 >= rlo && c - 1 < rhi && e > v) {
                     row = c - 1;
