@@ -771,16 +771,20 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
         rhi = (wave == NW - 1) ? row_hi : lower_bound(int64_t(Pw1));
         rhi = rhi < rlo ? rlo : (rhi > row_hi ? row_hi : rhi);
     };
-    if (__builtin_expect(reg_part, 1)) {
+    // The register partition, over the first NCH chunks of indptr (a product with fewer than
+    // 64 block-rows runs the one-chunk instance: less code to fetch on the way to its first
+    // unit).
+    auto reg_partition = [&](auto nch) {
+        constexpr int NCH = decltype(nch)::value;
 #pragma unroll
-        for (int j = 0; j < kIpChunks; ++j) ip[j] = clampi(ip[j], 0, nnzb);
+        for (int j = 0; j < NCH; ++j) ip[j] = clampi(ip[j], 0, nnzb);
         // Entry i (uniform, <= Nb) of a register-resident array: one lane read per chunk and a
         // scalar select (a dynamic register index would send the array to scratch memory).
         auto lane_read = [&](const int(&a)[kIpChunks], int i) -> int {
             const int l = i & 63, c = i >> 6;
             int v = __builtin_amdgcn_readlane(a[0], l);
 #pragma unroll
-            for (int j = 1; j < kIpChunks; ++j) {
+            for (int j = 1; j < NCH; ++j) {
                 const int x = __builtin_amdgcn_readlane(a[j], l);
                 v = c == j ? x : v;
             }
@@ -789,13 +793,13 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
         // Number of rows i < Nb meeting a per-entry predicate; for a monotone predicate on
         // the non-decreasing indptr this is a lower bound.  (Lane masks of the rows < Nb are
         // formed once; each count is then one compare, mask and bit count per chunk.)
-        unsigned long long in_rows[kIpChunks];
+        unsigned long long in_rows[NCH];
 #pragma unroll
-        for (int j = 0; j < kIpChunks; ++j) in_rows[j] = __ballot(64 * j + lane < Nb);
+        for (int j = 0; j < NCH; ++j) in_rows[j] = __ballot(64 * j + lane < Nb);
         auto count_rows = [&](auto pred) -> int {
             int c = 0;
 #pragma unroll
-            for (int j = 0; j < kIpChunks; ++j) c += __popcll(__ballot(pred(ip[j])) & in_rows[j]);
+            for (int j = 0; j < NCH; ++j) c += __popcll(__ballot(pred(ip[j])) & in_rows[j]);
             return c;
         };
         k = lane_read(ip, Nb);
@@ -833,6 +837,11 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
                 }
             }
         }
+    };
+    if (__builtin_expect(Nb < 64, 1)) {
+        reg_partition(std::integral_constant<int, 1>{});
+    } else if (__builtin_expect(reg_part, 1)) {
+        reg_partition(std::integral_constant<int, kIpChunks>{});
     } else {
         for (int i = threadIdx.x; i <= Nb; i += kThreads) s_indptr[i] = clampi(indptr[i], 0, nnzb);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
