@@ -288,11 +288,21 @@ def main() -> int:
     return 0
 
 
+TILED_SHAPES = ((32, 1), (16, 1), (32, 32), (16, 16))
+VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1), (8, 1), (2, 2),
+               (4, 4), (8, 8))
+
+
 def tiled_kernel_name(c) -> str:
-    """The kernel libbsr launches for this product (its tiled variants are fp32 only)."""
-    tiled = c["M"].dtype == 0 and (c["R"], c["C"]) in ((32, 1), (16, 1), (32, 32), (16, 16))
-    if tiled:
-        return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16> via bsr_spmm_batched"
+    """The kernel libbsr's automatic choice launches for this product: the matrix-core tiled
+    kernel, else the vector-ALU tile kernel, else the generic kernel."""
+    bf = c["M"].dtype == 1
+    shape = (c["R"], c["C"])
+    flag = "true" if bf else "false"
+    if shape in TILED_SHAPES:
+        return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}> via bsr_spmm_batched"
+    if shape in VALU_SHAPES and not (bf and shape == (1, 1)):
+        return f"spmm_vtile_kernel<{c['R']}, {c['C']}, {flag}> via bsr_spmm_batched"
     return "spmm_generic_kernel via bsr_spmm_batched"
 
 

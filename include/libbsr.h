@@ -131,17 +131,23 @@ LIBBSR_API bsr_status bsr_spmm(const void *X, bsr_dtype x_dtype, int64_t T, int6
                     const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
                     void *stream);
 
-/* Kernel choice for bsr_spmm_ex (bsr_spmm uses BSR_KERNEL_AUTO). */
+/* Kernel choice for bsr_spmm_ex (bsr_spmm uses BSR_KERNEL_AUTO: the matrix-core kernel where
+ * it has the shape, else the vector-ALU tile kernel, else the generic kernel). */
 typedef enum {
     BSR_KERNEL_AUTO = 0,     /* the library picks                                           */
     BSR_KERNEL_GENERIC = 1,  /* one thread per output element; every block shape and dtype   */
-    BSR_KERNEL_TILED = 2     /* LDS-staged token tiles on matrix cores; 32x1, 16x1, 32x32,
+    BSR_KERNEL_TILED = 2,    /* LDS-staged token tiles on matrix cores; 32x1, 16x1, 32x32,
                                 16x16 blocks (BSR_ERR_UNSUPPORTED for other shapes)          */
+    BSR_KERNEL_VALU = 3      /* LDS-staged token tiles on the vector ALUs; 1x1, 1x2, 1x4, 1x8,
+                                1x16, 1x32, 2x1, 4x1, 8x1, 2x2, 4x4, 8x8 blocks (fp32; bf16
+                                except 1x1), K up to about 1270 (BSR_ERR_UNSUPPORTED
+                                otherwise)                                                   */
 } bsr_kernel;
 
 typedef struct {
     int32_t kernel;     /* a bsr_kernel value                                                */
-    int32_t slices;     /* tiled kernel: block-row slices per 32-token tile; 0 = automatic   */
+    int32_t slices;     /* tiled and vector-ALU kernels: block-row slices per 32-token tile;
+                           0 = automatic                                                     */
     void *start_event;  /* hipEvent_t or NULL: recorded when the product kernel starts       */
     void *stop_event;   /* hipEvent_t or NULL: recorded when it ends (both or neither)       */
 } bsr_spmm_options_t;

@@ -24,7 +24,7 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 EXPORTS = ["bsr_prune_count", "bsr_prune_workspace_bytes", "bsr_prune_from_dense", "bsr_spmm",
            "bsr_spmm_ex", "bsr_spmm_batched", "bsr_to_dense", "bsr_cast_f32_bf16",
            "bsr_status_str", "bsr_last_hip_error"]
-KERNEL_AUTO, KERNEL_GENERIC, KERNEL_TILED = 0, 1, 2
+KERNEL_AUTO, KERNEL_GENERIC, KERNEL_TILED, KERNEL_VALU = 0, 1, 2, 3
 
 
 class BSRError(RuntimeError):

@@ -124,11 +124,13 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         ev.start = opts->start_event;
         ev.stop = opts->stop_event;
     }
-    if (kernel < BSR_KERNEL_AUTO || kernel > BSR_KERNEL_TILED || slices < 0) return BSR_ERR_ARG;
+    if (kernel < BSR_KERNEL_AUTO || kernel > BSR_KERNEL_VALU || slices < 0) return BSR_ERR_ARG;
     if ((ev.start == nullptr) != (ev.stop == nullptr)) return BSR_ERR_ARG;
 
-    // Plan: every non-empty product goes to the tiled kernel when it supports the shape (and
-    // the kernel is not forced to generic), else to the generic kernel.
+    // Plan: every non-empty product goes to the matrix-core tiled kernel when it has the shape,
+    // else to the vector-ALU tile kernel, else to the generic kernel (a forced kernel choice
+    // narrows this; a forced tiled kernel that does not fit is an error).
+    enum Kind { kGeneric = 0, kTiled = 1, kVtile = 2 };
     std::vector<int> work;
     for (int32_t i = 0; i < n_items; ++i)
         if (items[i].T > 0) work.push_back(i);
@@ -138,43 +140,50 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     const int cus = bsr::device_cu_count();
     const size_t lds_limit = bsr::device_lds_per_block();
     std::vector<bsr::TiledWork> tiled(work.size());
-    std::vector<char> is_tiled(work.size(), 0);
+    std::vector<int> kind(work.size(), kGeneric);
     int64_t total_tiles = 0;
     for (size_t w = 0; w < work.size(); ++w) {
         const bsr_spmm_item_t &it = items[work[w]];
-        if (kernel != BSR_KERNEL_GENERIC && bsr::tiled_supported(it.W->R, it.W->C, it.W->dtype)) {
-            // A trial plan with one slice decides whether the shape fits.
-            if (bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok) {
-                is_tiled[w] = 1;
-                total_tiles += (it.T + 31) / 32;
-            }
-        }
-        if (!is_tiled[w] && kernel == BSR_KERNEL_TILED) return BSR_ERR_UNSUPPORTED;
+        const int R = it.W->R, C = it.W->C, dt = it.W->dtype;
+        // A trial plan with one slice decides whether the shape fits.
+        if ((kernel == BSR_KERNEL_AUTO || kernel == BSR_KERNEL_TILED) &&
+            bsr::tiled_supported(R, C, dt) &&
+            bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok)
+            kind[w] = kTiled;
+        else if ((kernel == BSR_KERNEL_AUTO || kernel == BSR_KERNEL_VALU) &&
+                 bsr::vtile_supported(R, C, dt) &&
+                 bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok)
+            kind[w] = kVtile;
+        if (kind[w] != kGeneric) total_tiles += (it.T + 31) / 32;
+        if (kind[w] == kGeneric && (kernel == BSR_KERNEL_TILED || kernel == BSR_KERNEL_VALU))
+            return BSR_ERR_UNSUPPORTED;
     }
     for (size_t w = 0; w < work.size(); ++w) {
-        if (!is_tiled[w]) continue;
+        if (kind[w] == kGeneric) continue;
         const bsr_spmm_item_t &it = items[work[w]];
         const int S = slices > 0
                           ? slices
                           : bsr::auto_slices(total_tiles, it.W->n_rows / it.W->R, cus);
-        tiled[w] = bsr::TiledWork{bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit), it.X,
-                                  it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
+        const bsr::TiledPlan plan =
+            kind[w] == kTiled ? bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit)
+                              : bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
+        tiled[w] = bsr::TiledWork{plan, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
     }
 
-    // Launch order: tiled products grouped by block shape and dtype, up to kMaxItems per launch,
-    // then generic products one by one.  With an event pair, the start event goes with the first
-    // launch and the stop event with the last.
+    // Launch order: tiled and vector-ALU products grouped by kernel, block shape and dtype, up
+    // to kMaxItems per launch, then generic products one by one.  With an event pair, the start
+    // event goes with the first launch and the stop event with the last.
     struct Launch {
-        bool tiled;
+        int kind;
         std::vector<int> members;  // indices into `work`
     };
     std::vector<Launch> launches;
     std::vector<char> done(work.size(), 0);
     for (size_t w = 0; w < work.size(); ++w) {
-        if (!is_tiled[w] || done[w]) continue;
-        Launch l{true, {}};
+        if (kind[w] == kGeneric || done[w]) continue;
+        Launch l{kind[w], {}};
         for (size_t v = w; v < work.size(); ++v) {
-            if (!is_tiled[v] || done[v]) continue;
+            if (kind[v] != kind[w] || done[v]) continue;
             if (items[work[v]].W->R != items[work[w]].W->R ||
                 items[work[v]].W->C != items[work[w]].W->C ||
                 items[work[v]].W->dtype != items[work[w]].W->dtype)
@@ -189,17 +198,18 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         if (!l.members.empty()) launches.push_back(l);
     }
     for (size_t w = 0; w < work.size(); ++w)
-        if (!is_tiled[w]) launches.push_back(Launch{false, {int(w)}});
+        if (kind[w] == kGeneric) launches.push_back(Launch{kGeneric, {int(w)}});
 
     for (size_t li = 0; li < launches.size(); ++li) {
         bsr::LaunchEvents lev;
         if (li == 0) lev.start = ev.start;
         if (li + 1 == launches.size()) lev.stop = ev.stop;
         const Launch &l = launches[li];
-        if (l.tiled) {
+        if (l.kind != kGeneric) {
             bsr::TiledWork batch[bsr::kMaxItems];
             for (size_t m = 0; m < l.members.size(); ++m) batch[m] = tiled[l.members[m]];
-            s = bsr::launch_spmm_tiled(batch, int(l.members.size()), stream, lev);
+            s = l.kind == kTiled ? bsr::launch_spmm_tiled(batch, int(l.members.size()), stream, lev)
+                                 : bsr::launch_spmm_vtile(batch, int(l.members.size()), stream, lev);
         } else {
             const bsr_spmm_item_t &it = items[work[l.members[0]]];
             s = bsr::launch_spmm_generic(it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy, stream,

@@ -40,6 +40,16 @@ __device__ __forceinline__ int clampi(int v, int lo, int hi) {
     return v < lo ? lo : (v > hi ? hi : v);
 }
 
+// A value the compiler may treat as uniform across the wave (lane 0's copy).
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Raw buffer resource over [base, base + bytes): loads past the end return 0 and stores past
+// it are dropped.  Word 3 is the default raw-buffer configuration for gfx9-family chips.  The
+// launch plans keep every range below 2^31 bytes.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, unsigned bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, int(bytes), 0x00020000);
+}
+
 // bf16 bit pattern -> fp32 value (exact widening).
 __device__ __forceinline__ float bf16_bits_to_float(unsigned short h) {
     return __uint_as_float(static_cast<unsigned int>(h) << 16);

@@ -1,4 +1,4 @@
-// Launch planning for the tiled (MFMA) BSR product kernels.
+// Launch planning for the LDS-tiled BSR product kernels (matrix-core and vector-ALU).
 #pragma once
 
 #include <stddef.h>
@@ -63,5 +63,12 @@ struct TiledBatch {
 
 // Launch 1..kMaxItems planned products of one block shape as a single kernel.
 bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream, const LaunchEvents &ev);
+
+// The vector-ALU tile kernel (shapes without a matrix-core kernel: 1 x C, 2x1 .. 8x1, 2x2 ..
+// 8x8).  Same plan and batch structures; the plan fills num_tiles, slices, x_pitch, lds_bytes.
+bool vtile_supported(int R, int C, int dtype);
+TiledPlan plan_vtile(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int64_t ldy,
+                     int slices, size_t lds_limit);
+bsr_status launch_spmm_vtile(const TiledWork *work, int n, void *stream, const LaunchEvents &ev);
 
 }  // namespace bsr

@@ -77,15 +77,6 @@ __device__ __forceinline__ int wave_lower_bound(const int *s_indptr, int n, int6
 // registers, issues its MFMAs (all lanes, or only the blocks in an offset range [lo, hi) of the
 // unit when it crosses a row end), and stores a finished row tile to Y.
 
-__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
-
-// Raw buffer resource over [base, base + bytes): loads past the end return 0 and stores past
-// it are dropped.  Word 3 is the default raw-buffer configuration for gfx9-family chips.  The
-// plan keeps every range below 2^31 bytes.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, unsigned bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, int(bytes), 0x00020000);
-}
-
 typedef __attribute__((address_space(3))) void lds_void;
 
 // Cache policy of the Y stores: nontemporal (Y is written once and not read here).

@@ -1,0 +1,397 @@
+// LDS-tiled BSR product on the vector ALUs, for block shapes without a matrix-core kernel:
+// one-row blocks 1 x C (1x1 .. 1x32), narrow column blocks 2x1 .. 8x1 and small squares 2x2,
+// 4x4, 8x8; fp32 or bf16 inputs, fp32 accumulation, fp32 output.
+//
+// Y[t][n] = bias[n] + sum over stored blocks p of block-row i = n / R of
+//           sum over c < C of X[t][indices[p] * C + c] * data[p][n - iR][c]          (Sec. 2.2)
+//
+// For R = 1 the rows of W share no input columns, so the product has no dense contraction to
+// hand to the matrix cores; for 2x1 .. 8x8 a matrix-core tile would be mostly padding.  These
+// shapes run as fp32 fused multiply-adds:
+//   * one workgroup = a 32-token tile x a slice of block-rows (equal row counts); the X tile
+//     [32][K] is staged once into LDS as fp32 (bf16 widened, exactly) with a row pitch XP that
+//     makes a read of one column segment by the 32 tokens hit distinct banks;
+//   * each wave walks whole block-rows of the slice, round robin; lane l is token l % 32 of
+//     half l / 32, and the two halves take alternate chunks of U blocks of the row;
+//   * a lane accumulates the R outputs of its token over its chunks in fp32 (block column c
+//     outer, output row r inner); the halves are summed at the row end (both halves then hold
+//     the same bits) and each half stores its share of Y[t][iR .. iR + R);
+//   * the weights of a chunk are read from global memory by all 32 lanes of a half (a
+//     broadcast), double-buffered in registers one chunk ahead; X comes from LDS.
+// The summation order depends only on the launch shape, so results are bitwise reproducible.
+#include "device_common.h"
+#include "spmm_tiled.h"
+
+namespace bsr {
+
+namespace {
+
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef unsigned uintx2 __attribute__((ext_vector_type(2)));
+typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kVT = 32;   // tokens per workgroup
+
+template <int R, int C>
+struct VShape {
+    static constexpr int RC = R * C;
+    // Blocks per chunk: about 32 weights per chunk, at most 8 blocks.
+    static constexpr int U = RC >= 32 ? 1 : (32 / RC > 8 ? 8 : 32 / RC);
+    static constexpr int NWORDS = U * RC;   // weights per chunk
+    // Width of the LDS reads of a block's X segment (C is a multiple of it).
+    static constexpr int VW = C % 4 == 0 ? 4 : (C % 2 == 0 ? 2 : 1);
+    // Waves per workgroup: 16 (128 registers per lane) for chunks of up to 16 weights, else 8
+    // (256 registers: two chunks in flight plus the X segments they read).
+    static constexpr int NW = NWORDS <= 16 ? 16 : 8;
+    static_assert(NWORDS % 8 == 0, "a chunk's weights are whole 16-byte loads of bf16 or fp32");
+};
+
+template <int N>
+struct VecOf;
+template <>
+struct VecOf<1> {
+    typedef float type;
+};
+template <>
+struct VecOf<2> {
+    typedef floatx2 type;
+};
+template <>
+struct VecOf<4> {
+    typedef floatx4 type;
+};
+
+// Operands of one chunk: U block columns and U * R * C weights (fp32).
+template <int R, int C>
+struct VOps {
+    int j[VShape<R, C>::U];
+    float w[VShape<R, C>::NWORDS];
+};
+
+// Loads the chunk that starts `o` blocks into the row (the row's arrays are the buffer ranges
+// ri / rd, so a chunk past the row end reads 0 and touches no memory).
+template <int R, int C, bool BF>
+__device__ __forceinline__ void vload(VOps<R, C> &ops, __amdgpu_buffer_rsrc_t ri,
+                                      __amdgpu_buffer_rsrc_t rd, int o) {
+    using S = VShape<R, C>;
+    if constexpr (S::U == 8) {
+        const uintx4 a = __builtin_amdgcn_raw_buffer_load_b128(ri, o * 4, 0, 0);
+        const uintx4 b = __builtin_amdgcn_raw_buffer_load_b128(ri, o * 4, 16, 0);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            ops.j[u] = int(a[u]);
+            ops.j[4 + u] = int(b[u]);
+        }
+    } else if constexpr (S::U == 4) {
+        const uintx4 a = __builtin_amdgcn_raw_buffer_load_b128(ri, o * 4, 0, 0);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) ops.j[u] = int(a[u]);
+    } else if constexpr (S::U == 2) {
+        const uintx2 a = __builtin_amdgcn_raw_buffer_load_b64(ri, o * 4, 0, 0);
+        ops.j[0] = int(a[0]);
+        ops.j[1] = int(a[1]);
+    } else {
+        ops.j[0] = int(__builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, 0, 0));
+    }
+    if constexpr (BF) {
+        // 8 bf16 weights per 16-byte load, widened exactly to fp32.
+#pragma unroll
+        for (int q = 0; q < S::NWORDS / 8; ++q) {
+            const uintx4 v = __builtin_amdgcn_raw_buffer_load_b128(rd, o * (S::RC * 2), 16 * q, 0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                ops.w[8 * q + 2 * e] = __uint_as_float(v[e] << 16);
+                ops.w[8 * q + 2 * e + 1] = __uint_as_float(v[e] & 0xffff0000u);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < S::NWORDS / 4; ++q) {
+            const uintx4 v = __builtin_amdgcn_raw_buffer_load_b128(rd, o * (S::RC * 4), 16 * q, 0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ops.w[4 * q + e] = __uint_as_float(v[e]);
+        }
+    }
+}
+
+// acc[r] += sum over the chunk's first nv blocks (all U when !MASKED) and their columns c of
+// X[t][j * C + c] * w[r][c].  xrow is this lane's token row of the LDS tile.  Block columns are
+// clamped into [0, Kb), so a malformed index reads a wrong column of the tile, never outside it.
+template <int R, int C, bool MASKED>
+__device__ __forceinline__ void vcompute(float (&acc)[R], const VOps<R, C> &ops,
+                                         const float *xrow, int Kb, int nv) {
+    using S = VShape<R, C>;
+    using V = typename VecOf<S::VW>::type;
+#pragma unroll
+    for (int u = 0; u < S::U; ++u) {
+        if (MASKED && u >= nv) break;
+        const unsigned col = min(unsigned(ops.j[u]), unsigned(Kb - 1)) * unsigned(C);
+        const float *xs = xrow + col;
+#pragma unroll
+        for (int c0 = 0; c0 < C; c0 += S::VW) {
+            const V xv = *reinterpret_cast<const V *>(xs + c0);
+#pragma unroll
+            for (int cc = 0; cc < S::VW; ++cc) {
+                float x;
+                if constexpr (S::VW == 1) x = xv;
+                else x = xv[cc];
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    acc[r] = __builtin_fmaf(x, ops.w[u * S::RC + r * C + c0 + cc], acc[r]);
+            }
+        }
+    }
+}
+
+template <int R, int C, bool BF>
+__global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_kernel(const TiledBatch batch) {
+    using S = VShape<R, C>;
+    constexpr int NW = S::NW, U = S::U;
+    extern __shared__ float smem[];
+    float *Xs = smem;
+
+    const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
+    const int t = lane & 31, h = lane >> 5;
+
+    const TiledItem &I = batch.item[blockIdx.y];
+    const void *__restrict__ X = I.X;
+    const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
+    const int32_t *__restrict__ indptr = I.indptr;
+    const int32_t *__restrict__ indices = I.indices;
+    const void *__restrict__ data = I.data;
+    const float *__restrict__ bias = I.bias;
+    float *__restrict__ Y = I.Y;
+    const int K = I.K, nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
+              slices = I.slices, XP = I.XP;
+
+    // Workgroup -> (token tile, slice): workgroups are dealt to the 8 XCDs round robin (the
+    // grid's x extent is a multiple of 8), and the product's (tile, slice) pairs, tile-major,
+    // are cut into 8 contiguous ranges, one per XCD, so a tile's slices share few L2s.
+    const int g = blockIdx.x, xcd = g & 7, rank = g >> 3;
+    const int pairs = num_tiles * slices, per_xcd = (pairs + 7) >> 3;
+    const int q = xcd * per_xcd + rank;
+    if (rank >= per_xcd || q >= pairs) return;
+    const int tile = q / slices, s = q - tile * slices;
+    const int64_t t0 = int64_t(tile) * kVT;
+    const int rows = int(T - t0 < kVT ? T - t0 : kVT);
+    const int row_lo = int(int64_t(s) * Nb / slices), row_hi = int(int64_t(s + 1) * Nb / slices);
+
+    // Stage X[t0 : t0 + 32][0 : K] as fp32, row pitch XP.  Each wave moves whole rows, eight
+    // 64-column groups of loads in flight before their LDS stores; rows past T read as 0 (an
+    // empty buffer range).
+    {
+        constexpr int kXBytes = BF ? 2 : 4;
+        constexpr int kG = 8;
+#pragma unroll 1
+        for (int tr = wave; tr < kVT; tr += NW) {
+            const int src = tr < rows ? tr : 0;
+            const __amdgpu_buffer_rsrc_t rx =
+                buffer_rsrc(static_cast<const char *>(X) + (t0 + src) * ldx * kXBytes,
+                            tr < rows ? unsigned(K) * kXBytes : 0u);
+            float *dst = Xs + tr * XP;
+            float *spare = Xs + kVT * XP + lane;
+#pragma unroll 1
+            for (int c0 = 0; c0 < K; c0 += 64 * kG) {
+                float v[kG];
+#pragma unroll
+                for (int m = 0; m < kG; ++m) {
+                    const int c = c0 + 64 * m + lane;
+                    if constexpr (BF)
+                        v[m] = __uint_as_float(unsigned(__builtin_amdgcn_raw_buffer_load_b16(
+                                                   rx, c * 2, 0, 0))
+                                               << 16);
+                    else
+                        v[m] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rx, c * 4, 0, 0));
+                }
+                // Branch-free stores: a lane past the end of the row writes its word of the
+                // spare region after the tile, which nothing reads.
+#pragma unroll
+                for (int m = 0; m < kG; ++m) {
+                    const int c = c0 + 64 * m + lane;
+                    *(c < K ? dst + c : spare) = v[m];
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    const float *xrow = Xs + t * XP;
+    const int ldy4 = int(ldy) * 4;
+    const __amdgpu_buffer_rsrc_t ry =
+        buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(ldy4));
+    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(bias, bias ? unsigned(Nb * R) * 4u : 0u);
+    constexpr int kEs = BF ? 2 : 4;   // bytes per stored weight
+
+#pragma unroll 1
+    for (int row = row_lo + wave; row < row_hi; row += NW) {
+        const int p0 = clampi(uniform(indptr[row]), 0, nnzb);
+        const int p1 = clampi(uniform(indptr[row + 1]), p0, nnzb);
+        const int m = p1 - p0;
+        const int n0 = row * R;
+        float acc[R];
+        // Half 0 starts from the bias (a NULL bias reads 0), half 1 from zero.
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const float b = __uint_as_float(
+                __builtin_amdgcn_raw_buffer_load_b32(rb, (n0 + r) * 4, 0, 0));
+            acc[r] = h == 0 ? b : 0.0f;
+        }
+        if (m > 0) {
+            const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p0, unsigned(m) * 4u);
+            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
+                static_cast<const char *>(data) + int64_t(p0) * S::RC * kEs,
+                unsigned(m) * unsigned(S::RC * kEs));
+            const int nq = (m + U - 1) / U, iters = (nq + 1) >> 1;
+            // Chunk `it` of this half starts (2 it + h) U blocks into the row; every chunk
+            // before the last iteration is full.
+            VOps<R, C> A, B;
+            vload<R, C, BF>(A, ri, rd, h * U);
+            int it = 0;
+            while (true) {
+                if (it + 1 < iters) vload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
+                __builtin_amdgcn_sched_barrier(0);
+                if (it + 1 >= iters) {
+                    vcompute<R, C, true>(acc, A, xrow, Kb, m - (2 * it + h) * U);
+                    break;
+                }
+                vcompute<R, C, false>(acc, A, xrow, Kb, U);
+                __builtin_amdgcn_sched_barrier(0);
+                ++it;
+                if (it + 1 < iters) vload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
+                __builtin_amdgcn_sched_barrier(0);
+                if (it + 1 >= iters) {
+                    vcompute<R, C, true>(acc, B, xrow, Kb, m - (2 * it + h) * U);
+                    break;
+                }
+                vcompute<R, C, false>(acc, B, xrow, Kb, U);
+                __builtin_amdgcn_sched_barrier(0);
+                ++it;
+            }
+        }
+        // Sum the halves and store.  v_permlane32_swap(P, Q) exchanges the upper half of P
+        // with the lower half of Q, giving P' = [P_lo | Q_lo] and Q' = [P_hi | Q_hi]; so with
+        // P = acc[r] and Q = acc[R/2 + r], P' + Q' is the total of output r on half 0 and of
+        // output R/2 + r on half 1, both summed as (half 0) + (half 1).  Half h then stores
+        // outputs [h R/2, (h+1) R/2) of its token (R = 1: P = Q, and half 0 stores).
+        const int vo = t * ldy4 + n0 * 4;
+        constexpr int kHalf = R == 1 ? 1 : R / 2;
+        static_assert(R == 1 || R % 2 == 0, "two-half stores need an even R");
+#pragma unroll
+        for (int r = 0; r < kHalf; ++r) {
+            const float P = acc[r], Q = acc[R == 1 ? 0 : R / 2 + r];
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(P),
+                                                             __float_as_uint(Q), false, false);
+            const float y = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+            if (R > 1 || h == 0)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), ry,
+                                                      vo + (h * kHalf + r) * 4 * (R > 1), 0, 0);
+        }
+    }
+}
+
+template <int R, int C, bool BF>
+bsr_status launch_vtile_variant(const TiledBatch &batch, dim3 grid, size_t lds, hipStream_t st,
+                                const LaunchEvents &ev) {
+    launch_kernel(spmm_vtile_kernel<R, C, BF>, grid, dim3(VShape<R, C>::NW * 64), lds, st, ev,
+                  batch);
+    return launch_status();
+}
+
+// The shapes instantiated here, for one dtype.
+template <bool BF>
+bsr_status launch_vtile_shape(int R, int C, const TiledBatch &b, dim3 g, size_t lds,
+                              hipStream_t st, const LaunchEvents &ev) {
+#define BSR_VTILE(RR, CC) \
+    if (R == RR && C == CC) return launch_vtile_variant<RR, CC, BF>(b, g, lds, st, ev);
+    if constexpr (!BF) {
+        BSR_VTILE(1, 1)
+    }
+    BSR_VTILE(1, 2)
+    BSR_VTILE(1, 4)
+    BSR_VTILE(1, 8)
+    BSR_VTILE(1, 16)
+    BSR_VTILE(1, 32)
+    BSR_VTILE(2, 1)
+    BSR_VTILE(4, 1)
+    BSR_VTILE(8, 1)
+    BSR_VTILE(2, 2)
+    BSR_VTILE(4, 4)
+    BSR_VTILE(8, 8)
+#undef BSR_VTILE
+    return BSR_ERR_UNSUPPORTED;
+}
+
+}  // namespace
+
+bool vtile_supported(int R, int C, int dtype) {
+    if (dtype != BSR_F32 && dtype != BSR_BF16) return false;
+    const bool shape = (R == 1 && (C == 1 || C == 2 || C == 4 || C == 8 || C == 16 || C == 32)) ||
+                       (C == 1 && (R == 2 || R == 4 || R == 8)) ||
+                       (R == C && (R == 2 || R == 4 || R == 8));
+    // bf16 blocks of one element would start at 2-byte offsets; the loads want 4.
+    return shape && !(dtype == BSR_BF16 && R * C == 1);
+}
+
+TiledPlan plan_vtile(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int64_t ldy,
+                     int slices, size_t lds_limit) {
+    TiledPlan p{};
+    const int R = W->R, C = W->C;
+    if (!vtile_supported(R, C, W->dtype)) return p;
+    const int64_t K = W->n_cols, Nb = W->n_rows / R;
+    // Row pitch XP >= K with XP = VW (mod 2 VW): reads of VW floats by consecutive tokens
+    // start VW banks apart (mod 2 VW), so a column segment read by 32 tokens is conflict-free.
+    const int vw = C % 4 == 0 ? 4 : (C % 2 == 0 ? 2 : 1);
+    const int64_t xp = K + (((vw - K) % (2 * vw)) + 2 * vw) % (2 * vw);
+    p.x_pitch = int(xp);
+    p.lds_bytes = (size_t(kVT) * size_t(xp) + 64) * 4;   // the tile, then 64 spare words
+    if (p.lds_bytes > lds_limit) return TiledPlan{};
+    // 32-bit buffer ranges: the blocks of one row, one X row and a 32-row tile of Y.
+    if (W->nnzb * R * C >= (int64_t(1) << 29)) return TiledPlan{};
+    if (ldy >= (int64_t(1) << 24) || K >= (int64_t(1) << 24)) return TiledPlan{};
+    p.num_tiles = int((T + kVT - 1) / kVT);
+    p.slices = slices > 0 ? slices : 1;
+    if (p.slices > Nb) p.slices = int(Nb);
+    p.ok = true;
+    return p;
+}
+
+bsr_status launch_spmm_vtile(const TiledWork *work, int n, void *stream,
+                             const LaunchEvents &ev) {
+    if (n < 1 || n > kMaxItems) return BSR_ERR_ARG;
+    const int R = work[0].W->R, C = work[0].W->C, dtype = work[0].W->dtype;
+    TiledBatch batch{};
+    batch.n = n;
+    int gx = 0;
+    size_t lds = 0;
+    for (int i = 0; i < n; ++i) {
+        const TiledWork &w = work[i];
+        if (w.W->R != R || w.W->C != C || w.W->dtype != dtype) return BSR_ERR_ARG;
+        TiledItem &it = batch.item[i];
+        it.X = w.X;
+        it.T = w.T;
+        it.ldx = w.ldx;
+        it.indptr = w.W->indptr;
+        it.indices = w.W->indices;
+        it.data = w.W->data;
+        it.bias = w.bias;
+        it.Y = w.Y;
+        it.ldy = w.ldy;
+        it.K = int(w.W->n_cols);
+        it.nnzb = int(w.W->nnzb);
+        it.Nb = int(w.W->n_rows / R);
+        it.Kb = int(w.W->n_cols / C);
+        it.num_tiles = w.plan.num_tiles;
+        it.slices = w.plan.slices;
+        it.XP = w.plan.x_pitch;
+        const int wgs = ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
+        if (wgs > gx) gx = wgs;
+        if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
+    }
+    hipStream_t st = as_stream(stream);
+    const dim3 grid(gx, n);
+    if (dtype == BSR_BF16) return launch_vtile_shape<true>(R, C, batch, grid, lds, st, ev);
+    return launch_vtile_shape<false>(R, C, batch, grid, lds, st, ev);
+}
+
+}  // namespace bsr

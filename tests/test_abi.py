@@ -158,7 +158,7 @@ def test_python_binding_rejects_cpu_tensors(L):
 
 
 @pytest.mark.parametrize("kernel,slices,start,stop", [
-    (3, 0, None, None), (-1, 0, None, None), (0, -1, None, None),
+    (4, 0, None, None), (-1, 0, None, None), (0, -1, None, None),
     (0, 0, FAKE, None), (0, 0, None, FAKE),
 ])
 def test_spmm_ex_option_errors(L, lib, kernel, slices, start, stop):
