@@ -7,12 +7,16 @@ tables or helpers with the GPU kernels, and it imports nothing from the library 
 What is computed, and which passage of the paper defines it:
 
 * Blocks and their norm -- Sec. 2.1, Eq. 3: the structured norm of a weight matrix is a sum over
-  its N blocks of a per-block norm.  The per-block norm is read as the l2 group norm (the
-  group-lasso definition that Sec. 2.1 keeps in its source as a commented-out draft).  The key of
-  a block is its squared l2 norm, which orders blocks exactly as the norm does.
+  its N blocks of a per-block norm.  The default per-block norm is the l2 group norm (the
+  group-lasso definition that Sec. 2.1 keeps in its source as a commented-out draft); its key is
+  the squared l2 norm, which orders blocks exactly as the norm does.  The l1 block norm (Eq. 1
+  and Eq. 2 allow p in {0, 1}; Table 1's header names l1) is the alternative key: the sum of
+  absolute values over the block.
 * Selection -- Sec. 2.1, Eq. 2: the constrained form with tolerance tau on the number of nonzero
   groups.  With tau = k blocks, the Euclidean projection of W onto that set keeps the k blocks of
-  largest key.  Ties go to the lower row-major block id, which makes the result unique.
+  largest key.  Ties go to the lower row-major block id, which makes the result unique.  The
+  per-row balanced form applies the same constraint to every block-row separately (tau = k_row
+  blocks in each row), so every block-row keeps the same number of blocks.
 * Storage -- Sec. 2.2, second bullet: BSR as data values, indices and indptr, following SciPy.
 * Product -- Sec. 2.2, first and second bullets: only stored blocks are multiplied with the input
   tensor.  The operation is Y = X W^T + b with W the pruned weight (BERT projections, Sec. 2.3).
@@ -21,8 +25,9 @@ Conventions (the paper leaves these open; the readings are listed with the desig
 * W is N x K, row-major [out][in]; a block R x C covers R output rows and C input columns.
   Block (i, j) covers W[iR:(i+1)R, jC:(j+1)C]; its id is i*Kb + j with Kb = K/C.
 * k = floor(density * nb + 0.5), computed in fp64, clamped to [0, nb].
-* Keys are fp64, summed sequentially with r outer and c inner from +0.0.  A NaN key ranks above
-  +inf.
+* Keys are fp64, summed sequentially with r outer and c inner from +0.0 (l2: x*x, l1: |x|, both
+  exact in fp64).  A NaN key ranks above +inf.
+* Per-row balanced selection keeps k_row = floor(density * Kb + 0.5) blocks in every row.
 * Products accumulate in fp64.  bf16 inputs are rounded to nearest, ties to even.
 """
 
@@ -49,28 +54,37 @@ def check_shape(N: int, K: int, R: int, C: int) -> tuple[int, int]:
     return N // R, K // C
 
 
-def prune_count(N: int, K: int, R: int, C: int, density: float) -> int:
+def prune_count(N: int, K: int, R: int, C: int, density: float, per_row: bool = False) -> int:
     """Number of blocks kept at a block density: floor(density * nb + 0.5), in [0, nb].
 
     Eq. 2 bounds the count of nonzero groups by tau; density d names tau = round(d * nb)
-    with halves rounded up.
+    with halves rounded up.  With per_row, the bound applies to every block-row: each keeps
+    floor(density * Kb + 0.5) of its Kb blocks, and the total is Nb times that.
     """
     Nb, Kb = check_shape(N, K, R, C)
     d = float(density)
     if not (0.0 <= d <= 1.0):  # also rejects NaN
         raise ValueError("density must lie in [0, 1]")
+    if per_row:
+        k_row = max(0, min(Kb, math.floor(d * Kb + 0.5)))
+        return Nb * k_row
     nb = Nb * Kb
     k = math.floor(d * nb + 0.5)
     return max(0, min(nb, k))
 
 
-def block_keys(W: np.ndarray, R: int, C: int) -> np.ndarray:
-    """Squared l2 norm of every block, fp64, in row-major block-id order (Eq. 3, l2 reading).
+def block_keys(W: np.ndarray, R: int, C: int, norm: str = "l2") -> np.ndarray:
+    """Key of every block, fp64, in row-major block-id order (Eq. 3).
 
+    norm "l2": the squared l2 norm (sum of x*x), the key of the l2 group norm.
+    norm "l1": the l1 norm (sum of |x|), the p = 1 case of Eq. 1 and Eq. 2.
     The sum runs sequentially over the block's elements, row r outer and column c inner, starting
     from +0.0.  It is vectorised across blocks only, so the rounding of each key is that of the
-    plain sequential loop.
+    plain sequential loop.  Both terms are exact in fp64 (a product of two fp32 values has at
+    most 48 significant bits), so only the additions round.
     """
+    if norm not in ("l2", "l1"):
+        raise ValueError("norm must be 'l2' or 'l1'")
     W = np.asarray(W, dtype=np.float32)
     N, K = W.shape
     Nb, Kb = check_shape(N, K, R, C)
@@ -79,7 +93,7 @@ def block_keys(W: np.ndarray, R: int, C: int) -> np.ndarray:
     for r in range(R):
         for c in range(C):
             x = blocks[:, r, :, c]
-            key = key + x * x
+            key = key + (x * x if norm == "l2" else np.abs(x))
     return key.reshape(-1)
 
 
@@ -109,6 +123,25 @@ def select_topk(key: np.ndarray, k: int) -> np.ndarray:
     return mask
 
 
+def select_topk_rows(key: np.ndarray, Nb: int, Kb: int, k_row: int) -> np.ndarray:
+    """Boolean mask keeping, in every block-row, the k_row blocks that come first in the order
+    (key descending, id ascending) among that row's blocks.
+
+    This is Eq. 2 with the block-count constraint tau = k_row imposed on each block-row
+    separately; the rows do not compete with each other.
+    """
+    key = np.asarray(key, dtype=np.float64).reshape(Nb, Kb)
+    if not (0 <= k_row <= Kb):
+        raise ValueError("k_row must lie in [0, Kb]")
+    mask = np.zeros((Nb, Kb), dtype=bool)
+    for i in range(Nb):
+        bits = _rank_bits(key[i])
+        cols = np.arange(Kb, dtype=np.int64)
+        order = np.lexsort((cols, ~bits))
+        mask[i, order[:k_row]] = True
+    return mask.reshape(-1)
+
+
 def build_bsr(W: np.ndarray, R: int, C: int, mask: np.ndarray):
     """BSR arrays (indptr int32[Nb+1], indices int32[k], data float32[k, R, C]) of W under mask.
 
@@ -134,10 +167,13 @@ def build_bsr(W: np.ndarray, R: int, C: int, mask: np.ndarray):
     return indptr, np.asarray(indices, dtype=np.int32), data
 
 
-def prune(W: np.ndarray, R: int, C: int, density: float | None = None, k: int | None = None):
-    """Dense W -> BSR keeping the top-k blocks by l2 norm (Eq. 2 and Eq. 3).
+def prune(W: np.ndarray, R: int, C: int, density: float | None = None, k: int | None = None,
+          norm: str = "l2", per_row: bool = False):
+    """Dense W -> BSR keeping the top-k blocks by block norm (Eq. 2 and Eq. 3).
 
-    Give exactly one of density and k.  Returns (indptr, indices, data).
+    Give exactly one of density and k.  norm is "l2" or "l1" (block_keys).  With per_row, k is
+    the total over all block-rows and must be a multiple of Nb; every row keeps k / Nb blocks.
+    Returns (indptr, indices, data).
     """
     W = np.asarray(W, dtype=np.float32)
     N, K = W.shape
@@ -145,8 +181,14 @@ def prune(W: np.ndarray, R: int, C: int, density: float | None = None, k: int | 
     if (density is None) == (k is None):
         raise ValueError("give exactly one of density and k")
     if k is None:
-        k = prune_count(N, K, R, C, density)
-    mask = select_topk(block_keys(W, R, C), int(k))
+        k = prune_count(N, K, R, C, density, per_row=per_row)
+    key = block_keys(W, R, C, norm)
+    if per_row:
+        if Nb == 0 or int(k) % Nb:
+            raise ValueError("per-row selection needs k to be a multiple of Nb")
+        mask = select_topk_rows(key, Nb, Kb, int(k) // Nb)
+    else:
+        mask = select_topk(key, int(k))
     return build_bsr(W, R, C, mask)
 
 

@@ -30,37 +30,72 @@ def _nan_ranks_lowest(key, k):
     return m
 
 
-def _l1_keys(W, R, C):
+def _l1_keys(W, R, C, norm="l2"):
     W = np.asarray(W, dtype=np.float32)
     N, K = W.shape
     return np.abs(W.astype(np.float64)).reshape(N // R, R, K // C, C).sum(axis=(1, 3)).ravel()
 
 
-def _pairwise_keys(W, R, C):
+def _pairwise_keys(W, R, C, norm="l2"):
     W = np.asarray(W, dtype=np.float32)
     N, K = W.shape
     x = W.astype(np.float64).reshape(N // R, R, K // C, C)
-    return np.sum(x * x, axis=(1, 3)).ravel()
+    t = x * x if norm == "l2" else np.abs(x)
+    return np.sum(t, axis=(1, 3)).ravel()
 
 
-def _column_major_block_order(W, R, C):
-    key = O.__dict__["_orig_block_keys"](W, R, C)
+def _column_major_block_order(W, R, C, norm="l2"):
+    key = O.__dict__["_orig_block_keys"](W, R, C, norm)
     N, K = np.asarray(W).shape
     return key.reshape(N // R, K // C).T.ravel()
 
 
-def _round_half_even(N, K, R, C, d):
+def _l1_as_squares(W, R, C, norm="l2"):
+    return O.__dict__["_orig_block_keys"](W, R, C, "l2")
+
+
+def _l1_signed_sum(W, R, C, norm="l2"):
+    if norm == "l2":
+        return O.__dict__["_orig_block_keys"](W, R, C, "l2")
+    W = np.asarray(W, dtype=np.float32)
+    N, K = W.shape
+    x = W.astype(np.float64).reshape(N // R, R, K // C, C)
+    key = np.zeros((N // R, K // C))
+    for r in range(R):
+        for c in range(C):
+            key = key + x[:, r, :, c]
+    return key.ravel()
+
+
+def _round_half_even(N, K, R, C, d, per_row=False):
     Nb, Kb = O.check_shape(N, K, R, C)
     if not (0.0 <= d <= 1.0):
         raise ValueError
-    return round(d * Nb * Kb)
+    return Nb * round(d * Kb) if per_row else round(d * Nb * Kb)
 
 
-def _truncating_count(N, K, R, C, d):
+def _truncating_count(N, K, R, C, d, per_row=False):
     Nb, Kb = O.check_shape(N, K, R, C)
     if not (0.0 <= d <= 1.0):
         raise ValueError
-    return int(d * Nb * Kb)
+    return Nb * int(d * Kb) if per_row else int(d * Nb * Kb)
+
+
+def _per_row_count_from_global(N, K, R, C, d, per_row=False):
+    return O.__dict__["_orig_prune_count"](N, K, R, C, d)
+
+
+def _rows_ties_to_higher_column(key, Nb, Kb, k_row):
+    key = np.asarray(key, dtype=np.float64).reshape(Nb, Kb)
+    m = np.zeros((Nb, Kb), dtype=bool)
+    for i in range(Nb):
+        order = np.lexsort((-np.arange(Kb), ~O._rank_bits(key[i])))
+        m[i, order[:k_row]] = True
+    return m.ravel()
+
+
+def _rows_as_global_topk(key, Nb, Kb, k_row):
+    return O.select_topk(key, Nb * k_row)
 
 
 def _spmm_untransposed(X, indptr, indices, data, N, bias=None):
@@ -138,8 +173,13 @@ MUTANTS = {
     "l1 block key": ("block_keys", _l1_keys),
     "pairwise-summed key": ("block_keys", _pairwise_keys),
     "column-major block ids": ("block_keys", _column_major_block_order),
+    "l1 key sums squares": ("block_keys", _l1_as_squares),
+    "l1 key sums signed values": ("block_keys", _l1_signed_sum),
     "k rounds half to even": ("prune_count", _round_half_even),
     "k truncates": ("prune_count", _truncating_count),
+    "per-row count is the global count": ("prune_count", _per_row_count_from_global),
+    "per-row ties go to the higher column": ("select_topk_rows", _rows_ties_to_higher_column),
+    "per-row selection is a global top-k": ("select_topk_rows", _rows_as_global_topk),
     "block not transposed in the product": ("spmm_loop", _spmm_untransposed),
     "bias dropped": ("spmm_loop", _spmm_no_bias),
     "last block of each row skipped": ("spmm_loop", _spmm_off_by_one_row),
@@ -162,6 +202,16 @@ def _all_pins():
         ("keys-int", P.test_keys_integer_entries_are_exact),
         ("keys-seq", P.test_keys_sequential_order_matters_at_the_last_bit),
         ("keys-nonfinite", P.test_keys_nonfinite),
+        ("l1-unit", P.test_l1_keys_unit_blocks_are_exact_magnitudes),
+        ("l1-int", P.test_l1_keys_integer_entries_are_exact),
+        ("l1-const", P.test_l1_keys_sign_blind_constant),
+        ("l1-seq", P.test_l1_keys_sequential_order_matters_at_the_last_bit),
+        ("l1-mass", lambda: P.test_l1_selection_keeps_the_largest_l1_mass(16, 16, 3)),
+        ("row-count", lambda: [P.test_per_row_count_closed_form(768, 768, 32, 1, 0.1, 24 * 77),
+                               P.test_per_row_count_closed_form(96, 40, 3, 5, 0.4, 96)]),
+        ("row-brute", lambda: [P.test_per_row_matches_brute_force(s) for s in range(5)]),
+        ("row-projection", lambda: P.test_per_row_keeps_equal_counts_and_is_the_row_projection("l2")),
+        ("row-ties", P.test_per_row_ties_keep_lowest_columns),
         ("select-brute", lambda: [P.test_select_matches_brute_force(s) for s in range(6)]),
         ("select-zero", P.test_select_ties_all_zero_keeps_lowest_ids),
         ("select-dup", P.test_select_duplicate_and_sign_flipped_blocks),

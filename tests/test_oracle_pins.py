@@ -33,9 +33,10 @@ def _golden():
 def test_hand_examples(ex):
     W = np.array(ex["W"], dtype=np.float32)
     R, C = ex["R"], ex["C"]
-    assert O.block_keys(W, R, C).tolist() == ex["keys"]
-    assert O.prune_count(W.shape[0], W.shape[1], R, C, ex["density"]) == ex["k"]
-    indptr, indices, data = O.prune(W, R, C, density=ex["density"])
+    norm, per_row = ex.get("norm", "l2"), ex.get("per_row", False)
+    assert O.block_keys(W, R, C, norm).tolist() == ex["keys"]
+    assert O.prune_count(W.shape[0], W.shape[1], R, C, ex["density"], per_row=per_row) == ex["k"]
+    indptr, indices, data = O.prune(W, R, C, density=ex["density"], norm=norm, per_row=per_row)
     assert indptr.tolist() == ex["indptr"]
     assert indices.tolist() == ex["indices"]
     assert data.tolist() == ex["data"]
@@ -243,6 +244,139 @@ def test_select_nan_ranks_above_inf():
     key = np.array([1.0, np.inf, np.nan, 2.0])
     assert O.select_topk(key, 1).nonzero()[0].tolist() == [2]
     assert O.select_topk(key, 2).nonzero()[0].tolist() == [1, 2]
+
+
+# ---------------------------------------------------------------- l1 keys (p = 1 of Eq. 1, 2)
+
+
+def test_l1_keys_unit_blocks_are_exact_magnitudes():
+    W = rng(11).standard_normal((16, 24)).astype(np.float32)
+    assert np.array_equal(O.block_keys(W, 1, 1, "l1"), np.abs(W.astype(np.float64)).ravel())
+
+
+def test_l1_keys_integer_entries_are_exact():
+    W = rng(12).integers(-1000, 1000, size=(32, 64)).astype(np.float32)
+    Wi = np.abs(W.astype(np.int64))
+    for R, C in [(32, 1), (1, 32), (4, 4), (8, 8), (32, 32)]:
+        Nb, Kb = 32 // R, 64 // C
+        exact = [int(Wi[i * R:(i + 1) * R, j * C:(j + 1) * C].sum())
+                 for i in range(Nb) for j in range(Kb)]
+        assert O.block_keys(W, R, C, "l1").tolist() == [float(e) for e in exact]
+
+
+def test_l1_keys_sign_blind_constant():
+    W = np.full((64, 64), -0.5, dtype=np.float32)
+    W[::2] = 0.5
+    for R, C in [(32, 1), (4, 4), (32, 32)]:
+        assert np.all(O.block_keys(W, R, C, "l1") == R * C / 2)
+
+
+def test_l1_keys_within_fsum_bound():
+    W = rng(13).standard_normal((64, 64)).astype(np.float32)
+    for R, C in [(32, 1), (32, 32), (16, 16)]:
+        key = O.block_keys(W, R, C, "l1")
+        Kb, n = 64 // C, R * C
+        gamma = n * 2.0 ** -53 / (1 - n * 2.0 ** -53)
+        for b, kv in enumerate(key):
+            i, j = divmod(b, Kb)
+            ref = math.fsum(abs(float(x)) for x in W[i * R:(i + 1) * R, j * C:(j + 1) * C].ravel())
+            assert abs(kv - ref) <= gamma * ref
+
+
+def test_l1_keys_sequential_order_matters_at_the_last_bit():
+    # 1 + 2^-53 is a tie that rounds to even (1); a pairwise sum would first add the two tiny
+    # terms exactly (2^-52) and end at 1 + 2^-52.
+    W = np.array([[1.0, 2.0 ** -53, -(2.0 ** -53)]], dtype=np.float32)
+    assert O.block_keys(W, 1, 3, "l1")[0] == 1.0
+    W = np.array([[2.0 ** -53, -(2.0 ** -53), 1.0]], dtype=np.float32)
+    assert O.block_keys(W, 1, 3, "l1")[0] == 1.0 + 2.0 ** -52
+
+
+def test_l1_keys_nonfinite():
+    W = np.ones((2, 4), dtype=np.float32)
+    W[0, 1] = -np.inf
+    W[1, 2] = np.nan
+    key = O.block_keys(W, 1, 2, "l1")
+    assert key[0] == np.inf and key[1] == 2.0 and key[2] == 2.0 and np.isnan(key[3])
+
+
+@pytest.mark.parametrize("R,C,k", [(16, 16, 3), (32, 16, 4), (8, 32, 5)])
+def test_l1_selection_keeps_the_largest_l1_mass(R, C, k):
+    """The kept set has the largest total l1 norm of all k-subsets (exact rationals)."""
+    W = rng(14 + R + C + k).standard_normal((64, 64)).astype(np.float32)
+    Nb, Kb = 64 // R, 64 // C
+    mass = [sum(abs(Fraction(float(x))) for x in W[i * R:(i + 1) * R, j * C:(j + 1) * C].ravel())
+            for i in range(Nb) for j in range(Kb)]
+    best = max(sum(mass[b] for b in sub) for sub in itertools.combinations(range(Nb * Kb), k))
+    indptr, indices, _ = O.prune(W, R, C, k=k, norm="l1")
+    kept = [i * Kb + int(indices[p]) for i in range(Nb) for p in range(indptr[i], indptr[i + 1])]
+    assert len(kept) == k and sum(mass[b] for b in kept) == best
+
+
+def test_block_keys_rejects_other_norms():
+    with pytest.raises(ValueError):
+        O.block_keys(np.ones((4, 4), np.float32), 2, 2, "l0")
+
+
+# ------------------------------------------------------------------ per-row balanced selection
+
+
+@pytest.mark.parametrize("N,K,R,C,d,k", [
+    (768, 768, 32, 1, 0.1, 24 * 77),     # k_row = floor(76.8 + 0.5) = 77
+    (768, 768, 1, 1, 0.2, 768 * 154),    # floor(153.6 + 0.5) = 154
+    (2304, 768, 16, 16, 0.05, 144 * 2),  # floor(2.4 + 0.5) = 2
+    (64, 64, 8, 8, 0.0, 0), (64, 64, 8, 8, 1.0, 64),
+    (96, 40, 3, 5, 0.4, 32 * 3),         # floor(3.2 + 0.5) = 3
+])
+def test_per_row_count_closed_form(N, K, R, C, d, k):
+    assert O.prune_count(N, K, R, C, d, per_row=True) == k
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_per_row_matches_brute_force(seed):
+    """In every row, a block is kept iff fewer than k_row blocks of that row beat it."""
+    g = rng(200 + seed)
+    Nb, Kb = int(g.integers(1, 7)), int(g.integers(1, 12))
+    key = g.integers(0, 5, size=Nb * Kb).astype(np.float64) * 0.5
+    if seed % 2:
+        key[g.integers(0, Nb * Kb)] = np.inf
+        key[g.integers(0, Nb * Kb)] = np.nan
+    for k_row in sorted({0, 1, Kb // 2, Kb}):
+        m = O.select_topk_rows(key, Nb, Kb, k_row).reshape(Nb, Kb)
+        for i in range(Nb):
+            row = key[i * Kb:(i + 1) * Kb]
+            assert np.array_equal(m[i], _brute_force_mask(row, k_row))
+
+
+@pytest.mark.parametrize("norm", ["l2", "l1"])
+def test_per_row_keeps_equal_counts_and_is_the_row_projection(norm):
+    """Every row keeps k_row blocks; for l2 the kept set minimises ||W - W*M||_F^2 over all
+    masks with k_row blocks in each row (exact rationals, all combinations)."""
+    W = rng(15).standard_normal((48, 64)).astype(np.float32)
+    R, C, k_row = 16, 16, 2
+    Nb, Kb = 3, 4
+    indptr, indices, data = O.prune(W, R, C, k=Nb * k_row, norm=norm, per_row=True)
+    assert np.diff(indptr).tolist() == [k_row] * Nb
+    if norm == "l2":
+        energy = [[sum(Fraction(float(x)) ** 2 for x in W[i * R:(i + 1) * R, j * C:(j + 1) * C].ravel())
+                   for j in range(Kb)] for i in range(Nb)]
+        best = sum(min(sum(energy[i]) - sum(energy[i][j] for j in sub)
+                       for sub in itertools.combinations(range(Kb), k_row)) for i in range(Nb))
+        got = sum(sum(energy[i]) - sum(energy[i][int(j)] for j in indices[indptr[i]:indptr[i + 1]])
+                  for i in range(Nb))
+        assert got == best
+
+
+def test_per_row_ties_keep_lowest_columns():
+    key = np.zeros(12)
+    m = O.select_topk_rows(key, 3, 4, 2).reshape(3, 4)
+    assert all(np.nonzero(m[i])[0].tolist() == [0, 1] for i in range(3))
+
+
+def test_per_row_rejects_uneven_k():
+    W = np.ones((64, 64), np.float32)
+    with pytest.raises(ValueError):
+        O.prune(W, 32, 32, k=3, per_row=True)
 
 
 # --------------------------------------------------------------------- BSR build and to_dense
