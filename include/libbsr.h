@@ -113,6 +113,49 @@ LIBBSR_API bsr_status bsr_prune_from_dense(const float *W, int64_t N, int64_t K,
                                 float *data, int64_t capacity_blocks, void *workspace,
                                 size_t ws_bytes, void *stream);
 
+/* Pruning variants for the _ex entry points (Sec. 2.1). */
+typedef enum {
+    BSR_NORM_L2 = 0,  /* block key = sum of w^2 (the l2 group norm, squared)                  */
+    BSR_NORM_L1 = 1   /* block key = sum of |w| (the l1 norm, p = 1 in Eq. 1 and Eq. 2)       */
+} bsr_norm;
+typedef enum {
+    BSR_SELECT_GLOBAL = 0,  /* keep the k best blocks of the whole matrix (Eq. 2, tau = k)     */
+    BSR_SELECT_PER_ROW = 1  /* keep the k / Nb best blocks of every block-row (Eq. 2 applied to
+                               each block-row, tau = k / Nb): every row keeps as many blocks   */
+} bsr_select;
+typedef struct {
+    int32_t norm;    /* a bsr_norm value   */
+    int32_t select;  /* a bsr_select value */
+} bsr_prune_options_t;
+
+/*
+ * bsr_prune_count for a pruning variant: with BSR_SELECT_PER_ROW, k = Nb * k_row where
+ * k_row = floor(density * Kb + 0.5) computed in double, clamped to [0, Kb]; otherwise as
+ * bsr_prune_count.  opts may be NULL (l2, global).  Host only.  Errors: those of
+ * bsr_prune_count, and BSR_ERR_ARG for an unknown norm or selection.
+ */
+LIBBSR_API bsr_status bsr_prune_count_ex(int64_t N, int64_t K, int32_t R, int32_t C,
+                                         double density, const bsr_prune_options_t *opts,
+                                         int64_t *k);
+
+/*
+ * bsr_prune_from_dense with a choice of block norm and selection (Sec. 2.1):
+ *   BSR_NORM_L1: key(i, j) = sum of |w| over the block, in fp64, summed row r outer, column c
+ *   inner from +0.0 (|w| is exact in fp64, so the key is bit-identical to a sequential CPU sum;
+ *   a NaN key ranks above +inf).  BSR_NORM_L2 is bsr_prune_from_dense's key.
+ *   BSR_SELECT_PER_ROW: every block-row keeps its k / Nb blocks that come first in the order
+ *   (key descending, block column ascending); k must be a multiple of Nb, and then
+ *   indptr[i] = i * (k / Nb).
+ * Arguments, outputs, workspace and errors as bsr_prune_from_dense, plus BSR_ERR_ARG for an
+ * unknown norm or selection or (per-row) a k that is not a multiple of Nb.  opts may be NULL.
+ */
+LIBBSR_API bsr_status bsr_prune_from_dense_ex(const float *W, int64_t N, int64_t K, int64_t ldw,
+                                              int32_t R, int32_t C, int64_t k,
+                                              int32_t *indptr, int32_t *indices, float *data,
+                                              int64_t capacity_blocks, void *workspace,
+                                              size_t ws_bytes, const bsr_prune_options_t *opts,
+                                              void *stream);
+
 /*
  * The BSR product (Sec. 2.2; BERT attention projections, Sec. 2.3):
  *   Y[t][n] = bias[n] + sum over stored blocks p of block-row i = floor(n / R), sum over c < C of

@@ -21,9 +21,12 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
           8: "BSR_ERR_ARCH", 9: "BSR_ERR_UNSUPPORTED"}
 
 # The C ABI's exported entry points (the tests check this list against include/libbsr.h).
-EXPORTS = ["bsr_prune_count", "bsr_prune_workspace_bytes", "bsr_prune_from_dense", "bsr_spmm",
-           "bsr_spmm_ex", "bsr_spmm_batched", "bsr_to_dense", "bsr_cast_f32_bf16",
-           "bsr_status_str", "bsr_last_hip_error"]
+EXPORTS = ["bsr_prune_count", "bsr_prune_count_ex", "bsr_prune_workspace_bytes",
+           "bsr_prune_from_dense", "bsr_prune_from_dense_ex", "bsr_spmm", "bsr_spmm_ex",
+           "bsr_spmm_batched", "bsr_to_dense", "bsr_cast_f32_bf16", "bsr_status_str",
+           "bsr_last_hip_error"]
+NORM_L2, NORM_L1 = 0, 1
+SELECT_GLOBAL, SELECT_PER_ROW = 0, 1
 KERNEL_AUTO, KERNEL_GENERIC, KERNEL_TILED, KERNEL_VALU = 0, 1, 2, 3
 
 
@@ -40,6 +43,10 @@ class BSRError(RuntimeError):
 class bsr_spmm_options_t(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_int32), ("slices", ctypes.c_int32),
                 ("start_event", ctypes.c_void_p), ("stop_event", ctypes.c_void_p)]
+
+
+class bsr_prune_options_t(ctypes.Structure):
+    _fields_ = [("norm", ctypes.c_int32), ("select", ctypes.c_int32)]
 
 
 class bsr_matrix_t(ctypes.Structure):
@@ -70,6 +77,13 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_prune_count.argtypes = [i64, i64, i32, i32, ctypes.c_double,
                                         ctypes.POINTER(i64)]
         lib.bsr_prune_count.restype = st
+        lib.bsr_prune_count_ex.argtypes = [i64, i64, i32, i32, ctypes.c_double,
+                                           ctypes.POINTER(bsr_prune_options_t),
+                                           ctypes.POINTER(i64)]
+        lib.bsr_prune_count_ex.restype = st
+        lib.bsr_prune_from_dense_ex.argtypes = [p, i64, i64, i64, i32, i32, i64, p, p, p, i64,
+                                                p, sz, ctypes.POINTER(bsr_prune_options_t), p]
+        lib.bsr_prune_from_dense_ex.restype = st
         lib.bsr_prune_workspace_bytes.argtypes = [i64, i64, i32, i32]
         lib.bsr_prune_workspace_bytes.restype = sz
         lib.bsr_prune_from_dense.argtypes = [p, i64, i64, i64, i32, i32, i64, p, p, p, i64, p,
@@ -162,10 +176,22 @@ class BSRMatrix:
                          data, self.nnzb)
 
 
-def bsr_prune_count(N: int, K: int, R: int, C: int, density: float) -> int:
+def _prune_opts(norm: str, per_row: bool) -> bsr_prune_options_t:
+    if norm not in ("l2", "l1"):
+        raise ValueError("norm must be 'l2' or 'l1'")
+    return bsr_prune_options_t(NORM_L1 if norm == "l1" else NORM_L2,
+                               SELECT_PER_ROW if per_row else SELECT_GLOBAL)
+
+
+def bsr_prune_count(N: int, K: int, R: int, C: int, density: float, per_row: bool = False) -> int:
     k = ctypes.c_int64(0)
-    _check(_lib().bsr_prune_count(N, K, R, C, float(density), ctypes.byref(k)),
-           "bsr_prune_count")
+    if per_row:
+        opts = _prune_opts("l2", True)
+        _check(_lib().bsr_prune_count_ex(N, K, R, C, float(density), ctypes.byref(opts),
+                                         ctypes.byref(k)), "bsr_prune_count_ex")
+    else:
+        _check(_lib().bsr_prune_count(N, K, R, C, float(density), ctypes.byref(k)),
+               "bsr_prune_count")
     return k.value
 
 
@@ -175,15 +201,19 @@ def bsr_prune_workspace_bytes(N: int, K: int, R: int, C: int) -> int:
 
 def bsr_prune_from_dense(W: torch.Tensor, R: int, C: int, k: int | None = None,
                          density: float | None = None, workspace: torch.Tensor | None = None,
-                         stream=None) -> BSRMatrix:
-    """Prune dense fp32 W (device, [N, K]) to BSR with R x C blocks, keeping k blocks."""
+                         stream=None, norm: str = "l2", per_row: bool = False) -> BSRMatrix:
+    """Prune dense fp32 W (device, [N, K]) to BSR with R x C blocks, keeping k blocks.
+
+    norm "l2" (default) or "l1" selects the block key; per_row keeps k / Nb blocks in every
+    block-row (bsr_prune_from_dense_ex); the defaults call bsr_prune_from_dense."""
     _require_cuda(W, "W", torch.float32)
     N, K = W.shape
     ldw = _pitch(W, "W")
     if (k is None) == (density is None):
         raise ValueError("give exactly one of k and density")
+    opts = _prune_opts(norm, per_row)
     if k is None:
-        k = bsr_prune_count(N, K, R, C, density)
+        k = bsr_prune_count(N, K, R, C, density, per_row=per_row)
     dev = W.device
     Nb = N // R if R > 0 and N % R == 0 else 0
     indptr = torch.empty(Nb + 1, dtype=torch.int32, device=dev)
@@ -192,11 +222,18 @@ def bsr_prune_from_dense(W: torch.Tensor, R: int, C: int, k: int | None = None,
     ws_bytes = bsr_prune_workspace_bytes(N, K, R, C)
     if workspace is None:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
-    _check(_lib().bsr_prune_from_dense(_ptr(W), N, K, ldw, R, C, k, _ptr(indptr),
-                                       _ptr(indices), _ptr(data), max(k, 1), _ptr(workspace),
-                                       workspace.numel() * workspace.element_size(),
-                                       _stream(stream)),
-           "bsr_prune_from_dense")
+    ws_len = workspace.numel() * workspace.element_size()
+    if norm == "l2" and not per_row:
+        _check(_lib().bsr_prune_from_dense(_ptr(W), N, K, ldw, R, C, k, _ptr(indptr),
+                                           _ptr(indices), _ptr(data), max(k, 1), _ptr(workspace),
+                                           ws_len, _stream(stream)),
+               "bsr_prune_from_dense")
+    else:
+        _check(_lib().bsr_prune_from_dense_ex(_ptr(W), N, K, ldw, R, C, k, _ptr(indptr),
+                                              _ptr(indices), _ptr(data), max(k, 1),
+                                              _ptr(workspace), ws_len, ctypes.byref(opts),
+                                              _stream(stream)),
+               "bsr_prune_from_dense_ex")
     return BSRMatrix(N, K, R, C, indptr, indices, data, k)
 
 

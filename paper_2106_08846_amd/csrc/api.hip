@@ -98,7 +98,23 @@ bsr_status bsr_prune_from_dense(const float *W, int64_t N, int64_t K, int64_t ld
                                     capacity_blocks, workspace, ws_bytes);
     if (s != BSR_OK) return s;
     if ((s = bsr::ensure_device()) != BSR_OK) return s;
-    return bsr::launch_prune(W, N, K, ldw, R, C, k, indptr, indices, data, workspace, stream);
+    return bsr::launch_prune(W, N, K, ldw, R, C, k, indptr, indices, data, workspace,
+                             BSR_NORM_L2, BSR_SELECT_GLOBAL, stream);
+}
+
+bsr_status bsr_prune_from_dense_ex(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R,
+                                   int32_t C, int64_t k, int32_t *indptr, int32_t *indices,
+                                   float *data, int64_t capacity_blocks, void *workspace,
+                                   size_t ws_bytes, const bsr_prune_options_t *opts,
+                                   void *stream) {
+    bsr_status s = bsr::check_prune(W, N, K, ldw, R, C, k, indptr, indices, data,
+                                    capacity_blocks, workspace, ws_bytes);
+    if (s != BSR_OK) return s;
+    if ((s = bsr::check_prune_options(opts, N, R, k)) != BSR_OK) return s;
+    if ((s = bsr::ensure_device()) != BSR_OK) return s;
+    return bsr::launch_prune(W, N, K, ldw, R, C, k, indptr, indices, data, workspace,
+                             opts ? opts->norm : BSR_NORM_L2,
+                             opts ? opts->select : BSR_SELECT_GLOBAL, stream);
 }
 
 bsr_status bsr_spmm_ex(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,

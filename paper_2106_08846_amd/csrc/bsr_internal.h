@@ -22,6 +22,8 @@ bsr_status check_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_
                        int64_t k, const int32_t *indptr, const int32_t *indices,
                        const float *data, int64_t capacity_blocks, const void *workspace,
                        size_t ws_bytes);
+// Options of the _ex pruning entry point (after check_prune: N, R valid, k in [0, nb]).
+bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32_t R, int64_t k);
 bsr_status check_matrix(const bsr_matrix_t *W);
 bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const bsr_matrix_t *W,
                       const float *Y, int64_t ldy);
@@ -36,7 +38,7 @@ size_t device_lds_per_block();
 
 bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,
                         int64_t k, int32_t *indptr, int32_t *indices, float *data,
-                        void *workspace, void *stream);
+                        void *workspace, int norm, int select, void *stream);
 bsr_status launch_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *stream);
 bsr_status launch_cast(const float *src, uint16_t *dst, int64_t n, void *stream);
 // Optional event pair recorded at a product kernel's start and end (hipExtLaunchKernel).

@@ -49,6 +49,16 @@ bsr_status check_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_
     return BSR_OK;
 }
 
+bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32_t R,
+                               int64_t k) {
+    if (!opts) return BSR_OK;
+    if (opts->norm != BSR_NORM_L2 && opts->norm != BSR_NORM_L1) return BSR_ERR_ARG;
+    if (opts->select != BSR_SELECT_GLOBAL && opts->select != BSR_SELECT_PER_ROW)
+        return BSR_ERR_ARG;
+    if (opts->select == BSR_SELECT_PER_ROW && k % (N / R) != 0) return BSR_ERR_ARG;
+    return BSR_OK;
+}
+
 bsr_status check_matrix(const bsr_matrix_t *W) {
     if (!W) return BSR_ERR_NULL;
     if (W->dtype != BSR_F32 && W->dtype != BSR_BF16) return BSR_ERR_ARG;
@@ -110,6 +120,25 @@ bsr_status bsr_prune_count(int64_t N, int64_t K, int32_t R, int32_t C, double de
     if (kk < 0) kk = 0;
     if (kk > nb) kk = nb;
     *k = kk;
+    return BSR_OK;
+}
+
+bsr_status bsr_prune_count_ex(int64_t N, int64_t K, int32_t R, int32_t C, double density,
+                              const bsr_prune_options_t *opts, int64_t *k) {
+    const int32_t norm = opts ? opts->norm : BSR_NORM_L2;
+    const int32_t select = opts ? opts->select : BSR_SELECT_GLOBAL;
+    if (norm != BSR_NORM_L2 && norm != BSR_NORM_L1) return BSR_ERR_ARG;
+    if (select != BSR_SELECT_GLOBAL && select != BSR_SELECT_PER_ROW) return BSR_ERR_ARG;
+    if (select == BSR_SELECT_GLOBAL) return bsr_prune_count(N, K, R, C, density, k);
+    if (!k) return BSR_ERR_NULL;
+    if (!tiles(N, K, R, C)) return BSR_ERR_SHAPE;
+    if (!(density >= 0.0 && density <= 1.0)) return BSR_ERR_ARG;
+    const int64_t Nb = N / R, Kb = K / C;
+    if (Nb > kMaxBlocks / Kb) return BSR_ERR_UNSUPPORTED;
+    int64_t kr = int64_t(std::floor(density * double(Kb) + 0.5));
+    if (kr < 0) kr = 0;
+    if (kr > Kb) kr = Kb;
+    *k = Nb * kr;
     return BSR_OK;
 }
 

@@ -185,3 +185,53 @@ def test_spmm_batched_errors(L, lib):
     assert lib.bsr_spmm_batched(empty, 2, None, None) == 0     # nothing to launch
     one_event = L.bsr_spmm_options_t(0, 0, FAKE, None)
     assert lib.bsr_spmm_batched(empty, 2, ctypes.byref(one_event), None) == 3
+
+
+# ------------------------------------------------------------------ pruning variants (_ex calls)
+
+
+@pytest.mark.parametrize("N,K,R,C,d", [(768, 768, 32, 1, 0.1), (768, 768, 1, 1, 0.2),
+                                       (2304, 768, 16, 16, 0.05), (96, 40, 3, 5, 0.4),
+                                       (64, 64, 8, 8, 0.0), (64, 64, 8, 8, 1.0)])
+@pytest.mark.parametrize("per_row", [False, True])
+def test_prune_count_ex_matches_oracle(L, N, K, R, C, d, per_row):
+    assert L.bsr_prune_count(N, K, R, C, d, per_row=per_row) == O.prune_count(
+        N, K, R, C, d, per_row=per_row)
+
+
+def test_prune_count_ex_errors(L, lib):
+    k = ctypes.c_int64(-1)
+    for norm, sel in [(2, 0), (-1, 0), (0, 2), (0, -1)]:
+        opts = L.bsr_prune_options_t(norm, sel)
+        assert lib.bsr_prune_count_ex(64, 64, 8, 8, ctypes.c_double(0.5), ctypes.byref(opts),
+                                      ctypes.byref(k)) == 3
+    opts = L.bsr_prune_options_t(1, 1)
+    assert lib.bsr_prune_count_ex(64, 64, 7, 8, ctypes.c_double(0.5), ctypes.byref(opts),
+                                  ctypes.byref(k)) == 2
+    assert lib.bsr_prune_count_ex(64, 64, 8, 8, ctypes.c_double(1.5), ctypes.byref(opts),
+                                  ctypes.byref(k)) == 3
+    assert lib.bsr_prune_count_ex(64, 64, 8, 8, ctypes.c_double(0.5), ctypes.byref(opts),
+                                  None) == 1
+    assert k.value == -1
+    assert lib.bsr_prune_count_ex(64, 64, 8, 8, ctypes.c_double(0.5), None, ctypes.byref(k)) == 0
+    assert k.value == 32
+
+
+def _prune_ex(L, lib, norm=0, sel=0, k=6, **kw):
+    opts = L.bsr_prune_options_t(norm, sel)
+    a = dict(W=FAKE, N=64, K=64, ldw=64, R=8, C=8, indptr=FAKE, indices=FAKE, data=FAKE, cap=64,
+             ws=FAKE, ws_bytes=1 << 20)
+    a.update(kw)
+    return lib.bsr_prune_from_dense_ex(a["W"], a["N"], a["K"], a["ldw"], a["R"], a["C"], k,
+                                       a["indptr"], a["indices"], a["data"], a["cap"], a["ws"],
+                                       a["ws_bytes"], ctypes.byref(opts), None)
+
+
+@pytest.mark.parametrize("norm,sel,k,kw,status", [
+    (2, 0, 6, {}, 3), (0, 5, 6, {}, 3),          # unknown norm / selection
+    (0, 1, 6, {}, 3), (1, 1, 9, {}, 3),          # per-row k not a multiple of Nb = 8
+    (0, 1, 8, {"W": None}, 1), (1, 0, 6, {"R": 7}, 2), (0, 1, 72, {}, 3),
+    (1, 1, 16, {"cap": 15}, 5), (1, 1, 16, {"ws": None}, 6),
+])
+def test_prune_ex_errors(L, lib, norm, sel, k, kw, status):
+    assert _prune_ex(L, lib, norm, sel, k, **kw) == status
