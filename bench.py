@@ -47,7 +47,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="bert_base_attn",
                     help="bert_base_attn | single_768 | sweep:RxC | "
-                         "fused_qkv:RxC:density[:bf16] | bert_large:RxC")
+                         "fused_qkv:RxC:density[:bf16] | bert_large:RxC | "
+                         "attn_block[:RxC[:density[:batch[:seq]]]]")
     ap.add_argument("--slices", type=int, default=0,
                     help="block-row slices per token tile (0: the library's choice)")
     ap.add_argument("--graph", action="store_true",
@@ -137,6 +138,8 @@ def main() -> int:
         return 1
     if args.calibrate_copy:
         return calibrate_copy(args)
+    if args.workload.startswith("attn_block"):
+        return bench_attention_block(args)
     dev = torch.device("cuda:0")
     wl = build_workload(args.workload)
     bf16 = wl.bf16
@@ -284,6 +287,81 @@ def main() -> int:
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, calls, args.cpu_seconds)
 
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def bench_attention_block(args) -> int:
+    """The BERT-base attention block on pruned weights: Q/K/V BSR products (one launch),
+    scaled dot-product attention (bsr_attention), the O BSR product; beside it the same block
+    with dense hipBLASLt GEMMs on the unpruned weights and the same attention kernel.
+
+    --workload attn_block[:RxC[:density[:batch[:seq]]]], default 32x1, 0.1, 1 x 128 tokens."""
+    import torch
+    from paper_2106_08846_amd import bsr as B
+    from paper_2106_08846_amd import workloads as G
+
+    parts = args.workload.split(":")
+    R, C = (int(v) for v in parts[1].split("x")) if len(parts) > 1 else (32, 1)
+    density = float(parts[2]) if len(parts) > 2 else 0.1
+    batch = int(parts[3]) if len(parts) > 3 else 1
+    seq = int(parts[4]) if len(parts) > 4 else 128
+    heads = 12
+    dev = torch.device("cuda:0")
+    wl = G.bert_base_attention(R, C, density, tokens=batch * seq)
+    X = torch.from_numpy(wl.X[0]).to(dev)
+    mats, biases, dense = [], [], []
+    for p in wl.projections:
+        Wd = torch.from_numpy(p.W).to(dev)
+        mats.append(B.bsr_prune_from_dense(Wd, R, C, k=B.bsr_prune_count(768, 768, R, C, density)))
+        biases.append(torch.from_numpy(p.bias).to(dev))
+        dense.append(Wd)
+    call = B.AttentionBlockCall(X, mats[0], biases[0], mats[1], biases[1], mats[2], biases[2],
+                                mats[3], biases[3], batch, seq, heads)
+    T = batch * seq
+    Wqkv = torch.cat(dense[:3], 0).contiguous()
+    bqkv = torch.cat(biases[:3], 0).contiguous()
+    qkv = torch.empty((T, 3 * 768), device=dev)
+    ctx = torch.empty((T, 768), device=dev)
+    Yd = torch.empty((T, 768), device=dev)
+
+    def dense_block():
+        torch.addmm(bqkv, X, Wqkv.t(), out=qkv)
+        B.bsr_attention(qkv[:, :768], qkv[:, 768:1536], qkv[:, 1536:], batch, seq, heads, O=ctx)
+        torch.addmm(biases[3], ctx, dense[3].t(), out=Yd)
+
+    # Time per block: `n` blocks issued back to back (prepared calls, one foreign call per
+    # kernel), between two events on the current stream; the launch gaps are included.
+    def timed(fn, n):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n * 1e3
+
+    sparse_us = timed(call, args.steps)
+    dense_us = timed(dense_block, args.steps)
+    qkv_us = timed(call.qkv, args.steps)
+    attn_us = timed(call.attention, args.steps)
+    out_us = timed(call.out, args.steps)
+    flops = sum(2.0 * m.nnzb * m.R * m.C * T for m in mats) + 4.0 * batch * heads * seq * seq * 64
+    out = {
+        "metric": "BERT attention block latency (BSR Q/K/V/O products + attention)",
+        "value": sparse_us, "unit": "us", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": sparse_us / 1e3, "higher_is_better": False,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"attn_block_bert_base_{R}x{C}_d{int(round(density * 100))}"
+                               f"_b{batch}_s{seq}", "tokens": T, "heads": heads,
+                   "block": f"{R}x{C}", "density": density},
+        "dense_block_us": dense_us, "sparse_over_dense": sparse_us / dense_us,
+        "breakdown_us": {"qkv_products": qkv_us, "attention": attn_us, "o_product": out_us},
+        "effective_gflops": flops / (sparse_us * 1e-6) / 1e9,
+    }
     print(json.dumps(out), flush=True)
     return 0
 

@@ -241,6 +241,25 @@ LIBBSR_API bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_i
                                        const bsr_spmm_options_t *opts, void *stream);
 
 /*
+ * Scaled dot-product attention of the BERT attention block (Sec. 2.3 prunes BERT's attention
+ * weights; its Q, K, V and output projections are the BSR products above):
+ *   O[b*seq + s][h*64 + d] = sum_j p_j V[b*seq + j][h*64 + d],
+ *   p_j = softmax over j < seq of scale * sum_e Q[b*seq + s][h*64 + e] * K[b*seq + j][h*64 + e].
+ * Rows are tokens (batch-major), head h owns columns h*64 .. h*64 + 63; no mask.  fp32 inputs,
+ * fp32 arithmetic (online softmax with expf), fp32 output.
+ * Q, K, V: device fp32 with row pitches ldq, ldk, ldv >= heads * 64, 16-byte aligned bases and
+ *   pitches that are multiples of 4.  O: device fp32, row pitch ldo >= heads * 64; it must not
+ *   overlap Q, K or V.  head_dim must be 64.  batch = 0 or seq = 0 is a no-op.
+ * Errors: BSR_ERR_NULL, BSR_ERR_SHAPE (negative sizes, heads < 1, a pitch below heads * 64),
+ *   BSR_ERR_ARG (scale not finite), BSR_ERR_UNSUPPORTED (head_dim != 64, misaligned inputs,
+ *   batch or heads above 65535), BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
+                                    const float *V, int64_t ldv, float *O, int64_t ldo,
+                                    int32_t batch, int32_t seq, int32_t heads, int32_t head_dim,
+                                    float scale, void *stream);
+
+/*
  * Expand an fp32 BSR matrix to dense (Sec. 2.2 layout): out[n][k] = the stored element covering
  * (n, k), or +0.0 where no block is stored.  out: device fp32, N x K with row pitch ldo >= K.
  * Errors: BSR_ERR_NULL, BSR_ERR_SHAPE, BSR_ERR_DTYPE (bf16 data), BSR_ERR_UNSUPPORTED,

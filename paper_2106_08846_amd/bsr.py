@@ -23,8 +23,8 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 # The C ABI's exported entry points (the tests check this list against include/libbsr.h).
 EXPORTS = ["bsr_prune_count", "bsr_prune_count_ex", "bsr_prune_workspace_bytes",
            "bsr_prune_from_dense", "bsr_prune_from_dense_ex", "bsr_spmm", "bsr_spmm_ex",
-           "bsr_spmm_batched", "bsr_to_dense", "bsr_cast_f32_bf16", "bsr_status_str",
-           "bsr_last_hip_error"]
+           "bsr_spmm_batched", "bsr_attention", "bsr_to_dense", "bsr_cast_f32_bf16",
+           "bsr_status_str", "bsr_last_hip_error"]
 NORM_L2, NORM_L1 = 0, 1
 SELECT_GLOBAL, SELECT_PER_ROW = 0, 1
 KERNEL_AUTO, KERNEL_GENERIC, KERNEL_TILED, KERNEL_VALU = 0, 1, 2, 3
@@ -100,6 +100,9 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_spmm_batched.restype = st
         lib.bsr_to_dense.argtypes = [ctypes.POINTER(bsr_matrix_t), p, i64, p]
         lib.bsr_to_dense.restype = st
+        lib.bsr_attention.argtypes = [p, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32,
+                                      ctypes.c_float, p]
+        lib.bsr_attention.restype = st
         lib.bsr_cast_f32_bf16.argtypes = [p, p, i64, p]
         lib.bsr_cast_f32_bf16.restype = st
         lib.bsr_status_str.argtypes = [ctypes.c_int]
@@ -381,6 +384,64 @@ def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> 
     _check(_lib().bsr_to_dense(ctypes.byref(m), _ptr(out), _pitch(out, "out"), _stream(stream)),
            "bsr_to_dense")
     return out
+
+
+def bsr_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, batch: int, seq: int,
+                  heads: int, O: torch.Tensor | None = None, scale: float | None = None,
+                  stream=None) -> torch.Tensor:
+    """Scaled dot-product attention per (sequence, head) of [batch*seq, heads*64] fp32 tensors
+    (row pitch from the tensors' strides); returns O."""
+    head_dim = 64
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _require_cuda(t, n, torch.float32)
+    if O is None:
+        O = torch.empty((batch * seq, heads * head_dim), dtype=torch.float32, device=Q.device)
+    _require_cuda(O, "O", torch.float32)
+    if scale is None:
+        scale = head_dim ** -0.5
+    _check(_lib().bsr_attention(_ptr(Q), _pitch(Q, "Q"), _ptr(K), _pitch(K, "K"), _ptr(V),
+                                _pitch(V, "V"), _ptr(O), _pitch(O, "O"), batch, seq, heads,
+                                head_dim, float(scale), _stream(stream)),
+           "bsr_attention")
+    return O
+
+
+class AttentionBlockCall:
+    """The BERT attention block on pruned weights, prepared once and re-issued:
+    Q, K, V = three BSR products of X (one bsr_spmm_batched launch), ctx = bsr_attention,
+    Y = the O BSR product of ctx.  Buffers are allocated here, on construction."""
+
+    def __init__(self, X: torch.Tensor, Wq: "BSRMatrix", bq, Wk: "BSRMatrix", bk,
+                 Wv: "BSRMatrix", bv, Wo: "BSRMatrix", bo, batch: int, seq: int, heads: int,
+                 kernel: int | None = None):
+        T = batch * seq
+        dev = X.device
+        self.batch, self.seq, self.heads = batch, seq, heads
+        self.Q = torch.empty((T, Wq.n_rows), dtype=torch.float32, device=dev)
+        self.K = torch.empty((T, Wk.n_rows), dtype=torch.float32, device=dev)
+        self.V = torch.empty((T, Wv.n_rows), dtype=torch.float32, device=dev)
+        self.ctx = torch.empty((T, heads * 64), dtype=torch.float32, device=dev)
+        self.Y = torch.empty((T, Wo.n_rows), dtype=torch.float32, device=dev)
+        self.qkv = SpmmBatchCall([(X, Wq, bq, self.Q), (X, Wk, bk, self.K), (X, Wv, bv, self.V)],
+                                 kernel=kernel)
+        self.out = SpmmCall(self.ctx, Wo, bo, self.Y, kernel=kernel)
+        bsr_attention(self.Q, self.K, self.V, batch, seq, heads, O=self.ctx)   # checks once
+        lib = _lib()
+        args = (_ptr(self.Q), _pitch(self.Q, "Q"), _ptr(self.K), _pitch(self.K, "K"),
+                _ptr(self.V), _pitch(self.V, "V"), _ptr(self.ctx), _pitch(self.ctx, "O"),
+                batch, seq, heads, 64, ctypes.c_float(64 ** -0.5))
+        self._attn = lambda st: lib.bsr_attention(*args, st)
+
+    def attention(self, stream=None) -> torch.Tensor:
+        st = self._attn(_stream(stream))
+        if st != 0:
+            _check(st, "bsr_attention")
+        return self.ctx
+
+    def __call__(self, stream=None) -> torch.Tensor:
+        self.qkv(stream)
+        self.attention(stream)
+        return self.out(stream)
 
 
 def bsr_cast_f32_bf16(src: torch.Tensor, dst: torch.Tensor | None = None,

@@ -249,6 +249,19 @@ bsr_status bsr_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *st
     return bsr::launch_to_dense(W, out, ldo, stream);
 }
 
+bsr_status bsr_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
+                         const float *V, int64_t ldv, float *O, int64_t ldo, int32_t batch,
+                         int32_t seq, int32_t heads, int32_t head_dim, float scale,
+                         void *stream) {
+    bsr_status s = bsr::check_attention(Q, ldq, K, ldk, V, ldv, O, ldo, batch, seq, heads,
+                                        head_dim, scale);
+    if (s != BSR_OK) return s;
+    if (int64_t(batch) * seq == 0) return BSR_OK;
+    if ((s = bsr::ensure_device()) != BSR_OK) return s;
+    return bsr::launch_attention(Q, ldq, K, ldk, V, ldv, O, ldo, batch, seq, heads, scale,
+                                 stream);
+}
+
 bsr_status bsr_cast_f32_bf16(const float *src, uint16_t *dst, int64_t n, void *stream) {
     bsr_status s = bsr::check_cast(src, dst, n);
     if (s != BSR_OK) return s;

@@ -29,6 +29,10 @@ bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const 
                       const float *Y, int64_t ldy);
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo);
 bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
+bsr_status check_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
+                           const float *V, int64_t ldv, const float *O, int64_t ldo,
+                           int32_t batch, int32_t seq, int32_t heads, int32_t head_dim,
+                           float scale);
 
 // Device-side entry points (implemented in the .hip files).  Arguments are already validated.
 bsr_status ensure_device();  // current device is gfx950; caches its properties
@@ -50,6 +54,10 @@ struct LaunchEvents {
 bsr_status launch_spmm_generic(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W,
                                const float *bias, float *Y, int64_t ldy, void *stream,
                                const LaunchEvents &ev);
+
+bsr_status launch_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
+                            const float *V, int64_t ldv, float *O, int64_t ldo, int batch,
+                            int seq, int heads, float scale, void *stream);
 
 void set_last_hip_error(const char *msg);
 

@@ -3,6 +3,7 @@
 // Every check here runs before anything is enqueued, so a rejected call launches nothing and
 // leaves its outputs untouched.
 #include <cmath>
+#include <cstdint>
 #include <cstring>
 
 #include "bsr_internal.h"
@@ -100,6 +101,27 @@ bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n) {
     if (n < 0) return BSR_ERR_SHAPE;
     if (n > 0 && (!src || !dst)) return BSR_ERR_NULL;
     if (n > kMaxElems) return BSR_ERR_UNSUPPORTED;
+    return BSR_OK;
+}
+
+bsr_status check_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
+                           const float *V, int64_t ldv, const float *O, int64_t ldo,
+                           int32_t batch, int32_t seq, int32_t heads, int32_t head_dim,
+                           float scale) {
+    if (batch < 0 || seq < 0 || heads < 1 || head_dim < 1) return BSR_ERR_SHAPE;
+    const int64_t width = int64_t(heads) * head_dim;
+    if (ldq < width || ldk < width || ldv < width || ldo < width) return BSR_ERR_SHAPE;
+    if (!std::isfinite(scale)) return BSR_ERR_ARG;
+    if (int64_t(batch) * seq == 0) return BSR_OK;
+    if (!Q || !K || !V || !O) return BSR_ERR_NULL;
+    if (head_dim != 64 || batch > 65535 || heads > 65535) return BSR_ERR_UNSUPPORTED;
+    auto aligned = [](const void *p, int64_t ld) {
+        return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 4 == 0;
+    };
+    if (!aligned(Q, ldq) || !aligned(K, ldk) || !aligned(V, ldv)) return BSR_ERR_UNSUPPORTED;
+    const int64_t T = int64_t(batch) * seq;
+    if (T > kMaxElems / ldq || T > kMaxElems / ldk || T > kMaxElems / ldv || T > kMaxElems / ldo)
+        return BSR_ERR_UNSUPPORTED;
     return BSR_OK;
 }
 

@@ -235,3 +235,22 @@ def _prune_ex(L, lib, norm=0, sel=0, k=6, **kw):
 ])
 def test_prune_ex_errors(L, lib, norm, sel, k, kw, status):
     assert _prune_ex(L, lib, norm, sel, k, **kw) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    # (Q, ldq, K, ldk, V, ldv, O, ldo, batch, seq, heads, head_dim, scale)
+    ((None, 128, FAKE, 128, FAKE, 128, FAKE, 128, 1, 4, 2, 64, 0.1), 1),
+    ((FAKE, 128, FAKE, 128, FAKE, 128, None, 128, 1, 4, 2, 64, 0.1), 1),
+    ((FAKE, 127, FAKE, 128, FAKE, 128, FAKE, 128, 1, 4, 2, 64, 0.1), 2),
+    ((FAKE, 128, FAKE, 128, FAKE, 128, FAKE, 100, 1, 4, 2, 64, 0.1), 2),
+    ((FAKE, 128, FAKE, 128, FAKE, 128, FAKE, 128, -1, 4, 2, 64, 0.1), 2),
+    ((FAKE, 128, FAKE, 128, FAKE, 128, FAKE, 128, 1, 4, 0, 64, 0.1), 2),
+    ((FAKE, 128, FAKE, 128, FAKE, 128, FAKE, 128, 1, 4, 2, 64, float("inf")), 3),
+    ((FAKE, 128, FAKE, 128, FAKE, 128, FAKE, 128, 1, 4, 4, 32, 0.1), 9),
+    ((FAKE + 4, 128, FAKE, 128, FAKE, 128, FAKE, 128, 1, 4, 2, 64, 0.1), 9),
+    ((FAKE, 130, FAKE, 128, FAKE, 128, FAKE, 128, 1, 4, 2, 64, 0.1), 9),
+    ((None, 128, None, 128, None, 128, None, 128, 0, 4, 2, 64, 0.1), 0),   # no-op
+    ((None, 128, None, 128, None, 128, None, 128, 3, 0, 2, 64, 0.1), 0),   # no-op
+])
+def test_attention_errors(lib, args, status):
+    assert lib.bsr_attention(*args, None) == status
