@@ -48,7 +48,9 @@ def parse():
     ap.add_argument("--workload", default="bert_base_attn",
                     help="bert_base_attn | single_768 | sweep:RxC | "
                          "fused_qkv:RxC:density[:bf16] | bert_large:RxC | "
-                         "attn_block[:RxC[:density[:batch[:seq]]]]")
+                         "ffn:RxC[:density[:tokens]][:bf16] | "
+                         "attn_block[:RxC[:density[:batch[:seq]]]]; RxC@R2xC2 prunes with "
+                         "R x C blocks and multiplies the matrix re-blocked to R2 x C2")
     ap.add_argument("--slices", type=int, default=0,
                     help="block-row slices per token tile (0: the library's choice)")
     ap.add_argument("--graph", action="store_true",
@@ -73,14 +75,28 @@ def build_workload(spec: str):
         return G.bert_base_attention()
     if kind == "single_768":
         return G.single_768()
-    R, C = (int(v) for v in parts[1].split("x")) if len(parts) > 1 else (32, 1)
+    # A block field "RxC@R2xC2" prunes with R x C blocks and runs the product on the same
+    # matrix re-blocked to R2 x C2 (bsr_reblock).
+    block = parts[1].split("@") if len(parts) > 1 else ["32x1"]
+    R, C = (int(v) for v in block[0].split("x"))
+    fine = tuple(int(v) for v in block[1].split("x")) if len(block) > 1 else None
+    bf16 = parts[-1] == "bf16"
     if kind == "sweep":
-        return G.block_sweep(R, C)
-    if kind == "fused_qkv":
-        return G.fused_qkv(R, C, float(parts[2]), bf16=len(parts) > 3 and parts[3] == "bf16")
-    if kind == "bert_large":
-        return G.bert_large_zipf(R, C)
-    raise SystemExit(f"unknown workload {spec}")
+        wl = G.block_sweep(R, C)
+    elif kind == "fused_qkv":
+        wl = G.fused_qkv(R, C, float(parts[2]), bf16=bf16)
+    elif kind == "bert_large":
+        wl = G.bert_large_zipf(R, C)
+    elif kind == "ffn":
+        density = float(parts[2]) if len(parts) > 2 and parts[2] != "bf16" else 0.1
+        tokens = int(parts[3]) if len(parts) > 3 and parts[3] != "bf16" else 128
+        wl = G.bert_base_ffn(R, C, density, tokens=tokens, bf16=bf16)
+    else:
+        raise SystemExit(f"unknown workload {spec}")
+    if fine is not None:
+        wl.notes["reblock"] = fine
+        wl.name += f"_as_{fine[0]}x{fine[1]}"
+    return wl
 
 
 def kernel_source_hash() -> str:
@@ -157,11 +173,13 @@ def main() -> int:
         M = B.bsr_prune_from_dense(Wd, p.R, p.C, k=k)
         if bf16:
             M = M.to_bf16()
+        if "reblock" in wl.notes:
+            M = B.bsr_reblock(M, *wl.notes["reblock"])
         bias = torch.from_numpy(p.bias).to(dev)
         T = wl.X[p.x_index].shape[0]
         Y = torch.empty((T, N), dtype=torch.float32, device=dev)
-        calls.append(dict(X=Xs[p.x_index], M=M, bias=bias, Y=Y, Wd=Wd, T=T, N=N, K=K, R=p.R,
-                          C=p.C, k=k))
+        calls.append(dict(X=Xs[p.x_index], M=M, bias=bias, Y=Y, Wd=Wd, T=T, N=N, K=K, R=M.R,
+                          C=M.C, k=M.nnzb))
     # The step's products go to bsr_spmm_batched in groups of up to 8 (one kernel launch each:
     # Q, K, V and O of a layer share one launch).
     groups = [calls[i:i + 8] for i in range(0, len(calls), 8)]
@@ -246,7 +264,8 @@ def main() -> int:
                 "frac": gbs / HBM_PEAK_GBS}
     tr = measured_traffic(wl.name)
     roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
-                 "kernel": tiled_kernel_name(calls[0]), "launch_us": launch_ms * 1e3,
+                 "kernel": " + ".join(dict.fromkeys(tiled_kernel_name(c) for c in calls)),
+                 "launch_us": launch_ms * 1e3,
                  "algorithmic_bytes_per_launch": bytes_launch,
                  "flops_per_launch": flops_launch, "arithmetic_intensity": ai,
                  "achieved_gbs": gbs, "achieved_tflops": tfs})
@@ -377,6 +396,12 @@ def tiled_kernel_name(c) -> str:
     bf = c["M"].dtype == 1
     shape = (c["R"], c["C"])
     flag = "true" if bf else "false"
+    # Both tile kernels hold a 32-token X tile, the bias and indptr in the 160 KiB of LDS; a
+    # wider K (the 3072-column FFN input) leaves only the generic kernel.  (An estimate for the
+    # label: the library's plan decides, and the kernel trace shows what ran.)
+    xb = 2 if bf and shape != (16, 1) else 4
+    if 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) > 160 * 1024:
+        return "spmm_generic_kernel via bsr_spmm_batched"
     if shape in TILED_SHAPES:
         return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}> via bsr_spmm_batched"
     if shape in VALU_SHAPES and not (bf and shape == (1, 1)):

@@ -260,6 +260,29 @@ LIBBSR_API bsr_status bsr_attention(const float *Q, int64_t ldq, const float *K,
                                     float scale, void *stream);
 
 /*
+ * The same matrix stored with finer R2 x C2 blocks, R2 a divisor of W->R and C2 of W->C (the
+ * Sec. 2.2 layout at a smaller block size, as SciPy converts a BSR matrix to one).  With
+ * a = R / R2 and b = C / C2, the q-th of the n stored blocks of block-row i (column
+ * j = indices[p]) is cut into a x b pieces; piece (r, s) holds rows r*R2 .. r*R2 + R2 - 1 and
+ * columns s*C2 .. s*C2 + C2 - 1 of the block and is stored
+ *   in fine block-row i*a + r, at position indptr[i]*a*b + r*n*b + q*b + s, column j*b + s,
+ * so indptr_out[i*a + r] = indptr[i]*a*b + r*n*b and every fine block-row keeps its columns
+ * ascending.  Values are copied bit for bit; a piece that is all zeros stays stored.  A matrix
+ * pruned with a large block (64 x 64, 1 x 64 ... 1 x 384, 64 x 1) then runs on the product
+ * kernels of a divisor shape (32 x 32, 1 x 32, 32 x 1) with unchanged results up to the order
+ * of the sums.
+ * Outputs (device, caller-owned, not overlapping W's arrays): indptr_out int32[N/R2 + 1],
+ * indices_out int32[nnzb*a*b], data_out [nnzb*a*b][R2][C2] elements of W's dtype.  The fine
+ * matrix is {N, K, R2, C2, nnzb*a*b, indptr_out, indices_out, data_out, W->dtype}.
+ * Errors: BSR_ERR_NULL, BSR_ERR_ARG (W's dtype or nnzb), BSR_ERR_SHAPE (W's shape, or R2 or C2
+ *   not a positive divisor of R or C), BSR_ERR_UNSUPPORTED (more than 2^31 - 1 fine blocks),
+ *   BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2,
+                                  int32_t *indptr_out, int32_t *indices_out, void *data_out,
+                                  void *stream);
+
+/*
  * Expand an fp32 BSR matrix to dense (Sec. 2.2 layout): out[n][k] = the stored element covering
  * (n, k), or +0.0 where no block is stored.  out: device fp32, N x K with row pitch ldo >= K.
  * Errors: BSR_ERR_NULL, BSR_ERR_SHAPE, BSR_ERR_DTYPE (bf16 data), BSR_ERR_UNSUPPORTED,

@@ -192,6 +192,38 @@ def prune(W: np.ndarray, R: int, C: int, density: float | None = None, k: int | 
     return build_bsr(W, R, C, mask)
 
 
+def reblock(indptr, indices, data, R2: int, C2: int):
+    """The same matrix in finer blocks R2 x C2 (R2 | R, C2 | C): every stored R x C block is cut
+    into (R/R2) x (C/C2) stored blocks.  Values are bit copies; the stored pattern is the
+    original one refined (a zero R2 x C2 piece of a stored block stays stored).
+
+    Sec. 2.2 stores a matrix as data/indices/indptr for one block shape; this is SciPy's
+    conversion of a BSR matrix to a smaller block size, written out: fine block-row i * a + r
+    (a = R/R2, r < a) holds, for each stored block p of block-row i in column order, the pieces
+    s < b = C/C2 with block-column indices[p] * b + s.
+    """
+    data = np.asarray(data)
+    R, C = data.shape[1], data.shape[2]
+    if R2 <= 0 or C2 <= 0 or R % R2 or C % C2:
+        raise ValueError("the new block shape must divide the old one")
+    a, b = R // R2, C // C2
+    indptr = np.asarray(indptr, dtype=np.int64)
+    Nb = indptr.size - 1
+    new_ptr = [0]
+    new_idx: list[int] = []
+    new_data: list[np.ndarray] = []
+    for i in range(Nb):
+        for r in range(a):
+            for p in range(indptr[i], indptr[i + 1]):
+                for s_ in range(b):
+                    new_idx.append(int(indices[p]) * b + s_)
+                    new_data.append(data[p, r * R2:(r + 1) * R2, s_ * C2:(s_ + 1) * C2])
+            new_ptr.append(len(new_idx))
+    out = (np.stack(new_data) if new_data else np.zeros((0, R2, C2), dtype=data.dtype))
+    return (np.asarray(new_ptr, dtype=np.int32), np.asarray(new_idx, dtype=np.int32),
+            out.astype(data.dtype))
+
+
 def to_dense(indptr, indices, data, N: int, K: int) -> np.ndarray:
     """Expand BSR arrays to a dense N x K matrix; positions outside stored blocks are +0.0."""
     data = np.asarray(data)

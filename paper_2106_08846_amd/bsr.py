@@ -23,7 +23,8 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 # The C ABI's exported entry points (the tests check this list against include/libbsr.h).
 EXPORTS = ["bsr_prune_count", "bsr_prune_count_ex", "bsr_prune_workspace_bytes",
            "bsr_prune_from_dense", "bsr_prune_from_dense_ex", "bsr_spmm", "bsr_spmm_ex",
-           "bsr_spmm_batched", "bsr_attention", "bsr_to_dense", "bsr_cast_f32_bf16",
+           "bsr_spmm_batched", "bsr_attention", "bsr_reblock", "bsr_to_dense",
+           "bsr_cast_f32_bf16",
            "bsr_status_str", "bsr_last_hip_error"]
 NORM_L2, NORM_L1 = 0, 1
 SELECT_GLOBAL, SELECT_PER_ROW = 0, 1
@@ -103,6 +104,8 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_attention.argtypes = [p, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32,
                                       ctypes.c_float, p]
         lib.bsr_attention.restype = st
+        lib.bsr_reblock.argtypes = [ctypes.POINTER(bsr_matrix_t), i32, i32, p, p, p, p]
+        lib.bsr_reblock.restype = st
         lib.bsr_cast_f32_bf16.argtypes = [p, p, i64, p]
         lib.bsr_cast_f32_bf16.restype = st
         lib.bsr_status_str.argtypes = [ctypes.c_int]
@@ -384,6 +387,23 @@ def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> 
     _check(_lib().bsr_to_dense(ctypes.byref(m), _ptr(out), _pitch(out, "out"), _stream(stream)),
            "bsr_to_dense")
     return out
+
+
+def bsr_reblock(W: BSRMatrix, R2: int, C2: int, stream=None) -> BSRMatrix:
+    """The same matrix with finer R2 x C2 blocks (R2 | R, C2 | C), in new device tensors."""
+    if R2 <= 0 or C2 <= 0 or W.R % R2 or W.C % C2:
+        pieces, nb2 = 1, 1
+    else:
+        pieces, nb2 = (W.R // R2) * (W.C // C2), W.n_rows // R2
+    n2 = W.nnzb * pieces
+    dev = W.indptr.device
+    indptr = torch.empty(nb2 + 1, dtype=torch.int32, device=dev)
+    indices = torch.empty(max(n2, 1), dtype=torch.int32, device=dev)
+    data = torch.empty((max(n2, 1), max(R2, 1), max(C2, 1)), dtype=W.data.dtype, device=dev)
+    m = W.struct()
+    _check(_lib().bsr_reblock(ctypes.byref(m), R2, C2, _ptr(indptr), _ptr(indices), _ptr(data),
+                              _stream(stream)), "bsr_reblock")
+    return BSRMatrix(W.n_rows, W.n_cols, R2, C2, indptr, indices, data, n2)
 
 
 def bsr_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, batch: int, seq: int,

@@ -262,6 +262,14 @@ bsr_status bsr_attention(const float *Q, int64_t ldq, const float *K, int64_t ld
                                  stream);
 }
 
+bsr_status bsr_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2, int32_t *indptr_out,
+                       int32_t *indices_out, void *data_out, void *stream) {
+    bsr_status s = bsr::check_reblock(W, R2, C2, indptr_out, indices_out, data_out);
+    if (s != BSR_OK) return s;
+    if ((s = bsr::ensure_device()) != BSR_OK) return s;
+    return bsr::launch_reblock(W, R2, C2, indptr_out, indices_out, data_out, stream);
+}
+
 bsr_status bsr_cast_f32_bf16(const float *src, uint16_t *dst, int64_t n, void *stream) {
     bsr_status s = bsr::check_cast(src, dst, n);
     if (s != BSR_OK) return s;

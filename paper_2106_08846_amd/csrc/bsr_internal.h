@@ -29,6 +29,9 @@ bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const 
                       const float *Y, int64_t ldy);
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo);
 bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
+bsr_status check_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2,
+                         const int32_t *indptr_out, const int32_t *indices_out,
+                         const void *data_out);
 bsr_status check_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
                            const float *V, int64_t ldv, const float *O, int64_t ldo,
                            int32_t batch, int32_t seq, int32_t heads, int32_t head_dim,
@@ -45,6 +48,8 @@ bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32
                         void *workspace, int norm, int select, void *stream);
 bsr_status launch_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *stream);
 bsr_status launch_cast(const float *src, uint16_t *dst, int64_t n, void *stream);
+bsr_status launch_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2, int32_t *indptr_out,
+                          int32_t *indices_out, void *data_out, void *stream);
 // Optional event pair recorded at a product kernel's start and end (hipExtLaunchKernel).
 struct LaunchEvents {
     void *start = nullptr;

@@ -97,6 +97,21 @@ bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo) 
     return BSR_OK;
 }
 
+bsr_status check_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2,
+                         const int32_t *indptr_out, const int32_t *indices_out,
+                         const void *data_out) {
+    bsr_status s = check_matrix(W);
+    if (s != BSR_OK) return s;
+    if (R2 <= 0 || C2 <= 0 || W->R % R2 != 0 || W->C % C2 != 0) return BSR_ERR_SHAPE;
+    if (!indptr_out) return BSR_ERR_NULL;
+    if (W->nnzb > 0 && (!indices_out || !data_out)) return BSR_ERR_NULL;
+    const int64_t pieces = int64_t(W->R / R2) * (W->C / C2);
+    const int64_t Nb = W->n_rows / R2, Kb = W->n_cols / C2;
+    if (Nb > kMaxBlocks / Kb) return BSR_ERR_UNSUPPORTED;
+    if (W->nnzb > kMaxBlocks / pieces) return BSR_ERR_UNSUPPORTED;
+    return BSR_OK;
+}
+
 bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n) {
     if (n < 0) return BSR_ERR_SHAPE;
     if (n > 0 && (!src || !dst)) return BSR_ERR_NULL;

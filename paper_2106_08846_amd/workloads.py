@@ -204,3 +204,23 @@ def bert_large_zipf(R: int, C: int, density: float = 0.1, layers: int = 24,
          for l in range(layers)]
     return Workload(f"bert_large_{layers}x4_1024_{R}x{C}_d{int(round(density * 100))}"
                     f"_T{tokens}_zipf", X, projs, notes={"row_counts_by_rank": counts.tolist()})
+
+
+def bert_base_ffn(R: int, C: int, density: float = 0.1, tokens: int = 128, bf16: bool = False,
+                  seed_config: int = 6) -> Workload:
+    """BERT-base feed-forward weights: W1 3072x768 (hidden -> intermediate) and W2 768x3072
+    (intermediate -> hidden), batch 1 x seq `tokens`.
+
+    W2 reads its own activation matrix (tokens x 3072), drawn like X; in a real layer it would
+    be W1's output after GELU, which has the same shape and cost.
+    """
+    W1 = draw_normal(item_seed(seed_config, 0), (3072, 768), W_SIGMA)
+    W2 = draw_normal(item_seed(seed_config, 1), (768, 3072), W_SIGMA)
+    b1 = draw_normal(item_seed(seed_config, 2), (3072,), B_SIGMA)
+    b2 = draw_normal(item_seed(seed_config, 3), (768,), B_SIGMA)
+    X1 = draw_normal(item_seed(seed_config, 4), (tokens, 768), X_SIGMA)
+    X2 = draw_normal(item_seed(seed_config, 5), (tokens, 3072), X_SIGMA)
+    tag = "bf16" if bf16 else "fp32"
+    return Workload(f"bert_base_ffn_3072x768_{R}x{C}_d{int(round(density * 100))}_T{tokens}_{tag}",
+                    [X1, X2], [Projection("W1", W1, b1, R, C, density, x_index=0),
+                               Projection("W2", W2, b2, R, C, density, x_index=1)], bf16=bf16)

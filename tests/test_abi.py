@@ -144,6 +144,20 @@ def test_to_dense_errors(L, lib, mkw, ldo, out, status):
     assert lib.bsr_to_dense(ctypes.byref(m), out, ldo, None) == status
 
 
+@pytest.mark.parametrize("mkw,R2,C2,outs,status", [
+    ({}, 4, 4, (None, FAKE, FAKE), 1), ({}, 4, 4, (FAKE, None, FAKE), 1),
+    ({}, 4, 4, (FAKE, FAKE, None), 1), ({"indptr": None}, 4, 4, (FAKE, FAKE, FAKE), 1),
+    ({}, 3, 4, (FAKE, FAKE, FAKE), 2), ({}, 4, 0, (FAKE, FAKE, FAKE), 2),
+    ({}, 16, 8, (FAKE, FAKE, FAKE), 2), ({}, -8, 8, (FAKE, FAKE, FAKE), 2),
+    ({"R": 7}, 1, 1, (FAKE, FAKE, FAKE), 2), ({"nnzb": 65}, 4, 4, (FAKE, FAKE, FAKE), 3),
+    ({"dtype": 3}, 4, 4, (FAKE, FAKE, FAKE), 3),
+    ({"N": 1 << 20, "K": 1 << 20, "R": 64, "C": 64}, 1, 1, (FAKE, FAKE, FAKE), 9),
+])
+def test_reblock_errors(L, lib, mkw, R2, C2, outs, status):
+    m = _matrix(L, **mkw)
+    assert lib.bsr_reblock(ctypes.byref(m), R2, C2, *outs, None) == status
+
+
 def test_cast_errors(lib):
     assert lib.bsr_cast_f32_bf16(FAKE, FAKE, -1, None) == 2
     assert lib.bsr_cast_f32_bf16(None, FAKE, 4, None) == 1

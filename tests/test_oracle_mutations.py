@@ -67,6 +67,27 @@ def _l1_signed_sum(W, R, C, norm="l2"):
     return key.ravel()
 
 
+def _reblock_pieces_column_major(indptr, indices, data, R2, C2):
+    """Pieces of each stored block listed column-major (s outer) inside a fine row."""
+    ip2, ix2, dt2 = O.__dict__["_orig_reblock"](indptr, indices, data, R2, C2)
+    C = np.asarray(data).shape[2]
+    b = C // C2
+    if b > 1:
+        for i2 in range(len(ip2) - 1):
+            a0, a1 = ip2[i2], ip2[i2 + 1]
+            n = (a1 - a0) // b
+            order = np.arange(a1 - a0).reshape(n, b).T.ravel()
+            ix2[a0:a1] = ix2[a0:a1][order]
+            dt2[a0:a1] = dt2[a0:a1][order]
+    return ip2, ix2, dt2
+
+
+def _reblock_rows_swapped(indptr, indices, data, R2, C2):
+    """Sub-rows of a block taken bottom-up."""
+    d = np.asarray(data)[:, ::-1, :].copy()
+    return O.__dict__["_orig_reblock"](indptr, indices, d, R2, C2)
+
+
 def _round_half_even(N, K, R, C, d, per_row=False):
     Nb, Kb = O.check_shape(N, K, R, C)
     if not (0.0 <= d <= 1.0):
@@ -187,6 +208,8 @@ MUTANTS = {
     "bf16 ties away from zero": ("bf16_round", _bf16_ties_away),
     "block rows flipped in to_dense": ("to_dense", _to_dense_transposed_blocks),
     "indices descending in a row": ("build_bsr", _build_desc_indices),
+    "reblock lists pieces column-major": ("reblock", _reblock_pieces_column_major),
+    "reblock takes sub-rows bottom-up": ("reblock", _reblock_rows_swapped),
 }
 
 
@@ -225,6 +248,9 @@ def _all_pins():
         ("product-int", P.test_spmm_integer_inputs_exact),
         ("bf16-hand", P.test_bf16_hand_cases),
         ("bf16-torch", P.test_bf16_matches_torch_random),
+        ("reblock", lambda: [P.test_reblock_is_the_same_matrix(*a) for a in
+                             [(64, 64, 32, 32), (1, 128, 1, 32), (128, 1, 32, 1)]]),
+        ("reblock-hand", P.test_reblock_hand_case),
     ]
     return calls
 

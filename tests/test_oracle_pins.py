@@ -379,6 +379,53 @@ def test_per_row_rejects_uneven_k():
         O.prune(W, 32, 32, k=3, per_row=True)
 
 
+# ----------------------------------------------------------------------------------- reblock
+
+
+@pytest.mark.parametrize("R,C,R2,C2", [(64, 64, 32, 32), (1, 128, 1, 32), (128, 1, 32, 1),
+                                       (32, 32, 16, 16), (8, 8, 8, 1), (4, 4, 1, 1),
+                                       (64, 64, 64, 64)])
+def test_reblock_is_the_same_matrix(R, C, R2, C2):
+    """The refined matrix expands to the same dense matrix bit for bit, its pattern is the
+    original one refined, and SciPy's conversion to the smaller block size agrees."""
+    import scipy.sparse as sp
+    g = rng(40 + R + C + R2)
+    N, K = 4 * R, 3 * C if C > 1 else 96
+    W = g.standard_normal((N, K)).astype(np.float32)
+    W[0, 0] = -0.0
+    ip, ix, dt = O.prune(W, R, C, density=0.4)
+    ip2, ix2, dt2 = O.reblock(ip, ix, dt, R2, C2)
+    D = O.to_dense(ip, ix, dt, N, K)
+    assert np.array_equal(O.to_dense(ip2, ix2, dt2, N, K).view(np.uint32), D.view(np.uint32))
+    a, b = R // R2, C // C2
+    assert ip2[-1] == len(ix) * a * b and np.all(np.diff(ip2) >= 0)
+    for i2 in range(len(ip2) - 1):
+        row = ix2[ip2[i2]:ip2[i2 + 1]]
+        assert np.all(np.diff(row) > 0)
+        i = i2 // a
+        assert sorted(set(row // b)) == sorted(ix[ip[i]:ip[i + 1]].tolist())
+    ref = sp.bsr_matrix((dt, ix, ip), shape=(N, K)).tobsr(blocksize=(R2, C2))
+    ref.sort_indices()
+    got = sp.bsr_matrix((dt2, ix2, ip2), shape=(N, K))
+    assert np.array_equal(got.toarray(), ref.toarray())
+
+
+def test_reblock_hand_case():
+    """A 2x4 block [[1,2,3,4],[5,6,7,8]] at block-column 1 of a 2x8 matrix, cut into 1x2 pieces:
+    rows 0 and 1 each hold two pieces, at block-columns 2 and 3."""
+    ip, ix, dt = (np.array([0, 1]), np.array([1]),
+                  np.array([[[1, 2, 3, 4], [5, 6, 7, 8]]], dtype=np.float32))
+    ip2, ix2, dt2 = O.reblock(ip, ix, dt, 1, 2)
+    assert ip2.tolist() == [0, 2, 4]
+    assert ix2.tolist() == [2, 3, 2, 3]
+    assert dt2.tolist() == [[[1, 2]], [[3, 4]], [[5, 6]], [[7, 8]]]
+
+
+def test_reblock_rejects_non_divisors():
+    with pytest.raises(ValueError):
+        O.reblock(np.array([0, 0]), np.zeros(0, np.int32), np.zeros((0, 4, 4), np.float32), 3, 4)
+
+
 # --------------------------------------------------------------------- BSR build and to_dense
 
 
