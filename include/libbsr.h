@@ -180,7 +180,9 @@ typedef enum {
     BSR_KERNEL_AUTO = 0,     /* the library picks                                           */
     BSR_KERNEL_GENERIC = 1,  /* one thread per output element; every block shape and dtype   */
     BSR_KERNEL_TILED = 2,    /* LDS-staged token tiles on matrix cores; 32x1, 16x1, 32x32,
-                                16x16 blocks (BSR_ERR_UNSUPPORTED for other shapes)          */
+                                16x16 blocks (BSR_ERR_UNSUPPORTED for other shapes).  An
+                                input too wide for one LDS tile (e.g. K = 3072) is staged in
+                                column chunks, each row's sum continuing across them         */
     BSR_KERNEL_VALU = 3      /* LDS-staged token tiles on the vector ALUs; 1x1, 1x2, 1x4, 1x8,
                                 1x16, 1x32, 2x1, 4x1, 8x1, 2x2, 4x4, 8x8 blocks (fp32; bf16
                                 except 1x1), K up to about 1270 (BSR_ERR_UNSUPPORTED

@@ -144,9 +144,10 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     if ((ev.start == nullptr) != (ev.stop == nullptr)) return BSR_ERR_ARG;
 
     // Plan: every non-empty product goes to the matrix-core tiled kernel when it has the shape,
-    // else to the vector-ALU tile kernel, else to the generic kernel (a forced kernel choice
-    // narrows this; a forced tiled kernel that does not fit is an error).
-    enum Kind { kGeneric = 0, kTiled = 1, kVtile = 2 };
+    // or, when its X tile is too wide for LDS, to the column-chunked matrix-core kernel; else to
+    // the vector-ALU tile kernel, else to the generic kernel (a forced kernel choice narrows
+    // this; a forced tiled kernel that does not fit is an error).
+    enum Kind { kGeneric = 0, kTiled = 1, kVtile = 2, kKchunk = 3 };
     std::vector<int> work;
     for (int32_t i = 0; i < n_items; ++i)
         if (items[i].T > 0) work.push_back(i);
@@ -156,6 +157,7 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     const int cus = bsr::device_cu_count();
     const size_t lds_limit = bsr::device_lds_per_block();
     std::vector<bsr::TiledWork> tiled(work.size());
+    std::vector<bsr::KchunkWork> kchunk(work.size());
     std::vector<int> kind(work.size(), kGeneric);
     int64_t total_tiles = 0;
     for (size_t w = 0; w < work.size(); ++w) {
@@ -166,6 +168,10 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
             bsr::tiled_supported(R, C, dt) &&
             bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok)
             kind[w] = kTiled;
+        else if ((kernel == BSR_KERNEL_AUTO || kernel == BSR_KERNEL_TILED) &&
+                 bsr::tiled_supported(R, C, dt) &&
+                 bsr::plan_kchunk(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).base.ok)
+            kind[w] = kKchunk;
         else if ((kernel == BSR_KERNEL_AUTO || kernel == BSR_KERNEL_VALU) &&
                  bsr::vtile_supported(R, C, dt) &&
                  bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok)
@@ -180,6 +186,12 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         const int S = slices > 0
                           ? slices
                           : bsr::auto_slices(total_tiles, it.W->n_rows / it.W->R, cus);
+        if (kind[w] == kKchunk) {
+            const bsr::KchunkPlan kp =
+                bsr::plan_kchunk(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
+            kchunk[w] = bsr::KchunkWork{kp, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
+            continue;
+        }
         const bsr::TiledPlan plan =
             kind[w] == kTiled ? bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit)
                               : bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
@@ -221,7 +233,11 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         if (li == 0) lev.start = ev.start;
         if (li + 1 == launches.size()) lev.stop = ev.stop;
         const Launch &l = launches[li];
-        if (l.kind != kGeneric) {
+        if (l.kind == kKchunk) {
+            bsr::KchunkWork batch[bsr::kMaxItems];
+            for (size_t m = 0; m < l.members.size(); ++m) batch[m] = kchunk[l.members[m]];
+            s = bsr::launch_spmm_kchunk(batch, int(l.members.size()), stream, lev);
+        } else if (l.kind != kGeneric) {
             bsr::TiledWork batch[bsr::kMaxItems];
             for (size_t m = 0; m < l.members.size(); ++m) batch[m] = tiled[l.members[m]];
             s = l.kind == kTiled ? bsr::launch_spmm_tiled(batch, int(l.members.size()), stream, lev)

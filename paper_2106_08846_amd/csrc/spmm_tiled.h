@@ -64,6 +64,46 @@ struct TiledBatch {
 // Launch 1..kMaxItems planned products of one block shape as a single kernel.
 bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream, const LaunchEvents &ev);
 
+// The column-chunked matrix-core kernel, for inputs too wide for one LDS X tile: same units
+// and shapes as the tiled kernel; the plan also fills chunk_blocks and nchunks.
+struct KchunkPlan {
+    TiledPlan base;
+    int chunk_blocks = 0;   // block-columns per chunk (the last chunk may be narrower)
+    int nchunks = 0;
+};
+KchunkPlan plan_kchunk(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W,
+                       int64_t ldy, int slices, size_t lds_limit);
+
+struct KchunkItem {
+    const void *X;
+    int64_t T, ldx;
+    const int32_t *indptr;
+    const int32_t *indices;
+    const void *data;
+    const float *bias;
+    float *Y;
+    int64_t ldy;
+    int nnzb, Nb, Kb;
+    int num_tiles, slices, XP, bias_words, wbuf_offset, chunk_blocks, nchunks;
+};
+
+struct KchunkBatch {
+    int n;
+    KchunkItem item[kMaxItems];
+};
+
+struct KchunkWork {
+    KchunkPlan plan;
+    const void *X;
+    int64_t T, ldx;
+    const bsr_matrix_t *W;
+    const float *bias;
+    float *Y;
+    int64_t ldy;
+};
+bsr_status launch_spmm_kchunk(const KchunkWork *work, int n, void *stream,
+                              const LaunchEvents &ev);
+
 // The vector-ALU tile kernel (shapes without a matrix-core kernel: 1 x C, 2x1 .. 8x1, 2x2 ..
 // 8x8).  Same plan and batch structures; the plan fills num_tiles, slices, x_pitch, lds_bytes.
 bool vtile_supported(int R, int C, int dtype);

@@ -5,17 +5,7 @@
 //
 // For one block-row and a tile of tokens this is a small dense product once the input columns
 // named by `indices` are gathered: Y_tile (tokens x R) += X_tile[:, cols] (tokens x m*C) times
-// the row's blocks (m*C x R).  The kernels below run it on MFMA:
-//
-//   * R x 1 blocks (32x1, 16x1): the contraction index is the block.  32x1 uses
-//     v_mfma_f32_32x32x2_f32 with two blocks per instruction; lane l supplies token l%32 of
-//     block l/32 (gathered from the LDS X tile) and feature l%32 of that block's data, so the B
-//     operand is one contiguous 256-byte load per instruction.  16x1 uses
-//     v_mfma_f32_16x16x4_f32, four blocks per instruction, for two 16-token halves.
-//   * R x R blocks (32x32, 16x16): the contraction index is the block column c.  Each lane
-//     loads 16 contiguous bytes of the block (one float4 of a block row), and the order of c
-//     inside each instruction is permuted identically for the A and B operands, which the sum
-//     does not see.  A comes from the LDS X tile with 16-byte reads.
+// the row's blocks (m*C x R).  The matrix-core units of spmm_units.h run it on MFMA.
 //
 // Work decomposition (one workgroup = 32 tokens x one slice of block-rows):
 //   * the X tile [32 tokens][K] is staged once into LDS by direct global->LDS loads (no
@@ -33,563 +23,11 @@
 
 #include "device_common.h"
 #include "spmm_tiled.h"
+#include "spmm_units.h"
 
 namespace bsr {
 
 namespace {
-
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef short shortx4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
-typedef unsigned uintx2 __attribute__((ext_vector_type(2)));
-typedef unsigned short bf16_t;  // a bf16 value as its bit pattern
-typedef short shortx8 __attribute__((ext_vector_type(8)));
-typedef __attribute__((address_space(3))) shortx4 lds_shortx4;
-
-constexpr int kTT = 32;           // tokens per workgroup
-constexpr int kStageChunks = 12;  // 64-column chunks of an X row in flight per wave
-
-__device__ __forceinline__ floatx16 mfma32(float a, float b, floatx16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ floatx4 mfma16(float a, float b, floatx4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
-// First index i in [0, n) with s_indptr[i] >= v (n if none); s_indptr is non-decreasing.
-__device__ __forceinline__ int wave_lower_bound(const int *s_indptr, int n, int64_t v) {
-    const int lane = threadIdx.x & 63;
-    for (int base = 0; base < n; base += 64) {
-        const int idx = base + lane;
-        const bool pred = idx < n && s_indptr[idx] >= v;
-        const unsigned long long m = __ballot(pred);
-        if (m) return base + __ffsll(static_cast<long long>(m)) - 1;
-    }
-    return n;
-}
-
-// ------------------------------------------------------------------------------------ units
-// A wave walks its stored blocks as a stream of fixed-size "units" of four MFMA steps: 8 blocks
-// for 32x1 (2 per v_mfma_f32_32x32x2_f32), 16 for 16x1 (4 per v_mfma_f32_16x16x4_f32, for each
-// 16-token half), one block for square shapes.  A unit policy loads a unit's operands into
-// registers, issues its MFMAs (all lanes, or only the blocks in an offset range [lo, hi) of the
-// unit when it crosses a row end), and stores a finished row tile to Y.
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Cache policy of the Y stores: nontemporal (Y is written once and not read here).
-constexpr int kStoreNT = 2;
-
-// Destination of one 32-token tile of Y: a buffer resource over the tile's valid rows (rows
-// past the last token of the product fall outside it, and the hardware drops those stores).
-// The row offset goes in the range-checked vector offset, the column in the scalar offset.
-struct TileOut {
-    __amdgpu_buffer_rsrc_t rsrc;  // Y + t0 * ldy, over rows * ldy * 4 bytes
-    int ldy4;                     // ldy * 4 bytes
-};
-
-// Clamp a block column read from memory into [0, Kb) (unsigned compare also catches negatives).
-__device__ __forceinline__ int clamp_col(int j, int Kb) {
-    return int(min(unsigned(j), unsigned(Kb - 1)));
-}
-
-template <int R, int C, bool BF>
-struct Unit;
-
-// R x 1 blocks.  For R = 32, lane l supplies block l/32 of a step (A: token l%32 of the X tile;
-// B: feature l%32 of the block), acc[v] holds Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].
-// For R = 16, lane l supplies block l/16 of a step for both token halves, acc.h[h][v] holds
-// Y[t0 + 16h + 4(l/16) + v][n0 + l%16].
-// With bf16 data the operands are widened to fp32 as they are loaded (exact) and the same fp32
-// MFMAs run; the X tile is staged widened to fp32 as well.
-template <int R, bool BF>
-struct LinearUnit {
-    static constexpr int kPer = 64 / R;     // blocks per MFMA step
-    static constexpr int kSteps = 4;
-    static constexpr int KB = kPer * kSteps;
-    static constexpr int kPad = 1;
-    static constexpr bool kTileBF16 = false;
-    static constexpr bool kTransposed = false;
-    struct Ops {
-        int j[kSteps];
-        float b[kSteps];
-    };
-    __device__ static int offset_in_step() { return (threadIdx.x & 63) / R; }
-    __device__ static int feature() { return (threadIdx.x & 63) % R; }
-    // Loads every lane's operands for the unit at p through raw buffer loads based at the
-    // unit: one code path for every unit, no per-lane address arithmetic, and lanes past the
-    // end of the arrays (nnzb blocks) read 0.  Lanes past the unit's row segment read the next
-    // row's blocks; mask() zeroes them before the MFMAs.
-    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const void *__restrict__ data) {
-        const int o = offset_in_step(), f = feature();
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        if constexpr (BF) {
-            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
-                static_cast<const bf16_t *>(data) + int64_t(p) * R, left * (R * 2u));
-#pragma unroll
-            for (int m = 0; m < kSteps; ++m) {
-                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
-                ops.b[m] = __uint_as_float(unsigned(__builtin_amdgcn_raw_buffer_load_b16(
-                                               rd, (o * R + f) * 2, m * kPer * R * 2, 0))
-                                           << 16);
-            }
-        } else {
-            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
-                static_cast<const float *>(data) + int64_t(p) * R, left * (R * 4u));
-#pragma unroll
-            for (int m = 0; m < kSteps; ++m) {
-                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
-                ops.b[m] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                         rd, (o * R + f) * 4, m * kPer * R * 4, 0));
-            }
-        }
-    }
-    // Zero the operands of lanes whose block offset in the unit is >= nvalid (partial units).
-    __device__ static void mask(Ops &ops, int nvalid) {
-        const int o = offset_in_step();
-#pragma unroll
-        for (int m = 0; m < kSteps; ++m) {
-            const bool in = m * kPer + o < nvalid;
-            ops.j[m] = in ? ops.j[m] : -1;
-            ops.b[m] = in ? ops.b[m] : 0.0f;
-        }
-    }
-};
-
-template <bool BF>
-struct Unit<32, 1, BF> : LinearUnit<32, BF> {
-    using Ops = typename LinearUnit<32, BF>::Ops;
-    using LinearUnit<32, BF>::feature;
-    static constexpr int kRegs = 16;
-    using Acc = floatx16;
-    __device__ static void zero(Acc &acc) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
-    }
-    // Every element of the tile starts at its column's bias (s_bias: the bias staged in LDS).
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        const float b = s_bias[n0 + (threadIdx.x & 31)];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[v] = b;
-    }
-    // MFMAs of one unit.  Column indices are clamped to [0, Kb]; column Kb of the X tile is
-    // the zero pad column that masked lanes point at.
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
-        constexpr int kSteps = LinearUnit<32, BF>::kSteps;
-        const float *xrow = static_cast<const float *>(Xs) + feature() * XP;
-        float a[kSteps];
-#pragma unroll
-        for (int m = 0; m < kSteps; ++m) a[m] = xrow[clamp_col(ops.j[m], Kb + 1)];
-#pragma unroll
-        for (int m = 0; m < kSteps; ++m) acc = mfma32(a[m], ops.b[m], acc);
-    }
-    // Element v of lane l is Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const int vo = 4 * kh * o.ldy4 + tl * 4;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int r = 8 * (v >> 2) + (v & 3);
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), o.rsrc,
-                                                  vo + r * o.ldy4, n0 * 4, kStoreNT);
-        }
-    }
-    // Register v of every lane alone (v uniform).
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const int r = 8 * (v >> 2) + (v & 3);
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), o.rsrc,
-                                              (4 * kh + r) * o.ldy4 + tl * 4, n0 * 4, kStoreNT);
-    }
-    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
-    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
-};
-
-template <bool BF>
-struct Unit<16, 1, BF> : LinearUnit<16, BF> {
-    using Ops = typename LinearUnit<16, BF>::Ops;
-    using LinearUnit<16, BF>::feature;
-    static constexpr int kRegs = 8;
-    struct Acc {
-        floatx4 h[2];
-    };
-    __device__ static void zero(Acc &acc) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = 0.0f;
-    }
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        const float b = s_bias[n0 + (threadIdx.x & 15)];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = b;
-    }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
-        constexpr int kSteps = LinearUnit<16, BF>::kSteps;
-        const float *x0 = static_cast<const float *>(Xs) + feature() * XP;
-        const float *x1 = x0 + 16 * XP;
-        float a0[kSteps], a1[kSteps];
-#pragma unroll
-        for (int m = 0; m < kSteps; ++m) {
-            const int j = clamp_col(ops.j[m], Kb + 1);
-            a0[m] = x0[j];
-            a1[m] = x1[j];
-        }
-#pragma unroll
-        for (int m = 0; m < kSteps; ++m) {
-            acc.h[0] = mfma16(a0[m], ops.b[m], acc.h[0]);
-            acc.h[1] = mfma16(a1[m], ops.b[m], acc.h[1]);
-        }
-    }
-    // Element (h, v) of lane l is Y[t0 + 16h + 4(l/16) + v][n0 + l%16].
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const int vo = 4 * kq * o.ldy4 + tl * 4;
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc.h[h][v]), o.rsrc,
-                                                      vo + (16 * h + v) * o.ldy4, n0 * 4,
-                                                      kStoreNT);
-    }
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), o.rsrc,
-                                              (4 * kq + 16 * (v >> 2) + (v & 3)) * o.ldy4 + tl * 4,
-                                              n0 * 4, kStoreNT);
-    }
-    __device__ static float get(const Acc &acc, int v) { return acc.h[v >> 2][v & 3]; }
-    __device__ static void add(Acc &acc, int v, float x) { acc.h[v >> 2][v & 3] += x; }
-};
-
-// LDS transpose read (ds_read_b64_tr_b16): within each group of 16 lanes, lane i receives
-// element i % 4 of the 8-byte chunks addressed by lanes 4c + i / 4 of its group, c = 0..3.
-__device__ __forceinline__ shortx4 lds_read_tr16(const char *p) {
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_shortx4 *)((__attribute__((address_space(3))) char *)p));
-}
-
-// 32x1 bf16 blocks on v_mfma_f32_32x32x16_bf16: the contraction index is the block, 16 blocks
-// per instruction, two instructions per unit.  Lane l supplies k-slots 8(l/32) .. +7 for token
-// l%32 (A) and feature l%32 (B); both operands are assembled by transpose reads, four chunks
-// (c = 0..3) per read:
-//   * A from the transposed X tile (each column holds the 32 tokens contiguously, 2 bytes each,
-//     column pitch XP bf16): lane 4c + q of group g addresses tokens 16(g%2) + 4q .. +3 of
-//     column indices[16m + 8(g/2) + 4s + c] for read s of instruction m;
-//   * B from a per-wave LDS copy of the unit's blocks ([block][32 features]): the same lane
-//     addresses features 16(g%2) + 4q .. +3 of block 16m + 8(g/2) + 4s + c.
-// Blocks past the segment end read the tile's zero pad column (A) and zero weights (B).
-template <>
-struct Unit<32, 1, true> {
-    static constexpr int KB = 32;
-    static constexpr int kPad = 0;
-    static constexpr bool kTileBF16 = true;
-    static constexpr bool kTransposed = true;
-    static constexpr int kRegs = 16;
-    static constexpr int kSlotBytes = 2048;  // LDS per wave for the unit's blocks
-    using Acc = floatx16;
-    struct Ops {
-        int j[4];     // index for read (m, s) = 2m + s
-        uintx4 w[2];  // instruction m: block 16m + l/4, features 8(l%4) .. +7
-    };
-    __device__ static void zero(Acc &acc) { Unit<32, 1, false>::zero(acc); }
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        Unit<32, 1, false>::init(acc, s_bias, n0);
-    }
-    __device__ static int read_block(int r) {   // block of read r within the unit, this lane
-        const int l = threadIdx.x & 63;
-        return 16 * (r >> 1) + 8 * (l >> 5) + 4 * (r & 1) + ((l & 15) >> 2);
-    }
-    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const void *__restrict__ data) {
-        const int l = threadIdx.x & 63;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 32, left * 64u);
-        const int io = (8 * (l >> 5) + ((l & 15) >> 2)) * 4;
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            ops.j[r] = __builtin_amdgcn_raw_buffer_load_b32(ri, io, (16 * (r >> 1) + 4 * (r & 1)) * 4, 0);
-#pragma unroll
-        for (int m = 0; m < 2; ++m) ops.w[m] = __builtin_amdgcn_raw_buffer_load_b128(rd, l * 16, m * 1024, 0);
-    }
-    __device__ static void mask(Ops &ops, int nvalid) {
-        const int l = threadIdx.x & 63;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) ops.j[r] = read_block(r) < nvalid ? ops.j[r] : -1;
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-            const bool in = 16 * m + (l >> 2) < nvalid;
-            ops.w[m] = in ? ops.w[m] : uintx4{0u, 0u, 0u, 0u};
-        }
-    }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                               char *wslot) {
-        const int l = threadIdx.x & 63, g = l >> 4, c = (l & 15) >> 2, q = l & 3;
-        uintx4 *ws = reinterpret_cast<uintx4 *>(wslot);
-        ws[l] = ops.w[0];
-        ws[64 + l] = ops.w[1];
-        const char *xt = static_cast<const char *>(Xs);
-        const int tok = (16 * (g & 1) + 4 * q) * 2;            // byte offset within a column
-        const int boff = (8 * (g >> 1) + c) * 64 + tok;        // byte offset within the slot
-        shortx4 a[4], b[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            a[r] = lds_read_tr16(xt + clamp_col(ops.j[r], Kb + 1) * (2 * XP) + tok);
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            b[r] = lds_read_tr16(wslot + (r >> 1) * 1024 + (r & 1) * 256 + boff);
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-            const shortx8 av = __builtin_shufflevector(a[2 * m], a[2 * m + 1], 0, 1, 2, 3, 4, 5, 6, 7);
-            const shortx8 bv = __builtin_shufflevector(b[2 * m], b[2 * m + 1], 0, 1, 2, 3, 4, 5, 6, 7);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
-                                                         __builtin_bit_cast(bf16x8, bv), acc,
-                                                         0, 0, 0);
-        }
-    }
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        Unit<32, 1, false>::store(acc, o, n0);
-    }
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        Unit<32, 1, false>::store_reg(x, o, n0, v);
-    }
-    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
-    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
-};
-
-// Accumulator, bias and store plumbing shared by the square units (the output layouts of the
-// 32x32 and 16x16 MFMAs do not depend on the input type).
-template <int R>
-using LinearBase = Unit<R, 1, false>;
-
-// 32x32 fp32 blocks, v_mfma_f32_32x32x2_f32.  Lane l loads columns 8u + 4(l/32) .. +3 of block
-// row l%32 (u = 0..3); for step (u, e) its k-slot l/32 stands for c = 8u + 4(l/32) + e in both
-// operands.
-template <>
-struct Unit<32, 32, false> {
-    static constexpr int KB = 1;
-    static constexpr int kPad = 4;
-    static constexpr bool kTileBF16 = false;
-    static constexpr bool kTransposed = false;
-    static constexpr int kRegs = 16;
-    using Acc = floatx16;
-    struct Ops {
-        int j;
-        floatx4 d[4];
-    };
-    __device__ static void zero(Acc &acc) { LinearBase<32>::zero(acc); }
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        LinearBase<32>::init(acc, s_bias, n0);
-    }
-    __device__ static void mask(Ops &, int) {}
-    // Range-checked loads based at the unit, as for the R x 1 units: a position at or past
-    // nnzb reads 0 and touches no memory.
-    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const void *__restrict__ data) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const float *>(data) + int64_t(p) * 1024, left * 4096u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-            ops.d[u] = __builtin_bit_cast(
-                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rd, (tl * 8 + kh) * 16, 32 * u, 0));
-    }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const float *xb =
-            static_cast<const float *>(Xs) + tl * XP + 4 * kh + clamp_col(ops.j, Kb) * 32;
-        floatx4 a[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) a[u] = *reinterpret_cast<const floatx4 *>(xb + 8 * u);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc = mfma32(a[u][e], ops.d[u][e], acc);
-        }
-    }
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        LinearBase<32>::store(acc, o, n0);
-    }
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        LinearBase<32>::store_reg(x, o, n0, v);
-    }
-    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
-    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
-};
-
-// 32x32 bf16 blocks, v_mfma_f32_32x32x16_bf16, two instructions per block.  For half u of the
-// block's columns, lane l supplies k-slots 8(l/32) .. +7, standing for c = 16u + 8(l/32) + e:
-// 16 contiguous bytes of token l%32's X row (from the bf16 LDS tile) and of block row l%32.
-template <>
-struct Unit<32, 32, true> {
-    static constexpr int KB = 1;
-    static constexpr int kPad = 8;
-    static constexpr bool kTileBF16 = true;
-    static constexpr bool kTransposed = false;
-    static constexpr int kRegs = 16;
-    using Acc = floatx16;
-    struct Ops {
-        int j;
-        uintx4 d[2];
-    };
-    __device__ static void zero(Acc &acc) { LinearBase<32>::zero(acc); }
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        LinearBase<32>::init(acc, s_bias, n0);
-    }
-    __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const void *__restrict__ data) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 1024, left * 2048u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-            ops.d[u] = __builtin_amdgcn_raw_buffer_load_b128(rd, (tl * 4 + kh) * 16, 32 * u, 0);
-    }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
-        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const bf16_t *xb =
-            static_cast<const bf16_t *>(Xs) + tl * XP + 8 * kh + clamp_col(ops.j, Kb) * 32;
-        uintx4 a[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) a[u] = *reinterpret_cast<const uintx4 *>(xb + 16 * u);
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[u]),
-                                                         __builtin_bit_cast(bf16x8, ops.d[u]),
-                                                         acc, 0, 0, 0);
-    }
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        LinearBase<32>::store(acc, o, n0);
-    }
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        LinearBase<32>::store_reg(x, o, n0, v);
-    }
-    __device__ static float get(const Acc &acc, int v) { return acc[v]; }
-    __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
-};
-
-// 16x16 fp32 blocks, v_mfma_f32_16x16x4_f32 on two 16-token halves.  Lane l loads row l%16,
-// columns 4(l/16)..+3 of the block (the whole block in one instruction); k-slot l/16 of step e
-// stands for c = 4(l/16) + e.
-template <>
-struct Unit<16, 16, false> {
-    static constexpr int KB = 1;
-    static constexpr int kPad = 4;
-    static constexpr bool kTileBF16 = false;
-    static constexpr bool kTransposed = false;
-    static constexpr int kRegs = 8;
-    using Acc = typename LinearBase<16>::Acc;
-    struct Ops {
-        int j;
-        floatx4 d;
-    };
-    __device__ static void zero(Acc &acc) { LinearBase<16>::zero(acc); }
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        LinearBase<16>::init(acc, s_bias, n0);
-    }
-    __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const void *__restrict__ data) {
-        const int lane = threadIdx.x & 63;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const float *>(data) + int64_t(p) * 256, left * 1024u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
-        ops.d = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                rd, ((lane & 15) * 4 + (lane >> 4)) * 16, 0, 0));
-    }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
-        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const float *xb =
-            static_cast<const float *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
-        const floatx4 a0 = *reinterpret_cast<const floatx4 *>(xb);
-        const floatx4 a1 = *reinterpret_cast<const floatx4 *>(xb + 16 * XP);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            acc.h[0] = mfma16(a0[e], ops.d[e], acc.h[0]);
-            acc.h[1] = mfma16(a1[e], ops.d[e], acc.h[1]);
-        }
-    }
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        LinearBase<16>::store(acc, o, n0);
-    }
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        LinearBase<16>::store_reg(x, o, n0, v);
-    }
-    __device__ static float get(const Acc &acc, int v) { return LinearBase<16>::get(acc, v); }
-    __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
-};
-
-// 16x16 bf16 blocks, v_mfma_f32_16x16x16_bf16 on two 16-token halves, one instruction per
-// block and half.  Lane l supplies k-slots 4(l/16) .. +3, standing for c = 4(l/16) + e: 8
-// contiguous bytes of token l%16's X row and of block row l%16.
-template <>
-struct Unit<16, 16, true> {
-    static constexpr int KB = 1;
-    static constexpr int kPad = 8;
-    static constexpr bool kTileBF16 = true;
-    static constexpr bool kTransposed = false;
-    static constexpr int kRegs = 8;
-    using Acc = typename LinearBase<16>::Acc;
-    struct Ops {
-        int j;
-        uintx2 d;
-    };
-    __device__ static void zero(Acc &acc) { LinearBase<16>::zero(acc); }
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        LinearBase<16>::init(acc, s_bias, n0);
-    }
-    __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const void *__restrict__ data) {
-        const int lane = threadIdx.x & 63;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 256, left * 512u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
-        ops.d = __builtin_amdgcn_raw_buffer_load_b64(rd, ((lane & 15) * 4 + (lane >> 4)) * 8, 0, 0);
-    }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
-        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const bf16_t *xb =
-            static_cast<const bf16_t *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
-        const uintx2 a0 = *reinterpret_cast<const uintx2 *>(xb);
-        const uintx2 a1 = *reinterpret_cast<const uintx2 *>(xb + 16 * XP);
-        const shortx4 b = __builtin_bit_cast(shortx4, ops.d);
-        acc.h[0] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, a0), b,
-                                                            acc.h[0], 0, 0, 0);
-        acc.h[1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, a1), b,
-                                                            acc.h[1], 0, 0, 0);
-    }
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        LinearBase<16>::store(acc, o, n0);
-    }
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        LinearBase<16>::store_reg(x, o, n0, v);
-    }
-    __device__ static float get(const Acc &acc, int v) { return LinearBase<16>::get(acc, v); }
-    __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
-};
 
 // -------------------------------------------------------------------------------- the kernel
 
