@@ -6,8 +6,9 @@
 //             sum over c < C of X[t][indices[p] * C + c] * data[p][n - iR][c]      (Sec. 2.2)
 //
 // The input columns are cut into chunks of chunk_blocks block-columns.  One workgroup covers 32
-// tokens and one slice of block-rows; each wave owns up to kMR whole block-rows of the slice and
-// keeps their accumulators in registers from the first chunk to the last.  Per chunk:
+// tokens and one slice of block-rows; each wave owns up to kMR whole block-rows of the slice, or
+// a slice of few rows gives each row a group of waves that split its blocks, and the waves keep
+// their accumulators in registers from the first chunk to the last.  Per chunk:
 //   * the workgroup stages X[t0 : t0 + 32][chunk columns] into LDS, in the layout the block
 //     shape's unit reads (the same units and layouts as the tiled kernel);
 //   * each wave finds where each of its rows leaves the chunk: indices ascend within a row, so
@@ -15,8 +16,9 @@
 //     indices), and runs the row's units from its current position up to there;
 //   * the next chunk continues each row from where the previous one stopped, so every stored
 //     block is visited once, in position order.
-// A row tile starts at the bias and is stored once, after the last chunk.  The order of every
-// sum is fixed by the plan, so results are bitwise reproducible.
+// A row tile starts at the bias and is stored once, after the last chunk (for a wave group,
+// once the members' partial tiles have been added in member order).  The order of every sum is
+// fixed by the plan, so results are bitwise reproducible.
 #include <type_traits>
 
 #include "device_common.h"
@@ -81,11 +83,22 @@ __global__ __launch_bounds__(kNW * 64) void spmm_kchunk_kernel(const KchunkBatch
     for (int i = threadIdx.x; i < (row_hi - row_lo) * R; i += kThreads)
         s_bias[i] = bias ? bias[int64_t(row_lo) * R + i] : 0.0f;
 
-    // This wave's rows row_lo + wave + kNW * i and their block ranges [pos, end).
+    // Rows of the waves.  A slice of at most kNW / 2 rows gives each row a group of G >= 2
+    // waves (wave w: row w / G, member w % G), which split the row's blocks of every chunk into
+    // G contiguous parts and add their partial tiles in member order at the end; otherwise
+    // (G = 1) wave w owns rows row_lo + w + kNW * i, i < kMR.  Slot i of a wave holds row
+    // row_of(i), or a row >= row_hi when the slot is unused.
+    const int nr = row_hi - row_lo;
+    const int G = 2 * nr <= kNW ? kNW / nr : 1;
+    const int member = wave % G;
+    auto row_of = [&](int i) -> int {
+        if (G > 1) return (i == 0 && wave / G < nr) ? row_lo + wave / G : row_hi;
+        return row_lo + wave + kNW * i;
+    };
     int pos[kMR], end[kMR];
 #pragma unroll
     for (int i = 0; i < kMR; ++i) {
-        const int row = row_lo + wave + kNW * i;
+        const int row = row_of(i);
         pos[i] = end[i] = 0;
         if (row < row_hi) {
             pos[i] = uniform(clampi(indptr[row], 0, nnzb));
@@ -202,14 +215,18 @@ __global__ __launch_bounds__(kNW * 64) void spmm_kchunk_kernel(const KchunkBatch
         if (c == 0) {
 #pragma unroll
             for (int i = 0; i < kMR; ++i) {
-                const int row = row_lo + wave + kNW * i;
-                if (row < row_hi) U::init(acc[i], s_bias, (row - row_lo) * R);
+                const int row = row_of(i);
+                if (row < row_hi && member == 0) U::init(acc[i], s_bias, (row - row_lo) * R);
                 else U::zero(acc[i]);
             }
         }
 #pragma unroll
         for (int i = 0; i < kMR; ++i) {
-            run(acc[i], pos[i], cend[i], jlo, jhi - jlo);
+            // This member's part of the row's positions in the chunk (all of them when G = 1).
+            const int len = cend[i] - pos[i];
+            const int lo = pos[i] + int((int64_t(len) * member) / G);
+            const int hi = pos[i] + int((int64_t(len) * (member + 1)) / G);
+            run(acc[i], lo, hi, jlo, jhi - jlo);
             pos[i] = cend[i];
         }
     }
@@ -217,10 +234,32 @@ __global__ __launch_bounds__(kNW * 64) void spmm_kchunk_kernel(const KchunkBatch
     TileOut out;
     out.ldy4 = int(ldy) * 4;
     out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(out.ldy4));
+    if (G == 1) {
 #pragma unroll
-    for (int i = 0; i < kMR; ++i) {
-        const int row = row_lo + wave + kNW * i;
-        if (row < row_hi) U::store(acc[i], out, row * R);
+        for (int i = 0; i < kMR; ++i) {
+            const int row = row_of(i);
+            if (row < row_hi) U::store(acc[i], out, row * R);
+        }
+        return;
+    }
+    // Wave groups: members 1 .. G-1 leave their partial tiles in LDS (the X tile is dead after
+    // the barrier); member 0 adds them in member order and stores the row.
+    constexpr int kSlot = U::kRegs * 64;
+    float *P = Xs;
+    __syncthreads();
+    if (member > 0) {
+#pragma unroll
+        for (int v = 0; v < U::kRegs; ++v) P[(wave * U::kRegs + v) * 64 + lane] = U::get(acc[0], v);
+    }
+    __syncthreads();
+    const int row = row_of(0);
+    if (member == 0 && row < row_hi) {
+        for (int m = 1; m < G; ++m) {
+            const float *src = P + (wave + m) * kSlot;
+#pragma unroll
+            for (int v = 0; v < U::kRegs; ++v) U::add(acc[0], v, src[v * 64 + lane]);
+        }
+        U::store(acc[0], out, row * R);
     }
 }
 
@@ -273,6 +312,9 @@ KchunkPlan plan_kchunk(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t
         p.wbuf_offset = 0;
         tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
     }
+    // After the last chunk the tile's LDS holds the partial tiles of wave groups.
+    const size_t partial_bytes = size_t(kNW) * (R == 32 ? 16 : 8) * 64 * 4;
+    if (tile_bytes < partial_bytes) tile_bytes = partial_bytes;
     p.lds_bytes = size_t(p.bias_words) * 4 + tile_bytes;
     if (p.lds_bytes > lds_limit) return KchunkPlan{};
     // Buffer ranges are 32-bit (block data, one X row, a 32-row tile of Y); square units read

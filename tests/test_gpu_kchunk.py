@@ -63,6 +63,15 @@ def test_kchunk_two_rows_per_wave(device, R, C, slices):
     case(9500 + R + C + slices, N, 3072, 70, R, C, 0.05, False, slices=slices)
 
 
+@pytest.mark.parametrize("slices", [3, 4, 5, 8, 12, 24])
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+def test_kchunk_wave_groups(device, slices, bf16):
+    """24 block-rows in `slices` slices of 8 .. 1 rows: groups of 2 .. 16 waves split each row
+    (and some waves stay idle), with their partial tiles added at the end."""
+    case(9550 + slices + bf16, 768, 3072, 77, 32, 1, 0.1, bf16, slices=slices)
+    case(9560 + slices + bf16, 768, 3072, 77, 32, 32, 0.1, bf16, slices=slices)
+
+
 @pytest.mark.parametrize("T", [1, 31, 32, 33, 97])
 def test_kchunk_ragged_tokens(device, T):
     case(9600 + T, 768, 3072, T, 32, 1, 0.1, False)
