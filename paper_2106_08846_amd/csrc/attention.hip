@@ -26,6 +26,7 @@ namespace {
 constexpr int kKB = 64;       // keys per block
 constexpr int kD = 64;        // head width
 constexpr int kPitch = 68;    // LDS row pitch, floats
+constexpr int kMfmaMinSeq = 128;   // shortest sequence for the matrix-core kernel
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
@@ -159,14 +160,172 @@ __global__ __launch_bounds__(kQT * 8) void attention_kernel(
     }
 }
 
+// ------------------------------------------------------------------- matrix-core version
+// One wave computes 32 queries of one (sequence, head) on v_mfma_f32_32x32x2_f32; kWQ waves of
+// a workgroup share the staged keys and values (blocks of 64, as above).  Lane l serves query
+// l % 32 as half hh = l / 32.
+//   Scores, transposed: S^T = K Q^T for each group of 32 keys.  Step s (s < 32) contracts
+//   dimension s + 32hh in slot hh: A = K[key l%32][s + 32hh] (LDS), B = the lane's pre-scaled
+//   q[s + 32hh] (registers).  Register v of lane l then holds the score of query l % 32 and
+//   key 8(v/4) + 4hh + v%4 of the group, so a query's 32 scores sit in the lane pair
+//   (l, l ^ 32): the group maximum and sum take 15 register operations and one exchange.
+//   Output, transposed: O^T += V^T P^T.  Step v contracts the two keys that register v holds in
+//   the two halves: A = V[that key][32t + l%32] (LDS; output column tile t = 0, 1), B = this
+//   lane's weight p[v], so the weights never leave their registers.
+// The online softmax is the one above (running maximum and sum per query, output rescaled by
+// exp(m_old - m_new)); each query's running values are kept, identical, in both its lanes.
+template <int kWQ>
+__global__ __launch_bounds__(kWQ * 64) void attention_mfma_kernel(
+    const float *__restrict__ Q, int64_t ldq, const float *__restrict__ K, int64_t ldk,
+    const float *__restrict__ V, int64_t ldv, float *__restrict__ O, int64_t ldo, int seq,
+    float scale) {
+    typedef float floatx16 __attribute__((ext_vector_type(16)));
+    constexpr int kThreads = kWQ * 64;
+    __shared__ float Ks[kKB * kPitch];
+    __shared__ float Vs[kKB * kPitch];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ql = lane & 31, hh = lane >> 5;
+    const int qrow = (blockIdx.x * kWQ + wave) * 32 + ql, h = blockIdx.y;
+    const int64_t tok0 = int64_t(blockIdx.z) * seq;
+    const bool qvalid = qrow < seq;
+
+    // Half hh of this lane's query row, pre-scaled (rows past the sequence read row 0; never
+    // stored).
+    float q[32];
+    {
+        const float *qp = Q + (tok0 + (qvalid ? qrow : 0)) * ldq + h * kD + 32 * hh;
+#pragma unroll
+        for (int d = 0; d < 32; d += 4) {
+            const floatx4 v = load4(qp + d);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) q[d + e] = v[e] * scale;
+        }
+    }
+    float m = -INFINITY, l = 0.0f;
+    floatx16 o0, o1;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) o0[v] = o1[v] = 0.0f;
+
+    for (int k0 = 0; k0 < seq; k0 += kKB) {
+        __syncthreads();   // the previous block's LDS reads are done
+        // Stage K and V rows k0 .. k0 + 63 of this head (rows past the sequence are zero).
+        constexpr int kPer = kKB * (kD / 4) / kThreads;   // 16-byte pieces per thread
+        constexpr int kBatch = kPer < 4 ? kPer : 4;
+#pragma unroll
+        for (int n0 = 0; n0 < kPer; n0 += kBatch) {
+            floatx4 kst[kBatch], vst[kBatch];
+#pragma unroll
+            for (int n = 0; n < kBatch; ++n) {
+                const int i = tid + (n0 + n) * kThreads;
+                const int r = i >> 4, c4 = (i & 15) * 4;
+                const int key = k0 + r < seq ? k0 + r : seq - 1;   // past the end: zeroed below
+                kst[n] = load4(K + (tok0 + key) * ldk + h * kD + c4);
+                vst[n] = load4(V + (tok0 + key) * ldv + h * kD + c4);
+            }
+#pragma unroll
+            for (int n = 0; n < kBatch; ++n) {
+                const int i = tid + (n0 + n) * kThreads;
+                const int r = i >> 4, c4 = (i & 15) * 4;
+                const floatx4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+                *reinterpret_cast<floatx4 *>(&Ks[r * kPitch + c4]) = k0 + r < seq ? kst[n] : z;
+                *reinterpret_cast<floatx4 *>(&Vs[r * kPitch + c4]) = k0 + r < seq ? vst[n] : z;
+            }
+        }
+        __syncthreads();
+
+#pragma unroll
+        for (int g = 0; g < kKB / 32; ++g) {
+            const int kg = k0 + 32 * g;
+            if (kg >= seq) break;   // the whole group is past the end
+            floatx16 s;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) s[v] = 0.0f;
+            const float *kr = &Ks[(32 * g + ql) * kPitch + 32 * hh];
+#pragma unroll
+            for (int d = 0; d < 32; d += 4) {
+                const floatx4 kv = load4(kr + d);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    s = __builtin_amdgcn_mfma_f32_32x32x2f32(kv[e], q[d + e], s, 0, 0, 0);
+            }
+            // Keys past the sequence get -inf (weight 0); the group's first key exists.
+            float mx = -INFINITY;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int key = kg + 8 * (v >> 2) + 4 * hh + (v & 3);
+                if (key >= seq) s[v] = -INFINITY;
+                mx = fmaxf(mx, s[v]);
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float mn = fmaxf(m, mx);
+            const float corr = expf(m - mn);   // 0 on the first group (m = -inf)
+            float ps = 0.0f;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                s[v] = expf(s[v] - mn);
+                ps += s[v];
+            }
+            ps += __shfl_xor(ps, 32);
+            l = l * corr + ps;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                o0[v] *= corr;
+                o1[v] *= corr;
+            }
+            m = mn;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float *vr = &Vs[(32 * g + 8 * (v >> 2) + 4 * hh + (v & 3)) * kPitch + ql];
+                o0 = __builtin_amdgcn_mfma_f32_32x32x2f32(vr[0], s[v], o0, 0, 0, 0);
+                o1 = __builtin_amdgcn_mfma_f32_32x32x2f32(vr[32], s[v], o1, 0, 0, 0);
+            }
+        }
+    }
+    // Register v of tile t holds O[query][32t + 8(v/4) + 4hh + v%4]: four consecutive columns
+    // per group of four registers, stored as 16 bytes.
+    if (qvalid) {
+        float *op = O + (tok0 + qrow) * ldo + h * kD + 4 * hh;
+#pragma unroll
+        for (int v4 = 0; v4 < 4; ++v4) {
+            floatx4 a, b;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                a[e] = o0[4 * v4 + e] / l;
+                b[e] = o1[4 * v4 + e] / l;
+            }
+            *reinterpret_cast<floatx4 *>(op + 8 * v4) = a;
+            *reinterpret_cast<floatx4 *>(op + 32 + 8 * v4) = b;
+        }
+    }
+}
+
 }  // namespace
 
 bsr_status launch_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
                             const float *V, int64_t ldv, float *O, int64_t ldo, int batch,
                             int seq, int heads, float scale, void *stream) {
-    // 32-query tiles when they give at least one workgroup per CU, else 8-query tiles.
     const int64_t tiles32 = int64_t((seq + 31) / 32) * heads * batch;
     const int cus = device_cu_count() > 0 ? device_cu_count() : 256;
+    // The matrix-core kernel when there are at least three 32-query tiles per CU and
+    // sequences of kMfmaMinSeq keys or more (its per-wave chain of key groups is long, so it
+    // needs many waves; measured on MI355X, fewer tiles or shorter sequences run faster on the
+    // vector ALUs).  Four query tiles per workgroup when that still gives every CU a
+    // workgroup, else one.
+    if (seq >= kMfmaMinSeq && tiles32 >= 3 * int64_t(cus)) {
+        const int64_t wg4 = int64_t((seq + 127) / 128) * heads * batch;
+        if (wg4 >= cus) {
+            const dim3 grid(unsigned((seq + 127) / 128), unsigned(heads), unsigned(batch));
+            hipLaunchKernelGGL(attention_mfma_kernel<4>, grid, dim3(256), 0, as_stream(stream), Q,
+                               ldq, K, ldk, V, ldv, O, ldo, seq, scale);
+        } else {
+            const dim3 grid(unsigned((seq + 31) / 32), unsigned(heads), unsigned(batch));
+            hipLaunchKernelGGL(attention_mfma_kernel<1>, grid, dim3(64), 0, as_stream(stream), Q,
+                               ldq, K, ldk, V, ldv, O, ldo, seq, scale);
+        }
+        return launch_status();
+    }
+    // Vector-ALU kernel: 32-query tiles when they give at least one workgroup per CU, else
+    // 8-query tiles.
     if (tiles32 >= cus) {
         const dim3 grid(unsigned((seq + 31) / 32), unsigned(heads), unsigned(batch));
         hipLaunchKernelGGL(attention_kernel<32>, grid, dim3(256), 0, as_stream(stream), Q, ldq, K,

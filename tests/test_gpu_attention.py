@@ -30,7 +30,14 @@ def check_attention(Q, K, V, ctx_gpu, batch, seq, heads):
 
 @pytest.mark.parametrize("batch,seq,heads,sd", [(1, 128, 12, 1.0), (2, 77, 3, 1.0), (1, 1, 1, 1.0),
                                                 (1, 33, 2, 4.0), (3, 64, 4, 0.3), (1, 200, 1, 2.0),
-                                                (8, 512, 2, 1.0), (1, 65, 1, 8.0)])
+                                                (8, 512, 2, 1.0), (1, 65, 1, 8.0),
+                                                (1, 256, 3, 1.0), (2, 300, 2, 2.0),
+                                                (1, 1000, 1, 1.0), (4, 257, 2, 0.5),
+                                                (1, 384, 12, 4.0),
+                                                # matrix-core kernel (>= 768 tiles of 32 queries)
+                                                (8, 512, 6, 1.0), (16, 256, 12, 1.0),
+                                                (8, 300, 12, 2.0), (3, 1000, 12, 0.5),
+                                                (24, 130, 12, 4.0)])
 def test_attention_matches_oracle(device, batch, seq, heads, sd):
     g = rng(9500 + batch * 1000 + seq + heads)
     T, W = batch * seq, heads * 64
