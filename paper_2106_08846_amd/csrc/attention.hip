@@ -27,6 +27,7 @@ constexpr int kKB = 64;       // keys per block
 constexpr int kD = 64;        // head width
 constexpr int kPitch = 68;    // LDS row pitch, floats
 constexpr int kMfmaMinSeq = 128;   // shortest sequence for the matrix-core kernel
+constexpr int kSplitBelow = 2;     // key-split 8-query tiles below this many tiles per CU
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
@@ -151,6 +152,169 @@ __global__ __launch_bounds__(kQT * 8) void attention_kernel(
                 acc[e] = __builtin_fmaf(p, v0[e], acc[e]);
                 acc[4 + e] = __builtin_fmaf(p, v1[e], acc[4 + e]);
             }
+        }
+    }
+    if (qvalid) {
+        float *op = O + (tok0 + qrow) * ldo + h * kD + 8 * u;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) op[e] = acc[e] / l;
+    }
+}
+
+// Short sequences with few (sequence, head) pairs: kKS groups of 8 queries x 8 lanes (one wave
+// each) serve the same queries; group ks takes the key blocks ks, ks + kKS, ... with the online
+// softmax above, and the groups' partial results are merged at the end.  Each group has its own
+// K, V and P buffers in (dynamic) LDS.
+template <int kKS>
+__global__ __launch_bounds__(64 * kKS) void attention_split_kernel(
+    const float *__restrict__ Q, int64_t ldq, const float *__restrict__ K, int64_t ldk,
+    const float *__restrict__ V, int64_t ldv, float *__restrict__ O, int64_t ldo, int seq,
+    float scale) {
+    constexpr int kQT = 8;
+    constexpr int kThreads = kQT * 8;             // threads per group
+    constexpr int kGroupFloats = 2 * kKB * kPitch + kQT * kPitch;
+    extern __shared__ float smem[];
+    const int ks = threadIdx.x / kThreads, tid = threadIdx.x % kThreads;
+    float *Ks = smem + ks * kGroupFloats;
+    float *Vs = Ks + kKB * kPitch;
+    float *Ps = Vs + kKB * kPitch;
+    const int qi = tid >> 3, u = tid & 7;
+    const int q0 = blockIdx.x * kQT, h = blockIdx.y;
+    const int64_t tok0 = int64_t(blockIdx.z) * seq;
+    const int qrow = q0 + qi;
+    const bool qvalid = qrow < seq;
+
+    // This thread's query row, pre-scaled (rows past the sequence read row 0; never stored).
+    float q[kD];
+    {
+        const float *qp = Q + (tok0 + (qvalid ? qrow : 0)) * ldq + h * kD;
+#pragma unroll
+        for (int d = 0; d < kD; d += 4) {
+            const floatx4 v = load4(qp + d);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) q[d + e] = v[e] * scale;
+        }
+    }
+    float m = -INFINITY, l = 0.0f, acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+
+    // Every group runs the same number of rounds (and barriers); a group whose block is past
+    // the end of the sequence idles through its round.
+    const int nblk = (seq + kKB - 1) / kKB;
+    const int rounds = (nblk + kKS - 1) / kKS;
+    for (int it = 0; it < rounds; ++it) {
+        const int k0 = (ks + kKS * it) * kKB;
+        const bool active = k0 < seq;
+        __syncthreads();   // the previous block's LDS reads are done
+        // Stage K and V rows k0 .. k0 + 63 of this head (rows past the sequence are zero).
+        // Four 16-byte pieces of K and of V per thread in flight, then their LDS stores.
+        constexpr int kPer = kKB * (kD / 4) / kThreads;   // pieces per thread
+        constexpr int kBatch = kPer < 4 ? kPer : 4;
+        if (active) {
+#pragma unroll
+            for (int n0 = 0; n0 < kPer; n0 += kBatch) {
+                floatx4 kst[kBatch], vst[kBatch];
+#pragma unroll
+                for (int n = 0; n < kBatch; ++n) {
+                    const int i = tid + (n0 + n) * kThreads;
+                    const int r = i >> 4, c4 = (i & 15) * 4;
+                    const int key = k0 + r < seq ? k0 + r : seq - 1;   // past the end: zeroed
+                    kst[n] = load4(K + (tok0 + key) * ldk + h * kD + c4);
+                    vst[n] = load4(V + (tok0 + key) * ldv + h * kD + c4);
+                }
+#pragma unroll
+                for (int n = 0; n < kBatch; ++n) {
+                    const int i = tid + (n0 + n) * kThreads;
+                    const int r = i >> 4, c4 = (i & 15) * 4;
+                    const floatx4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+                    *reinterpret_cast<floatx4 *>(&Ks[r * kPitch + c4]) = k0 + r < seq ? kst[n] : z;
+                    *reinterpret_cast<floatx4 *>(&Vs[r * kPitch + c4]) = k0 + r < seq ? vst[n] : z;
+                }
+            }
+        }
+        __syncthreads();
+
+        if (active) {
+            // Scores of keys u + 8j (j < 8), the eight dot products advanced together (eight
+            // independent FMA chains); keys past the sequence get -inf (weight 0).
+            float s[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s[j] = 0.0f;
+#pragma unroll
+            for (int d = 0; d < kD; d += 4) {
+                floatx4 kv[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) kv[j] = load4(&Ks[(u + 8 * j) * kPitch + d]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) s[j] = __builtin_fmaf(q[d + e], kv[j][e], s[j]);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (k0 + u + 8 * j >= seq) s[j] = -INFINITY;
+            float bm = s[0];
+#pragma unroll
+            for (int j = 1; j < 8; ++j) bm = fmaxf(bm, s[j]);
+            const float mn = fmaxf(m, row_max8(bm));   // finite: key k0 exists
+            const float corr = expf(m - mn);           // 0 on the group's first block
+            float ps = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float p = expf(s[j] - mn);
+                ps += p;
+                Ps[qi * kPitch + u + 8 * j] = p;
+            }
+            l = l * corr + row_sum8(ps);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] *= corr;
+            m = mn;
+        }
+        __syncthreads();   // the row's weights are in LDS
+
+        if (active) {
+            const float *pr = &Ps[qi * kPitch];
+#pragma unroll 8
+            for (int r = 0; r < kKB; ++r) {
+                const float p = pr[r];
+                const floatx4 v0 = load4(&Vs[r * kPitch + 8 * u]);
+                const floatx4 v1 = load4(&Vs[r * kPitch + 8 * u + 4]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[e] = __builtin_fmaf(p, v0[e], acc[e]);
+                    acc[4 + e] = __builtin_fmaf(p, v1[e], acc[4 + e]);
+                }
+            }
+        }
+    }
+    {
+        // Merge the groups in group order: with M the largest running maximum,
+        // out = sum_g acc_g exp(m_g - M) / sum_g l_g exp(m_g - M).  A group that saw no key
+        // has m = -inf, l = 0 and adds nothing; group 0 always saw key 0.
+        constexpr int kSlot = 8 * 8 + 2;   // per thread: acc, then m and l
+        __syncthreads();
+        float *C = smem + (ks * kThreads + tid) * kSlot;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) C[e] = acc[e];
+        C[64] = m;
+        C[65] = l;
+        __syncthreads();
+        if (ks != 0) return;
+        float M = m;
+#pragma unroll
+        for (int g = 1; g < kKS; ++g) M = fmaxf(M, smem[(g * kThreads + tid) * kSlot + 64]);
+        const float w0 = expf(m - M);
+        l *= w0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] *= w0;
+#pragma unroll
+        for (int g = 1; g < kKS; ++g) {
+            const float *Cg = smem + (g * kThreads + tid) * kSlot;
+            const float w = expf(Cg[64] - M);   // 0 for a group without keys
+            l = __builtin_fmaf(Cg[65], w, l);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = __builtin_fmaf(Cg[e], w, acc[e]);
         }
     }
     if (qvalid) {
@@ -324,17 +488,29 @@ bsr_status launch_attention(const float *Q, int64_t ldq, const float *K, int64_t
         }
         return launch_status();
     }
-    // Vector-ALU kernel: 32-query tiles when they give at least one workgroup per CU, else
-    // 8-query tiles.
+    // Vector-ALU kernels: 32-query tiles when they give at least one workgroup per CU, else
+    // 8-query tiles; when even those give fewer than kSplitBelow waves per CU, two or four
+    // waves split the keys of each tile.
+    const int nblk = (seq + kKB - 1) / kKB;
+    const int64_t tiles8 = int64_t((seq + 7) / 8) * heads * batch;
     if (tiles32 >= cus) {
         const dim3 grid(unsigned((seq + 31) / 32), unsigned(heads), unsigned(batch));
         hipLaunchKernelGGL(attention_kernel<32>, grid, dim3(256), 0, as_stream(stream), Q, ldq, K,
                            ldk, V, ldv, O, ldo, seq, scale);
-    } else {
-        const dim3 grid(unsigned((seq + 7) / 8), unsigned(heads), unsigned(batch));
+        return launch_status();
+    }
+    const dim3 grid(unsigned((seq + 7) / 8), unsigned(heads), unsigned(batch));
+    const int ks = tiles8 >= kSplitBelow * int64_t(cus) || nblk < 2 ? 1 : (nblk < 4 ? 2 : 4);
+    const size_t lds = size_t(ks) * (2 * kKB * kPitch + 8 * kPitch) * sizeof(float);
+    if (ks == 1)
         hipLaunchKernelGGL(attention_kernel<8>, grid, dim3(64), 0, as_stream(stream), Q, ldq, K,
                            ldk, V, ldv, O, ldo, seq, scale);
-    }
+    else if (ks == 2)
+        hipLaunchKernelGGL(attention_split_kernel<2>, grid, dim3(128), lds, as_stream(stream), Q,
+                           ldq, K, ldk, V, ldv, O, ldo, seq, scale);
+    else
+        hipLaunchKernelGGL(attention_split_kernel<4>, grid, dim3(256), lds, as_stream(stream), Q,
+                           ldq, K, ldk, V, ldv, O, ldo, seq, scale);
     return launch_status();
 }
 
