@@ -65,13 +65,21 @@ bsr_status ensure_device() {
     return ok ? BSR_OK : BSR_ERR_ARCH;
 }
 
-int auto_slices(int64_t total_tiles, int64_t Nb, int cu_count) {
-    // Enough workgroups to give every CU one: token tiles (over every product of the launch)
-    // times slices >= CUs, with at least one block-row per slice.
-    int64_t S = (cu_count > 0 ? cu_count : 256) / (total_tiles > 0 ? total_tiles : 1);
-    if (S < 1) S = 1;
-    if (S > Nb) S = Nb;
-    return int(S);
+int auto_slices(const int64_t *tiles, int n, int cu_count) {
+    // The largest slice count S with every workgroup resident at once: a product of t token
+    // tiles launches ceil(t S / 8) workgroups per XCD (its grid is rounded to a multiple of 8
+    // and dealt round robin to the 8 XCDs), and an XCD runs one workgroup per CU at a time
+    // (the X tile fills most of a CU's LDS).  One more workgroup per XCD than it has CUs
+    // would start a second round and nearly double the time.
+    const int64_t per_xcd = (cu_count > 0 ? cu_count : 256) / 8;
+    int best = 1;
+    for (int S = 2; S <= 1024; ++S) {
+        int64_t wgs = 0;
+        for (int i = 0; i < n; ++i) wgs += (tiles[i] * S + 7) / 8;
+        if (wgs > per_xcd) break;
+        best = S;
+    }
+    return best;
 }
 
 int device_cu_count() {
@@ -159,7 +167,6 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     std::vector<bsr::TiledWork> tiled(work.size());
     std::vector<bsr::KchunkWork> kchunk(work.size());
     std::vector<int> kind(work.size(), kGeneric);
-    int64_t total_tiles = 0;
     for (size_t w = 0; w < work.size(); ++w) {
         const bsr_spmm_item_t &it = items[work[w]];
         const int R = it.W->R, C = it.W->C, dt = it.W->dtype;
@@ -176,28 +183,9 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
                  bsr::vtile_supported(R, C, dt) &&
                  bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok)
             kind[w] = kVtile;
-        if (kind[w] != kGeneric) total_tiles += (it.T + 31) / 32;
         if (kind[w] == kGeneric && (kernel == BSR_KERNEL_TILED || kernel == BSR_KERNEL_VALU))
             return BSR_ERR_UNSUPPORTED;
     }
-    for (size_t w = 0; w < work.size(); ++w) {
-        if (kind[w] == kGeneric) continue;
-        const bsr_spmm_item_t &it = items[work[w]];
-        const int S = slices > 0
-                          ? slices
-                          : bsr::auto_slices(total_tiles, it.W->n_rows / it.W->R, cus);
-        if (kind[w] == kKchunk) {
-            const bsr::KchunkPlan kp =
-                bsr::plan_kchunk(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
-            kchunk[w] = bsr::KchunkWork{kp, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
-            continue;
-        }
-        const bsr::TiledPlan plan =
-            kind[w] == kTiled ? bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit)
-                              : bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
-        tiled[w] = bsr::TiledWork{plan, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
-    }
-
     // Launch order: tiled and vector-ALU products grouped by kernel, block shape and dtype, up
     // to kMaxItems per launch, then generic products one by one.  With an event pair, the start
     // event goes with the first launch and the stop event with the last.
@@ -227,6 +215,31 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     }
     for (size_t w = 0; w < work.size(); ++w)
         if (kind[w] == kGeneric) launches.push_back(Launch{kGeneric, {int(w)}});
+
+    // Slices per launch: the automatic count is chosen for the token tiles of the products
+    // that share the launch (launches run one after another).
+    for (const Launch &l : launches) {
+        if (l.kind == kGeneric) continue;
+        std::vector<int64_t> tiles;
+        for (int w : l.members) tiles.push_back((items[work[w]].T + 31) / 32);
+        const int auto_S = bsr::auto_slices(tiles.data(), int(tiles.size()), cus);
+        for (int w : l.members) {
+            const bsr_spmm_item_t &it = items[work[w]];
+            const int64_t Nb = it.W->n_rows / it.W->R;
+            const int S = slices > 0 ? slices : int(auto_S < Nb ? auto_S : Nb);
+            if (kind[w] == kKchunk) {
+                const bsr::KchunkPlan kp =
+                    bsr::plan_kchunk(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
+                kchunk[w] = bsr::KchunkWork{kp, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
+                continue;
+            }
+            const bsr::TiledPlan plan =
+                kind[w] == kTiled
+                    ? bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit)
+                    : bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
+            tiled[w] = bsr::TiledWork{plan, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
+        }
+    }
 
     for (size_t li = 0; li < launches.size(); ++li) {
         bsr::LaunchEvents lev;

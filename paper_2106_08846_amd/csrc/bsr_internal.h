@@ -40,7 +40,7 @@ bsr_status check_attention(const float *Q, int64_t ldq, const float *K, int64_t 
 // Device-side entry points (implemented in the .hip files).  Arguments are already validated.
 bsr_status ensure_device();  // current device is gfx950; caches its properties
 int device_cu_count();
-int auto_slices(int64_t total_tiles, int64_t Nb, int cu_count);
+int auto_slices(const int64_t *tiles, int n, int cu_count);  // token tiles per product
 size_t device_lds_per_block();
 
 bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,
