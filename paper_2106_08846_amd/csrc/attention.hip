@@ -338,18 +338,23 @@ __global__ __launch_bounds__(64 * kKS) void attention_split_kernel(
 //   lane's weight p[v], so the weights never leave their registers.
 // The online softmax is the one above (running maximum and sum per query, output rescaled by
 // exp(m_old - m_new)); each query's running values are kept, identical, in both its lanes.
-template <int kWQ>
-__global__ __launch_bounds__(kWQ * 64) void attention_mfma_kernel(
+template <int kWQ, int kKS>
+__global__ __launch_bounds__(kWQ * kKS * 64) __attribute__((amdgpu_waves_per_eu(3)))
+void attention_mfma_kernel(
     const float *__restrict__ Q, int64_t ldq, const float *__restrict__ K, int64_t ldk,
     const float *__restrict__ V, int64_t ldv, float *__restrict__ O, int64_t ldo, int seq,
     float scale) {
+    // kKS = 2: two waves serve each query tile, one taking the first 32 keys of every staged
+    // block and the other the second 32, and merge their results at the end.
+    static_assert(kKS == 1 || kKS == 2, "one or two waves per query tile");
     typedef float floatx16 __attribute__((ext_vector_type(16)));
-    constexpr int kThreads = kWQ * 64;
+    constexpr int kThreads = kWQ * kKS * 64;
     __shared__ float Ks[kKB * kPitch];
     __shared__ float Vs[kKB * kPitch];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int qw = wave % kWQ, ks = wave / kWQ;
     const int ql = lane & 31, hh = lane >> 5;
-    const int qrow = (blockIdx.x * kWQ + wave) * 32 + ql, h = blockIdx.y;
+    const int qrow = (blockIdx.x * kWQ + qw) * 32 + ql, h = blockIdx.y;
     const int64_t tok0 = int64_t(blockIdx.z) * seq;
     const bool qvalid = qrow < seq;
 
@@ -398,7 +403,8 @@ __global__ __launch_bounds__(kWQ * 64) void attention_mfma_kernel(
         __syncthreads();
 
 #pragma unroll
-        for (int g = 0; g < kKB / 32; ++g) {
+        for (int gi = 0; gi < kKB / 32 / kKS; ++gi) {
+            const int g = gi * kKS + ks;
             const int kg = k0 + 32 * g;
             if (kg >= seq) break;   // the whole group is past the end
             floatx16 s;
@@ -445,6 +451,35 @@ __global__ __launch_bounds__(kWQ * 64) void attention_mfma_kernel(
             }
         }
     }
+    if constexpr (kKS == 2) {
+        // Merge the two key halves: the second wave of each tile leaves its running maximum,
+        // sum and output in LDS (the K buffer is free after the barrier); the first adds
+        // them, both rescaled to the larger maximum.  A wave that saw no key (sequences of at
+        // most 32) has m = -inf, l = 0 and adds nothing.
+        constexpr int kSlot = 34;   // floats per lane: o0, o1, m, l
+        static_assert(kWQ * 64 * kSlot <= kKB * kPitch, "merge buffer fits in the K buffer");
+        __syncthreads();
+        float *C = Ks + (qw * 64 + lane) * kSlot;
+        if (ks == 1) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                C[v] = o0[v];
+                C[16 + v] = o1[v];
+            }
+            C[32] = m;
+            C[33] = l;
+        }
+        __syncthreads();
+        if (ks == 1) return;
+        const float m1 = C[32], M = fmaxf(m, m1);
+        const float w0 = expf(m - M), w1 = expf(m1 - M);
+        l = l * w0 + C[33] * w1;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            o0[v] = o0[v] * w0 + C[v] * w1;
+            o1[v] = o1[v] * w0 + C[16 + v] * w1;
+        }
+    }
     // Register v of tile t holds O[query][32t + 8(v/4) + 4hh + v%4]: four consecutive columns
     // per group of four registers, stored as 16 bytes.
     if (qvalid) {
@@ -473,18 +508,17 @@ bsr_status launch_attention(const float *Q, int64_t ldq, const float *K, int64_t
     // The matrix-core kernel when there are at least three 32-query tiles per CU and
     // sequences of kMfmaMinSeq keys or more (its per-wave chain of key groups is long, so it
     // needs many waves; measured on MI355X, fewer tiles or shorter sequences run faster on the
-    // vector ALUs).  Four query tiles per workgroup when that still gives every CU a
-    // workgroup, else one.
+    // vector ALUs).  Up to eight tiles per CU, two waves split each tile's keys (twice the
+    // waves); beyond that, four tiles share each workgroup's staged keys.
     if (seq >= kMfmaMinSeq && tiles32 >= 3 * int64_t(cus)) {
-        const int64_t wg4 = int64_t((seq + 127) / 128) * heads * batch;
-        if (wg4 >= cus) {
+        if (tiles32 >= 8 * int64_t(cus)) {
             const dim3 grid(unsigned((seq + 127) / 128), unsigned(heads), unsigned(batch));
-            hipLaunchKernelGGL(attention_mfma_kernel<4>, grid, dim3(256), 0, as_stream(stream), Q,
-                               ldq, K, ldk, V, ldv, O, ldo, seq, scale);
+            hipLaunchKernelGGL((attention_mfma_kernel<4, 1>), grid, dim3(256), 0,
+                               as_stream(stream), Q, ldq, K, ldk, V, ldv, O, ldo, seq, scale);
         } else {
-            const dim3 grid(unsigned((seq + 31) / 32), unsigned(heads), unsigned(batch));
-            hipLaunchKernelGGL(attention_mfma_kernel<1>, grid, dim3(64), 0, as_stream(stream), Q,
-                               ldq, K, ldk, V, ldv, O, ldo, seq, scale);
+            const dim3 grid(unsigned((seq + 63) / 64), unsigned(heads), unsigned(batch));
+            hipLaunchKernelGGL((attention_mfma_kernel<2, 2>), grid, dim3(256), 0,
+                               as_stream(stream), Q, ldq, K, ldk, V, ldv, O, ldo, seq, scale);
         }
         return launch_status();
     }
