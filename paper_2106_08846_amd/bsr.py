@@ -127,8 +127,16 @@ def _check(status: int, where: str) -> None:
         raise BSRError(status, where, detail)
 
 
+# torch's current stream as a raw handle, without building a torch.cuda.Stream object (that
+# costs about 3 us per call, more than a kernel launch's host time here).
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_cur_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
 def _stream(stream) -> int | None:
     if stream is None:
+        if _raw_stream is not None and _cur_device is not None:
+            return _raw_stream(_cur_device())
         return torch.cuda.current_stream().cuda_stream
     if isinstance(stream, torch.cuda.Stream):
         return stream.cuda_stream
@@ -459,9 +467,10 @@ class AttentionBlockCall:
         return self.ctx
 
     def __call__(self, stream=None) -> torch.Tensor:
-        self.qkv(stream)
-        self.attention(stream)
-        return self.out(stream)
+        st = _stream(stream)
+        self.qkv(st)
+        self.attention(st)
+        return self.out(st)
 
 
 def bsr_cast_f32_bf16(src: torch.Tensor, dst: torch.Tensor | None = None,
