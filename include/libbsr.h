@@ -167,8 +167,9 @@ LIBBSR_API bsr_status bsr_prune_from_dense_ex(const float *W, int64_t N, int64_t
  *   bit patterns); x_dtype must equal W->dtype.
  * W: host pointer to a bsr_matrix_t describing device arrays.
  * bias: device fp32[N] or NULL.  Y: device fp32, T x N with row pitch ldy.
- * T = 0 is a no-op.  Errors: BSR_ERR_NULL, BSR_ERR_SHAPE, BSR_ERR_ARG, BSR_ERR_DTYPE,
- *   BSR_ERR_UNSUPPORTED, BSR_ERR_ARCH, BSR_ERR_HIP.
+ * T = 0 is a no-op.  Errors: BSR_ERR_NULL, BSR_ERR_SHAPE, BSR_ERR_ARG (also: the byte range
+ *   of Y overlaps X, bias or W's arrays), BSR_ERR_DTYPE, BSR_ERR_UNSUPPORTED, BSR_ERR_ARCH,
+ *   BSR_ERR_HIP.
  */
 LIBBSR_API bsr_status bsr_spmm(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
                     const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
@@ -273,10 +274,12 @@ LIBBSR_API bsr_status bsr_attention(const float *Q, int64_t ldq, const float *K,
  * pruned with a large block (64 x 64, 1 x 64 ... 1 x 384, 64 x 1) then runs on the product
  * kernels of a divisor shape (32 x 32, 1 x 32, 32 x 1) with unchanged results up to the order
  * of the sums.
- * Outputs (device, caller-owned, not overlapping W's arrays): indptr_out int32[N/R2 + 1],
+ * Outputs (device, caller-owned, not overlapping W's arrays or each other): indptr_out
+ *   int32[N/R2 + 1],
  * indices_out int32[nnzb*a*b], data_out [nnzb*a*b][R2][C2] elements of W's dtype.  The fine
  * matrix is {N, K, R2, C2, nnzb*a*b, indptr_out, indices_out, data_out, W->dtype}.
- * Errors: BSR_ERR_NULL, BSR_ERR_ARG (W's dtype or nnzb), BSR_ERR_SHAPE (W's shape, or R2 or C2
+ * Errors: BSR_ERR_NULL, BSR_ERR_ARG (W's dtype or nnzb, or overlapping byte ranges of the
+ *   arrays), BSR_ERR_SHAPE (W's shape, or R2 or C2
  *   not a positive divisor of R or C), BSR_ERR_UNSUPPORTED (more than 2^31 - 1 fine blocks),
  *   BSR_ERR_ARCH, BSR_ERR_HIP.
  */

@@ -138,7 +138,8 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     if (n_items > 0 && !items) return BSR_ERR_NULL;
     for (int32_t i = 0; i < n_items; ++i) {
         const bsr_spmm_item_t &it = items[i];
-        bsr_status s = bsr::check_spmm(it.X, int(it.x_dtype), it.T, it.ldx, it.W, it.Y, it.ldy);
+        bsr_status s =
+            bsr::check_spmm(it.X, int(it.x_dtype), it.T, it.ldx, it.W, it.Y, it.ldy, it.bias);
         if (s != BSR_OK) return s;
     }
     const int kernel = opts ? opts->kernel : BSR_KERNEL_AUTO;

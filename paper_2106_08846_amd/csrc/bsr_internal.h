@@ -26,7 +26,7 @@ bsr_status check_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_
 bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32_t R, int64_t k);
 bsr_status check_matrix(const bsr_matrix_t *W);
 bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const bsr_matrix_t *W,
-                      const float *Y, int64_t ldy);
+                      const float *Y, int64_t ldy, const float *bias);
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo);
 bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
 bsr_status check_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2,

@@ -74,8 +74,25 @@ bsr_status check_matrix(const bsr_matrix_t *W) {
     return BSR_OK;
 }
 
+namespace {
+
+// Whether the byte ranges [a, a + na) and [b, b + nb) intersect (empty ranges never do).
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+    if (!a || !b || na <= 0 || nb <= 0) return false;
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return pa < pb + uint64_t(nb) && pb < pa + uint64_t(na);
+}
+
+// Bytes spanned by the arrays of a valid matrix.
+int64_t indptr_bytes(const bsr_matrix_t *W) { return (W->n_rows / W->R + 1) * 4; }
+int64_t data_bytes(const bsr_matrix_t *W) {
+    return W->nnzb * W->R * W->C * (W->dtype == BSR_BF16 ? 2 : 4);
+}
+
+}  // namespace
+
 bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const bsr_matrix_t *W,
-                      const float *Y, int64_t ldy) {
+                      const float *Y, int64_t ldy, const float *bias) {
     if (!W) return BSR_ERR_NULL;
     bsr_status s = check_matrix(W);
     if (s != BSR_OK) return s;
@@ -84,6 +101,15 @@ bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const 
     if (T < 0 || ldx < W->n_cols || ldy < W->n_rows) return BSR_ERR_SHAPE;
     if (T > 0 && (!X || !Y)) return BSR_ERR_NULL;
     if (T > kMaxElems / ldx || T > kMaxElems / ldy) return BSR_ERR_UNSUPPORTED;
+    if (T > 0) {
+        // Y must not overlap the product's inputs.
+        const int64_t yb = ((T - 1) * ldy + W->n_rows) * 4;
+        const int64_t xb = ((T - 1) * ldx + W->n_cols) * (x_dtype == BSR_BF16 ? 2 : 4);
+        if (overlaps(Y, yb, X, xb) || overlaps(Y, yb, bias, W->n_rows * 4) ||
+            overlaps(Y, yb, W->indptr, indptr_bytes(W)) ||
+            overlaps(Y, yb, W->indices, W->nnzb * 4) || overlaps(Y, yb, W->data, data_bytes(W)))
+            return BSR_ERR_ARG;
+    }
     return BSR_OK;
 }
 
@@ -109,6 +135,18 @@ bsr_status check_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2,
     const int64_t Nb = W->n_rows / R2, Kb = W->n_cols / C2;
     if (Nb > kMaxBlocks / Kb) return BSR_ERR_UNSUPPORTED;
     if (W->nnzb > kMaxBlocks / pieces) return BSR_ERR_UNSUPPORTED;
+    // Outputs must not overlap the inputs or each other.
+    const int64_t n2 = W->nnzb * pieces;
+    const int64_t outs[3] = {(Nb + 1) * 4, n2 * 4, data_bytes(W)};
+    const void *optr[3] = {indptr_out, indices_out, data_out};
+    const void *iptr[3] = {W->indptr, W->indices, W->data};
+    const int64_t ins[3] = {indptr_bytes(W), W->nnzb * 4, data_bytes(W)};
+    for (int i = 0; i < 3; ++i) {
+        for (int j = 0; j < 3; ++j)
+            if (overlaps(optr[i], outs[i], iptr[j], ins[j])) return BSR_ERR_ARG;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(optr[i], outs[i], optr[j], outs[j])) return BSR_ERR_ARG;
+    }
     return BSR_OK;
 }
 

@@ -87,6 +87,7 @@ def test_prune_workspace_bytes(lib):
 
 
 FAKE = 0x10000  # never dereferenced: every call below fails validation first
+FAKE_Y = 0x20000  # an output address whose range stays clear of FAKE's inputs
 
 
 def _prune(lib, W=FAKE, N=64, K=64, ldw=64, R=8, C=8, k=6, indptr=FAKE, indices=FAKE,
@@ -110,7 +111,7 @@ def _matrix(L, N=64, K=64, R=8, C=8, nnzb=6, indptr=FAKE, indices=FAKE, data=FAK
     return L.bsr_matrix_t(N, K, R, C, nnzb, indptr, indices, data, dtype)
 
 
-def _spmm(L, lib, m=None, X=FAKE, x_dtype=0, T=4, ldx=64, Y=FAKE, ldy=64):
+def _spmm(L, lib, m=None, X=FAKE, x_dtype=0, T=4, ldx=64, Y=FAKE_Y, ldy=64):
     m = m if m is not None else _matrix(L)
     return lib.bsr_spmm(X, x_dtype, T, ldx, ctypes.byref(m), None, Y, ldy, None)
 
@@ -125,6 +126,19 @@ def _spmm(L, lib, m=None, X=FAKE, x_dtype=0, T=4, ldx=64, Y=FAKE, ldy=64):
 ])
 def test_spmm_errors(L, lib, kw, mkw, status):
     assert _spmm(L, lib, m=_matrix(L, **mkw), **kw) == status
+
+
+@pytest.mark.parametrize("where", ["X", "bias", "indptr", "indices", "data"])
+def test_spmm_output_overlapping_an_input(L, lib, where):
+    """Y's byte range (T x ldy fp32 = 4 x 64 x 4 bytes from 0x100000) overlapping an input is
+    BSR_ERR_ARG."""
+    Y = 0x100000
+    inside, outside = Y + 1000, Y + 4096
+    ptrs = {"X": outside, "bias": outside, "indptr": 0x200000, "indices": 0x300000,
+            "data": 0x400000}
+    ptrs[where] = inside
+    m = _matrix(L, indptr=ptrs["indptr"], indices=ptrs["indices"], data=ptrs["data"])
+    assert lib.bsr_spmm(ptrs["X"], 0, 4, 64, ctypes.byref(m), ptrs["bias"], Y, 64, None) == 3
 
 
 def test_spmm_null_matrix(lib):
@@ -152,6 +166,8 @@ def test_to_dense_errors(L, lib, mkw, ldo, out, status):
     ({"R": 7}, 1, 1, (FAKE, FAKE, FAKE), 2), ({"nnzb": 65}, 4, 4, (FAKE, FAKE, FAKE), 3),
     ({"dtype": 3}, 4, 4, (FAKE, FAKE, FAKE), 3),
     ({"N": 1 << 20, "K": 1 << 20, "R": 64, "C": 64}, 1, 1, (FAKE, FAKE, FAKE), 9),
+    ({}, 4, 4, (FAKE, 0x200000, 0x300000), 3),          # indptr_out over W's indptr (FAKE)
+    ({}, 4, 4, (0x200000, 0x200000 + 8, 0x300000), 3),  # indices_out inside indptr_out
 ])
 def test_reblock_errors(L, lib, mkw, R2, C2, outs, status):
     m = _matrix(L, **mkw)
@@ -183,7 +199,7 @@ def test_spmm_ex_option_errors(L, lib, kernel, slices, start, stop):
 
 
 
-def _item(L, m, X=FAKE, x_dtype=0, T=4, ldx=64, Y=FAKE, ldy=64):
+def _item(L, m, X=FAKE, x_dtype=0, T=4, ldx=64, Y=FAKE_Y, ldy=64):
     return L.bsr_spmm_item_t(X, x_dtype, T, ldx, ctypes.pointer(m), None, Y, ldy)
 
 
