@@ -142,7 +142,7 @@ def calibrate_copy(args) -> int:
 def main() -> int:
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no "
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library has no "
               "multi-GPU path, so run it with --gpus 1.", file=sys.stderr, flush=True)
         return 2
 

@@ -14,7 +14,9 @@ def test_draws_are_seeded_and_scaled():
     assert not np.array_equal(a, c)
 
 
-# Row counts of the capped Zipf(1.2) allocation, worked out independently in the design survey.
+# Row counts of the capped Zipf(1.2) allocation (shares of the total in proportion to r^-1.2, rows
+# over the cap pinned there and the excess re-spread, then largest-remainder rounding), worked
+# out independently of the generator.
 ZIPF_32x1 = [1024, 467, 287, 203, 156, 125, 104, 88, 77, 68, 60, 54, 49, 45, 42, 39, 36, 33, 31,
              29, 28, 26, 25, 24, 23, 22, 21, 20, 19, 18, 17, 17]
 ZIPF_32x32 = [32, 14, 9, 6, 5, 4, 3, 3, 2, 2, 2, 2] + [1] * 18 + [0, 0]
