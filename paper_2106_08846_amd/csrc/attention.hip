@@ -505,12 +505,12 @@ bsr_status launch_attention(const float *Q, int64_t ldq, const float *K, int64_t
                             int seq, int heads, float scale, void *stream) {
     const int64_t tiles32 = int64_t((seq + 31) / 32) * heads * batch;
     const int cus = device_cu_count() > 0 ? device_cu_count() : 256;
-    // The matrix-core kernel when there are at least three 32-query tiles per CU and
-    // sequences of kMfmaMinSeq keys or more (its per-wave chain of key groups is long, so it
-    // needs many waves; measured on MI355X, fewer tiles or shorter sequences run faster on the
-    // vector ALUs).  Up to eight tiles per CU, two waves split each tile's keys (twice the
+    // The matrix-core kernel for sequences of 2 * kMfmaMinSeq keys or more, and for sequences
+    // of kMfmaMinSeq keys or more when there are at least three 32-query tiles per CU (its
+    // per-wave chain of key groups is long; measured on MI355X, shorter sequences with fewer
+    // tiles run faster on the vector ALUs).  Up to eight tiles per CU, two waves split each tile's keys (twice the
     // waves); beyond that, four tiles share each workgroup's staged keys.
-    if (seq >= kMfmaMinSeq && tiles32 >= 3 * int64_t(cus)) {
+    if (seq >= 2 * kMfmaMinSeq || (seq >= kMfmaMinSeq && tiles32 >= 3 * int64_t(cus))) {
         if (tiles32 >= 8 * int64_t(cus)) {
             const dim3 grid(unsigned((seq + 127) / 128), unsigned(heads), unsigned(batch));
             hipLaunchKernelGGL((attention_mfma_kernel<4, 1>), grid, dim3(256), 0,

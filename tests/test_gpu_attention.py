@@ -34,8 +34,11 @@ def check_attention(Q, K, V, ctx_gpu, batch, seq, heads):
                                                 (1, 256, 3, 1.0), (2, 300, 2, 2.0),
                                                 (1, 1000, 1, 1.0), (4, 257, 2, 0.5),
                                                 (1, 384, 12, 4.0),
+                                                # vector kernel, 32-query tiles; key split
+                                                # with an idle round
+                                                (24, 64, 12, 1.0), (8, 200, 12, 2.0),
+                                                (1, 150, 2, 1.0),
                                                 # matrix-core kernel, key halves on two waves
-                                                # (768 .. 2047 tiles of 32 queries)
                                                 (8, 512, 6, 1.0), (16, 256, 12, 1.0),
                                                 (8, 300, 12, 2.0), (3, 1000, 12, 0.5),
                                                 (24, 130, 12, 4.0),
