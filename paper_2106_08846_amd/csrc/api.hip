@@ -154,9 +154,9 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
 
     // Plan: every non-empty product goes to the matrix-core tiled kernel when it has the shape,
     // or, when its X tile is too wide for LDS, to the column-chunked matrix-core kernel; else to
-    // the vector-ALU tile kernel, else to the generic kernel (a forced kernel choice narrows
-    // this; a forced tiled kernel that does not fit is an error).
-    enum Kind { kGeneric = 0, kTiled = 1, kVtile = 2, kKchunk = 3 };
+    // the vector-ALU tile kernel or its column-chunked form; else to the generic kernel (a
+    // forced kernel choice narrows this; a forced kernel that does not fit is an error).
+    enum Kind { kGeneric = 0, kTiled = 1, kVtile = 2, kKchunk = 3, kVchunk = 4 };
     std::vector<int> work;
     for (int32_t i = 0; i < n_items; ++i)
         if (items[i].T > 0) work.push_back(i);
@@ -184,6 +184,10 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
                  bsr::vtile_supported(R, C, dt) &&
                  bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).ok)
             kind[w] = kVtile;
+        else if ((kernel == BSR_KERNEL_AUTO || kernel == BSR_KERNEL_VALU) &&
+                 bsr::vtile_supported(R, C, dt) &&
+                 bsr::plan_vchunk(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).base.ok)
+            kind[w] = kVchunk;
         if (kind[w] == kGeneric && (kernel == BSR_KERNEL_TILED || kernel == BSR_KERNEL_VALU))
             return BSR_ERR_UNSUPPORTED;
     }
@@ -228,9 +232,11 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
             const bsr_spmm_item_t &it = items[work[w]];
             const int64_t Nb = it.W->n_rows / it.W->R;
             const int S = slices > 0 ? slices : int(auto_S < Nb ? auto_S : Nb);
-            if (kind[w] == kKchunk) {
+            if (kind[w] == kKchunk || kind[w] == kVchunk) {
                 const bsr::KchunkPlan kp =
-                    bsr::plan_kchunk(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
+                    kind[w] == kKchunk
+                        ? bsr::plan_kchunk(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit)
+                        : bsr::plan_vchunk(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
                 kchunk[w] = bsr::KchunkWork{kp, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
                 continue;
             }
@@ -247,10 +253,12 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         if (li == 0) lev.start = ev.start;
         if (li + 1 == launches.size()) lev.stop = ev.stop;
         const Launch &l = launches[li];
-        if (l.kind == kKchunk) {
+        if (l.kind == kKchunk || l.kind == kVchunk) {
             bsr::KchunkWork batch[bsr::kMaxItems];
             for (size_t m = 0; m < l.members.size(); ++m) batch[m] = kchunk[l.members[m]];
-            s = bsr::launch_spmm_kchunk(batch, int(l.members.size()), stream, lev);
+            s = l.kind == kKchunk
+                    ? bsr::launch_spmm_kchunk(batch, int(l.members.size()), stream, lev)
+                    : bsr::launch_spmm_vchunk(batch, int(l.members.size()), stream, lev);
         } else if (l.kind != kGeneric) {
             bsr::TiledWork batch[bsr::kMaxItems];
             for (size_t m = 0; m < l.members.size(); ++m) batch[m] = tiled[l.members[m]];

@@ -111,4 +111,10 @@ TiledPlan plan_vtile(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
                      int slices, size_t lds_limit);
 bsr_status launch_spmm_vtile(const TiledWork *work, int n, void *stream, const LaunchEvents &ev);
 
+// The column-chunked vector-ALU kernel, for the same shapes when the X tile does not fit.
+KchunkPlan plan_vchunk(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W,
+                       int64_t ldy, int slices, size_t lds_limit);
+bsr_status launch_spmm_vchunk(const KchunkWork *work, int n, void *stream,
+                              const LaunchEvents &ev);
+
 }  // namespace bsr

@@ -118,15 +118,17 @@ __device__ __forceinline__ void vload(VOps<R, C> &ops, __amdgpu_buffer_rsrc_t ri
 // acc[r] += sum over the chunk's first nv blocks (all U when !MASKED) and their columns c of
 // X[t][j * C + c] * w[r][c].  xrow is this lane's token row of the LDS tile.  Block columns are
 // clamped into [0, Kb), so a malformed index reads a wrong column of the tile, never outside it.
+// jlo: the tile's first block column (0 for a whole-row tile; the chunk's first column for the
+// column-chunked kernel); columns are clamped into [jlo, jlo + Kb).
 template <int R, int C, bool MASKED>
 __device__ __forceinline__ void vcompute(float (&acc)[R], const VOps<R, C> &ops,
-                                         const float *xrow, int Kb, int nv) {
+                                         const float *xrow, int Kb, int nv, int jlo = 0) {
     using S = VShape<R, C>;
     using V = typename VecOf<S::VW>::type;
 #pragma unroll
     for (int u = 0; u < S::U; ++u) {
         if (MASKED && u >= nv) break;
-        const unsigned col = min(unsigned(ops.j[u]), unsigned(Kb - 1)) * unsigned(C);
+        const unsigned col = min(unsigned(ops.j[u] - jlo), unsigned(Kb - 1)) * unsigned(C);
         const float *xs = xrow + col;
 #pragma unroll
         for (int c0 = 0; c0 < C; c0 += S::VW) {
@@ -290,6 +292,226 @@ __global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_kernel(con
     }
 }
 
+// ---------------------------------------------------------------- column-chunked variant
+// Inputs too wide for one LDS X tile (e.g. the 3072-column input of BERT's FFN output layer):
+// the same lanes, chunks of U blocks and two halves per row as above, with the input columns
+// cut into chunks of chunk_blocks block-columns as in the column-chunked matrix-core kernel.
+// Each wave owns up to VChunkRows<R> rows of the slice (row_lo + wave + NW i) and keeps their
+// accumulators in registers from the first chunk to the last; per chunk it stages the chunk's
+// columns of the X tile, finds where each of its rows leaves the chunk (indices ascend within
+// a row: the first index at or past the chunk's end, by ballots over 256 indices at a time)
+// and runs the row's blocks up to there.  Rows are stored once, after the last chunk.
+template <int R>
+struct VChunkRows {
+    static constexpr int value = R == 1 ? 8 : (R <= 4 ? 4 : 2);
+};
+
+template <int R, int C, bool BF>
+__global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_chunk_kernel(
+    const KchunkBatch batch) {
+    using S = VShape<R, C>;
+    constexpr int NW = S::NW, U = S::U, MR = VChunkRows<R>::value;
+    extern __shared__ float smem[];
+    float *Xs = smem;
+
+    const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
+    const int t = lane & 31, h = lane >> 5;
+
+    const KchunkItem &I = batch.item[blockIdx.y];
+    const void *__restrict__ X = I.X;
+    const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
+    const int32_t *__restrict__ indptr = I.indptr;
+    const int32_t *__restrict__ indices = I.indices;
+    const void *__restrict__ data = I.data;
+    const float *__restrict__ bias = I.bias;
+    float *__restrict__ Y = I.Y;
+    const int nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
+              slices = I.slices, XP = I.XP, kcb = I.chunk_blocks, nchunks = I.nchunks;
+
+    const int g = blockIdx.x, xcd = g & 7, rank = g >> 3;
+    const int pairs = num_tiles * slices, per_xcd = (pairs + 7) >> 3;
+    const int q = xcd * per_xcd + rank;
+    if (rank >= per_xcd || q >= pairs) return;
+    const int tile = q / slices, s = q - tile * slices;
+    const int64_t t0 = int64_t(tile) * kVT;
+    const int rows = int(T - t0 < kVT ? T - t0 : kVT);
+    const int row_lo = int(int64_t(s) * Nb / slices), row_hi = int(int64_t(s + 1) * Nb / slices);
+
+    // This wave's rows, their block ranges [pos, end) and accumulators (half 0 starts from the
+    // bias, half 1 from zero).
+    const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(bias, bias ? unsigned(Nb * R) * 4u : 0u);
+    int pos[MR], end[MR];
+    float acc[MR][R];
+#pragma unroll
+    for (int i = 0; i < MR; ++i) {
+        const int row = row_lo + wave + NW * i;
+        pos[i] = end[i] = 0;
+        if (row < row_hi) {
+            pos[i] = clampi(uniform(indptr[row]), 0, nnzb);
+            end[i] = clampi(uniform(indptr[row + 1]), pos[i], nnzb);
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const float b = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                rb, (row < row_hi ? row * R + r : 0) * 4, 0, 0));
+            acc[i][r] = h == 0 && row < row_hi ? b : 0.0f;
+        }
+    }
+
+    // First position in [p, e) whose block column is >= jhi, else e.
+    auto crossing = [&](int p, int e, int jhi) -> int {
+        for (int base = p; base < e; base += 256) {
+            const __amdgpu_buffer_rsrc_t ri =
+                buffer_rsrc(indices + base, unsigned(e - base) * 4u);
+            int x[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                x[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, (lane + 64 * m) * 4, 0, 0);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const unsigned long long b = __ballot(base + 64 * m + lane < e && x[m] >= jhi);
+                if (b) return base + 64 * m + __ffsll(static_cast<long long>(b)) - 1;
+            }
+        }
+        return e;
+    };
+
+    const float *xrow = Xs + t * XP;
+    constexpr int kEs = BF ? 2 : 4;   // bytes per stored weight
+    for (int c = 0; c < nchunks; ++c) {
+        const int jlo = c * kcb;
+        const int jhi = c + 1 == nchunks ? Kb : jlo + kcb;
+        const int kbw = jhi - jlo, cols = kbw * C;
+        if (c > 0) __syncthreads();   // every wave is done with the previous chunk's tile
+        // Stage X[t0 : t0 + 32][jlo*C : jlo*C + cols] as fp32, row pitch XP (as above).
+        {
+            constexpr int kXBytes = BF ? 2 : 4;
+            constexpr int kG = 8;
+#pragma unroll 1
+            for (int tr = wave; tr < kVT; tr += NW) {
+                const int src = tr < rows ? tr : 0;
+                const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(
+                    static_cast<const char *>(X) + ((t0 + src) * ldx + int64_t(jlo) * C) * kXBytes,
+                    tr < rows ? unsigned(cols) * kXBytes : 0u);
+                float *dst = Xs + tr * XP;
+                float *spare = Xs + kVT * XP + lane;
+#pragma unroll 1
+                for (int c0 = 0; c0 < cols; c0 += 64 * kG) {
+                    float v[kG];
+#pragma unroll
+                    for (int m = 0; m < kG; ++m) {
+                        const int cc = c0 + 64 * m + lane;
+                        if constexpr (BF)
+                            v[m] = __uint_as_float(unsigned(__builtin_amdgcn_raw_buffer_load_b16(
+                                                       rx, cc * 2, 0, 0))
+                                                   << 16);
+                        else
+                            v[m] = __uint_as_float(
+                                __builtin_amdgcn_raw_buffer_load_b32(rx, cc * 4, 0, 0));
+                    }
+#pragma unroll
+                    for (int m = 0; m < kG; ++m) {
+                        const int cc = c0 + 64 * m + lane;
+                        *(cc < cols ? dst + cc : spare) = v[m];
+                    }
+                }
+            }
+        }
+        int cend[MR];
+#pragma unroll
+        for (int i = 0; i < MR; ++i)
+            cend[i] = c + 1 == nchunks ? end[i] : crossing(pos[i], end[i], jhi);
+        __syncthreads();
+
+#pragma unroll
+        for (int i = 0; i < MR; ++i) {
+            const int p0 = pos[i], m = cend[i] - pos[i];
+            pos[i] = cend[i];
+            if (m <= 0) continue;
+            const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p0, unsigned(m) * 4u);
+            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
+                static_cast<const char *>(data) + int64_t(p0) * S::RC * kEs,
+                unsigned(m) * unsigned(S::RC * kEs));
+            const int nq = (m + U - 1) / U, iters = (nq + 1) >> 1;
+            VOps<R, C> A, B;
+            vload<R, C, BF>(A, ri, rd, h * U);
+            int it = 0;
+            while (true) {
+                if (it + 1 < iters) vload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
+                __builtin_amdgcn_sched_barrier(0);
+                if (it + 1 >= iters) {
+                    vcompute<R, C, true>(acc[i], A, xrow, kbw, m - (2 * it + h) * U, jlo);
+                    break;
+                }
+                vcompute<R, C, false>(acc[i], A, xrow, kbw, U, jlo);
+                __builtin_amdgcn_sched_barrier(0);
+                ++it;
+                if (it + 1 < iters) vload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
+                __builtin_amdgcn_sched_barrier(0);
+                if (it + 1 >= iters) {
+                    vcompute<R, C, true>(acc[i], B, xrow, kbw, m - (2 * it + h) * U, jlo);
+                    break;
+                }
+                vcompute<R, C, false>(acc[i], B, xrow, kbw, U, jlo);
+                __builtin_amdgcn_sched_barrier(0);
+                ++it;
+            }
+        }
+    }
+
+    // Sum the halves and store, as above.
+    const int ldy4 = int(ldy) * 4;
+    const __amdgpu_buffer_rsrc_t ry = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(ldy4));
+    constexpr int kHalf = R == 1 ? 1 : R / 2;
+#pragma unroll
+    for (int i = 0; i < MR; ++i) {
+        const int row = row_lo + wave + NW * i;
+        if (row >= row_hi) continue;
+        const int vo = t * ldy4 + row * R * 4;
+#pragma unroll
+        for (int r = 0; r < kHalf; ++r) {
+            const float P = acc[i][r], Q = acc[i][R == 1 ? 0 : R / 2 + r];
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(P),
+                                                             __float_as_uint(Q), false, false);
+            const float y = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+            if (R > 1 || h == 0)
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(y), ry,
+                                                      vo + (h * kHalf + r) * 4 * (R > 1), 0, 0);
+        }
+    }
+}
+
+template <int R, int C, bool BF>
+bsr_status launch_vchunk_variant(const KchunkBatch &batch, dim3 grid, size_t lds, hipStream_t st,
+                                 const LaunchEvents &ev) {
+    launch_kernel(spmm_vtile_chunk_kernel<R, C, BF>, grid, dim3(VShape<R, C>::NW * 64), lds, st,
+                  ev, batch);
+    return launch_status();
+}
+
+template <bool BF>
+bsr_status launch_vchunk_shape(int R, int C, const KchunkBatch &b, dim3 g, size_t lds,
+                               hipStream_t st, const LaunchEvents &ev) {
+#define BSR_VCHUNK(RR, CC) \
+    if (R == RR && C == CC) return launch_vchunk_variant<RR, CC, BF>(b, g, lds, st, ev);
+    if constexpr (!BF) {
+        BSR_VCHUNK(1, 1)
+    }
+    BSR_VCHUNK(1, 2)
+    BSR_VCHUNK(1, 4)
+    BSR_VCHUNK(1, 8)
+    BSR_VCHUNK(1, 16)
+    BSR_VCHUNK(1, 32)
+    BSR_VCHUNK(2, 1)
+    BSR_VCHUNK(4, 1)
+    BSR_VCHUNK(8, 1)
+    BSR_VCHUNK(2, 2)
+    BSR_VCHUNK(4, 4)
+    BSR_VCHUNK(8, 8)
+#undef BSR_VCHUNK
+    return BSR_ERR_UNSUPPORTED;
+}
+
 template <int R, int C, bool BF>
 bsr_status launch_vtile_variant(const TiledBatch &batch, dim3 grid, size_t lds, hipStream_t st,
                                 const LaunchEvents &ev) {
@@ -392,6 +614,84 @@ bsr_status launch_spmm_vtile(const TiledWork *work, int n, void *stream,
     const dim3 grid(gx, n);
     if (dtype == BSR_BF16) return launch_vtile_shape<true>(R, C, batch, grid, lds, st, ev);
     return launch_vtile_shape<false>(R, C, batch, grid, lds, st, ev);
+}
+
+KchunkPlan plan_vchunk(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W,
+                       int64_t ldy, int slices, size_t lds_limit) {
+    KchunkPlan kp{};
+    const int R = W->R, C = W->C;
+    if (!vtile_supported(R, C, W->dtype)) return kp;
+    const int64_t K = W->n_cols, Nb = W->n_rows / R, Kb = K / C;
+    const int vw = C % 4 == 0 ? 4 : (C % 2 == 0 ? 2 : 1);
+    const int nw = R * C * (R * C >= 32 ? 1 : (32 / (R * C) > 8 ? 8 : 32 / (R * C))) <= 16 ? 16 : 8;
+    const int mr = R == 1 ? 8 : (R <= 4 ? 4 : 2);   // VChunkRows<R>
+    // Slices: at least enough that no wave owns more than mr rows.
+    int64_t S = slices > 0 ? slices : 1;
+    const int64_t min_s = (Nb + int64_t(nw) * mr - 1) / (int64_t(nw) * mr);
+    if (S < min_s) S = min_s;
+    if (S > Nb) S = Nb;
+    // The widest chunk whose fp32 tile (pitch = width rounded up to VW mod 2 VW, plus the 64
+    // spare words) fits.
+    const int64_t words = int64_t(lds_limit) / 4 - 64;
+    const int64_t cmax = words / kVT - 2 * vw;
+    const int64_t kcb_max = cmax / C;
+    if (kcb_max < 1) return KchunkPlan{};
+    const int64_t nch = (Kb + kcb_max - 1) / kcb_max;
+    const int64_t kcb = (Kb + nch - 1) / nch;
+    const int64_t kc = kcb * C;
+    TiledPlan &p = kp.base;
+    p.x_pitch = int(kc + (((vw - kc) % (2 * vw)) + 2 * vw) % (2 * vw));
+    p.lds_bytes = (size_t(kVT) * size_t(p.x_pitch) + 64) * 4;
+    if (p.lds_bytes > lds_limit) return KchunkPlan{};
+    if (W->nnzb * R * C >= (int64_t(1) << 29)) return KchunkPlan{};
+    if (ldy >= (int64_t(1) << 24) || K >= (int64_t(1) << 24)) return KchunkPlan{};
+    p.num_tiles = int((T + kVT - 1) / kVT);
+    p.slices = int(S);
+    p.ok = true;
+    kp.chunk_blocks = int(kcb);
+    kp.nchunks = int(nch);
+    return kp;
+}
+
+bsr_status launch_spmm_vchunk(const KchunkWork *work, int n, void *stream,
+                              const LaunchEvents &ev) {
+    if (n < 1 || n > kMaxItems) return BSR_ERR_ARG;
+    const int R = work[0].W->R, C = work[0].W->C, dtype = work[0].W->dtype;
+    KchunkBatch batch{};
+    batch.n = n;
+    int gx = 0;
+    size_t lds = 0;
+    for (int i = 0; i < n; ++i) {
+        const KchunkWork &w = work[i];
+        if (w.W->R != R || w.W->C != C || w.W->dtype != dtype) return BSR_ERR_ARG;
+        KchunkItem &it = batch.item[i];
+        it.X = w.X;
+        it.T = w.T;
+        it.ldx = w.ldx;
+        it.indptr = w.W->indptr;
+        it.indices = w.W->indices;
+        it.data = w.W->data;
+        it.bias = w.bias;
+        it.Y = w.Y;
+        it.ldy = w.ldy;
+        it.nnzb = int(w.W->nnzb);
+        it.Nb = int(w.W->n_rows / R);
+        it.Kb = int(w.W->n_cols / C);
+        it.num_tiles = w.plan.base.num_tiles;
+        it.slices = w.plan.base.slices;
+        it.XP = w.plan.base.x_pitch;
+        it.bias_words = 0;
+        it.wbuf_offset = 0;
+        it.chunk_blocks = w.plan.chunk_blocks;
+        it.nchunks = w.plan.nchunks;
+        const int wgs = ((w.plan.base.num_tiles * w.plan.base.slices + 7) / 8) * 8;
+        if (wgs > gx) gx = wgs;
+        if (w.plan.base.lds_bytes > lds) lds = w.plan.base.lds_bytes;
+    }
+    hipStream_t st = as_stream(stream);
+    const dim3 grid(gx, n);
+    if (dtype == BSR_BF16) return launch_vchunk_shape<true>(R, C, batch, grid, lds, st, ev);
+    return launch_vchunk_shape<false>(R, C, batch, grid, lds, st, ev);
 }
 
 }  // namespace bsr

@@ -1,6 +1,7 @@
-"""GPU parity of the column-chunked matrix-core kernel, which runs the tiled block shapes (32x1,
-16x1, 32x32, 16x16; fp32 and bf16) when a 32-token X tile is too wide for LDS: the BERT FFN
-output layer (K = 3072) and wider.  Every product is checked against the oracle's fp64 product
+"""GPU parity of the column-chunked kernels, which run when a 32-token X tile is too wide for
+LDS (the BERT FFN output layer, K = 3072, and wider): the matrix-core one for the tiled block
+shapes (32x1, 16x1, 32x32, 16x16) and the vector-ALU one for the others (1x1 .. 1x32, 2x1 ..
+8x1, 2x2 .. 8x8); fp32 and bf16.  Every product is checked against the oracle's fp64 product
 within |Y - Y64| <= 1e-5 * sum|x||w| + 1e-6 (bf16: on the bf16-rounded inputs), on integers
 bit for bit, and two calls must agree bit for bit.  Inputs are built by the oracle and uploaded.
 """
@@ -147,3 +148,60 @@ def test_ffn_w2_full_size_sampled_rows(device):
         torch.cuda.synchronize()
         Ys = Y[torch.from_numpy(rows).to(Y.device)]
         check_product(X[rows], ip, ix, O.bf16_to_f32(dtq) if bf16 else dt, N, K, b, Ys, bf16)
+
+
+VALU_SHAPES = [(1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1), (8, 1),
+               (2, 2), (4, 4), (8, 8)]
+
+
+@pytest.mark.parametrize("R,C", VALU_SHAPES)
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+def test_vchunk_shapes(device, R, C, bf16):
+    """Vector-ALU shapes with K = 3072 (three chunks in fp32), ragged T = 45, through the
+    automatic choice and through the forced vector-ALU kernel."""
+    if bf16 and (R, C) == (1, 1):
+        pytest.skip("bf16 1x1 blocks have no tile kernel")
+    for d in [0.02, 0.3]:
+        case(9900 + 10 * R + C + bf16, 256, 3072, 45, R, C, d, bf16, kernel=B.KERNEL_AUTO)
+    case(9950 + 10 * R + C + bf16, 256, 3072, 45, R, C, 0.1, bf16, kernel=B.KERNEL_VALU,
+         slices=1)
+
+
+@pytest.mark.parametrize("R,C", [(1, 1), (1, 32), (8, 8), (4, 1)])
+def test_vchunk_rows_per_wave_and_slices(device, R, C):
+    """Slices holding the most rows a wave may own (slices forced to 1 is raised to that
+    minimum), skewed rows, and rows whose blocks sit in one chunk."""
+    g = rng(9960 + R + C)
+    N, K, T = 1024, 4096, 70
+    Nb, Kb = N // R, K // C
+    W = g.standard_normal((N, K)).astype(np.float32)
+    mask = g.random((Nb, Kb)) < 0.05
+    mask[1, :] = True
+    mask[2, :] = False
+    mask[3, : Kb // 8] = True
+    mask[4, -Kb // 8:] = True
+    ip, ix, dt = O.build_bsr(W, R, C, mask)
+    X = g.standard_normal((T, K)).astype(np.float32)
+    b = g.standard_normal(N).astype(np.float32)
+    for slices in (1, 0):
+        Y = B.bsr_spmm_ex(dev(X), upload(ip, ix, dt, N, K), dev(b), kernel=B.KERNEL_VALU,
+                          slices=slices)
+        torch.cuda.synchronize()
+        check_product(X, ip, ix, dt, N, K, b, Y)
+
+
+@pytest.mark.parametrize("R,C", [(1, 32), (8, 8)])
+def test_vchunk_integers_bit_exact(device, R, C):
+    g = rng(9970 + R + C)
+    N, K, T = 256, 3072, 40
+    W = g.integers(-8, 9, size=(N, K)).astype(np.float32)
+    X = g.integers(-8, 9, size=(T, K)).astype(np.float32)
+    b = g.integers(-8, 9, size=N).astype(np.float32)
+    ip, ix, dt = O.prune(W, R, C, density=0.25)
+    M = upload(ip, ix, dt, N, K)
+    Y1 = B.bsr_spmm(dev(X), M, dev(b))
+    Y2 = B.bsr_spmm(dev(X), M, dev(b))
+    torch.cuda.synchronize()
+    assert torch.equal(Y1, Y2)
+    Y64 = X.astype(np.float64) @ O.to_dense(ip, ix, dt, N, K).T.astype(np.float64) + b
+    assert np.array_equal(host(Y1).astype(np.float64), Y64)
