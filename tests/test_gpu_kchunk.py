@@ -154,13 +154,12 @@ VALU_SHAPES = [(1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1),
                (2, 2), (4, 4), (8, 8)]
 
 
-@pytest.mark.parametrize("R,C", VALU_SHAPES)
-@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("R,C,bf16", [(R, C, bf) for R, C in VALU_SHAPES for bf in (False, True)
+                                      if not (bf and (R, C) == (1, 1))])
 def test_vchunk_shapes(device, R, C, bf16):
     """Vector-ALU shapes with K = 3072 (three chunks in fp32), ragged T = 45, through the
-    automatic choice and through the forced vector-ALU kernel."""
-    if bf16 and (R, C) == (1, 1):
-        pytest.skip("bf16 1x1 blocks have no tile kernel")
+    automatic choice and through the forced vector-ALU kernel (bf16 1x1 blocks have no tile
+    kernel)."""
     for d in [0.02, 0.3]:
         case(9900 + 10 * R + C + bf16, 256, 3072, 45, R, C, d, bf16, kernel=B.KERNEL_AUTO)
     case(9950 + 10 * R + C + bf16, 256, 3072, 45, R, C, 0.1, bf16, kernel=B.KERNEL_VALU,
