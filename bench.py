@@ -403,7 +403,9 @@ def tiled_kernel_name(c) -> str:
     if 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) > 160 * 1024:
         return "spmm_generic_kernel via bsr_spmm_batched"
     if shape in TILED_SHAPES:
-        return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}> via bsr_spmm_batched"
+        # 16x16 rows with at least 8 stored blocks on average run four-block units.
+        w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
+        return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}, {w}> via bsr_spmm_batched"
     if shape in VALU_SHAPES and not (bf and shape == (1, 1)):
         return f"spmm_vtile_kernel<{c['R']}, {c['C']}, {flag}> via bsr_spmm_batched"
     return "spmm_generic_kernel via bsr_spmm_batched"

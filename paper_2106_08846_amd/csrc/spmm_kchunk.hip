@@ -44,9 +44,9 @@ __device__ __forceinline__ void shift_cols(Ops &ops, int jlo) {
     }
 }
 
-template <int R, int C, bool BF>
+template <int R, int C, bool BF, int W = 1>
 __global__ __launch_bounds__(kNW * 64) void spmm_kchunk_kernel(const KchunkBatch batch) {
-    using U = Unit<R, C, BF>;
+    using U = typename UnitOf<R, C, BF, W>::type;
     extern __shared__ float smem[];
     constexpr int kThreads = kNW * 64;
     const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
@@ -263,10 +263,10 @@ __global__ __launch_bounds__(kNW * 64) void spmm_kchunk_kernel(const KchunkBatch
     }
 }
 
-template <int R, int C, bool BF>
+template <int R, int C, bool BF, int W = 1>
 bsr_status launch_kchunk_variant(const KchunkBatch &batch, dim3 grid, size_t lds, hipStream_t st,
                                  const LaunchEvents &ev) {
-    launch_kernel(spmm_kchunk_kernel<R, C, BF>, grid, dim3(kNW * 64), lds, st, ev, batch);
+    launch_kernel(spmm_kchunk_kernel<R, C, BF, W>, grid, dim3(kNW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
@@ -369,6 +369,16 @@ bsr_status launch_spmm_kchunk(const KchunkWork *work, int n, void *stream,
     }
     const dim3 grid(gx, n);
     hipStream_t st = as_stream(stream);
+    int64_t blocks = 0, rows = 0;
+    for (int i = 0; i < n; ++i) {
+        blocks += work[i].W->nnzb;
+        rows += work[i].W->n_rows / R;
+    }
+    if (R == 16 && C == 16 && blocks >= kWideUnitRowBlocks * rows) {
+        if (work[0].W->dtype == BSR_BF16)
+            return launch_kchunk_variant<16, 16, true, 4>(batch, grid, lds, st, ev);
+        return launch_kchunk_variant<16, 16, false, 4>(batch, grid, lds, st, ev);
+    }
     if (work[0].W->dtype == BSR_BF16) {
         if (R == 32 && C == 1) return launch_kchunk_variant<32, 1, true>(batch, grid, lds, st, ev);
         if (R == 16 && C == 1) return launch_kchunk_variant<16, 1, true>(batch, grid, lds, st, ev);

@@ -61,6 +61,11 @@ struct TiledBatch {
     TiledItem item[kMaxItems];
 };
 
+// 16x16 launches use four-block units when the products' block-rows hold at least this many
+// stored blocks on average (measured on MI355X: faster from about 8, slower below).
+constexpr int kWideUnitRowBlocks = 8;
+bool wide_units(const TiledWork *work, int n);
+
 // Launch 1..kMaxItems planned products of one block shape as a single kernel.
 bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream, const LaunchEvents &ev);
 

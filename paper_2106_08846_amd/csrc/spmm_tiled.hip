@@ -31,9 +31,9 @@ namespace {
 
 // -------------------------------------------------------------------------------- the kernel
 
-template <int R, int C, int NW, bool BF>
+template <int R, int C, int NW, bool BF, int W = 1>
 __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch batch) {
-    using U = Unit<R, C, BF>;
+    using U = typename UnitOf<R, C, BF, W>::type;
     extern __shared__ float smem[];
 
     // The wave index is uniform across a wave; readfirstlane tells the compiler so, which
@@ -518,14 +518,23 @@ __global__ __launch_bounds__(NW * 64) void spmm_tiled_kernel(const TiledBatch ba
     }
 }
 
-template <int R, int C, int NW, bool BF>
+template <int R, int C, int NW, bool BF, int W = 1>
 bsr_status launch_variant(const TiledBatch &batch, dim3 grid, size_t lds, hipStream_t st,
                           const LaunchEvents &ev) {
-    launch_kernel(spmm_tiled_kernel<R, C, NW, BF>, grid, dim3(NW * 64), lds, st, ev, batch);
+    launch_kernel(spmm_tiled_kernel<R, C, NW, BF, W>, grid, dim3(NW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
 }  // namespace
+
+bool wide_units(const TiledWork *work, int n) {
+    int64_t blocks = 0, rows = 0;
+    for (int i = 0; i < n; ++i) {
+        blocks += work[i].W->nnzb;
+        rows += work[i].W->n_rows / work[i].W->R;
+    }
+    return blocks >= kWideUnitRowBlocks * rows;
+}
 
 bool tiled_supported(int R, int C, int dtype) {
     if (dtype != BSR_F32 && dtype != BSR_BF16) return false;
@@ -621,6 +630,11 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
     }
     hipStream_t st = as_stream(stream);
+    if (R == 16 && C == 16 && wide_units(work, n)) {
+        if (work[0].W->dtype == BSR_BF16)
+            return launch_variant<16, 16, 16, true, 4>(batch, dim3(gx, n), lds, st, ev);
+        return launch_variant<16, 16, 16, false, 4>(batch, dim3(gx, n), lds, st, ev);
+    }
     if (work[0].W->dtype == BSR_BF16) {
         if (R == 32 && C == 1) return launch_variant<32, 1, 16, true>(batch, dim3(gx, n), lds, st, ev);
         if (R == 16 && C == 1) return launch_variant<16, 1, 16, true>(batch, dim3(gx, n), lds, st, ev);

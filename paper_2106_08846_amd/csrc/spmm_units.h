@@ -474,45 +474,88 @@ struct Unit<32, 32, true> {
 // 16x16 fp32 blocks, v_mfma_f32_16x16x4_f32 on two 16-token halves.  Lane l loads row l%16,
 // columns 4(l/16)..+3 of the block (the whole block in one instruction); k-slot l/16 of step e
 // stands for c = 4(l/16) + e.
-template <>
-struct Unit<16, 16, false> {
-    static constexpr int KB = 1;
-    static constexpr int kPad = 4;
-    static constexpr bool kTileBF16 = false;
+// 16x16 blocks, KBN blocks per unit (1, or 4 for rows with many blocks: one memory round trip
+// then feeds eight MFMAs instead of two).  A partial unit skips its missing blocks (their index
+// is set to -1), so no zero weight meets an infinite X element.
+//   fp32: v_mfma_f32_16x16x4_f32 on two 16-token halves.  Lane l loads row l%16, columns
+//   4(l/16)..+3 of the block (the whole block in one instruction); k-slot l/16 of step e stands
+//   for c = 4(l/16) + e.
+//   bf16: v_mfma_f32_16x16x16_bf16 on two 16-token halves, one instruction per block and half.
+//   Lane l supplies k-slots 4(l/16) .. +3, standing for c = 4(l/16) + e: 8 contiguous bytes of
+//   token l%16's X row and of block row l%16.
+template <bool BF, int KBN>
+struct Unit1616 {
+    static constexpr int KB = KBN;
+    static constexpr int kPad = BF ? 8 : 4;
+    static constexpr bool kTileBF16 = BF;
     static constexpr bool kTransposed = false;
     static constexpr int kRegs = 8;
+    static constexpr int kBlockBytes = BF ? 512 : 1024;
     using Acc = typename LinearBase<16>::Acc;
+    using Data = typename std::conditional<BF, uintx2, floatx4>::type;
     struct Ops {
-        int j;
-        floatx4 d;
+        int j[KB];
+        Data d[KB];
     };
     __device__ static void zero(Acc &acc) { LinearBase<16>::zero(acc); }
     __device__ static void init(Acc &acc, const float *s_bias, int n0) {
         LinearBase<16>::init(acc, s_bias, n0);
     }
-    __device__ static void mask(Ops &, int) {}
+    __device__ static void mask(Ops &ops, int nvalid) {
+#pragma unroll
+        for (int u = 1; u < KB; ++u) ops.j[u] = u < nvalid ? ops.j[u] : -1;
+    }
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63;
         const unsigned left = unsigned(nnzb - p);
         const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const float *>(data) + int64_t(p) * 256, left * 1024u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
-        ops.d = __builtin_bit_cast(floatx4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                rd, ((lane & 15) * 4 + (lane >> 4)) * 16, 0, 0));
+        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
+            static_cast<const char *>(data) + int64_t(p) * kBlockBytes, left * unsigned(kBlockBytes));
+        if constexpr (KB == 1) {
+            ops.j[0] = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
+        } else {
+            static_assert(KB == 4, "one 16-byte load of the unit's indices");
+            const uintx4 jj = __builtin_amdgcn_raw_buffer_load_b128(ri, 0, 0, 0);
+#pragma unroll
+            for (int u = 0; u < KB; ++u) ops.j[u] = uniform(int(jj[u]));
+        }
+        const int off = ((lane & 15) * 4 + (lane >> 4)) * (BF ? 8 : 16);
+#pragma unroll
+        for (int u = 0; u < KB; ++u) {
+            if constexpr (BF)
+                ops.d[u] = __builtin_amdgcn_raw_buffer_load_b64(rd, off, kBlockBytes * u, 0);
+            else
+                ops.d[u] = __builtin_bit_cast(
+                    floatx4, __builtin_amdgcn_raw_buffer_load_b128(rd, off, kBlockBytes * u, 0));
+        }
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                     char *) {
         const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const float *xb =
-            static_cast<const float *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
-        const floatx4 a0 = *reinterpret_cast<const floatx4 *>(xb);
-        const floatx4 a1 = *reinterpret_cast<const floatx4 *>(xb + 16 * XP);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            acc.h[0] = mfma16(a0[e], ops.d[e], acc.h[0]);
-            acc.h[1] = mfma16(a1[e], ops.d[e], acc.h[1]);
+        for (int u = 0; u < KB; ++u) {
+            if (u > 0 && ops.j[u] < 0) break;   // the rest of a partial unit
+            const int col = clamp_col(ops.j[u], Kb) * 16;
+            if constexpr (BF) {
+                const bf16_t *xb = static_cast<const bf16_t *>(Xs) + tl * XP + 4 * kq + col;
+                const uintx2 a0 = *reinterpret_cast<const uintx2 *>(xb);
+                const uintx2 a1 = *reinterpret_cast<const uintx2 *>(xb + 16 * XP);
+                const shortx4 b = __builtin_bit_cast(shortx4, ops.d[u]);
+                acc.h[0] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                    __builtin_bit_cast(shortx4, a0), b, acc.h[0], 0, 0, 0);
+                acc.h[1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                    __builtin_bit_cast(shortx4, a1), b, acc.h[1], 0, 0, 0);
+            } else {
+                const float *xb = static_cast<const float *>(Xs) + tl * XP + 4 * kq + col;
+                const floatx4 a0 = *reinterpret_cast<const floatx4 *>(xb);
+                const floatx4 a1 = *reinterpret_cast<const floatx4 *>(xb + 16 * XP);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc.h[0] = mfma16(a0[e], ops.d[u][e], acc.h[0]);
+                    acc.h[1] = mfma16(a1[e], ops.d[u][e], acc.h[1]);
+                }
+            }
         }
     }
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
@@ -525,57 +568,19 @@ struct Unit<16, 16, false> {
     __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
 };
 
-// 16x16 bf16 blocks, v_mfma_f32_16x16x16_bf16 on two 16-token halves, one instruction per
-// block and half.  Lane l supplies k-slots 4(l/16) .. +3, standing for c = 4(l/16) + e: 8
-// contiguous bytes of token l%16's X row and of block row l%16.
 template <>
-struct Unit<16, 16, true> {
-    static constexpr int KB = 1;
-    static constexpr int kPad = 8;
-    static constexpr bool kTileBF16 = true;
-    static constexpr bool kTransposed = false;
-    static constexpr int kRegs = 8;
-    using Acc = typename LinearBase<16>::Acc;
-    struct Ops {
-        int j;
-        uintx2 d;
-    };
-    __device__ static void zero(Acc &acc) { LinearBase<16>::zero(acc); }
-    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
-        LinearBase<16>::init(acc, s_bias, n0);
-    }
-    __device__ static void mask(Ops &, int) {}
-    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
-                                const void *__restrict__ data) {
-        const int lane = threadIdx.x & 63;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 256, left * 512u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
-        ops.d = __builtin_amdgcn_raw_buffer_load_b64(rd, ((lane & 15) * 4 + (lane >> 4)) * 8, 0, 0);
-    }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
-        const int lane = threadIdx.x & 63, tl = lane & 15, kq = lane >> 4;
-        const bf16_t *xb =
-            static_cast<const bf16_t *>(Xs) + tl * XP + 4 * kq + clamp_col(ops.j, Kb) * 16;
-        const uintx2 a0 = *reinterpret_cast<const uintx2 *>(xb);
-        const uintx2 a1 = *reinterpret_cast<const uintx2 *>(xb + 16 * XP);
-        const shortx4 b = __builtin_bit_cast(shortx4, ops.d);
-        acc.h[0] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, a0), b,
-                                                            acc.h[0], 0, 0, 0);
-        acc.h[1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(shortx4, a1), b,
-                                                            acc.h[1], 0, 0, 0);
-    }
-    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
-        LinearBase<16>::store(acc, o, n0);
-    }
-    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
-        LinearBase<16>::store_reg(x, o, n0, v);
-    }
-    __device__ static float get(const Acc &acc, int v) { return LinearBase<16>::get(acc, v); }
-    __device__ static void add(Acc &acc, int v, float x) { LinearBase<16>::add(acc, v, x); }
+struct Unit<16, 16, false> : Unit1616<false, 1> {};
+template <>
+struct Unit<16, 16, true> : Unit1616<true, 1> {};
+
+// The unit a kernel instantiation runs: Unit<R, C, BF>, or (W = 4) the four-block 16x16 unit.
+template <int R, int C, bool BF, int W>
+struct UnitOf {
+    using type = Unit<R, C, BF>;
+};
+template <bool BF>
+struct UnitOf<16, 16, BF, 4> {
+    using type = Unit1616<BF, 4>;
 };
 
 }  // namespace

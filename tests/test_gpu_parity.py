@@ -452,6 +452,28 @@ def test_kernels_agree_bitwise_on_integers_bf16(device, R, C):
     assert np.array_equal(host(Yt).astype(np.float64), Y64)
 
 
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
+@pytest.mark.parametrize("density", [0.55, 0.9])
+def test_16x16_four_block_units_bit_exact(device, bf16, density):
+    """16x16 rows averaging 8 or more blocks run four-block units (partial units at most row
+    ends); on integers they must equal the generic kernel and the exact product bit for bit."""
+    g = rng(7600 + int(density * 100) + bf16)
+    W = g.integers(-8, 9, size=(256, 256)).astype(np.float32)
+    X = g.integers(-8, 9, size=(75, 256)).astype(np.float32)
+    b = g.integers(-8, 9, size=256).astype(np.float32)
+    k = B.bsr_prune_count(256, 256, 16, 16, density)
+    assert k >= 8 * 16
+    M = _bf16_bsr(W, 16, 16, k) if bf16 else prune_on_gpu(W, 16, 16, k)
+    Xd = bf16_tensor(X) if bf16 else dev(X)
+    Yg = B.bsr_spmm_ex(Xd, M, dev(b), kernel=B.KERNEL_GENERIC)
+    for slices in (0, 1, 5):
+        Yt = B.bsr_spmm_ex(Xd, M, dev(b), kernel=B.KERNEL_TILED, slices=slices)
+        torch.cuda.synchronize()
+        assert torch.equal(Yg, Yt)
+    Y64 = X.astype(np.float64) @ O.to_dense(*oracle_bsr(M), 256, 256).T.astype(np.float64) + b
+    assert np.array_equal(host(Yt).astype(np.float64), Y64)
+
+
 @pytest.mark.parametrize("R,C", TILED_SHAPES)
 def test_generic_kernel_on_tiled_shapes(device, R, C):
     w = G.block_sweep(R, C)
