@@ -392,22 +392,23 @@ VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1),
 
 def tiled_kernel_name(c) -> str:
     """The kernel libbsr's automatic choice launches for this product: the matrix-core tiled
-    kernel, else the vector-ALU tile kernel, else the generic kernel."""
+    kernel, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
+    X tile does not fit in LDS, else the generic kernel.  (An estimate for the label: the
+    library's plan decides, and the kernel trace shows what ran.)"""
     bf = c["M"].dtype == 1
     shape = (c["R"], c["C"])
     flag = "true" if bf else "false"
-    # Both tile kernels hold a 32-token X tile, the bias and indptr in the 160 KiB of LDS; a
-    # wider K (the 3072-column FFN input) leaves only the generic kernel.  (An estimate for the
-    # label: the library's plan decides, and the kernel trace shows what ran.)
     xb = 2 if bf and shape != (16, 1) else 4
-    if 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) > 160 * 1024:
-        return "spmm_generic_kernel via bsr_spmm_batched"
+    fits = 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) <= 160 * 1024
     if shape in TILED_SHAPES:
         # 16x16 rows with at least 8 stored blocks on average run four-block units.
         w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
-        return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}, {w}> via bsr_spmm_batched"
+        if fits:
+            return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}, {w}> via bsr_spmm_batched"
+        return f"spmm_kchunk_kernel<{c['R']}, {c['C']}, {flag}, {w}> via bsr_spmm_batched"
     if shape in VALU_SHAPES and not (bf and shape == (1, 1)):
-        return f"spmm_vtile_kernel<{c['R']}, {c['C']}, {flag}> via bsr_spmm_batched"
+        kern = "spmm_vtile_kernel" if fits else "spmm_vtile_chunk_kernel"
+        return f"{kern}<{c['R']}, {c['C']}, {flag}> via bsr_spmm_batched"
     return "spmm_generic_kernel via bsr_spmm_batched"
 
 

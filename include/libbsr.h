@@ -176,7 +176,8 @@ LIBBSR_API bsr_status bsr_spmm(const void *X, bsr_dtype x_dtype, int64_t T, int6
                     void *stream);
 
 /* Kernel choice for bsr_spmm_ex (bsr_spmm uses BSR_KERNEL_AUTO: the matrix-core kernel where
- * it has the shape, else the vector-ALU tile kernel, else the generic kernel). */
+ * it has the shape, else the vector-ALU tile kernel, else the generic kernel; the first two
+ * stage an input too wide for one LDS tile in column chunks). */
 typedef enum {
     BSR_KERNEL_AUTO = 0,     /* the library picks                                           */
     BSR_KERNEL_GENERIC = 1,  /* one thread per output element; every block shape and dtype   */
@@ -186,8 +187,8 @@ typedef enum {
                                 column chunks, each row's sum continuing across them         */
     BSR_KERNEL_VALU = 3      /* LDS-staged token tiles on the vector ALUs; 1x1, 1x2, 1x4, 1x8,
                                 1x16, 1x32, 2x1, 4x1, 8x1, 2x2, 4x4, 8x8 blocks (fp32; bf16
-                                except 1x1), K up to about 1270 (BSR_ERR_UNSUPPORTED
-                                otherwise)                                                   */
+                                except 1x1; BSR_ERR_UNSUPPORTED for other shapes), column
+                                chunks for wide inputs as above                              */
 } bsr_kernel;
 
 typedef struct {

@@ -1,4 +1,4 @@
-// Tiled BSR product on gfx950 matrix cores (fp32 inputs, fp32 accumulate).
+// Tiled BSR product on gfx950 matrix cores (fp32 or bf16 inputs, fp32 accumulate).
 //
 // Y[t][n] = bias[n] + sum over stored blocks p of block-row i = n / R of
 //           sum over c < C of X[t][indices[p] * C + c] * data[p][n - iR][c]          (Sec. 2.2)
@@ -8,10 +8,12 @@
 // the row's blocks (m*C x R).  The matrix-core units of spmm_units.h run it on MFMA.
 //
 // Work decomposition (one workgroup = 32 tokens x one slice of block-rows):
-//   * the X tile [32 tokens][K] is staged once into LDS by direct global->LDS loads (no
-//     registers, no address arithmetic), row pitch K+1 (R x 1: conflict-free 4-byte gathers of
-//     one column for 32 tokens) or K+4 (square blocks: 16-byte aligned rows); the bias is
-//     staged beside it and is the initial value of every row the workgroup finishes;
+//   * the X tile [32 tokens][K] is staged once into LDS: coalesced buffer loads of one word per
+//     lane (constant offsets in the instruction) and conflict-free LDS stores, with row pitch
+//     K+1 (R x 1: conflict-free 4-byte gathers of one column for 32 tokens), K+4 or K+8
+//     (square blocks, fp32 or bf16: 16-byte aligned rows), or transposed with a 72-byte column
+//     pitch (bf16 32x1, for the LDS transpose reads); the bias is staged beside it and is the
+//     initial value of every row the workgroup finishes;
 //   * slices hold whole block-rows, balanced by stored-block count;
 //   * inside a slice the stored blocks are split evenly over the waves (so skewed rows are
 //     spread over several waves); a block-row cut by a wave boundary is summed by the wave where
