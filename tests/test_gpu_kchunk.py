@@ -204,3 +204,35 @@ def test_vchunk_integers_bit_exact(device, R, C):
     assert torch.equal(Y1, Y2)
     Y64 = X.astype(np.float64) @ O.to_dense(ip, ix, dt, N, K).T.astype(np.float64) + b
     assert np.array_equal(host(Y1).astype(np.float64), Y64)
+
+
+
+@pytest.mark.parametrize("R,C,bf16,kernel", [(32, 1, False, 2), (32, 1, True, 2),
+                                             (16, 16, False, 2), (1, 32, False, 3),
+                                             (8, 8, True, 3), (16, 16, True, 2)])
+def test_chunked_pitched_inputs_and_outputs(device, R, C, bf16, kernel):
+    """X a column window of a wider matrix (row pitch K + 5, odd) and Y a window of a wider
+    output: the chunked kernels read and write through both pitches and leave the columns past
+    the window alone.  bf16 square tiles load X in dwords, so an odd bf16 pitch is refused by
+    the forced matrix-core kernel, and the automatic choice takes the generic kernel."""
+    g = rng(9990 + R + C + bf16)
+    N, K, T = 256, 3072, 37
+    W = g.standard_normal((N, K)).astype(np.float32)
+    Xbig = g.standard_normal((T, K + 5)).astype(np.float32)
+    b = g.standard_normal(N).astype(np.float32)
+    ip, ix, dt = O.prune(W, R, C, density=0.1)
+    dtq = O.bf16_round(dt) if bf16 else dt
+    M = upload(ip, ix, dtq, N, K, bf16)
+    Xd = (bf16_tensor(Xbig) if bf16 else dev(Xbig))[:, :K]
+    Ybig = torch.full((T, N + 3), float("nan"), device="cuda:0")
+    Y = Ybig[:, :N]
+    log(f"pitched {R}x{C} bf16={bf16} kernel={kernel}")
+    if bf16 and C > 1 and kernel == B.KERNEL_TILED:
+        with pytest.raises(B.BSRError, match="UNSUPPORTED"):
+            B.bsr_spmm_ex(Xd, M, dev(b), Y=Y, kernel=kernel)
+        kernel = B.KERNEL_AUTO
+    B.bsr_spmm_ex(Xd, M, dev(b), Y=Y, kernel=kernel)
+    torch.cuda.synchronize()
+    check_product(np.ascontiguousarray(Xbig[:, :K]), ip, ix, O.bf16_to_f32(dtq) if bf16 else dt,
+                  N, K, b, Y, bf16)
+    assert torch.isnan(Ybig[:, N:]).all(), "wrote past the output window"
