@@ -281,7 +281,8 @@ KchunkPlan plan_kchunk(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t
     const bool bf = W->dtype == BSR_BF16;
     const bool transposed = bf && R == 32 && C == 1;        // Unit<32, 1, true>::kTransposed
     const bool tile_bf16 = bf && (C > 1 || transposed);     // Unit<R, C, BF>::kTileBF16
-    const int pad = (C == 1) ? 1 : (tile_bf16 ? 8 : 4);     // Unit<R, C, BF>::kPad
+    // Widest pitch padding tile_pitch() adds (the chunk width is not known yet).
+    const int pad = (C == 1) ? (R == 16 ? 32 : 2) : 8;
     // Slices: at least enough that no wave owns more than kMR rows, at most one row each.
     int64_t S = slices > 0 ? slices : 1;
     const int64_t min_s = (Nb + kNW * kMR - 1) / (kNW * kMR);
@@ -308,7 +309,7 @@ KchunkPlan plan_kchunk(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t
         p.wbuf_offset = int(((kc + 1) * 72 + 255) & ~int64_t(255));
         tile_bytes = size_t(p.wbuf_offset) + size_t(kNW) * 2048;
     } else {
-        p.x_pitch = int(kc + pad);
+        p.x_pitch = int(tile_pitch(R, C, tile_bf16, kc));
         p.wbuf_offset = 0;
         tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
     }

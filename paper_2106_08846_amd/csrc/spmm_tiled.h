@@ -23,6 +23,26 @@ struct TiledPlan {
 bool tiled_supported(int R, int C, int dtype);
 int tiled_waves(int R, int C);  // waves per workgroup
 
+// Row pitch, in elements, of a row-major X tile of `cols` columns for the matrix-core units.
+// The pitch decides which LDS banks the units' operand reads hit; these rules were measured
+// with SQ_LDS_BANK_CONFLICT on MI355X (gfx950):
+//  * 32x1 (ds_read_b32 gathers; a half-wave reads 32 tokens of one column): an odd pitch.
+//  * 16x1 (a half-wave reads 16 tokens of each of two columns): pitch = 2 (mod 32); two
+//    columns an odd distance apart then hit disjoint banks (an even distance still conflicts:
+//    with 32 banks no pitch separates every pair).
+//  * 32x32 fp32 (ds_read_b128; lane l reads token l % 32, quad l / 32): pitch = 4 (mod 8).
+//  * 16x16 fp32 (ds_read_b128; lane l reads token l % 16, quad l / 16): pitch = 8 (mod 16).
+//  * bf16 square tiles (ds_read_b64 of bf16 pairs): cols + 8 bf16.
+// The R x 1 tiles also hold a zero column at index `cols`, so their pitch is at least cols + 1.
+inline int64_t tile_pitch(int R, int C, bool tile_bf16, int64_t cols) {
+    if (C == 1) {
+        if (R == 16) return cols + 1 + (((1 - cols) % 32) + 32) % 32;
+        return cols + ((cols & 1) ? 2 : 1);
+    }
+    if (tile_bf16) return cols + 8;
+    return R == 16 ? cols + 8 : cols + 4;   // cols is a multiple of C
+}
+
 // Plan a tiled launch; plan.ok is false when the shape does not fit (LDS, alignment, sizes).
 // slices <= 0 leaves the slice count at 1; the caller picks it.
 TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *W, int64_t ldy,

@@ -557,7 +557,6 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     const bool bf = W->dtype == BSR_BF16;
     const bool transposed = bf && R == 32 && C == 1;   // Unit<32, 1, true>::kTransposed
     const bool tile_bf16 = bf && (C > 1 || transposed);   // Unit<R, C, BF>::kTileBF16
-    const int pad = (C == 1) ? 1 : (tile_bf16 ? 8 : 4);   // Unit<R, C, BF>::kPad
     const int regs = (R == 32) ? 16 : 8;
     const int NW = tiled_waves(R, C);
     p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3)) + 4;   // + a spare word, 16-byte multiple
@@ -570,7 +569,7 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
         p.wbuf_offset = int(((K + 1) * 72 + 255) & ~int64_t(255));
         tile_bytes = size_t(p.wbuf_offset) + size_t(NW) * 2048;
     } else {
-        p.x_pitch = int(K + pad);
+        p.x_pitch = int(tile_pitch(R, C, tile_bf16, K));
         p.wbuf_offset = 0;
         tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
     }

@@ -14,7 +14,9 @@
 //     does not see.  A comes from the LDS X tile with 16-byte reads.
 //
 // Every unit offers: zero / init (bias) / load / mask (partial unit) / mma / store / store_reg /
-// get / add, plus its tile layout (kPad, kTileBF16, kTransposed) and blocks per unit (KB).
+// get / add, plus its tile layout (kPad: the smallest pitch padding, 1 for the R x 1 tiles with
+// their zero column; kTileBF16, kTransposed) and blocks per unit (KB).  The planner's
+// tile_pitch() sets the pitch itself.
 // Column indices are relative to the X tile; lanes with index -1 read the tile's zero column.
 #pragma once
 
@@ -486,7 +488,7 @@ struct Unit<32, 32, true> {
 template <bool BF, int KBN>
 struct Unit1616 {
     static constexpr int KB = KBN;
-    static constexpr int kPad = BF ? 8 : 4;
+    static constexpr int kPad = 8;
     static constexpr bool kTileBF16 = BF;
     static constexpr bool kTransposed = false;
     static constexpr int kRegs = 8;
