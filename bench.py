@@ -81,6 +81,8 @@ def build_workload(spec: str):
     R, C = (int(v) for v in block[0].split("x"))
     fine = tuple(int(v) for v in block[1].split("x")) if len(block) > 1 else None
     bf16 = parts[-1] == "bf16"
+    if bf16 and kind in ("sweep", "bert_large"):
+        raise SystemExit(f"{spec}: the {kind} workload is fp32 only")
     if kind == "sweep":
         wl = G.block_sweep(R, C)
     elif kind == "fused_qkv":
