@@ -1,6 +1,8 @@
 """Pins for the attention oracle: closed forms, invariances, torch's fp64 attention and a
 40-digit reference; planted mistakes in the oracle must trip them."""
+import json
 import math
+import os
 from fractions import Fraction
 
 import mpmath
@@ -108,6 +110,41 @@ def pin_fp32_computation_is_within_the_bound():
                 assert np.all(np.abs(ctx32 - ctx64[r, c]) <= bound[r, c])
 
 
+def pin_bound_hand_worked():
+    """attention_error_bound on a case worked by hand (tests/golden/hand_examples.json)."""
+    with open(os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")) as f:
+        ex = json.load(f)["attention_examples"][0]
+    Q, K, V = (np.array(ex[n], dtype=np.float32) for n in ("Q", "K", "V"))
+    args = (ex["batch"], ex["seq"], ex["heads"], ex["head_dim"], ex["scale"])
+    ctx = A.attention(Q, K, V, *args)
+    assert np.allclose(ctx, np.array(ex["ctx"]), rtol=1e-15, atol=0)
+    bound = A.attention_error_bound(Q, K, V, *args)
+    want = np.array(ex["bound_in_units_of_2^-24"], dtype=np.float64) * 2.0 ** -24
+    assert np.allclose(bound, want, rtol=1e-12, atol=0)
+
+
+def pin_bound_is_not_loose():
+    """The bound is a first-order worst case, but not a loose one: on the same four fp32
+    evaluations as above, the largest error reaches at least 1/500 of it (measured: 0.011, 0.0067,
+    0.0019 and 0.011 of the bound).  A bound ten times too large fails here."""
+    worst = 0.0
+    for seed, (batch, seq, heads, d, sd) in enumerate([(1, 128, 4, 64, 0.3), (2, 77, 2, 64, 1.0),
+                                                      (1, 512, 1, 64, 0.2), (1, 33, 3, 32, 3.0)]):
+        Q, K, V = qkv(20 + seed, batch, seq, heads, d, sd)
+        ctx64 = A.attention(Q, K, V, batch, seq, heads, d)
+        bound = A.attention_error_bound(Q, K, V, batch, seq, heads, d)
+        scale = np.float32(1.0 / math.sqrt(d))
+        for b in range(batch):
+            r = slice(b * seq, (b + 1) * seq)
+            for h in range(heads):
+                c = slice(h * d, (h + 1) * d)
+                s = (Q[r, c] @ K[r, c].T) * scale
+                e = np.exp(s - s.max(axis=1, keepdims=True))
+                ctx32 = (e @ V[r, c]) / e.sum(axis=1, keepdims=True)
+                worst = max(worst, float((np.abs(ctx32 - ctx64[r, c]) / bound[r, c]).max()))
+    assert worst >= 2e-3, worst
+
+
 def pin_block_composes_the_products():
     g = rng(30)
     batch, seq, heads, d = 1, 8, 2, 4
@@ -124,7 +161,7 @@ def pin_block_composes_the_products():
 PINS = [pin_uniform_keys_give_the_mean, pin_single_token_is_v, pin_key_shift_invariance,
         pin_key_permutation_invariance, pin_matches_torch_sdpa_fp64,
         pin_matches_40_digit_reference, pin_fp32_computation_is_within_the_bound,
-        pin_block_composes_the_products]
+        pin_bound_hand_worked, pin_bound_is_not_loose, pin_block_composes_the_products]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
@@ -168,6 +205,50 @@ def _make(variant):
 def test_planted_attention_mistake_is_caught(variant, monkeypatch):
     monkeypatch.setitem(A.__dict__, "_orig_attention", A.attention)
     monkeypatch.setattr(A, "attention", _make(variant))
+    caught = []
+    for pin in PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError):
+            caught.append(pin.__name__)
+    assert caught, f"no pin catches: {variant}"
+
+
+def _bound_mutant(variant):
+    """attention_error_bound with one plausible mistake planted."""
+    orig = A.__dict__["_orig_attention_error_bound"]
+    u = 2.0 ** -24
+
+    def f(Q, K, V, batch, seq, heads, head_dim, scale=None):
+        if variant == "bound 100 times too large":
+            return 100.0 * orig(Q, K, V, batch, seq, heads, head_dim, scale)
+        if scale is None:
+            scale = 1.0 / math.sqrt(head_dim)
+        Q, K, V = (np.asarray(x, dtype=np.float64) for x in (Q, K, V))
+        out = np.zeros((batch * seq, heads * head_dim))
+        for b in range(batch):
+            r = slice(b * seq, (b + 1) * seq)
+            for h in range(heads):
+                c = slice(h * head_dim, (h + 1) * head_dim)
+                s = scale * (Q[r, c] @ K[r, c].T)
+                sigma = scale * (np.abs(Q[r, c]) @ np.abs(K[r, c]).T)
+                m = s.max(axis=1, keepdims=True)
+                p = np.exp(s - m)
+                p = p / p.sum(axis=1, keepdims=True)
+                width = 1 if variant == "score error without the head-width factor" else head_dim
+                eps = (width + 2) * u * sigma + u * np.abs(s - m) + 4 * u
+                Aabs = p @ np.abs(V[r, c])
+                seq_term = 0.0 if variant == "sequence-sum term dropped" else 2 * (seq + 2) * u * Aabs
+                out[r, c] = 2 * eps.max(axis=1, keepdims=True) * Aabs + seq_term + u * np.abs(p @ V[r, c])
+        return out
+    return f
+
+
+@pytest.mark.parametrize("variant", ["bound 100 times too large", "sequence-sum term dropped",
+                                     "score error without the head-width factor"])
+def test_planted_bound_mistake_is_caught(variant, monkeypatch):
+    monkeypatch.setitem(A.__dict__, "_orig_attention_error_bound", A.attention_error_bound)
+    monkeypatch.setattr(A, "attention_error_bound", _bound_mutant(variant))
     caught = []
     for pin in PINS:
         try:

@@ -188,6 +188,26 @@ def _build_desc_indices(W, R, C, mask):
     return indptr, indices, data
 
 
+def _scale_signed(X, W_masked):
+    return np.asarray(X, dtype=np.float64) @ np.asarray(W_masked, np.float64).T
+
+
+def _scale_abs_x_only(X, W_masked):
+    return np.abs(np.asarray(X, dtype=np.float64)) @ np.asarray(W_masked, np.float64).T
+
+
+def _scale_abs_w_only(X, W_masked):
+    return np.asarray(X, dtype=np.float64) @ np.abs(np.asarray(W_masked, np.float64)).T
+
+
+def _tolerance_rel_abs_swapped(S, rel=1e-5, abs_=1e-6):
+    return abs_ * S + rel
+
+
+def _tolerance_ten_times_loose(S, rel=1e-5, abs_=1e-6):
+    return 10 * rel * S + abs_
+
+
 MUTANTS = {
     "ties go to the higher id": ("select_topk", _ties_to_higher_id),
     "NaN keys rank lowest": ("select_topk", _nan_ranks_lowest),
@@ -210,6 +230,11 @@ MUTANTS = {
     "indices descending in a row": ("build_bsr", _build_desc_indices),
     "reblock lists pieces column-major": ("reblock", _reblock_pieces_column_major),
     "reblock takes sub-rows bottom-up": ("reblock", _reblock_rows_swapped),
+    "tolerance scale without abs": ("tolerance_scale", _scale_signed),
+    "tolerance scale with |X| only": ("tolerance_scale", _scale_abs_x_only),
+    "tolerance scale with |W| only": ("tolerance_scale", _scale_abs_w_only),
+    "tolerance rel and abs swapped": ("spmm_tolerance", _tolerance_rel_abs_swapped),
+    "tolerance ten times loose": ("spmm_tolerance", _tolerance_ten_times_loose),
 }
 
 

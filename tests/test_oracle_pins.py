@@ -44,6 +44,12 @@ def test_hand_examples(ex):
     b = np.array(ex["bias"], dtype=np.float32)
     Y = O.spmm_loop(X, indptr, indices, data, W.shape[0], b)
     assert Y.tolist() == ex["Y"]
+    if "S" in ex:
+        # The acceptance bound of every floating-point product check, worked by hand.
+        S = O.tolerance_scale(X, O.to_dense(indptr, indices, data, W.shape[0], W.shape[1]))
+        assert S.tolist() == ex["S"]
+        bound = O.spmm_tolerance(S)
+        assert np.allclose(bound, np.array(ex["bound"]), rtol=1e-12, atol=0)
 
 
 # ------------------------------------------------------------------------------ pruning count
