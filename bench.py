@@ -1,19 +1,29 @@
 #!/usr/bin/env python3
 """Benchmark of the BSR product Y = X W^T + b on one MI355X.
 
-Default workload: a BERT-base attention layer -- four 768x768 projections (Q, K, V, O), each
-pruned to 32x1 blocks at 10% block density, applied to one batch of 1 x 128 tokens.  One step
-computes the four products, issued as one bsr_spmm_batched call (one kernel launch; workloads
-with more products use one call per 8).  Inputs are seeded synthetic tensors
-(paper_2106_08846_amd/workloads.py), pruned on the GPU by bsr_prune_from_dense, and resident in
-device memory when timing starts.
+Default workload (the headline): BERT-large attention -- 24 layers x four 1024x1024 projections
+(Q, K, V, O), each pruned to linear 32x1 blocks at 10% block density with Zipf(1.2)-skewed
+block-rows, applied to 16 x 384 = 6144 tokens per layer.  One step computes all 96 products,
+issued as 12 bsr_spmm_batched calls of 8 products (one kernel launch each).  A step walks about
+3.4 GB of inputs and outputs, more than the 256 MB last-level cache holds, so every step runs
+cold.  Inputs are seeded synthetic tensors (paper_2106_08846_amd/workloads.py), pruned on the GPU
+by bsr_prune_from_dense, and resident in device memory when timing starts.
 
-The step is timed as --steps direct issues of its prepared calls (arguments marshalled once,
-one foreign call per launch); --graph times HIP graph replays of the same calls instead, and
-both figures are reported.
-Prints one JSON line: effective GFLOP/s (2 * nnz * tokens per call, summed over the step), the
-roofline position of the product kernel (average launch duration from HIP events recorded on
-the launch stream), the same-shape dense fp32/bf16 GEMM, and the CPU oracle on this host.
+Timing: --warmup untimed steps, then exactly --steps steps between two synchronisations, with an
+event between consecutive steps, so that the JSON line carries the mean step time (the value)
+and the median, p10 and p90 of the per-step times (at least 50 samples; more steps are sampled
+after the timed region when --steps is smaller).  The roofline position comes from HIP events
+that the library records at each product kernel's own start and end (hipExtLaunchKernel).
+
+Beside the headline, unless --no-rows, the same line carries the block-shape rows of the other
+configurations, each timed per launch with those kernel events and reported as median, p10, p90:
+  * the BERT-large 32x32 stack (fp32 matrix cores), cold by construction like the headline;
+  * the fused QKV weight 2304x768 at 4096 tokens, 32x1 and 16x16 blocks at 5-40% density, fp32
+    and bf16, cold: 8 rotating copies of (X, BSR, bias, Y), 400 MB or more in all;
+  * the 768x768 block-shape sweep at 128 tokens (nine shapes, the GPU analog of the paper's
+    Table 1) and the BERT-base Q/K/V/O step, with the same-shape dense GEMM beside each.
+The CPU oracle (plain C, fp64) is timed on this host's cores on a bounded sample of the headline
+workload, and one-threaded on the 128-token workloads.
 """
 from __future__ import annotations
 
@@ -38,33 +48,37 @@ BF16_PEAK_TFLOPS = 2516.6      # MI355X bf16 matrix (dense)
 METRIC = "BSR SpMM effective GFLOP/s (2*nnz*tokens)"
 KERNEL_SOURCES = "paper_2106_08846_amd/csrc"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm.md")
+MIN_SAMPLES = 50
+ROTATE_SETS = 8
 
 
-def parse():
+def parse(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="bert_base_attn",
-                    help="bert_base_attn | single_768 | sweep:RxC | "
-                         "fused_qkv:RxC:density[:bf16] | bert_large:RxC | "
-                         "ffn:RxC[:density[:tokens]][:bf16] | "
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="bert_large:32x1",
+                    help="bert_large:RxC | fused_qkv:RxC:density[:bf16] | sweep:RxC | "
+                         "bert_base_attn | single_768 | ffn:RxC[:density[:tokens]][:bf16] | "
                          "attn_block[:RxC[:density[:batch[:seq]]]]; RxC@R2xC2 prunes with "
                          "R x C blocks and multiplies the matrix re-blocked to R2 x C2")
     ap.add_argument("--slices", type=int, default=0,
                     help="block-row slices per token tile (0: the library's choice)")
+    ap.add_argument("--rotate", type=int, default=0,
+                    help="copies of every input and output to rotate through (0: 1 for "
+                         "workloads that exceed the last-level cache by themselves, else 8)")
     ap.add_argument("--graph", action="store_true",
                     help="time the step as HIP graph replays instead of direct calls")
-    ap.add_argument("--no-graph", action="store_true",
-                    help="skip the graph-replay figure (e.g. under counter collection)")
+    ap.add_argument("--no-rows", action="store_true",
+                    help="headline only: skip the block-shape rows of the other workloads")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="approximate CPU time spent timing the oracle baseline")
+                    help="approximate CPU time spent timing the oracle on the headline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB --steps times (the reference "
                          "kernel for scaling HBM byte counters) and exit")
-    return ap.parse_args()
+    return ap.parse_args(argv)
 
 
 def build_workload(spec: str):
@@ -88,7 +102,8 @@ def build_workload(spec: str):
     elif kind == "fused_qkv":
         wl = G.fused_qkv(R, C, float(parts[2]), bf16=bf16)
     elif kind == "bert_large":
-        wl = G.bert_large_zipf(R, C)
+        from paper_2106_08846_amd import bsr as B
+        wl = G.bert_large_zipf(R, C, B.bsr_prune_count(1024, 1024, R, C, 0.1))
     elif kind == "ffn":
         density = float(parts[2]) if len(parts) > 2 and parts[2] != "bf16" else 0.1
         tokens = int(parts[3]) if len(parts) > 3 and parts[3] != "bf16" else 128
@@ -128,6 +143,13 @@ def measured_traffic(workload: str) -> dict | None:
     return table.get("workloads", {}).get(workload)
 
 
+def pct(samples) -> dict:
+    """Median, p10, p90 and mean of a list of times."""
+    a = np.asarray(samples, dtype=np.float64)
+    return {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
+            "p90": float(np.percentile(a, 90)), "mean": float(a.mean()), "n": int(a.size)}
+
+
 def calibrate_copy(args) -> int:
     import torch
     n = args.calibrate_copy * (1 << 20) // 4
@@ -141,15 +163,333 @@ def calibrate_copy(args) -> int:
     return 0
 
 
-def main() -> int:
-    args = parse()
+# ------------------------------------------------------------------------------- device setup
+
+
+class Prepared:
+    """A workload on the device: every projection pruned on the GPU, its product prepared as
+    bsr_spmm_batched calls of up to 8 products, `sets` copies of every tensor to rotate through
+    (copy s of a launch only touches set s)."""
+
+    def __init__(self, wl, sets: int, slices: int = 0):
+        import torch
+        from paper_2106_08846_amd import bsr as B
+        dev = torch.device("cuda:0")
+        self.wl = wl
+        self.bf16 = wl.bf16
+        X32 = [torch.from_numpy(x).to(dev) for x in wl.X]
+        Xs = [B.bsr_cast_f32_bf16(x) for x in X32] if wl.bf16 else X32
+        del X32
+        self.calls = []          # one dict per projection (set 0)
+        self.dense = []          # dense weights (for the GEMM comparison)
+        mats = []
+        for p in wl.projections:
+            N, K = p.W.shape
+            k = p.k if p.k is not None else B.bsr_prune_count(N, K, p.R, p.C, p.density)
+            Wd = torch.from_numpy(p.W).to(dev)
+            M = B.bsr_prune_from_dense(Wd, p.R, p.C, k=k)
+            if wl.bf16:
+                M = M.to_bf16()
+            if "reblock" in wl.notes:
+                M = B.bsr_reblock(M, *wl.notes["reblock"])
+            self.dense.append(Wd.to(torch.bfloat16) if wl.bf16 else Wd)
+            mats.append((M, torch.from_numpy(p.bias).to(dev)))
+            T = wl.X[p.x_index].shape[0]
+            self.calls.append(dict(T=T, N=N, K=K, R=M.R, C=M.C, k=M.nnzb, x_index=p.x_index))
+        self.sets, self.products = [], []
+        for s in range(sets):
+            xs = Xs if s == 0 else [x.clone() for x in Xs]
+            prods = []
+            for c, (M, b) in zip(self.calls, mats):
+                if s > 0:
+                    M = B.BSRMatrix(M.n_rows, M.n_cols, M.R, M.C, M.indptr.clone(),
+                                    M.indices.clone(), M.data.clone(), M.nnzb)
+                    b = b.clone()
+                Y = torch.empty((c["T"], c["N"]), dtype=torch.float32, device=dev)
+                prods.append((xs[c["x_index"]], M, b, Y))
+            groups = [prods[i:i + 8] for i in range(0, len(prods), 8)]
+            self.sets.append([B.SpmmBatchCall(g, slices=slices or None) for g in groups])
+            self.products.append(prods)
+        self.Xs = Xs
+        torch.cuda.synchronize()
+
+    @property
+    def launches_per_step(self) -> int:
+        return len(self.sets[0])
+
+    def flops_step(self) -> float:
+        return sum(2.0 * c["k"] * c["R"] * c["C"] * c["T"] for c in self.calls)
+
+    def bytes_step(self) -> float:
+        """Algorithmic bytes: X read once per product, the BSR arrays, the bias, Y written."""
+        sx = 2 if self.bf16 else 4
+        tot = 0.0
+        for c in self.calls:
+            tot += (c["T"] * c["K"] * sx + c["k"] * c["R"] * c["C"] * sx + 4 * c["k"]
+                    + 4 * (c["N"] // c["R"] + 1) + 4 * c["N"] + 4 * c["T"] * c["N"])
+        return tot
+
+    def step(self, s: int = 0):
+        for run in self.sets[s]:
+            run()
+
+    def launch_times_us(self, rounds: int) -> list:
+        """Kernel-event durations of every launch, visiting the sets round robin."""
+        import torch
+        ev = []
+        for r in range(rounds):
+            for run in self.sets[r % len(self.sets)]:
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                b.record()
+                ev.append((run, a, b))
+        torch.cuda.synchronize()
+        for run, a, b in ev:
+            run.timed(a, b)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) * 1e3 for _, a, b in ev]
+
+
+def step_times_ms(fn, n: int, rotate: int = 1):
+    """Run fn(i % rotate) n times with an event between consecutive calls; returns (total ms
+    between the first and last event, per-call ms)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for i in range(n):
+        fn(i % rotate)
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(n)]
+    return ev[0].elapsed_time(ev[n]), per
+
+
+def roofline(prep, launch_us_mean: float) -> dict:
+    flops = prep.flops_step() / prep.launches_per_step
+    nbytes = prep.bytes_step() / prep.launches_per_step
+    peak = (BF16_PEAK_TFLOPS if prep.bf16 else FP32_PEAK_TFLOPS) * 1e12
+    ai = flops / nbytes
+    gbs = nbytes / (launch_us_mean * 1e-6) / 1e9
+    tfs = flops / (launch_us_mean * 1e-6) / 1e12
+    if ai > peak / (HBM_PEAK_GBS * 1e9):
+        r = {"bound": "mfma", "achieved": tfs, "peak": peak / 1e12, "unit": "TFLOP/s",
+             "frac": tfs / (peak / 1e12)}
+    else:
+        r = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+             "frac": gbs / HBM_PEAK_GBS}
+    r.update({"launch_us": launch_us_mean, "algorithmic_bytes_per_launch": nbytes,
+              "flops_per_launch": flops, "arithmetic_intensity": ai, "achieved_gbs": gbs,
+              "achieved_tflops": tfs})
+    return r
+
+
+def dense_times_us(prep, rounds: int) -> dict:
+    """Same-shape dense GEMM per launch group: torch.addmm (fp32) or matmul (bf16) on the
+    unpruned weights, timed per group of the step's products with events, sets rotated."""
+    import torch
+    outs = [[torch.empty((c["T"], c["N"]), dtype=torch.float32, device="cuda:0")
+             for c in prep.calls] for _ in range(len(prep.sets))]
+    biases = [[p[2] for p in prods] for prods in prep.products]
+    xs_sets = [[p[0] for p in prods] for prods in prep.products]
+    Ws = prep.dense
+
+    def group(s, lo, hi):
+        for i in range(lo, hi):
+            X, W, b, Y = xs_sets[s][i], Ws[i], biases[s][i], outs[s][i]
+            if prep.bf16:
+                Y.copy_(torch.matmul(X, W.t()).float() + b)
+            else:
+                torch.addmm(b, X, W.t(), out=Y)
+
+    n = len(prep.calls)
+    bounds = [(i, min(i + 8, n)) for i in range(0, n, 8)]
+    for s in range(len(prep.sets)):          # warm-up
+        for lo, hi in bounds:
+            group(s, lo, hi)
+    times = []
+    for r in range(rounds):
+        s = r % len(prep.sets)
+        for lo, hi in bounds:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            group(s, lo, hi)
+            b.record()
+            times.append((a, b))
+    torch.cuda.synchronize()
+    return pct([a.elapsed_time(b) * 1e3 for a, b in times])
+
+
+# ------------------------------------------------------------------------------------- rows
+
+
+def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = None) -> dict:
+    """One block-shape row: per-launch kernel-event times (median, p10, p90), effective rates,
+    roof fraction, and the dense GEMM beside it."""
+    import torch
+    print(f"# row {spec}", file=sys.stderr, flush=True)
+    wl = build_workload(spec)
+    prep = Prepared(wl, rotate)
+    for s in range(rotate):
+        prep.step(s)
+    torch.cuda.synchronize()
+    lt = pct(prep.launch_times_us(rounds))
+    r = roofline(prep, lt["mean"])
+    c0 = prep.calls[0]
+    out = {"workload": wl.name, "spec": spec, "block": f"{c0['R']}x{c0['C']}",
+           "dtype": "bf16" if wl.bf16 else "f32", "tokens": c0["T"],
+           "products_per_launch": len(prep.calls) // prep.launches_per_step,
+           "launches": lt["n"],
+           "protocol": (f"cold: {rotate} rotating copies of every input and output"
+                        if rotate > 1 else
+                        ("cold by construction: the stack exceeds the last-level cache"
+                         if spec.startswith("bert_large") else "warm, launches back to back")),
+           "launch_us": {k: lt[k] for k in ("median", "p10", "p90", "mean")},
+           "effective_tflops": r["achieved_tflops"], "effective_tbs": r["achieved_gbs"] / 1e3,
+           "roof": {k: r[k] for k in ("bound", "frac", "arithmetic_intensity")},
+           "frac_of_hbm": r["achieved_gbs"] / HBM_PEAK_GBS,
+           "frac_of_matrix_peak": r["achieved_tflops"] / ((BF16_PEAK_TFLOPS if wl.bf16 else
+                                                           FP32_PEAK_TFLOPS))}
+    if label:
+        out["label"] = label
+    if dense:
+        d = dense_times_us(prep, rounds)
+        out["dense_us"] = {k: d[k] for k in ("median", "p10", "p90")}
+        out["sparse_over_dense"] = lt["median"] / d["median"]
+    del prep
+    torch.cuda.empty_cache()
+    return out
+
+
+def rows(args) -> dict:
+    """The other configurations' block-shape rows (see the module docstring)."""
+    res = {}
+    dense = not args.no_dense
+    other = "bert_large:32x32" if args.workload != "bert_large:32x32" else "bert_large:32x1"
+    res["bert_large_zipf"] = [row(other, 1, 5, dense)]
+    qkv = []
+    for shape in ("32x1", "16x16"):
+        for dt in ("", ":bf16"):
+            for d in ("0.05", "0.1", "0.2", "0.4"):
+                qkv.append(row(f"fused_qkv:{shape}:{d}{dt}", ROTATE_SETS, 8 * ROTATE_SETS,
+                               dense))
+    res["fused_qkv"] = qkv
+    res["sweep_T128"] = [row(f"sweep:{s}", 1, 100, dense) for s in
+                         ("1x1", "8x1", "16x1", "32x1", "1x32", "4x4", "8x8", "16x16", "32x32")]
+    res["bert_base_attn_T128"] = [row("bert_base_attn", 1, 100, dense)]
+    return res
+
+
+# --------------------------------------------------------------------------- CPU baselines
+
+
+def cpu_baseline(wl, seconds: float) -> dict:
+    """The C oracle (fp64 naive BSR loop, OpenMP over tokens) on this host's cores, on a bounded
+    sample of the workload: its first product, pruned by the numpy oracle, over all its tokens;
+    three samples of about seconds / 3 each, median rate.  Plus one-thread runs of the
+    128-token workloads (whole steps), median of three samples each."""
+    from oracle import bsr_oracle as O
+    from oracle import cpu_oracle
+    cores = len(os.sched_getaffinity(0))
+
+    def host_product(wl, p):
+        ip, ix, dt = O.prune(p.W, p.R, p.C, k=p.k if p.k is not None else
+                             O.prune_count(p.W.shape[0], p.W.shape[1], p.R, p.C, p.density))
+        X = wl.X[p.x_index]
+        if wl.bf16:
+            X = O.bf16_roundtrip(X)
+            dt = O.bf16_roundtrip(dt)
+        return X, ip, ix, dt, p.W.shape[0], p.bias, 2.0 * len(ix) * p.R * p.C * X.shape[0]
+
+    def rate(prods, budget):
+        """Median over three samples of the rate of repeated whole passes over `prods`."""
+        rates = []
+        for _ in range(3):
+            flops, t0 = 0.0, time.perf_counter()
+            while True:
+                for X, ip, ix, dt, N, b, f in prods:
+                    cpu_oracle.spmm(X, ip, ix, dt, N, b)
+                    flops += f
+                if time.perf_counter() - t0 >= budget:
+                    break
+            rates.append(flops / (time.perf_counter() - t0) / 1e9)
+        return float(np.median(rates)), rates
+
+    cpu_oracle.set_num_threads(cores)
+    p0 = wl.projections[0]
+    head = [host_product(wl, p0)]
+    value, samples = rate(head, seconds / 3)
+    out = {"value": value, "unit": "GFLOP/s", "cores": cpu_oracle.num_threads(),
+           "kind": "oracle",
+           "sample": (f"product {p0.name} of {wl.name} ({p0.W.shape[0]}x{p0.W.shape[1]}, "
+                      f"{p0.R}x{p0.C} blocks, {wl.X[p0.x_index].shape[0]} tokens), repeated "
+                      f"for about {seconds / 3:.1f} s per sample; median of 3 samples"),
+           "samples_gflops": samples, "cpu": cpu_model()}
+    cpu_oracle.set_num_threads(1)
+    single = {}
+    for spec in ("single_768", "bert_base_attn", "sweep"):
+        if spec == "sweep":
+            from paper_2106_08846_amd import workloads as G
+            prods = []
+            for R, C in G.SHAPES_SWEEP:
+                w = G.block_sweep(R, C)
+                prods.append(host_product(w, w.projections[0]))
+        else:
+            w = build_workload(spec)
+            prods = [host_product(w, p) for p in w.projections]
+        single[spec] = rate(prods, 0.3)[0]
+    cpu_oracle.set_num_threads(cores)
+    out["single_thread_gflops"] = single
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.machine()
+
+
+# ------------------------------------------------------------------------------------- main
+
+
+TILED_SHAPES = ((32, 1), (16, 1), (32, 32), (16, 16))
+VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1), (8, 1), (2, 2),
+               (4, 4), (8, 8))
+
+
+def kernel_name(c, bf16: bool) -> str:
+    """The kernel libbsr's automatic choice launches for this product: the matrix-core tiled
+    kernel, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
+    X tile does not fit in LDS, else the generic kernel.  (A label: the library's plan decides,
+    and the kernel trace shows what ran.)"""
+    shape = (c["R"], c["C"])
+    flag = "true" if bf16 else "false"
+    xb = 2 if bf16 and shape != (16, 1) else 4
+    fits = 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) <= 160 * 1024
+    if shape in TILED_SHAPES:
+        w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
+        if fits:
+            return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}, {w}>"
+        return f"spmm_kchunk_kernel<{c['R']}, {c['C']}, {flag}, {w}>"
+    if shape in VALU_SHAPES and not (bf16 and shape == (1, 1)):
+        kern = "spmm_vtile_kernel" if fits else "spmm_vtile_chunk_kernel"
+        return f"{kern}<{c['R']}, {c['C']}, {flag}>"
+    return "spmm_generic_kernel"
+
+
+def main(argv=None) -> int:
+    args = parse(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library has no "
               "multi-GPU path, so run it with --gpus 1.", file=sys.stderr, flush=True)
         return 2
 
     import torch
-    from paper_2106_08846_amd import bsr as B
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -158,155 +498,85 @@ def main() -> int:
         return calibrate_copy(args)
     if args.workload.startswith("attn_block"):
         return bench_attention_block(args)
-    dev = torch.device("cuda:0")
     wl = build_workload(args.workload)
-    bf16 = wl.bf16
-    print(f"# workload {wl.name}: {len(wl.projections)} projections", file=sys.stderr,
+    rotate = args.rotate or (1 if args.workload.startswith("bert_large") else ROTATE_SETS)
+    print(f"# workload {wl.name}: {len(wl.projections)} projections, {rotate} set(s)",
+          file=sys.stderr, flush=True)
+    prep = Prepared(wl, rotate, args.slices)
+    for i in range(args.warmup):
+        prep.step(i % rotate)
+    torch.cuda.synchronize()
+
+    fn = prep.step
+    if args.graph:
+        graphs = []
+        side = torch.cuda.Stream()
+        for s in range(rotate):
+            g = torch.cuda.CUDAGraph()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                prep.step(s)
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g):
+                prep.step(s)
+            graphs.append(g)
+        for i in range(args.warmup):
+            graphs[i % rotate].replay()
+        fn = lambda s: graphs[s].replay()   # noqa: E731
+
+    # The timed region: exactly --steps steps.
+    total_ms, per_step = step_times_ms(fn, args.steps, rotate)
+    ms_per_step = total_ms / args.steps
+    samples = list(per_step)
+    if len(samples) < MIN_SAMPLES:     # more samples for the percentiles, outside the region
+        samples += step_times_ms(fn, MIN_SAMPLES - len(samples), rotate)[1]
+    st = pct(samples)
+    print(f"# timed {args.steps} steps: {ms_per_step:.4f} ms per step", file=sys.stderr,
           flush=True)
 
-    # Inputs to the device; prune every weight on the GPU.
-    X32 = [torch.from_numpy(x).to(dev) for x in wl.X]
-    Xs = [B.bsr_cast_f32_bf16(x) for x in X32] if bf16 else X32
-    calls = []
-    for p in wl.projections:
-        N, K = p.W.shape
-        k = p.k if p.k is not None else B.bsr_prune_count(N, K, p.R, p.C, p.density)
-        Wd = torch.from_numpy(p.W).to(dev)
-        M = B.bsr_prune_from_dense(Wd, p.R, p.C, k=k)
-        if bf16:
-            M = M.to_bf16()
-        if "reblock" in wl.notes:
-            M = B.bsr_reblock(M, *wl.notes["reblock"])
-        bias = torch.from_numpy(p.bias).to(dev)
-        T = wl.X[p.x_index].shape[0]
-        Y = torch.empty((T, N), dtype=torch.float32, device=dev)
-        calls.append(dict(X=Xs[p.x_index], M=M, bias=bias, Y=Y, Wd=Wd, T=T, N=N, K=K, R=M.R,
-                          C=M.C, k=M.nnzb))
-    # The step's products go to bsr_spmm_batched in groups of up to 8 (one kernel launch each:
-    # Q, K, V and O of a layer share one launch).
-    groups = [calls[i:i + 8] for i in range(0, len(calls), 8)]
-    runs = [B.SpmmBatchCall([(c["X"], c["M"], c["bias"], c["Y"]) for c in grp],
-                            slices=args.slices or None) for grp in groups]
-    torch.cuda.synchronize()
-
-    def step():
-        for run in runs:
-            run()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-    def time_steps(fn, n):
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(n):
-            fn()
-        end.record()
-        torch.cuda.synchronize()
-        return start.elapsed_time(end) / n
-
-    eager_ms = time_steps(step, args.steps)
-    graph_ms = None
-    if args.graph or not args.no_graph:
-        g = torch.cuda.CUDAGraph()
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            step()
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            step()
-        for _ in range(args.warmup):
-            g.replay()
-        graph_ms = time_steps(g.replay, args.steps)
-    ms_per_step = graph_ms if args.graph else eager_ms
-
-    flops_step = sum(2.0 * c["k"] * c["R"] * c["C"] * c["T"] for c in calls)
-    value = flops_step / (ms_per_step * 1e-3) / 1e9
-
-    # Roofline of the product kernel: average device duration of one launch.  Each launch gets a
-    # pair of HIP events that the library records at the kernel's own start and end on the
-    # launch stream (hipExtLaunchKernel), so host gaps and dispatch overhead are excluded.
-    sx = 2 if bf16 else 4
-    n_ev = max(1, min(args.steps, 400 // len(runs) + 1))
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(len(runs) * n_ev)]
-    for a, b in ev:
-        a.record()
-        b.record()
-    torch.cuda.synchronize()
-    i = 0
-    for _ in range(n_ev):
-        for run in runs:
-            run.timed(*ev[i])
-            i += 1
-    torch.cuda.synchronize()
-    launch_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-
-    def launch_bytes(c):
-        nb_rows = c["N"] // c["R"]
-        return (c["T"] * c["K"] * sx + c["k"] * c["R"] * c["C"] * sx + 4 * c["k"]
-                + 4 * (nb_rows + 1) + 4 * c["N"] + 4 * c["T"] * c["N"])
-
-    bytes_launch = sum(launch_bytes(c) for c in calls) / len(runs)
-    flops_launch = flops_step / len(runs)
-    peak_flops = (BF16_PEAK_TFLOPS if bf16 else FP32_PEAK_TFLOPS) * 1e12
-    ai = flops_launch / bytes_launch
-    gbs = bytes_launch / (launch_ms * 1e-3) / 1e9
-    tfs = flops_launch / (launch_ms * 1e-3) / 1e12
-    if ai > peak_flops / (HBM_PEAK_GBS * 1e9):
-        roof = {"bound": "mfma", "achieved": tfs, "peak": peak_flops / 1e12,
-                "unit": "TFLOP/s", "frac": tfs / (peak_flops / 1e12)}
-    else:
-        roof = {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": gbs / HBM_PEAK_GBS}
+    # Roofline of the product kernel: the average of the kernel-event durations of every
+    # launch over a few steps (at least 60 launches).
+    rounds = max(rotate, -(-60 // prep.launches_per_step))
+    lt = pct(prep.launch_times_us(rounds))
+    roof = roofline(prep, lt["mean"])
     tr = measured_traffic(wl.name)
     roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
-                 "kernel": " + ".join(dict.fromkeys(tiled_kernel_name(c) for c in calls)),
-                 "launch_us": launch_ms * 1e3,
-                 "algorithmic_bytes_per_launch": bytes_launch,
-                 "flops_per_launch": flops_launch, "arithmetic_intensity": ai,
-                 "achieved_gbs": gbs, "achieved_tflops": tfs})
+                 "kernel": " + ".join(dict.fromkeys(kernel_name(c, wl.bf16) for c in prep.calls)),
+                 "launch_us_median": lt["median"], "launch_us_p10": lt["p10"],
+                 "launch_us_p90": lt["p90"], "launches_timed": lt["n"]})
 
+    value = prep.flops_step() / (ms_per_step * 1e-3) / 1e9
+    c0 = prep.calls[0]
     out = {
         "metric": METRIC, "value": value, "unit": "GFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if bf16 else "f32", "data": "synthetic",
-        "config": {"workload": wl.name, "products_per_step": len(calls),
-                   "launches_per_step": len(runs),
-                   "tokens": calls[0]["T"], "N": calls[0]["N"], "K": calls[0]["K"],
-                   "block": f"{calls[0]['R']}x{calls[0]['C']}",
+        "dtype": "bf16" if wl.bf16 else "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "products_per_step": len(prep.calls),
+                   "launches_per_step": prep.launches_per_step,
+                   "tokens": c0["T"], "N": c0["N"], "K": c0["K"],
+                   "block": f"{c0['R']}x{c0['C']}",
                    "density": wl.projections[0].density,
-                   "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in calls][:8],
+                   "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in prep.calls][:8],
                    "timing": "hip_graph_replay" if args.graph else "direct_calls",
-                   "slices": args.slices or "auto"},
-        "eager_ms_per_step": eager_ms,
-        "graph_ms_per_step": graph_ms,
+                   "rotating_sets": rotate, "slices": args.slices or "auto"},
+        "step_ms": {k: st[k] for k in ("median", "p10", "p90", "n")},
         "roofline": roof,
     }
-
     if not args.no_dense:
-        Wds = [c["Wd"].to(torch.bfloat16) if bf16 else c["Wd"] for c in calls]
-        Xd = [c["X"] for c in calls]
+        d = dense_times_us(prep, rounds)
+        out["dense_gemm_ms_per_step"] = d["median"] * prep.launches_per_step / 1e3
+        out["dense_gemm_us_per_launch"] = {k: d[k] for k in ("median", "p10", "p90")}
+    del prep
+    torch.cuda.empty_cache()
 
-        def dense_step():
-            for c, W, X in zip(calls, Wds, Xd):
-                if bf16:
-                    c["Y"].copy_(torch.matmul(X, W.t()).float() + c["bias"])
-                else:
-                    torch.addmm(c["bias"], X, W.t(), out=c["Y"])
-
-        for _ in range(args.warmup):
-            dense_step()
-        out["dense_gemm_ms_per_step"] = time_steps(dense_step, args.steps)
-
+    if not args.no_rows:
+        print("# rows", file=sys.stderr, flush=True)
+        out["rows"] = rows(args)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, calls, args.cpu_seconds)
+        print("# cpu baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
 
     print(json.dumps(out), flush=True)
     return 0
@@ -385,87 +655,6 @@ def bench_attention_block(args) -> int:
     }
     print(json.dumps(out), flush=True)
     return 0
-
-
-TILED_SHAPES = ((32, 1), (16, 1), (32, 32), (16, 16))
-VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1), (8, 1), (2, 2),
-               (4, 4), (8, 8))
-
-
-def tiled_kernel_name(c) -> str:
-    """The kernel libbsr's automatic choice launches for this product: the matrix-core tiled
-    kernel, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
-    X tile does not fit in LDS, else the generic kernel.  (An estimate for the label: the
-    library's plan decides, and the kernel trace shows what ran.)"""
-    bf = c["M"].dtype == 1
-    shape = (c["R"], c["C"])
-    flag = "true" if bf else "false"
-    xb = 2 if bf and shape != (16, 1) else 4
-    fits = 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) <= 160 * 1024
-    if shape in TILED_SHAPES:
-        # 16x16 rows with at least 8 stored blocks on average run four-block units.
-        w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
-        if fits:
-            return f"spmm_tiled_kernel<{c['R']}, {c['C']}, 16, {flag}, {w}> via bsr_spmm_batched"
-        return f"spmm_kchunk_kernel<{c['R']}, {c['C']}, {flag}, {w}> via bsr_spmm_batched"
-    if shape in VALU_SHAPES and not (bf and shape == (1, 1)):
-        kern = "spmm_vtile_kernel" if fits else "spmm_vtile_chunk_kernel"
-        return f"{kern}<{c['R']}, {c['C']}, {flag}> via bsr_spmm_batched"
-    return "spmm_generic_kernel via bsr_spmm_batched"
-
-
-def cpu_baseline(wl, calls, seconds: float) -> dict:
-    """The C oracle (fp64 naive BSR loop, OpenMP over tokens) on this host's cores.
-
-    The sample is the whole step, repeated until about `seconds` of wall time have passed; the
-    rate is in GFLOP/s of the same metric (2 * nnz * tokens per call).
-    """
-    import torch
-    from oracle import bsr_oracle as O
-    from oracle import cpu_oracle
-    cores = len(os.sched_getaffinity(0))
-    cpu_oracle.set_num_threads(cores)
-    host = []
-    for c, p in zip(calls, wl.projections):
-        ip = c["M"].indptr.cpu().numpy()
-        ix = c["M"].indices.cpu().numpy()[:c["k"]]
-        d = c["M"].data[:c["k"]]
-        if d.dtype != torch.float32:
-            dt = O.bf16_to_f32(d.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
-        else:
-            dt = d.cpu().numpy()
-        X = wl.X[p.x_index]
-        if wl.bf16:
-            X = O.bf16_roundtrip(X)
-        host.append((X, ip, ix, dt.reshape(c["k"], c["R"], c["C"]), c["N"], p.bias, c))
-    # Run whole steps until the time budget is spent (at least one step).
-    step_tokens = sum(h[0].shape[0] for h in host)
-    flops = 0.0
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        for X, ip, ix, dt, N, b, c in host:
-            cpu_oracle.spmm(X, ip, ix, dt, N, b)
-            flops += 2.0 * c["k"] * c["R"] * c["C"] * X.shape[0]
-        reps += 1
-        if time.perf_counter() - t0 >= seconds:
-            break
-    sample = (f"{reps} x the full step ({len(host)} calls, {step_tokens} token-rows in all)")
-    el = time.perf_counter() - t0
-    return {"value": flops / el / 1e9, "unit": "GFLOP/s", "cores": cpu_oracle.num_threads(),
-            "kind": "oracle", "sample": sample, "seconds": el,
-            "cpu": cpu_model()}
-
-
-def cpu_model() -> str:
-    try:
-        with open("/proc/cpuinfo") as f:
-            for line in f:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
-    except OSError:
-        pass
-    return platform.machine()
 
 
 if __name__ == "__main__":

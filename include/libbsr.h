@@ -239,7 +239,9 @@ typedef struct {
  * in opts, the start event is recorded at the start of the first kernel and the stop event at
  * the end of the last one.  n_items = 0 (or all T = 0) is a no-op.
  * Errors: as bsr_spmm_ex for the first invalid item (nothing is launched if any item is
- *   invalid); BSR_ERR_ARG for n_items < 0; BSR_ERR_NULL for items = NULL with n_items > 0.
+ *   invalid); BSR_ERR_ARG for n_items < 0, and for a Y that overlaps another product's X,
+ *   bias, W arrays or Y (checked on the host, before anything is launched); BSR_ERR_NULL for
+ *   items = NULL with n_items > 0.
  */
 LIBBSR_API bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
                                        const bsr_spmm_options_t *opts, void *stream);

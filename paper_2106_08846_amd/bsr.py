@@ -179,7 +179,32 @@ class BSRMatrix:
     def dtype(self) -> int:
         return BSR_BF16 if self.data.dtype == torch.bfloat16 else BSR_F32
 
+    def check(self) -> None:
+        """Raise unless the tensors hold the arrays the descriptor names (the C side cannot see
+        a tensor's size): indptr int32 with at least N/R + 1 entries, indices int32 with at
+        least nnzb, data [>= nnzb, R, C] float32 or bfloat16, each contiguous on a GPU."""
+        if self.R <= 0 or self.C <= 0 or self.n_rows % self.R or self.n_cols % self.C:
+            raise ValueError(f"block {self.R}x{self.C} does not tile {self.n_rows}x{self.n_cols}")
+        nb_rows = self.n_rows // self.R
+        for t, n, dt, need in ((self.indptr, "indptr", torch.int32, nb_rows + 1),
+                               (self.indices, "indices", torch.int32, self.nnzb)):
+            if not isinstance(t, torch.Tensor) or t.dtype != dt or not t.is_contiguous():
+                raise ValueError(f"{n} must be a contiguous {dt} tensor")
+            if t.numel() < need:
+                raise ValueError(f"{n} holds {t.numel()} entries, the matrix needs {need}")
+        d = self.data
+        if (not isinstance(d, torch.Tensor) or d.dtype not in (torch.float32, torch.bfloat16)
+                or d.dim() != 3 or tuple(d.shape[1:]) != (self.R, self.C)
+                or not d.is_contiguous()):
+            raise ValueError(f"data must be a contiguous [nnzb, {self.R}, {self.C}] float32 or "
+                             "bfloat16 tensor")
+        if d.shape[0] < self.nnzb:
+            raise ValueError(f"data holds {d.shape[0]} blocks, the matrix has {self.nnzb}")
+        for t, n in ((self.indptr, "indptr"), (self.indices, "indices"), (d, "data")):
+            _require_cuda(t, n)
+
     def struct(self) -> bsr_matrix_t:
+        self.check()
         return bsr_matrix_t(self.n_rows, self.n_cols, self.R, self.C, self.nnzb,
                             _ptr(self.indptr), _ptr(self.indices), _ptr(self.data), self.dtype)
 
@@ -261,21 +286,12 @@ def bsr_spmm_ex(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
                 Y: torch.Tensor | None = None, kernel: int | None = None,
                 slices: int | None = None, stream=None) -> torch.Tensor:
     """bsr_spmm with an explicit kernel (KERNEL_*) and slice count; None = automatic."""
-    _require_cuda(X, "X")
-    if X.dtype not in (torch.float32, torch.bfloat16):
-        raise TypeError("X must be float32 or bfloat16")
+    if Y is None and isinstance(X, torch.Tensor) and X.dim() == 2:
+        Y = torch.empty((X.shape[0], W.n_rows), dtype=torch.float32, device=X.device)
+    _check_call(X, W, bias, Y)
     x_dtype = BSR_BF16 if X.dtype == torch.bfloat16 else BSR_F32
     T = X.shape[0]
     ldx = _pitch(X, "X")
-    if bias is not None:
-        _require_cuda(bias, "bias", torch.float32)
-        if bias.dim() != 1 or bias.numel() != W.n_rows or not bias.is_contiguous():
-            raise ValueError("bias must be a contiguous [N] float32 tensor")
-    if Y is None:
-        Y = torch.empty((T, W.n_rows), dtype=torch.float32, device=X.device)
-    _require_cuda(Y, "Y", torch.float32)
-    if Y.shape[0] != T:
-        raise ValueError("Y must have T rows")
     ldy = _pitch(Y, "Y")
     m = W.struct()
     if kernel is None and slices is None:
@@ -291,16 +307,22 @@ def bsr_spmm_ex(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,
 
 def _check_call(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None,
                 Y: torch.Tensor) -> None:
+    """Shapes before anything reaches the library: X is [T, K] and Y [T, N] with K, N the
+    matrix's, so every row the kernels read or write lies inside its tensor; then devices."""
+    if not isinstance(X, torch.Tensor) or X.dim() != 2 or X.shape[1] != W.n_cols:
+        raise ValueError(f"X must be [T, {W.n_cols}]")
+    if not isinstance(Y, torch.Tensor) or tuple(Y.shape) != (X.shape[0], W.n_rows):
+        raise ValueError(f"Y must be [{X.shape[0]}, {W.n_rows}]")
+    if bias is not None and (not isinstance(bias, torch.Tensor) or bias.dim() != 1
+                             or bias.numel() != W.n_rows or not bias.is_contiguous()):
+        raise ValueError("bias must be a contiguous [N] float32 tensor")
+    W.check()
     _require_cuda(X, "X")
     if X.dtype not in (torch.float32, torch.bfloat16):
         raise TypeError("X must be float32 or bfloat16")
     if bias is not None:
         _require_cuda(bias, "bias", torch.float32)
-        if bias.dim() != 1 or bias.numel() != W.n_rows or not bias.is_contiguous():
-            raise ValueError("bias must be a contiguous [N] float32 tensor")
     _require_cuda(Y, "Y", torch.float32)
-    if Y.shape[0] != X.shape[0]:
-        raise ValueError("Y must have T rows")
 
 
 class SpmmBatchCall:
@@ -390,6 +412,8 @@ def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> 
     """Dense fp32 [N, K] expansion of an fp32 BSR matrix."""
     if out is None:
         out = torch.empty((W.n_rows, W.n_cols), dtype=torch.float32, device=W.indptr.device)
+    if not isinstance(out, torch.Tensor) or tuple(out.shape) != (W.n_rows, W.n_cols):
+        raise ValueError(f"out must be [{W.n_rows}, {W.n_cols}]")
     _require_cuda(out, "out", torch.float32)
     m = W.struct()
     _check(_lib().bsr_to_dense(ctypes.byref(m), _ptr(out), _pitch(out, "out"), _stream(stream)),
@@ -414,17 +438,26 @@ def bsr_reblock(W: BSRMatrix, R2: int, C2: int, stream=None) -> BSRMatrix:
     return BSRMatrix(W.n_rows, W.n_cols, R2, C2, indptr, indices, data, n2)
 
 
+def _check_attention_shapes(Q, K, V, O, batch: int, seq: int, heads: int, head_dim: int):
+    """Every tensor has batch * seq rows and at least heads * head_dim columns (the kernel
+    reads and writes exactly that much of each)."""
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V"), (O, "O")):
+        if (not isinstance(t, torch.Tensor) or t.dim() != 2 or t.shape[0] != batch * seq
+                or t.shape[1] < heads * head_dim):
+            raise ValueError(f"{n} must be [{batch * seq}, >= {heads * head_dim}]")
+
+
 def bsr_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, batch: int, seq: int,
                   heads: int, O: torch.Tensor | None = None, scale: float | None = None,
                   stream=None) -> torch.Tensor:
     """Scaled dot-product attention per (sequence, head) of [batch*seq, heads*64] fp32 tensors
     (row pitch from the tensors' strides); returns O."""
     head_dim = 64
-    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
-        _require_cuda(t, n, torch.float32)
-    if O is None:
+    if O is None and isinstance(Q, torch.Tensor):
         O = torch.empty((batch * seq, heads * head_dim), dtype=torch.float32, device=Q.device)
-    _require_cuda(O, "O", torch.float32)
+    _check_attention_shapes(Q, K, V, O, batch, seq, heads, head_dim)
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V"), (O, "O")):
+        _require_cuda(t, n, torch.float32)
     if scale is None:
         scale = head_dim ** -0.5
     _check(_lib().bsr_attention(_ptr(Q), _pitch(Q, "Q"), _ptr(K), _pitch(K, "K"), _ptr(V),

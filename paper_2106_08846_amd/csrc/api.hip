@@ -142,6 +142,10 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
             bsr::check_spmm(it.X, int(it.x_dtype), it.T, it.ldx, it.W, it.Y, it.ldy, it.bias);
         if (s != BSR_OK) return s;
     }
+    if (n_items > 1) {
+        bsr_status s = bsr::check_spmm_items(items, n_items);
+        if (s != BSR_OK) return s;
+    }
     const int kernel = opts ? opts->kernel : BSR_KERNEL_AUTO;
     const int slices = opts ? opts->slices : 0;
     bsr::LaunchEvents ev;

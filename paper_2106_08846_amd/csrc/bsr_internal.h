@@ -27,6 +27,8 @@ bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32
 bsr_status check_matrix(const bsr_matrix_t *W);
 bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const bsr_matrix_t *W,
                       const float *Y, int64_t ldy, const float *bias);
+// Cross-product aliasing of a batched call (after check_spmm on every item).
+bsr_status check_spmm_items(const bsr_spmm_item_t *items, int32_t n);
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo);
 bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
 bsr_status check_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2,

@@ -113,6 +113,30 @@ bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const 
     return BSR_OK;
 }
 
+bsr_status check_spmm_items(const bsr_spmm_item_t *items, int32_t n) {
+    // Products of one call may run concurrently: each Y must be disjoint from every other
+    // product's inputs and output (inputs may be shared).  Items are already checked one by
+    // one, so every descriptor is valid here.
+    auto y_bytes = [](const bsr_spmm_item_t &it) { return ((it.T - 1) * it.ldy + it.W->n_rows) * 4; };
+    for (int32_t i = 0; i < n; ++i) {
+        const bsr_spmm_item_t &a = items[i];
+        if (a.T <= 0) continue;
+        const int64_t yb = y_bytes(a);
+        for (int32_t j = 0; j < n; ++j) {
+            const bsr_spmm_item_t &b = items[j];
+            if (j == i || b.T <= 0) continue;
+            const bsr_matrix_t *W = b.W;
+            const int64_t xb = ((b.T - 1) * b.ldx + W->n_cols) * (b.x_dtype == BSR_BF16 ? 2 : 4);
+            if (overlaps(a.Y, yb, b.X, xb) || overlaps(a.Y, yb, b.bias, W->n_rows * 4) ||
+                overlaps(a.Y, yb, W->indptr, indptr_bytes(W)) ||
+                overlaps(a.Y, yb, W->indices, W->nnzb * 4) ||
+                overlaps(a.Y, yb, W->data, data_bytes(W)) || overlaps(a.Y, yb, b.Y, y_bytes(b)))
+                return BSR_ERR_ARG;
+        }
+    }
+    return BSR_OK;
+}
+
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo) {
     if (!W || !out) return BSR_ERR_NULL;
     bsr_status s = check_matrix(W);

@@ -12,7 +12,6 @@ its own seed, scaled in fp64 and rounded to fp32.
 
 from __future__ import annotations
 
-import math
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -177,19 +176,19 @@ def fused_qkv(R: int, C: int, density: float, bf16: bool = False, tokens: int = 
                     [X], [Projection("QKV", W, b, R, C, density)], bf16=bf16)
 
 
-def bert_large_zipf(R: int, C: int, density: float = 0.1, layers: int = 24,
+def bert_large_zipf(R: int, C: int, k: int, density: float = 0.1, layers: int = 24,
                     tokens: int = 6144, seed_config: int = 5) -> Workload:
     """BERT-large attention: `layers` x four 1024x1024 weights, X 16 x 384 = 6144 tokens.
 
-    Per-block-row nonzero counts follow Zipf(1.2) (capped, same total as the uniform density):
-    blocks outside the chosen pattern are zeroed in W, so top-k pruning with k = total keeps
-    exactly that pattern (nonzero blocks outrank all-zero ones).
+    `k` is the number of kept blocks of each weight, which the caller derives from `density`
+    (the library's or the oracle's count; this module does no pruning arithmetic).  Per-block-row
+    nonzero counts follow Zipf(1.2) (capped) with that total: blocks outside the chosen pattern
+    are zeroed in W, so top-k pruning with k blocks keeps exactly that pattern (nonzero blocks
+    outrank all-zero ones).  `density` only names the workload.
     """
     N = K = 1024
     Nb, Kb = N // R, K // C
-    nb = Nb * Kb
-    k = max(0, min(nb, math.floor(float(density) * nb + 0.5)))
-    counts = zipf_counts(Nb, Kb, k)
+    counts = zipf_counts(Nb, Kb, int(k))
     nW = 4 * layers
     projs = []
     names = ["Q", "K", "V", "O"]

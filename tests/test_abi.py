@@ -284,3 +284,92 @@ def test_prune_ex_errors(L, lib, norm, sel, k, kw, status):
 ])
 def test_attention_errors(lib, args, status):
     assert lib.bsr_attention(*args, None) == status
+
+
+# ------------------------------------------- binding: tensor sizes checked before any C call
+
+
+def _cpu_matrix(L, N=64, K=64, R=8, C=8, nnzb=6, indptr_n=None, indices_n=None, data_n=None,
+                data_shape=None):
+    import torch
+    ip = torch.zeros(indptr_n if indptr_n is not None else N // R + 1, dtype=torch.int32)
+    ix = torch.zeros(indices_n if indices_n is not None else nnzb, dtype=torch.int32)
+    dshape = data_shape or (data_n if data_n is not None else nnzb, R, C)
+    return L.BSRMatrix(N, K, R, C, ip, ix, torch.zeros(dshape), nnzb)
+
+
+@pytest.mark.parametrize("case", ["x_narrow", "x_column_view", "y_short", "y_narrow",
+                                  "bias_short", "indptr_short", "indices_short", "data_short",
+                                  "data_block_shape"])
+def test_binding_rejects_wrong_sizes(L, case):
+    """Each case would read or write past a tensor if it reached the library; the binding
+    raises ValueError first (with CPU tensors, so nothing could be enqueued: the device check
+    comes after the size checks)."""
+    import torch
+    W = _cpu_matrix(L)
+    X = torch.zeros(4, 64)
+    Y = torch.zeros(4, 64)
+    bias = None
+    if case == "x_narrow":
+        X = torch.zeros(4, 63)
+    elif case == "x_column_view":
+        X = torch.zeros(4, 128)[:, 65:]
+    elif case == "y_short":
+        Y = torch.zeros(3, 64)
+    elif case == "y_narrow":
+        Y = torch.zeros(4, 128)[:, 70:]
+    elif case == "bias_short":
+        bias = torch.zeros(63)
+    elif case == "indptr_short":
+        W = _cpu_matrix(L, indptr_n=8)
+    elif case == "indices_short":
+        W = _cpu_matrix(L, indices_n=5)
+    elif case == "data_short":
+        W = _cpu_matrix(L, data_n=5)
+    elif case == "data_block_shape":
+        W = _cpu_matrix(L, data_shape=(6, 8, 4))
+    with pytest.raises(ValueError):
+        L.bsr_spmm(X, W, bias, Y)
+    with pytest.raises(ValueError):
+        L.SpmmBatchCall([(X, W, bias, Y)])
+
+
+def test_binding_accepts_right_sizes_then_requires_the_gpu(L):
+    import torch
+    W = _cpu_matrix(L)
+    with pytest.raises(TypeError):   # sizes pass; CPU tensors are then refused
+        L.bsr_spmm(torch.zeros(4, 64), W, torch.zeros(64), torch.zeros(4, 64))
+
+
+def test_binding_to_dense_and_attention_sizes(L):
+    import torch
+    W = _cpu_matrix(L)
+    with pytest.raises(ValueError):
+        L.bsr_to_dense(W, out=torch.zeros(63, 64))
+    with pytest.raises(ValueError):
+        L.bsr_to_dense(W, out=torch.zeros(64, 128)[:, 70:])
+    batch, seq, heads = 2, 3, 2
+    ok = torch.zeros(batch * seq, heads * 64)
+    for bad in (torch.zeros(batch * seq - 1, heads * 64), torch.zeros(batch * seq, 127)):
+        for i in range(4):
+            args = [ok, ok, ok, ok]
+            args[i] = bad
+            with pytest.raises(ValueError):
+                L.bsr_attention(args[0], args[1], args[2], batch, seq, heads, O=args[3])
+    with pytest.raises(TypeError):
+        L.bsr_attention(ok, ok, ok, batch, seq, heads, O=torch.zeros(batch * seq, heads * 64))
+
+
+def test_spmm_batched_rejects_aliasing_between_products(L, lib):
+    m = _matrix(L)
+    Y0, Y1 = 0x20000, 0x30000           # each Y spans (4 - 1) * 64 + 64 floats = 1 KiB
+    chained = (L.bsr_spmm_item_t * 2)(_item(L, m, Y=Y0), _item(L, m, X=Y0 + 64, Y=Y1))
+    assert lib.bsr_spmm_batched(chained, 2, None, None) == 3     # product 1 reads product 0's Y
+    same_y = (L.bsr_spmm_item_t * 2)(_item(L, m, Y=Y0), _item(L, m, Y=Y0 + 512))
+    assert lib.bsr_spmm_batched(same_y, 2, None, None) == 3      # the two outputs overlap
+    ws = _matrix(L, data=Y1 + 16)
+    into_w = (L.bsr_spmm_item_t * 2)(_item(L, m, Y=Y1), _item(L, ws, Y=Y0))
+    assert lib.bsr_spmm_batched(into_w, 2, None, None) == 3      # Y1 covers the other's data
+    shared_x = (L.bsr_spmm_item_t * 2)(_item(L, m, Y=Y0), _item(L, m, Y=Y1))
+    assert lib.bsr_spmm_batched(shared_x, 2, None, None) not in (1, 2, 3)  # valid: past checks
+

@@ -91,7 +91,7 @@ def test_fused_qkv(device, R, C, density, bf16):
 def test_bert_large_zipf(device, R, C):
     """All 96 projections on the GPU; the oracle checks 8 of them fully pruned and every
     product on a sample of 48 token rows."""
-    w = G.bert_large_zipf(R, C)
+    w = G.bert_large_zipf(R, C, B.bsr_prune_count(1024, 1024, R, C, 0.1))
     Xs = [dev(x) for x in w.X]
     sample = rng(5).choice(w.tokens, size=48, replace=False)
     sample.sort()
@@ -494,7 +494,7 @@ def test_forced_tiled_unsupported_shape(device):
 
 
 def test_tiled_deterministic_and_repeatable(device):
-    w = G.bert_large_zipf(32, 1, layers=1)
+    w = G.bert_large_zipf(32, 1, B.bsr_prune_count(1024, 1024, 32, 1, 0.1), layers=1)
     p = w.projections[0]
     M = prune_on_gpu(p.W, 32, 1, p.k)
     X = dev(w.X[0])

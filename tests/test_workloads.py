@@ -2,6 +2,7 @@
 import numpy as np
 import pytest
 
+from oracle import bsr_oracle as O
 from paper_2106_08846_amd import workloads as G
 
 
@@ -49,8 +50,19 @@ def test_workload_shapes():
     assert all(p.W.shape == (768, 768) and (p.R, p.C) == (32, 1) for p in w.projections)
     w = G.fused_qkv(16, 16, 0.2, bf16=True)
     assert w.X[0].shape == (4096, 768) and w.projections[0].W.shape == (2304, 768) and w.bf16
-    w = G.bert_large_zipf(32, 32, layers=2, tokens=64)
+    w = G.bert_large_zipf(32, 32, 102, layers=2, tokens=64)
     assert len(w.projections) == 8 and len(w.X) == 2 and w.projections[5].x_index == 1
     W = w.projections[0].W
     nz = (W.reshape(32, 32, 32, 32) != 0).any(axis=(1, 3))
     assert sorted(nz.sum(axis=1).tolist(), reverse=True) == ZIPF_32x32
+
+
+@pytest.mark.parametrize("R,C,total", [(32, 1, 3277), (32, 32, 102)])
+def test_skewed_workload_total_is_the_pruning_count(R, C, total):
+    """The skewed workload's block total is what the caller passes: at density 0.1 it is the
+    oracle's pruning count (the generator itself does no pruning arithmetic)."""
+    assert O.prune_count(1024, 1024, R, C, 0.1) == total
+    w = G.bert_large_zipf(R, C, total, layers=1, tokens=32)
+    W = w.projections[0].W
+    nz = (W.reshape(1024 // R, R, 1024 // C, C) != 0).any(axis=(1, 3))
+    assert int(nz.sum()) == total and w.projections[0].k == total
