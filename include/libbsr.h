@@ -113,6 +113,31 @@ LIBBSR_API bsr_status bsr_prune_from_dense(const float *W, int64_t N, int64_t K,
                                 float *data, int64_t capacity_blocks, void *workspace,
                                 size_t ws_bytes, void *stream);
 
+/* Most blocks (nb = (N / R) * (K / C)) that bsr_prune_from_dense_noalloc handles: its fixed
+ * workspace is 12 MiB of device memory per GPU. */
+#define BSR_NOALLOC_MAX_BLOCKS (1 << 20)
+
+/*
+ * bsr_prune_from_dense without a workspace argument, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Arguments, outputs and result are those of bsr_prune_from_dense (bit-identical to it); the
+ * workspace is a fixed array inside the library, one per GPU, held until the process ends, of
+ * the size bsr_prune_workspace_bytes() gives for BSR_NOALLOC_MAX_BLOCKS blocks.  The call
+ * allocates nothing (no hipMalloc, no library allocation); its first call on a device looks up
+ * that device's array with the device current.
+ * Every call on one GPU shares that GPU's array, so calls whose work overlaps in time on one
+ * GPU (on different streams, or from several threads without ordering) race and must not be
+ * issued; calls ordered on one stream are safe.  The array keeps the last call's contents;
+ * nothing in it needs to start at zero.
+ * Errors: those of bsr_prune_from_dense, with BSR_ERR_WORKSPACE when nb exceeds
+ * BSR_NOALLOC_MAX_BLOCKS (checked before anything is enqueued).
+ */
+LIBBSR_API bsr_status bsr_prune_from_dense_noalloc(const float *W, int64_t N, int64_t K,
+                                                   int64_t ldw, int32_t R, int32_t C, int64_t k,
+                                                   int32_t *indptr, int32_t *indices,
+                                                   float *data, int64_t capacity_blocks,
+                                                   void *stream);
+
 /* Pruning variants for the _ex entry points (Sec. 2.1). */
 typedef enum {
     BSR_NORM_L2 = 0,  /* block key = sum of w^2 (the l2 group norm, squared)                  */

@@ -22,7 +22,8 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 
 # The C ABI's exported entry points (the tests check this list against include/libbsr.h).
 EXPORTS = ["bsr_prune_count", "bsr_prune_count_ex", "bsr_prune_workspace_bytes",
-           "bsr_prune_from_dense", "bsr_prune_from_dense_ex", "bsr_spmm", "bsr_spmm_ex",
+           "bsr_prune_from_dense", "bsr_prune_from_dense_noalloc", "bsr_prune_from_dense_ex",
+           "bsr_spmm", "bsr_spmm_ex",
            "bsr_spmm_batched", "bsr_attention", "bsr_reblock", "bsr_to_dense",
            "bsr_cast_f32_bf16",
            "bsr_status_str", "bsr_last_hip_error"]
@@ -90,6 +91,9 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_prune_from_dense.argtypes = [p, i64, i64, i64, i32, i32, i64, p, p, p, i64, p,
                                              sz, p]
         lib.bsr_prune_from_dense.restype = st
+        lib.bsr_prune_from_dense_noalloc.argtypes = [p, i64, i64, i64, i32, i32, i64, p, p, p,
+                                                     i64, p]
+        lib.bsr_prune_from_dense_noalloc.restype = st
         lib.bsr_spmm.argtypes = [p, ctypes.c_int, i64, i64, ctypes.POINTER(bsr_matrix_t), p, p,
                                  i64, p]
         lib.bsr_spmm.restype = st
@@ -274,6 +278,33 @@ def bsr_prune_from_dense(W: torch.Tensor, R: int, C: int, k: int | None = None,
                                               _stream(stream)),
                "bsr_prune_from_dense_ex")
     return BSRMatrix(N, K, R, C, indptr, indices, data, k)
+
+
+NOALLOC_MAX_BLOCKS = 1 << 20
+
+
+def bsr_prune_from_dense_noalloc(W: torch.Tensor, R: int, C: int, k: int, indptr: torch.Tensor,
+                                 indices: torch.Tensor, data: torch.Tensor,
+                                 stream=None) -> BSRMatrix:
+    """bsr_prune_from_dense_noalloc into caller-allocated outputs (the library allocates
+    nothing: its workspace is a fixed array, at most NOALLOC_MAX_BLOCKS blocks)."""
+    _require_cuda(W, "W", torch.float32)
+    N, K = W.shape
+    ldw = _pitch(W, "W")
+    Nb = N // R if R > 0 and N % R == 0 else 0
+    if indptr.numel() < Nb + 1 or indices.numel() < k or data.numel() < k * R * C:
+        raise ValueError("output tensors are smaller than k blocks need")
+    for t, n, dt in ((indptr, "indptr", torch.int32), (indices, "indices", torch.int32),
+                     (data, "data", torch.float32)):
+        _require_cuda(t, n, dt)
+        if not t.is_contiguous():
+            raise ValueError(f"{n} must be contiguous")
+    cap = min(indices.numel(), data.numel() // max(R * C, 1))
+    _check(_lib().bsr_prune_from_dense_noalloc(_ptr(W), N, K, ldw, R, C, k, _ptr(indptr),
+                                               _ptr(indices), _ptr(data), cap, _stream(stream)),
+           "bsr_prune_from_dense_noalloc")
+    return BSRMatrix(N, K, R, C, indptr, indices, data.view(-1)[: max(cap, 1) * R * C]
+                     .view(max(cap, 1), R, C), k)
 
 
 def bsr_spmm(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None = None,

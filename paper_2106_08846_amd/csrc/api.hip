@@ -110,6 +110,20 @@ bsr_status bsr_prune_from_dense(const float *W, int64_t N, int64_t K, int64_t ld
                              BSR_NORM_L2, BSR_SELECT_GLOBAL, stream);
 }
 
+bsr_status bsr_prune_from_dense_noalloc(const float *W, int64_t N, int64_t K, int64_t ldw,
+                                        int32_t R, int32_t C, int64_t k, int32_t *indptr,
+                                        int32_t *indices, float *data, int64_t capacity_blocks,
+                                        void *stream) {
+    bsr_status s = bsr::check_prune_noalloc(W, N, K, ldw, R, C, k, indptr, indices, data,
+                                            capacity_blocks);
+    if (s != BSR_OK) return s;
+    if ((s = bsr::ensure_device()) != BSR_OK) return s;
+    void *scratch = nullptr;
+    if ((s = bsr::noalloc_scratch(&scratch)) != BSR_OK) return s;
+    return bsr::launch_prune(W, N, K, ldw, R, C, k, indptr, indices, data, scratch,
+                             BSR_NORM_L2, BSR_SELECT_GLOBAL, stream);
+}
+
 bsr_status bsr_prune_from_dense_ex(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R,
                                    int32_t C, int64_t k, int32_t *indptr, int32_t *indices,
                                    float *data, int64_t capacity_blocks, void *workspace,

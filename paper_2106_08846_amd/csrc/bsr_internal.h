@@ -22,6 +22,18 @@ bsr_status check_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_
                        int64_t k, const int32_t *indptr, const int32_t *indices,
                        const float *data, int64_t capacity_blocks, const void *workspace,
                        size_t ws_bytes);
+// bsr_prune_from_dense_noalloc: the workspace lives in a fixed device array of this many bytes,
+// the prune workspace of BSR_NOALLOC_MAX_BLOCKS blocks (8-byte keys, then 4-byte source ids,
+// each region a multiple of 256 bytes).
+constexpr size_t kNoallocScratchBytes = size_t(BSR_NOALLOC_MAX_BLOCKS) * 8 +
+                                        size_t(BSR_NOALLOC_MAX_BLOCKS) * 4;
+static_assert(BSR_NOALLOC_MAX_BLOCKS % 64 == 0, "both regions stay 256-byte multiples");
+bsr_status check_prune_noalloc(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R,
+                               int32_t C, int64_t k, const int32_t *indptr,
+                               const int32_t *indices, const float *data,
+                               int64_t capacity_blocks);
+// Device address of this device's scratch array (found once per device, with it current).
+bsr_status noalloc_scratch(void **ptr);
 // Options of the _ex pruning entry point (after check_prune: N, R valid, k in [0, nb]).
 bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32_t R, int64_t k);
 bsr_status check_matrix(const bsr_matrix_t *W);

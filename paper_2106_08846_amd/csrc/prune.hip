@@ -18,11 +18,22 @@
 //      Per-row selection (prune_select_rows_kernel) runs the same radix select and id-order
 //      sweep inside each block-row, one workgroup per row; indptr is then i * k_row.
 //   3. prune_copy_kernel: one thread per output element copies the kept blocks' bits.
+#include <mutex>
+
 #include "device_common.h"
 
 namespace bsr {
 
 namespace {
+
+// The workspace of bsr_prune_from_dense_noalloc: a fixed device array, one copy per GPU.  In
+// host code its name is only a stand-in for the symbol; the device address of each GPU's copy
+// comes from hipGetSymbolAddress, looked up once per device with that device current.
+__device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kScratchDevices = 64;
+void *g_scratch_ptr[kScratchDevices] = {};
+std::mutex g_scratch_mutex;
 
 constexpr int kKeyThreads = 256;
 constexpr int kSelThreads = 1024;
@@ -250,6 +261,29 @@ __global__ __launch_bounds__(256) void prune_copy_kernel(
 }
 
 }  // namespace
+
+bsr_status noalloc_scratch(void **ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        set_last_hip_error(hipGetErrorString(e));
+        return BSR_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kScratchDevices) return BSR_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr) {
+            set_last_hip_error(e != hipSuccess ? hipGetErrorString(e)
+                                               : "hipGetSymbolAddress returned NULL");
+            return BSR_ERR_HIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return BSR_OK;
+}
 
 bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R, int32_t C,
                         int64_t k, int32_t *indptr, int32_t *indices, float *data,

@@ -50,6 +50,24 @@ bsr_status check_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32_
     return BSR_OK;
 }
 
+bsr_status check_prune_noalloc(const float *W, int64_t N, int64_t K, int64_t ldw, int32_t R,
+                               int32_t C, int64_t k, const int32_t *indptr,
+                               const int32_t *indices, const float *data,
+                               int64_t capacity_blocks) {
+    // The same checks as check_prune, with the library's fixed scratch array standing in for
+    // the workspace: a matrix with more blocks than it holds is BSR_ERR_WORKSPACE.
+    if (tiles(N, K, R, C)) {
+        const int64_t Nb = N / R, Kb = K / C;
+        if (Nb <= kMaxBlocks / Kb && Nb * Kb > BSR_NOALLOC_MAX_BLOCKS) {
+            const bsr_status s = check_prune(W, N, K, ldw, R, C, k, indptr, indices, data,
+                                             capacity_blocks, &kMaxBlocks, 0);
+            return s == BSR_OK ? BSR_ERR_WORKSPACE : s;
+        }
+    }
+    return check_prune(W, N, K, ldw, R, C, k, indptr, indices, data, capacity_blocks,
+                       &kMaxBlocks, kNoallocScratchBytes);
+}
+
 bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32_t R,
                                int64_t k) {
     if (!opts) return BSR_OK;

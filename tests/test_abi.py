@@ -373,3 +373,19 @@ def test_spmm_batched_rejects_aliasing_between_products(L, lib):
     shared_x = (L.bsr_spmm_item_t * 2)(_item(L, m, Y=Y0), _item(L, m, Y=Y1))
     assert lib.bsr_spmm_batched(shared_x, 2, None, None) not in (1, 2, 3)  # valid: past checks
 
+
+def test_prune_noalloc_validation(lib):
+    """The allocation-free prune checks its arguments like bsr_prune_from_dense and refuses a
+    matrix with more blocks than its fixed workspace holds, before touching a device."""
+    def call(N=64, K=64, R=8, C=8, k=6, cap=6, W=FAKE, indptr=FAKE, indices=FAKE, data=FAKE):
+        return lib.bsr_prune_from_dense_noalloc(W, N, K, K, R, C, k, indptr, indices, data, cap,
+                                                None)
+    assert call(W=None) == 1
+    assert call(R=7) == 2
+    assert call(k=65) == 3
+    assert call(cap=5) == 5
+    big = 1 << 20                                # N * K blocks of 1 x 1: one past the maximum
+    assert call(N=1024, K=1025, R=1, C=1, k=10, cap=10) == 6
+    assert call(N=1024, K=1025, R=1, C=1, k=10, cap=10, W=None) == 1   # other errors first
+    assert call(N=1024, K=1024, R=1, C=1, k=10, cap=10) not in (1, 2, 3, 5, 6)  # fits: past checks
+    assert big == 1024 * 1024
