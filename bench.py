@@ -67,6 +67,8 @@ def parse(argv=None):
     ap.add_argument("--rotate", type=int, default=0,
                     help="copies of every input and output to rotate through (0: 1 for "
                          "workloads that exceed the last-level cache by themselves, else 8)")
+    ap.add_argument("--no-plan", action="store_true",
+                    help="run the products without per-matrix plans")
     ap.add_argument("--graph", action="store_true",
                     help="time the step as HIP graph replays instead of direct calls")
     ap.add_argument("--no-rows", action="store_true",
@@ -171,7 +173,7 @@ class Prepared:
     bsr_spmm_batched calls of up to 8 products, `sets` copies of every tensor to rotate through
     (copy s of a launch only touches set s)."""
 
-    def __init__(self, wl, sets: int, slices: int = 0):
+    def __init__(self, wl, sets: int, slices: int = 0, plans: bool = True):
         import torch
         from paper_2106_08846_amd import bsr as B
         dev = torch.device("cuda:0")
@@ -207,11 +209,24 @@ class Prepared:
                     b = b.clone()
                 Y = torch.empty((c["T"], c["N"]), dtype=torch.float32, device=dev)
                 prods.append((xs[c["x_index"]], M, b, Y))
-            groups = [prods[i:i + 8] for i in range(0, len(prods), 8)]
-            self.sets.append([B.SpmmBatchCall(g, slices=slices or None) for g in groups])
+            # Per-matrix plans (prepared once, like the pruning) where the block shape has one.
+            pls = [self._plan(B, p[1]) if plans else None for p in prods]
+            self.planned = any(pl is not None for pl in pls)
+            groups = [range(i, min(i + 8, len(prods))) for i in range(0, len(prods), 8)]
+            self.sets.append([B.SpmmBatchCall([prods[i] for i in g], slices=slices or None,
+                                              plans=[pls[i] for i in g]) for g in groups])
             self.products.append(prods)
         self.Xs = Xs
         torch.cuda.synchronize()
+
+    @staticmethod
+    def _plan(B, M):
+        try:
+            return B.bsr_plan_prepare(M)
+        except B.BSRError as e:
+            if e.status == 9:      # no plan for this block shape
+                return None
+            raise
 
     @property
     def launches_per_step(self) -> int:
@@ -323,13 +338,14 @@ def dense_times_us(prep, rounds: int) -> dict:
 # ------------------------------------------------------------------------------------- rows
 
 
-def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = None) -> dict:
+def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = None,
+        plans: bool = True) -> dict:
     """One block-shape row: per-launch kernel-event times (median, p10, p90), effective rates,
     roof fraction, and the dense GEMM beside it."""
     import torch
     print(f"# row {spec}", file=sys.stderr, flush=True)
     wl = build_workload(spec)
-    prep = Prepared(wl, rotate)
+    prep = Prepared(wl, rotate, plans=plans)
     for s in range(rotate):
         prep.step(s)
     torch.cuda.synchronize()
@@ -337,7 +353,7 @@ def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = No
     r = roofline(prep, lt["mean"])
     c0 = prep.calls[0]
     out = {"workload": wl.name, "spec": spec, "block": f"{c0['R']}x{c0['C']}",
-           "dtype": "bf16" if wl.bf16 else "f32", "tokens": c0["T"],
+           "dtype": "bf16" if wl.bf16 else "f32", "tokens": c0["T"], "plans": prep.planned,
            "products_per_launch": len(prep.calls) // prep.launches_per_step,
            "launches": lt["n"],
            "protocol": (f"cold: {rotate} rotating copies of every input and output"
@@ -365,18 +381,19 @@ def rows(args) -> dict:
     """The other configurations' block-shape rows (see the module docstring)."""
     res = {}
     dense = not args.no_dense
+    pl = not args.no_plan
     other = "bert_large:32x32" if args.workload != "bert_large:32x32" else "bert_large:32x1"
-    res["bert_large_zipf"] = [row(other, 1, 5, dense)]
+    res["bert_large_zipf"] = [row(other, 1, 5, dense, plans=pl)]
     qkv = []
     for shape in ("32x1", "16x16"):
         for dt in ("", ":bf16"):
             for d in ("0.05", "0.1", "0.2", "0.4"):
                 qkv.append(row(f"fused_qkv:{shape}:{d}{dt}", ROTATE_SETS, 8 * ROTATE_SETS,
-                               dense))
+                               dense, plans=pl))
     res["fused_qkv"] = qkv
-    res["sweep_T128"] = [row(f"sweep:{s}", 1, 100, dense) for s in
+    res["sweep_T128"] = [row(f"sweep:{s}", 1, 100, dense, plans=pl) for s in
                          ("1x1", "8x1", "16x1", "32x1", "1x32", "4x4", "8x8", "16x16", "32x32")]
-    res["bert_base_attn_T128"] = [row("bert_base_attn", 1, 100, dense)]
+    res["bert_base_attn_T128"] = [row("bert_base_attn", 1, 100, dense, plans=pl)]
     return res
 
 
@@ -502,7 +519,7 @@ def main(argv=None) -> int:
     rotate = args.rotate or (1 if args.workload.startswith("bert_large") else ROTATE_SETS)
     print(f"# workload {wl.name}: {len(wl.projections)} projections, {rotate} set(s)",
           file=sys.stderr, flush=True)
-    prep = Prepared(wl, rotate, args.slices)
+    prep = Prepared(wl, rotate, args.slices, plans=not args.no_plan)
     for i in range(args.warmup):
         prep.step(i % rotate)
     torch.cuda.synchronize()
@@ -560,7 +577,8 @@ def main(argv=None) -> int:
                    "density": wl.projections[0].density,
                    "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in prep.calls][:8],
                    "timing": "hip_graph_replay" if args.graph else "direct_calls",
-                   "rotating_sets": rotate, "slices": args.slices or "auto"},
+                   "rotating_sets": rotate, "slices": args.slices or "auto",
+                   "plans": prep.planned},
         "step_ms": {k: st[k] for k in ("median", "p10", "p90", "n")},
         "roofline": roof,
     }

@@ -272,6 +272,70 @@ LIBBSR_API bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_i
                                        const bsr_spmm_options_t *opts, void *stream);
 
 /*
+ * A per-matrix product plan: the work of a BSR product that depends only on the matrix,
+ * prepared once and reused by every product with that matrix (the paper's compiler keeps a
+ * buffer of sparse operators and reuses tasks whose sparse structure is identical, Sec. 2.2,
+ * third bullet).  The plan cuts every block-row into units of unit_blocks consecutive stored
+ * blocks (the last unit of a row padded with zero blocks) and stores
+ *   - uptr int32[N/R + 1]: the first unit of every block-row (a row pointer over units);
+ *   - the units' block columns and weights, packed in the order the matrix cores consume them,
+ *     so one 16-byte load per lane fetches a unit's operands;
+ * in caller-owned device memory.  A product with a plan computes the same sums in the same
+ * order as the product without one (bit-identical Y); it only reads its operands faster.
+ * Plans exist for 32x1 blocks (fp32 and bf16 data); bsr_plan_bytes reports
+ * BSR_ERR_UNSUPPORTED for other shapes.
+ * The struct is filled by bsr_plan_prepare and read by the planned products; it records the
+ * matrix it was prepared for, and a product whose matrix differs (shape, block shape, dtype,
+ * nnzb or array addresses) is rejected with BSR_ERR_ARG.  The plan's memory must stay
+ * allocated and unchanged while products use it; after the matrix's arrays change (same
+ * addresses, new contents), prepare the plan again.  The library checks the struct against
+ * the matrix, not the contents of mem: the products trust what bsr_plan_prepare wrote there
+ * (every column the plan stores is clamped into the X tile when it is packed, so a plan
+ * whose matrix indices were out of range still reads only inside the tile).
+ */
+typedef struct {
+    void *mem;                /* device memory holding the plan (caller-owned)                */
+    size_t bytes;             /* its size, >= bsr_plan_bytes()                                 */
+    int64_t n_rows, n_cols, nnzb;                    /* the matrix it was prepared for        */
+    int32_t R, C;
+    int32_t dtype;
+    const int32_t *indptr;
+    const int32_t *indices;
+    const void *data;
+    int32_t unit_blocks;      /* stored blocks per unit                                        */
+    int64_t max_units;        /* units the layout reserves: ceil(nnzb / unit_blocks) + N / R   */
+    int64_t uptr_offset;      /* byte offsets into mem of the three arrays                     */
+    int64_t col_offset;
+    int64_t val_offset;
+} bsr_plan_t;
+
+/* Device bytes a plan for W needs (host only).  Errors: BSR_ERR_NULL, those of a malformed
+ * descriptor (BSR_ERR_SHAPE, BSR_ERR_ARG), BSR_ERR_UNSUPPORTED (no planned kernel for the
+ * block shape, or sizes past int32 offsets). */
+LIBBSR_API bsr_status bsr_plan_bytes(const bsr_matrix_t *W, size_t *bytes);
+
+/*
+ * Prepare the plan of W in `mem` (device, caller-owned, at least bsr_plan_bytes(W) bytes, not
+ * overlapping W's arrays) and fill *plan.  Two kernels on `stream`: a scan of the per-row unit
+ * counts, then the packing of every unit's columns and weights.  Errors: those of
+ * bsr_plan_bytes, BSR_ERR_NULL (mem, plan), BSR_ERR_WORKSPACE (bytes too small), BSR_ERR_ARG
+ * (mem overlapping W's arrays), BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_plan_prepare(const bsr_matrix_t *W, void *mem, size_t bytes,
+                                       bsr_plan_t *plan, void *stream);
+
+/*
+ * bsr_spmm_batched with a plan per product (plans may be NULL, or plans[i] NULL for a product
+ * without one).  A planned product runs on the planned form of the matrix-core kernel and
+ * gives the same Y, bit for bit, as the same call without plans.  Products with and without
+ * plans never share a launch.  Errors: those of bsr_spmm_batched, and BSR_ERR_ARG for a plan
+ * that does not describe its product's matrix or whose memory overlaps a Y.
+ */
+LIBBSR_API bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items,
+                                               const bsr_plan_t *const *plans, int32_t n_items,
+                                               const bsr_spmm_options_t *opts, void *stream);
+
+/*
  * Scaled dot-product attention of the BERT attention block (Sec. 2.3 prunes BERT's attention
  * weights; its Q, K, V and output projections are the BSR products above):
  *   O[b*seq + s][h*64 + d] = sum_j p_j V[b*seq + j][h*64 + d],

@@ -24,7 +24,7 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 EXPORTS = ["bsr_prune_count", "bsr_prune_count_ex", "bsr_prune_workspace_bytes",
            "bsr_prune_from_dense", "bsr_prune_from_dense_noalloc", "bsr_prune_from_dense_ex",
            "bsr_spmm", "bsr_spmm_ex",
-           "bsr_spmm_batched", "bsr_attention", "bsr_reblock", "bsr_to_dense",
+           "bsr_spmm_batched", "bsr_plan_bytes", "bsr_plan_prepare", "bsr_spmm_batched_planned", "bsr_attention", "bsr_reblock", "bsr_to_dense",
            "bsr_cast_f32_bf16",
            "bsr_status_str", "bsr_last_hip_error"]
 NORM_L2, NORM_L1 = 0, 1
@@ -62,6 +62,16 @@ class bsr_spmm_item_t(ctypes.Structure):
     _fields_ = [("X", ctypes.c_void_p), ("x_dtype", ctypes.c_int), ("T", ctypes.c_int64),
                 ("ldx", ctypes.c_int64), ("W", ctypes.POINTER(bsr_matrix_t)),
                 ("bias", ctypes.c_void_p), ("Y", ctypes.c_void_p), ("ldy", ctypes.c_int64)]
+
+
+class bsr_plan_t(ctypes.Structure):
+    _fields_ = [("mem", ctypes.c_void_p), ("bytes", ctypes.c_size_t),
+                ("n_rows", ctypes.c_int64), ("n_cols", ctypes.c_int64), ("nnzb", ctypes.c_int64),
+                ("R", ctypes.c_int32), ("C", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p),
+                ("data", ctypes.c_void_p), ("unit_blocks", ctypes.c_int32),
+                ("max_units", ctypes.c_int64), ("uptr_offset", ctypes.c_int64),
+                ("col_offset", ctypes.c_int64), ("val_offset", ctypes.c_int64)]
 
 
 _LIB = None
@@ -103,6 +113,15 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_spmm_batched.argtypes = [ctypes.POINTER(bsr_spmm_item_t), i32,
                                          ctypes.POINTER(bsr_spmm_options_t), p]
         lib.bsr_spmm_batched.restype = st
+        lib.bsr_plan_bytes.argtypes = [ctypes.POINTER(bsr_matrix_t), ctypes.POINTER(sz)]
+        lib.bsr_plan_bytes.restype = st
+        lib.bsr_plan_prepare.argtypes = [ctypes.POINTER(bsr_matrix_t), p, sz,
+                                         ctypes.POINTER(bsr_plan_t), p]
+        lib.bsr_plan_prepare.restype = st
+        lib.bsr_spmm_batched_planned.argtypes = [ctypes.POINTER(bsr_spmm_item_t),
+                                                 ctypes.POINTER(ctypes.POINTER(bsr_plan_t)), i32,
+                                                 ctypes.POINTER(bsr_spmm_options_t), p]
+        lib.bsr_spmm_batched_planned.restype = st
         lib.bsr_to_dense.argtypes = [ctypes.POINTER(bsr_matrix_t), p, i64, p]
         lib.bsr_to_dense.restype = st
         lib.bsr_attention.argtypes = [p, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32,
@@ -356,16 +375,63 @@ def _check_call(X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None,
     _require_cuda(Y, "Y", torch.float32)
 
 
+class BSRPlan:
+    """A per-matrix product plan (bsr_plan_prepare) in a torch device buffer: the matrix's unit
+    row pointer and its units' columns and weights packed in the order the matrix cores read
+    them.  It stays valid while the matrix's arrays are unchanged."""
+
+    def __init__(self, W: BSRMatrix, mem: torch.Tensor, plan: bsr_plan_t):
+        self.W = W
+        self.mem = mem
+        self.struct = plan
+
+    @property
+    def unit_blocks(self) -> int:
+        return self.struct.unit_blocks
+
+    def uptr(self) -> torch.Tensor:
+        """The unit row pointer (a view into the plan's memory)."""
+        nb = self.W.n_rows // self.W.R + 1
+        off = self.struct.uptr_offset
+        return self.mem[off:off + 4 * nb].view(torch.int32)
+
+
+def bsr_plan_bytes(W: BSRMatrix) -> int:
+    """Device bytes of W's plan (raises BSRError BSR_ERR_UNSUPPORTED for shapes without one)."""
+    n = ctypes.c_size_t(0)
+    m = W.struct()
+    _check(_lib().bsr_plan_bytes(ctypes.byref(m), ctypes.byref(n)), "bsr_plan_bytes")
+    return int(n.value)
+
+
+def bsr_plan_prepare(W: BSRMatrix, mem: torch.Tensor | None = None, stream=None) -> BSRPlan:
+    """Prepare W's plan in `mem` (a uint8 device tensor of at least bsr_plan_bytes(W) bytes,
+    allocated here when None)."""
+    nbytes = bsr_plan_bytes(W)
+    if mem is None:
+        mem = torch.empty(nbytes, dtype=torch.uint8, device=W.indptr.device)
+    _require_cuda(mem, "mem", torch.uint8)
+    if not mem.is_contiguous():
+        raise ValueError("mem must be contiguous")
+    plan = bsr_plan_t()
+    m = W.struct()
+    _check(_lib().bsr_plan_prepare(ctypes.byref(m), _ptr(mem), mem.numel(), ctypes.byref(plan),
+                                   _stream(stream)), "bsr_plan_prepare")
+    return BSRPlan(W, mem, plan)
+
+
 class SpmmBatchCall:
     """A bsr_spmm_batched call with its arguments marshalled once.
 
-    `products` is a list of (X, W, bias, Y) tuples.  Calling the object re-issues the same C
-    call on the given stream, or on torch's current stream, which is what a serving loop or a
-    HIP graph capture needs: the per-call host cost is one foreign call.  The tensors stay
-    referenced by the object.
+    `products` is a list of (X, W, bias, Y) tuples; `plans` (optional) a list of the same
+    length whose entries are BSRPlan objects or None, making it a bsr_spmm_batched_planned
+    call.  Calling the object re-issues the same C call on the given stream, or on torch's
+    current stream, which is what a serving loop or a HIP graph capture needs: the per-call
+    host cost is one foreign call.  The tensors stay referenced by the object.
     """
 
-    def __init__(self, products, kernel: int | None = None, slices: int | None = None):
+    def __init__(self, products, kernel: int | None = None, slices: int | None = None,
+                 plans=None):
         self._keep = list(products)
         self._mats = []
         items = (bsr_spmm_item_t * max(len(products), 1))()
@@ -379,14 +445,32 @@ class SpmmBatchCall:
         self._items = items
         self._opts = bsr_spmm_options_t(kernel or 0, slices or 0, None, None)
         self._timed_opts = bsr_spmm_options_t(kernel or 0, slices or 0, None, None)
-        self._fn = _lib().bsr_spmm_batched
         self._n = len(products)
         self.Y = [p[3] for p in products]
+        self._plans = None
+        if plans is not None:
+            if len(plans) != len(products):
+                raise ValueError("give one plan (or None) per product")
+            self._keep_plans = list(plans)
+            arr = (ctypes.POINTER(bsr_plan_t) * max(len(plans), 1))()
+            for i, (pl, (X, W, bias, Y)) in enumerate(zip(plans, products)):
+                if pl is not None:
+                    if pl.W is not W:
+                        raise ValueError("a plan must be prepared for its product's matrix")
+                    arr[i] = ctypes.pointer(pl.struct)
+            self._plans = arr
+            fn = _lib().bsr_spmm_batched_planned
+            plans_arr = arr
+            self._fn = lambda items, n, opts, st: fn(items, plans_arr, n, opts, st)
+            self._name = "bsr_spmm_batched_planned"
+        else:
+            self._fn = _lib().bsr_spmm_batched
+            self._name = "bsr_spmm_batched"
 
     def __call__(self, stream=None):
         st = self._fn(self._items, self._n, ctypes.byref(self._opts), _stream(stream))
         if st != 0:
-            _check(st, "bsr_spmm_batched")
+            _check(st, self._name)
         return self.Y
 
     def timed(self, start: torch.cuda.Event, stop: torch.cuda.Event, stream=None):
@@ -403,7 +487,7 @@ class SpmmBatchCall:
         self._timed_opts.stop_event = stop.cuda_event
         st = self._fn(self._items, self._n, ctypes.byref(self._timed_opts), _stream(stream))
         if st != 0:
-            _check(st, "bsr_spmm_batched")
+            _check(st, self._name)
         return self.Y
 
 
@@ -411,8 +495,10 @@ class SpmmCall(SpmmBatchCall):
     """A single prepared product (a batch of one): bsr_spmm_ex with arguments marshalled once."""
 
     def __init__(self, X: torch.Tensor, W: BSRMatrix, bias: torch.Tensor | None,
-                 Y: torch.Tensor, kernel: int | None = None, slices: int | None = None):
-        super().__init__([(X, W, bias, Y)], kernel, slices)
+                 Y: torch.Tensor, kernel: int | None = None, slices: int | None = None,
+                 plan: "BSRPlan | None" = None):
+        super().__init__([(X, W, bias, Y)], kernel, slices,
+                         plans=None if plan is None else [plan])
         self.Y = Y
 
     def __call__(self, stream=None) -> torch.Tensor:
@@ -425,18 +511,19 @@ class SpmmCall(SpmmBatchCall):
 
 
 def bsr_spmm_batched(products, kernel: int | None = None, slices: int | None = None,
-                     stream=None) -> list:
+                     stream=None, plans=None) -> list:
     """Several products Y_i = X_i W_i^T + bias_i in as few launches as possible.
 
     `products` is a list of (X, W, bias, Y) with Y allocated by the caller (Y may be None to
-    allocate it).  Returns the list of Y tensors.
+    allocate it); `plans` optionally one BSRPlan (or None) per product
+    (bsr_spmm_batched_planned).  Returns the list of Y tensors.
     """
     full = []
     for X, W, bias, Y in products:
         if Y is None:
             Y = torch.empty((X.shape[0], W.n_rows), dtype=torch.float32, device=X.device)
         full.append((X, W, bias, Y))
-    return SpmmBatchCall(full, kernel, slices)(stream)
+    return SpmmBatchCall(full, kernel, slices, plans=plans)(stream)
 
 
 def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

@@ -148,6 +148,53 @@ bsr_status bsr_spmm_ex(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
 
 bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
                             const bsr_spmm_options_t *opts, void *stream) {
+    return bsr_spmm_batched_planned(items, nullptr, n_items, opts, stream);
+}
+
+bsr_status bsr_plan_bytes(const bsr_matrix_t *W, size_t *bytes) {
+    if (!W || !bytes) return BSR_ERR_NULL;
+    bsr_status s = bsr::check_matrix(W);
+    if (s != BSR_OK) return s;
+    const bsr::PlanLayout L = bsr::plan_layout(W);
+    if (L.unit_blocks == 0 || L.max_units * 64 >= (int64_t(1) << 31)) return BSR_ERR_UNSUPPORTED;
+    *bytes = size_t(L.total);
+    return BSR_OK;
+}
+
+bsr_status bsr_plan_prepare(const bsr_matrix_t *W, void *mem, size_t bytes, bsr_plan_t *plan,
+                            void *stream) {
+    size_t need = 0;
+    bsr_status s = bsr_plan_bytes(W, &need);
+    if (s != BSR_OK) return s;
+    if (!plan) return BSR_ERR_NULL;
+    const bsr::PlanLayout L = bsr::plan_layout(W);
+    if ((s = bsr::check_plan_prepare(W, mem, bytes, L.total)) != BSR_OK) return s;
+    if ((s = bsr::ensure_device()) != BSR_OK) return s;
+    if ((s = bsr::launch_plan_prepare(W, mem, L, stream)) != BSR_OK) return s;
+    bsr_plan_t p{};
+    p.mem = mem;
+    p.bytes = bytes;
+    p.n_rows = W->n_rows;
+    p.n_cols = W->n_cols;
+    p.nnzb = W->nnzb;
+    p.R = W->R;
+    p.C = W->C;
+    p.dtype = int32_t(W->dtype);
+    p.indptr = W->indptr;
+    p.indices = W->indices;
+    p.data = W->data;
+    p.unit_blocks = L.unit_blocks;
+    p.max_units = L.max_units;
+    p.uptr_offset = L.uptr_offset;
+    p.col_offset = L.col_offset;
+    p.val_offset = L.val_offset;
+    *plan = p;
+    return BSR_OK;
+}
+
+bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan_t *const *plans,
+                                    int32_t n_items, const bsr_spmm_options_t *opts,
+                                    void *stream) {
     if (n_items < 0) return BSR_ERR_ARG;
     if (n_items > 0 && !items) return BSR_ERR_NULL;
     for (int32_t i = 0; i < n_items; ++i) {
@@ -155,6 +202,15 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         bsr_status s =
             bsr::check_spmm(it.X, int(it.x_dtype), it.T, it.ldx, it.W, it.Y, it.ldy, it.bias);
         if (s != BSR_OK) return s;
+        const bsr_plan_t *pl = plans ? plans[i] : nullptr;
+        if (pl) {
+            const bsr::PlanLayout L = bsr::plan_layout(it.W);
+            if (L.unit_blocks == 0 || pl->unit_blocks != L.unit_blocks ||
+                pl->max_units != L.max_units || pl->uptr_offset != L.uptr_offset ||
+                pl->col_offset != L.col_offset || pl->val_offset != L.val_offset)
+                return BSR_ERR_ARG;
+            if ((s = bsr::check_plan_use(it, pl, L.total)) != BSR_OK) return s;
+        }
     }
     if (n_items > 1) {
         bsr_status s = bsr::check_spmm_items(items, n_items);
@@ -174,7 +230,7 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     // or, when its X tile is too wide for LDS, to the column-chunked matrix-core kernel; else to
     // the vector-ALU tile kernel or its column-chunked form; else to the generic kernel (a
     // forced kernel choice narrows this; a forced kernel that does not fit is an error).
-    enum Kind { kGeneric = 0, kTiled = 1, kVtile = 2, kKchunk = 3, kVchunk = 4 };
+    enum Kind { kGeneric = 0, kTiled = 1, kVtile = 2, kKchunk = 3, kVchunk = 4, kFlat = 5 };
     std::vector<int> work;
     for (int32_t i = 0; i < n_items; ++i)
         if (items[i].T > 0) work.push_back(i);
@@ -208,7 +264,14 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
             kind[w] = kVchunk;
         if (kind[w] == kGeneric && (kernel == BSR_KERNEL_TILED || kernel == BSR_KERNEL_VALU))
             return BSR_ERR_UNSUPPORTED;
+        // Linear R x 1 blocks run on the flat-stream form of the matrix-core kernel.
+        if (kind[w] == kTiled && bsr::flat_supported(R, C, dt)) kind[w] = kFlat;
     }
+    // A plan is used where its product runs on the flat kernel (elsewhere it is not needed:
+    // the result is the same without it).
+    std::vector<const bsr_plan_t *> plan_of(work.size(), nullptr);
+    for (size_t w = 0; w < work.size(); ++w)
+        if (plans && kind[w] == kFlat) plan_of[w] = plans[work[w]];
     // Launch order: tiled and vector-ALU products grouped by kernel, block shape and dtype, up
     // to kMaxItems per launch, then generic products one by one.  With an event pair, the start
     // event goes with the first launch and the stop event with the last.
@@ -225,7 +288,8 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
             if (kind[v] != kind[w] || done[v]) continue;
             if (items[work[v]].W->R != items[work[w]].W->R ||
                 items[work[v]].W->C != items[work[w]].W->C ||
-                items[work[v]].W->dtype != items[work[w]].W->dtype)
+                items[work[v]].W->dtype != items[work[w]].W->dtype ||
+                (plan_of[v] != nullptr) != (plan_of[w] != nullptr))
                 continue;
             l.members.push_back(int(v));
             done[v] = 1;
@@ -259,10 +323,17 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
                 continue;
             }
             const bsr::TiledPlan plan =
-                kind[w] == kTiled
-                    ? bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit)
-                    : bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
+                kind[w] == kVtile
+                    ? bsr::plan_vtile(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit)
+                    : bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, S, lds_limit);
             tiled[w] = bsr::TiledWork{plan, it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy};
+            if (const bsr_plan_t *pl = plan_of[w]) {
+                tiled[w].plan_mem = pl->mem;
+                tiled[w].plan_uptr_offset = pl->uptr_offset;
+                tiled[w].plan_col_offset = pl->col_offset;
+                tiled[w].plan_val_offset = pl->val_offset;
+                tiled[w].plan_max_units = pl->max_units;
+            }
         }
     }
 
@@ -280,8 +351,13 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
         } else if (l.kind != kGeneric) {
             bsr::TiledWork batch[bsr::kMaxItems];
             for (size_t m = 0; m < l.members.size(); ++m) batch[m] = tiled[l.members[m]];
-            s = l.kind == kTiled ? bsr::launch_spmm_tiled(batch, int(l.members.size()), stream, lev)
-                                 : bsr::launch_spmm_vtile(batch, int(l.members.size()), stream, lev);
+            const int nm = int(l.members.size());
+            if (l.kind == kFlat)
+                s = bsr::launch_spmm_flat(batch, nm, plan_of[l.members[0]] != nullptr, stream, lev);
+            else if (l.kind == kTiled)
+                s = bsr::launch_spmm_tiled(batch, nm, stream, lev);
+            else
+                s = bsr::launch_spmm_vtile(batch, nm, stream, lev);
         } else {
             const bsr_spmm_item_t &it = items[work[l.members[0]]];
             s = bsr::launch_spmm_generic(it.X, it.T, it.ldx, it.W, it.bias, it.Y, it.ldy, stream,

@@ -39,6 +39,13 @@ bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32
 bsr_status check_matrix(const bsr_matrix_t *W);
 bsr_status check_spmm(const void *X, int x_dtype, int64_t T, int64_t ldx, const bsr_matrix_t *W,
                       const float *Y, int64_t ldy, const float *bias);
+// A plan used by a product (after check_spmm): it describes the item's matrix, its recorded
+// size covers `layout_bytes`, and it does not overlap the item's Y.
+bsr_status check_plan_use(const bsr_spmm_item_t &it, const bsr_plan_t *plan,
+                          int64_t layout_bytes);
+// Plan memory for a matrix (after check_matrix): large enough, not overlapping the matrix.
+bsr_status check_plan_prepare(const bsr_matrix_t *W, const void *mem, size_t bytes,
+                              int64_t layout_bytes);
 // Cross-product aliasing of a batched call (after check_spmm on every item).
 bsr_status check_spmm_items(const bsr_spmm_item_t *items, int32_t n);
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo);

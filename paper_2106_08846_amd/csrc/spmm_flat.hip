@@ -1,0 +1,654 @@
+// BSR product for linear R x 1 blocks (32x1, 16x1; fp32 or bf16 inputs, fp32 accumulate) on
+// gfx950 matrix cores, as one flat stream of units per wave.
+//
+// Y[t][n] = bias[n] + sum over stored blocks p of block-row i = n / R of
+//           X[t][indices[p]] * data[p][n - iR]                                       (Sec. 2.2)
+//
+// Once the input columns named by a block-row's indices are gathered, the row times a token
+// tile is a small dense product whose contraction index is the block; the units of
+// spmm_units.h run it on MFMA.  This kernel differs from the square-block tiled kernel in how
+// a wave walks its work:
+//   * every block-row is cut into units of KB consecutive stored blocks from its first block
+//     (the last unit of a row is partial: its missing blocks read the tile's zero column with
+//     zero weights), and rows are numbered in units by a row pointer over units, uptr;
+//   * slices (whole block-rows) and the waves' shares inside a slice are balanced by units, so
+//     a wave's share starts and ends on unit boundaries and no unit is cut by a wave boundary;
+//   * a wave walks its units as one flat stream, row ends included, with the operands of the
+//     next kDepth units in flight while it multiplies the current one (a ring of kDepth + 1
+//     register buffers);
+//   * the operands come either from the BSR arrays (indices, data; uptr computed in the
+//     prologue from indptr) or from a plan prepared once per matrix (uptr, and every unit's
+//     columns and weights packed in lane order: two 16-byte loads per lane and unit).  Both
+//     give the same instructions on the same values, so Y is bit-identical with or without a
+//     plan.
+// The X tile staging, the bias, the combine of block-rows cut by wave boundaries (in wave
+// order, in LDS) and the stores are those of the tiled kernel.
+#include <type_traits>
+
+#include "device_common.h"
+#include "spmm_tiled.h"
+#include "spmm_units.h"
+
+namespace bsr {
+
+namespace {
+
+constexpr int kNW = 16;            // waves per workgroup
+constexpr int kDepth = 3;          // units in flight ahead of the one being multiplied
+constexpr int kRing = kDepth + 1;  // operand buffers per wave
+
+// Inclusive prefix sum over the 64 lanes of a wave: row shifts by 1, 2, 4 and 8 lanes sum each
+// row of 16 lanes, then the last lane of row 0 is added to row 1 and of row 2 to row 3, and
+// the last lane of row 1 (now rows 0 and 1) to rows 2 and 3.  Lanes a shift reads from
+// outside their row contribute 0.
+__device__ __forceinline__ int wave_scan_incl(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return v;
+}
+
+template <int R, bool BF, bool PL>
+__global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch batch) {
+    using U = Unit<R, 1, BF>;
+    using Src = std::conditional_t<PL, PlanUnit<R, 1, BF>, U>;
+    using Ops = typename Src::Ops;
+    constexpr int NW = kNW, KB = U::KB, kThreads = NW * 64;
+    extern __shared__ float smem[];
+
+    const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
+    const int g = blockIdx.x;
+    const TiledItem &I = batch.item[blockIdx.y];
+    const void *__restrict__ X = I.X;
+    const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
+    const int32_t *__restrict__ indptr = I.indptr;
+    const int32_t *__restrict__ indices = I.indices;
+    const void *__restrict__ data = I.data;
+    const int32_t *__restrict__ uptr = I.uptr;
+    const int32_t *__restrict__ ucol = I.ucol;
+    const void *__restrict__ uval = I.uval;
+    const float *__restrict__ bias = I.bias;
+    float *__restrict__ Y = I.Y;
+    const int K = I.K, nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
+              slices = I.slices, XP = I.XP;
+    // The largest unit position: a plan's reserved units, or (unplanned) nnzb, which bounds
+    // the units computed from indptr (every unit holds at least one block).
+    const int ucap = PL ? I.ucap : nnzb;
+    // LDS: the unit row pointer s_up[Nb + 1], the block row pointer s_ib[Nb + 1] (unplanned),
+    // a spare word, the bias, then the X tile (reused for partial tiles at the end).
+    int *s_up = reinterpret_cast<int *>(smem);
+    int *s_ib = s_up + I.ib_offset;
+    float *s_bias = smem + I.indptr_words;
+    float *Xs = s_bias + I.bias_words;
+
+    asm volatile("" ::"s"(X), "s"(T), "s"(ldx), "s"(ldy), "s"(indptr), "s"(indices), "s"(data),
+                 "s"(bias), "s"(Y));
+    asm volatile("" ::"s"(K), "s"(nnzb), "s"(Nb), "s"(Kb), "s"(num_tiles), "s"(slices), "s"(XP),
+                 "s"(I.indptr_words), "s"(I.bias_words), "s"(I.wbuf_offset));
+
+    // Workgroup -> (token tile, slice), XCD-aware as in the tiled kernel: ids with equal
+    // blockIdx.x mod 8 share an XCD; a product's (tile, slice) pairs in tile-major order are cut
+    // into 8 contiguous ranges, one per XCD.
+    const int xcd = g & 7, rank = g >> 3;
+    const int pairs = num_tiles * slices, per_xcd = (pairs + 7) >> 3;
+    const int q = xcd * per_xcd + rank;
+    if (rank >= per_xcd || q >= pairs) return;
+    const int tile = q / slices, s = q - tile * slices;
+    const int64_t t0 = int64_t(tile) * kTT;
+
+    const int rows = int(T - t0 < kTT ? T - t0 : kTT);
+    constexpr int kXBytes = BF ? 2 : 4;
+    constexpr int kRowsPerWave = kTT / NW;
+    static_assert(kTT % NW == 0, "every wave stages the same number of rows");
+
+    // Prologue, overlapping the latencies of the row pointers, the X tile and the first units:
+    //   (1) every wave loads the row pointers into registers, the bias, then its X-tile rows;
+    //   (2) it computes the unit row pointer (unplanned: from indptr, by a wave prefix sum),
+    //       its share of the slice and issues its first units' loads;
+    //   (3) row pointers, bias and the X tile go to LDS and one barrier ends the prologue.
+    // A product with 256 or more block-rows copies the row pointers to LDS first.
+    constexpr int kIpChunks = 4;   // row-pointer entries per wave in registers: 64 per chunk
+    constexpr int kBiasPer = 4;    // bias entries per thread staged through registers
+    const bool reg_part = Nb < 64 * kIpChunks;
+    int up[kIpChunks];   // uptr[64 j + lane]
+    int ib[kIpChunks];   // indptr[64 j + lane] (unplanned)
+    float bv[kBiasPer];
+    {
+        const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(bias, bias ? unsigned(Nb * R) * 4u : 0u);
+        const unsigned off = reg_part ? unsigned(lane) * 4u : 0x7ffff000u;
+        if constexpr (PL) {
+            const __amdgpu_buffer_rsrc_t rup = buffer_rsrc(uptr, unsigned(Nb + 1) * 4u);
+#pragma unroll
+            for (int j = 0; j < kIpChunks; ++j)
+                up[j] = __builtin_amdgcn_raw_buffer_load_b32(rup, off + 256 * j, 0, 0);
+        } else {
+            // indptr[i] and indptr[i + 1] per lane; a row's unit count is ceil(blocks / KB).
+            const __amdgpu_buffer_rsrc_t rip = buffer_rsrc(indptr, unsigned(Nb + 1) * 4u);
+            int ibn[kIpChunks];
+#pragma unroll
+            for (int j = 0; j < kIpChunks; ++j) {
+                ib[j] = __builtin_amdgcn_raw_buffer_load_b32(rip, off + 256 * j, 0, 0);
+                ibn[j] = __builtin_amdgcn_raw_buffer_load_b32(rip, off + 256 * j + 4, 0, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < kIpChunks; ++j) {
+                ib[j] = clampi(ib[j], 0, nnzb);
+                const int n = clampi(ibn[j], 0, nnzb) - ib[j];
+                up[j] = (64 * j + lane < Nb && n > 0) ? (n + KB - 1) / KB : 0;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kBiasPer; ++u)
+            bv[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                  rb, (threadIdx.x + u * kThreads) * 4, 0, 0));
+    }
+
+    // X tile staging (as in the tiled kernel): loads into v, then conflict-free LDS stores.
+    constexpr int kColsPerLane = 1;
+    const int lane_words = K;
+    unsigned v[kRowsPerWave][kStageChunks];
+    auto x_load = [&](int c0) {
+#pragma unroll
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            const int tr = t < rows ? t : rows - 1;
+            const __amdgpu_buffer_rsrc_t rx =
+                buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
+                            t < rows ? unsigned(K) * kXBytes : 0u);
+#pragma unroll
+            for (int m = 0; m < kStageChunks; ++m) {
+                if constexpr (BF)
+                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b16(rx, (c0 + lane) * 2 + 128 * m,
+                                                                   0, 0);
+                else
+                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b32(rx, (c0 + lane) * 4 + 256 * m,
+                                                                   0, 0);
+            }
+        }
+    };
+    auto x_store = [&](int c0, auto clamp) {
+#pragma unroll
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            if constexpr (U::kTransposed) {
+                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs) + t;
+#pragma unroll
+                for (int m = 0; m < kStageChunks; ++m) {
+                    const int c = c0 + 64 * m + lane;
+                    xt[(decltype(clamp)::value ? min(c, K) : c) * XP] = bf16_t(v[r][m]);
+                }
+            } else {
+                unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * XP;
+#pragma unroll
+                for (int m = 0; m < kStageChunks; ++m) {
+                    unsigned w = v[r][m];
+                    if constexpr (BF) w <<= 16;   // bf16 -> fp32, exact
+                    const int c = c0 + 64 * m + lane;
+                    dst[decltype(clamp)::value ? min(c, lane_words) : c] = w;
+                }
+            }
+        }
+    };
+    static_assert(kColsPerLane == 1, "R x 1 tiles move one column per lane");
+    using Clamp = std::true_type;
+    using NoClamp = std::false_type;
+    x_load(0);
+
+    // The wave's share, in units.  Slice s covers whole block-rows [row_lo, row_hi), row_lo the
+    // first row whose unit start is >= floor(s U / slices); its units [Q0, Q1) are split evenly
+    // over the waves (wave w: [Pw, Pw1)).  A wave owns the rows whose first unit lies in its
+    // range (the last wave also owns trailing empty rows); units at the front of its range that
+    // belong to row rlo - 1 are a head, summed into that row by the wave that owns it.
+    int64_t k, Q0, Q1;
+    int row_lo, row_hi, Pw, Pw1, rlo, rhi, head_end, row, p, end;
+    int ws = 0, wsn = 0;   // wave starts, one per lane: wave `lane` and wave lane + 1
+    auto share = [&](auto lower_bound) {
+        static_assert(NW == 16, "wave starts use a division by 16");
+        const unsigned span = unsigned(Q1 - Q0), hi = span >> 4, lo = span & 15u;
+        const unsigned l0 = unsigned(lane), l1 = l0 + 1;
+        ws = int(Q0) + int(hi * l0 + ((lo * l0) >> 4));
+        wsn = int(Q0) + int(hi * l1 + ((lo * l1) >> 4));
+        Pw = __builtin_amdgcn_readlane(ws, wave);
+        Pw1 = __builtin_amdgcn_readlane(wsn, wave);
+        rlo = (wave == 0) ? row_lo : lower_bound(int64_t(Pw));
+        rlo = rlo < row_lo ? row_lo : (rlo > row_hi ? row_hi : rlo);
+        rhi = (wave == NW - 1) ? row_hi : lower_bound(int64_t(Pw1));
+        rhi = rhi < rlo ? rlo : (rhi > row_hi ? row_hi : rhi);
+    };
+    // Entry i (uniform, <= Nb) of a register-resident row pointer: one lane read per chunk and
+    // a scalar select.
+    auto lane_read = [&](const int(&a)[kIpChunks], int i, auto nch) -> int {
+        constexpr int NCH = decltype(nch)::value;
+        const int l = i & 63, c = i >> 6;
+        int x = __builtin_amdgcn_readlane(a[0], l);
+#pragma unroll
+        for (int j = 1; j < NCH; ++j) {
+            const int y = __builtin_amdgcn_readlane(a[j], l);
+            x = c == j ? y : x;
+        }
+        return x;
+    };
+    auto reg_partition = [&](auto nch) {
+        constexpr int NCH = decltype(nch)::value;
+        if constexpr (PL) {
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) up[j] = clampi(up[j], 0, ucap);
+        } else {
+            // Exclusive prefix of the per-row unit counts, chunk by chunk.
+            int carry = 0;
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) {
+                const int incl = wave_scan_incl(up[j]) + carry;
+                const int excl = incl - up[j];
+                carry = __builtin_amdgcn_readlane(incl, 63);
+                up[j] = excl;
+            }
+        }
+        unsigned long long in_rows[NCH];
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) in_rows[j] = __ballot(64 * j + lane < Nb);
+        auto count_rows = [&](auto pred) -> int {
+            int c = 0;
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) c += __popcll(__ballot(pred(up[j])) & in_rows[j]);
+            return c;
+        };
+        k = lane_read(up, Nb, nch);
+        auto slice_start = [&](int s2) -> int {
+            const uint64_t sk = uint64_t(s2) * uint64_t(k);
+            return count_rows([&](int x) { return uint64_t(x + 1) * uint64_t(slices) <= sk; });
+        };
+        row_lo = (s == 0) ? 0 : slice_start(s);
+        row_hi = (s == slices - 1) ? Nb : slice_start(s + 1);
+        Q0 = lane_read(up, row_lo, nch);
+        Q1 = lane_read(up, row_hi, nch);
+        if (Q1 < Q0) Q1 = Q0;
+        share([&](int64_t v) { return count_rows([&](int x) { return x < int(v); }); });
+        head_end = (rlo < rhi) ? lane_read(up, rlo, nch) : Pw1;
+        head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
+        if (head_end > Pw) {
+            row = rlo - 1;
+            p = Pw;
+            end = head_end;
+        } else {
+            // First owned row with units: the last row i with uptr[i] <= uptr[rlo], if its
+            // units extend past that start.
+            row = rhi;
+            p = end = 0;
+            if (rlo < rhi) {
+                const int v0 = lane_read(up, rlo, nch);
+                const int c = count_rows([&](int x) { return x < v0 + 1; });
+                const int e = lane_read(up, c, nch);
+                if (c - 1 >= rlo && c - 1 < rhi && e > v0) {
+                    row = c - 1;
+                    p = v0;
+                    end = e < Pw1 ? e : Pw1;
+                }
+            }
+        }
+    };
+    if (__builtin_expect(Nb < 64, 1)) {
+        reg_partition(std::integral_constant<int, 1>{});
+    } else if (__builtin_expect(reg_part, 1)) {
+        reg_partition(std::integral_constant<int, kIpChunks>{});
+    } else {
+        // Row pointers in LDS; unplanned, wave 0 forms the unit row pointer by prefix sums.
+        if constexpr (PL) {
+            for (int i = threadIdx.x; i <= Nb; i += kThreads) s_up[i] = clampi(uptr[i], 0, ucap);
+        } else {
+            for (int i = threadIdx.x; i <= Nb; i += kThreads) s_ib[i] = clampi(indptr[i], 0, nnzb);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        if constexpr (!PL) {
+            if (wave == 0) {
+                int carry = 0;
+                for (int base = 0; base <= Nb; base += 64) {
+                    const int i = base + lane;
+                    const int n = i < Nb ? s_ib[i + 1] - s_ib[i] : 0;
+                    const int cnt = n > 0 ? (n + KB - 1) / KB : 0;
+                    const int incl = wave_scan_incl(cnt) + carry;
+                    if (i <= Nb) s_up[i] = incl - cnt;
+                    carry = __builtin_amdgcn_readlane(incl, 63);
+                }
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        }
+        k = uniform(s_up[Nb]);
+        row_lo = (s == 0) ? 0 : uniform(wave_lower_bound(s_up, Nb, int64_t(s) * k / slices));
+        row_hi = (s == slices - 1)
+                     ? Nb
+                     : uniform(wave_lower_bound(s_up, Nb, int64_t(s + 1) * k / slices));
+        Q0 = uniform(s_up[row_lo]);
+        Q1 = uniform(s_up[row_hi]);
+        if (Q1 < Q0) Q1 = Q0;
+        share([&](int64_t v) { return uniform(wave_lower_bound(s_up, Nb, v)); });
+        head_end = (rlo < rhi) ? uniform(s_up[rlo]) : Pw1;
+        head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
+        row = rlo - 1;
+        p = Pw;
+        end = head_end;
+        if (head_end <= Pw) {
+            for (row = rlo; row < rhi; ++row) {
+                p = uniform(s_up[row]);
+                const int e = uniform(s_up[row + 1]);
+                if (p < e) {
+                    end = e < Pw1 ? e : Pw1;
+                    break;
+                }
+            }
+            if (row >= rhi) p = end = 0;
+        }
+    }
+    const bool has_head = head_end > Pw;
+
+    // Compute cursor: the row of the unit being multiplied and the end of its piece.
+    int r = row;
+    int r_end = end;
+    // Prefetch cursor (unplanned): the row of the next unit to load, its units [pr_u0, pr_u1)
+    // and blocks [pr_b0, pr_b1).
+    int pr = row, pr_u0 = 0, pr_u1 = 0, pr_b0 = 0, pr_b1 = 0;
+    auto read_up_lds = [&](int i) { return uniform(s_up[i]); };
+    auto read_ib_lds = [&](int i) { return uniform(s_ib[i]); };
+    // Loads the operands of unit uu (units past the wave's range fetch nothing).
+    auto fetch = [&](Ops &o, int &nvalid, int uu, auto readU, auto readB) {
+        if constexpr (PL) {
+            Src::load(o, uu, Pw1, ucol, uval);
+            nvalid = KB;
+        } else {
+            int p0 = nnzb, nv = KB;
+            if (uu < Pw1) {
+                while (uu >= pr_u1 && pr < Nb - 1) {
+                    ++pr;
+                    pr_u0 = pr_u1;
+                    pr_u1 = readU(pr + 1);
+                    pr_b0 = readB(pr);
+                    pr_b1 = readB(pr + 1);
+                }
+                p0 = pr_b0 + KB * (uu - pr_u0);
+                p0 = p0 < nnzb ? p0 : nnzb;
+                nv = pr_b1 - p0 < KB ? pr_b1 - p0 : KB;
+            }
+            U::load(o, p0, nnzb, indices, data);
+            nvalid = nv;
+        }
+    };
+    Ops ring[kRing];
+    int nvr[kRing];
+    // Prime the ring with the first kDepth units (issued under the X-tile stores).
+    auto prime = [&](auto readU, auto readB) {
+        if constexpr (!PL) {
+            if (row < rhi) {
+                pr_u0 = readU(row);
+                pr_u1 = readU(row + 1);
+                pr_b0 = readB(row);
+                pr_b1 = readB(row + 1);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < kDepth; ++d) fetch(ring[d], nvr[d], Pw + d, readU, readB);
+    };
+    if (reg_part) {
+        if (Nb < 64)
+            prime([&](int i) { return lane_read(up, i, std::integral_constant<int, 1>{}); },
+                  [&](int i) { return lane_read(ib, i, std::integral_constant<int, 1>{}); });
+        else
+            prime([&](int i) { return lane_read(up, i, std::integral_constant<int, kIpChunks>{}); },
+                  [&](int i) { return lane_read(ib, i, std::integral_constant<int, kIpChunks>{}); });
+    } else {
+        prime(read_up_lds, read_ib_lds);
+    }
+
+    // Row pointers (register path: wave 0) and bias into LDS.  Threads past the arrays write a
+    // spare word at the end of the row-pointer region.
+    int *s_spare = s_up + I.indptr_words - 1;
+    if (reg_part && wave == 0) {
+#pragma unroll
+        for (int j = 0; j < kIpChunks; ++j) {
+            const int i = 64 * j + lane;
+            *(i <= Nb ? s_up + i : s_spare) = up[j];
+            if constexpr (!PL) *(i <= Nb ? s_ib + i : s_spare) = ib[j];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kBiasPer; ++u) {
+        const int i = threadIdx.x + u * kThreads;
+        *(i < Nb * R ? reinterpret_cast<int *>(s_bias) + i : s_spare) = __float_as_int(bv[u]);
+    }
+    for (int i = threadIdx.x + kBiasPer * kThreads; i < Nb * R; i += kThreads)
+        s_bias[i] = bias ? bias[i] : 0.0f;
+
+    if (lane_words >= 64 * kStageChunks)
+        x_store(0, NoClamp{});
+    else
+        x_store(0, Clamp{});
+    for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
+        x_load(c0);
+        x_store(c0, Clamp{});
+    }
+    if constexpr (U::kPad == 1) {   // the fp32 tile's zero pad column
+        if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
+    }
+    if constexpr (U::kTransposed) {   // the transposed tile's zero pad column K
+        if (threadIdx.x < kTT) reinterpret_cast<bf16_t *>(Xs)[K * XP + threadIdx.x] = 0;
+    }
+    __syncthreads();
+
+    char *wslot = reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048;
+    TileOut out;
+    out.ldy4 = int(ldy) * 4;
+    out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(out.ldy4));
+
+    // Empty owned rows: Y = bias.
+    for (int rr = rlo; rr < rhi; ++rr) {
+        if (uniform(s_up[rr + 1]) == uniform(s_up[rr])) {
+            typename U::Acc z;
+            U::init(z, s_bias, rr * R);
+            U::store(z, out, rr * R);
+        }
+    }
+
+    // First row after r with units (rhi if none); returns its start and clipped end.
+    auto next_row = [&](int rr, int &start, int &end_) -> int {
+        for (++rr; rr < rhi; ++rr) {
+            start = uniform(s_up[rr]);
+            const int e = uniform(s_up[rr + 1]);
+            if (start < e) {
+                end_ = e < Pw1 ? e : Pw1;
+                return rr;
+            }
+        }
+        start = end_ = 0;
+        return rhi;
+    };
+
+    // The stream.  Unit u is multiplied in ring slot (u - Pw) mod kRing, after the loads of
+    // unit u + kDepth are issued into the slot freed by unit u - 1.  At the last unit of a row
+    // piece the accumulator goes to Y (a complete row), to `head` (a row another wave finishes)
+    // or stays as the tail (a row continuing past Pw1), and the next row starts at its bias.
+    typename U::Acc acc, head;
+    U::zero(head);
+    int tail_row = -1;
+    if (has_head) U::zero(acc);
+    else if (r < rhi) U::init(acc, s_bias, r * R);
+    else U::zero(acc);
+    // Every phase issues its loads (past the wave's range they fetch nothing) and the loop
+    // exits only at its top, so every path through the loop issues the same loads in the same
+    // order: the compiler then counts kDepth units' loads between a unit's loads and its use
+    // and waits for that unit alone.
+    for (int base = Pw; base < Pw1; base += kRing) {
+#pragma unroll
+        for (int ph = 0; ph < kRing; ++ph) {
+            const int u = base + ph;
+            fetch(ring[(ph + kDepth) % kRing], nvr[(ph + kDepth) % kRing], u + kDepth,
+                  read_up_lds, read_ib_lds);
+            __builtin_amdgcn_sched_barrier(0);
+            if (u >= Pw1) continue;
+            if constexpr (PL) {
+                Src::mma(acc, ring[ph], Xs, XP, Kb, wslot);
+            } else {
+                if (nvr[ph] < KB) U::mask(ring[ph], nvr[ph]);
+                U::mma(acc, ring[ph], Xs, XP, Kb, wslot);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (u + 1 == r_end) {
+                if (r == rlo - 1) {
+                    head = acc;
+                } else if (uniform(s_up[r + 1]) <= Pw1) {
+                    U::store(acc, out, r * R);
+                } else {
+                    tail_row = r;
+                }
+                int np, nend;
+                r = next_row(r, np, nend);
+                r_end = nend;
+                if (r < rhi) U::init(acc, s_bias, r * R);
+            }
+        }
+    }
+
+    // Combine rows cut by wave boundaries, in wave order (as in the tiled kernel): the owner's
+    // partial (bias and its units), then each later wave's head partial.  The X tile is dead
+    // now; its LDS holds the head partials P[w][v][lane], the partials of wide tails
+    // T[w][v][lane] and one word per wave naming its wide tail row.
+    constexpr int kLocalHeads = 2;
+    constexpr int kSlot = U::kRegs * 64;
+    __syncthreads();
+    float *P = reinterpret_cast<float *>(Xs);
+    float *Tw = P + NW * kSlot;
+    int *s_wide = reinterpret_cast<int *>(Tw + NW * kSlot);
+    unsigned tail_heads = 0;
+    if (tail_row >= 0) {
+        const int e = uniform(s_up[tail_row + 1]);
+        tail_heads = unsigned(__ballot(lane > wave && lane < NW && ws < e && wsn != ws));
+    }
+    const bool wide = __popc(tail_heads) > kLocalHeads;
+    if (has_head) {
+#pragma unroll
+        for (int vv = 0; vv < U::kRegs; ++vv) P[(wave * U::kRegs + vv) * 64 + lane] = U::get(head, vv);
+    }
+    if (wide) {
+#pragma unroll
+        for (int vv = 0; vv < U::kRegs; ++vv) Tw[(wave * U::kRegs + vv) * 64 + lane] = U::get(acc, vv);
+    }
+    s_wide[wave] = wide ? tail_row : -1;
+    s_wide[NW + wave] = int(tail_heads);
+    __syncthreads();
+    if (tail_row >= 0 && !wide) {
+        for (unsigned m = tail_heads; m; m &= m - 1) {
+            const int w2 = __ffs(m) - 1;
+            float h[U::kRegs];
+#pragma unroll
+            for (int vv = 0; vv < U::kRegs; ++vv) h[vv] = P[(w2 * U::kRegs + vv) * 64 + lane];
+#pragma unroll
+            for (int vv = 0; vv < U::kRegs; ++vv) U::add(acc, vv, h[vv]);
+        }
+        U::store(acc, out, tail_row * R);
+    }
+    const int wv = lane < NW ? s_wide[lane] : -1;
+    const int whm = lane < NW ? s_wide[NW + lane] : 0;
+    for (unsigned long long m = __ballot(wv >= 0); m; m &= m - 1) {
+        const int w = __ffsll(static_cast<long long>(m)) - 1;
+        const int trow = __builtin_amdgcn_readlane(wv, w);
+        if (wave < U::kRegs) {
+            const unsigned hm = unsigned(__builtin_amdgcn_readlane(whm, w));
+            const int vv = wave;
+            float x = Tw[(w * U::kRegs + vv) * 64 + lane];
+            float h[NW - 1];
+#pragma unroll
+            for (int i = 0; i < NW - 1; ++i) h[i] = P[((i + 1) * U::kRegs + vv) * 64 + lane];
+#pragma unroll
+            for (int i = 0; i < NW - 1; ++i) x += (hm >> (i + 1)) & 1u ? h[i] : -0.0f;
+            U::store_reg(x, out, trow * R, vv);
+        }
+    }
+}
+
+template <int R, bool BF, bool PL>
+bsr_status launch_flat_variant(const TiledBatch &batch, dim3 grid, size_t lds, hipStream_t st,
+                               const LaunchEvents &ev) {
+    launch_kernel(spmm_flat_kernel<R, BF, PL>, grid, dim3(kNW * 64), lds, st, ev, batch);
+    return launch_status();
+}
+
+}  // namespace
+
+bool flat_supported(int R, int C, int dtype) {
+    return (dtype == BSR_F32 || dtype == BSR_BF16) && C == 1 && (R == 32 || R == 16);
+}
+
+bool plan_supported(int R, int C, int dtype) {
+    return (dtype == BSR_F32 || dtype == BSR_BF16) && C == 1 && R == 32;
+}
+
+int flat_unit_blocks(int R, int C, int dtype) {
+    if (!flat_supported(R, C, dtype)) return 0;
+    if (R == 32) return dtype == BSR_BF16 ? Unit<32, 1, true>::KB : Unit<32, 1, false>::KB;
+    return Unit<16, 1, false>::KB;
+}
+
+bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *stream,
+                            const LaunchEvents &ev) {
+    if (n < 1 || n > kMaxItems) return BSR_ERR_ARG;
+    const int R = work[0].W->R, C = work[0].W->C;
+    const bool bf = work[0].W->dtype == BSR_BF16;
+    TiledBatch batch{};
+    batch.n = n;
+    int gx = 0;
+    size_t lds = 0;
+    for (int i = 0; i < n; ++i) {
+        const TiledWork &w = work[i];
+        if (w.W->R != R || w.W->C != C || w.W->dtype != work[0].W->dtype) return BSR_ERR_ARG;
+        if ((w.plan_mem != nullptr) != planned) return BSR_ERR_ARG;
+        TiledItem &it = batch.item[i];
+        it.X = w.X;
+        it.T = w.T;
+        it.ldx = w.ldx;
+        it.indptr = w.W->indptr;
+        it.indices = w.W->indices;
+        it.data = w.W->data;
+        it.bias = w.bias;
+        it.Y = w.Y;
+        it.ldy = w.ldy;
+        it.K = int(w.W->n_cols);
+        it.nnzb = int(w.W->nnzb);
+        it.Nb = int(w.W->n_rows / R);
+        it.Kb = int(w.W->n_cols / C);
+        it.num_tiles = w.plan.num_tiles;
+        it.slices = w.plan.slices;
+        it.XP = w.plan.x_pitch;
+        it.indptr_words = w.plan.indptr_words;
+        it.bias_words = w.plan.bias_words;
+        it.wbuf_offset = w.plan.wbuf_offset;
+        it.ib_offset = w.plan.ib_offset;
+        if (planned) {
+            const char *base = static_cast<const char *>(w.plan_mem);
+            it.uptr = reinterpret_cast<const int32_t *>(base + w.plan_uptr_offset);
+            it.ucol = reinterpret_cast<const int32_t *>(base + w.plan_col_offset);
+            it.uval = base + w.plan_val_offset;
+            it.ucap = int(w.plan_max_units);
+        }
+        const int wgs = ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
+        if (wgs > gx) gx = wgs;
+        if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
+    }
+    hipStream_t st = as_stream(stream);
+    const dim3 grid(gx, n);
+    if (R == 32) {
+        if (bf) return planned ? launch_flat_variant<32, true, true>(batch, grid, lds, st, ev)
+                               : launch_flat_variant<32, true, false>(batch, grid, lds, st, ev);
+        return planned ? launch_flat_variant<32, false, true>(batch, grid, lds, st, ev)
+                       : launch_flat_variant<32, false, false>(batch, grid, lds, st, ev);
+    }
+    if (planned) return BSR_ERR_UNSUPPORTED;
+    if (bf) return launch_flat_variant<16, true, false>(batch, grid, lds, st, ev);
+    return launch_flat_variant<16, false, false>(batch, grid, lds, st, ev);
+}
+
+}  // namespace bsr

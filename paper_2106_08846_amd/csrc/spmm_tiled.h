@@ -16,6 +16,7 @@ struct TiledPlan {
     int indptr_words = 0;   // LDS words reserved for indptr
     int bias_words = 0;     // LDS words reserved for the bias
     int wbuf_offset = 0;    // bytes from the X tile to the per-wave block scratch (if any)
+    int ib_offset = 0;      // R x 1 kernels: LDS words from the unit row pointer to indptr
     size_t lds_bytes = 0;   // dynamic LDS per workgroup
 };
 
@@ -51,7 +52,8 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
 // Most products one tiled launch takes (all with the same block shape and dtype).
 constexpr int kMaxItems = 8;
 
-// One product of a tiled launch, as planned on the host.
+// One product of a tiled launch, as planned on the host (plan_mem and the offsets: the
+// product's per-matrix plan, or NULL).
 struct TiledWork {
     TiledPlan plan;
     const void *X;
@@ -60,6 +62,8 @@ struct TiledWork {
     const float *bias;
     float *Y;
     int64_t ldy;
+    const void *plan_mem = nullptr;
+    int64_t plan_uptr_offset = 0, plan_col_offset = 0, plan_val_offset = 0, plan_max_units = 0;
 };
 
 // The device-side view of one product, passed by value in the kernel arguments.
@@ -74,6 +78,12 @@ struct TiledItem {
     int64_t ldy;
     int K, nnzb, Nb, Kb;
     int num_tiles, slices, XP, indptr_words, bias_words, wbuf_offset;
+    // R x 1 kernels: LDS words from the unit row pointer to indptr; with a plan, its unit row
+    // pointer, packed columns and weights, and its reserved units.
+    int ib_offset, ucap;
+    const int32_t *uptr;
+    const int32_t *ucol;
+    const void *uval;
 };
 
 struct TiledBatch {
@@ -88,6 +98,25 @@ bool wide_units(const TiledWork *work, int n);
 
 // Launch 1..kMaxItems planned products of one block shape as a single kernel.
 bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream, const LaunchEvents &ev);
+
+// The flat-stream kernel for linear R x 1 blocks (32x1, 16x1): same plan and batch structures
+// as the tiled kernel; `planned` launches read per-matrix plans (32x1 only), and every product
+// of one launch has a plan or none has.
+bool flat_supported(int R, int C, int dtype);
+bool plan_supported(int R, int C, int dtype);
+int flat_unit_blocks(int R, int C, int dtype);   // blocks per unit (0 if unsupported)
+bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *stream,
+                            const LaunchEvents &ev);
+
+// Per-matrix plans: layout and the preparing kernels (plan.hip).
+struct PlanLayout {
+    int unit_blocks = 0;
+    int64_t max_units = 0;
+    int64_t uptr_offset = 0, col_offset = 0, val_offset = 0, total = 0;
+};
+PlanLayout plan_layout(const bsr_matrix_t *W);   // unit_blocks = 0 when unsupported
+bsr_status launch_plan_prepare(const bsr_matrix_t *W, void *mem, const PlanLayout &L,
+                               void *stream);
 
 // The column-chunked matrix-core kernel, for inputs too wide for one LDS X tile: same units
 // and shapes as the tiled kernel; the plan also fills chunk_blocks and nchunks.

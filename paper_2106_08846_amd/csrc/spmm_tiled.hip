@@ -559,7 +559,9 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     const bool tile_bf16 = bf && (C > 1 || transposed);   // Unit<R, C, BF>::kTileBF16
     const int regs = (R == 32) ? 16 : 8;
     const int NW = tiled_waves(R, C);
-    p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3)) + 4;   // + a spare word, 16-byte multiple
+    // Row pointers: indptr (square blocks); the unit row pointer and indptr (R x 1 blocks).
+    p.ib_offset = C == 1 ? int((Nb + 1 + 3) & ~int64_t(3)) : 0;
+    p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3)) + p.ib_offset + 4;   // + a spare word
     p.bias_words = int((W->n_rows + 3) & ~int64_t(3));
     size_t tile_bytes;
     if (transposed) {
@@ -626,6 +628,7 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
         it.indptr_words = w.plan.indptr_words;
         it.bias_words = w.plan.bias_words;
         it.wbuf_offset = w.plan.wbuf_offset;
+        it.ib_offset = w.plan.ib_offset;
         const int wgs = ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
         if (wgs > gx) gx = wgs;
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
@@ -636,14 +639,11 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream,
             return launch_variant<16, 16, 16, true, 4>(batch, dim3(gx, n), lds, st, ev);
         return launch_variant<16, 16, 16, false, 4>(batch, dim3(gx, n), lds, st, ev);
     }
+    // Linear R x 1 blocks run on the flat-stream kernel (spmm_flat.hip).
     if (work[0].W->dtype == BSR_BF16) {
-        if (R == 32 && C == 1) return launch_variant<32, 1, 16, true>(batch, dim3(gx, n), lds, st, ev);
-        if (R == 16 && C == 1) return launch_variant<16, 1, 16, true>(batch, dim3(gx, n), lds, st, ev);
         if (R == 32 && C == 32) return launch_variant<32, 32, 16, true>(batch, dim3(gx, n), lds, st, ev);
         if (R == 16 && C == 16) return launch_variant<16, 16, 16, true>(batch, dim3(gx, n), lds, st, ev);
     } else {
-        if (R == 32 && C == 1) return launch_variant<32, 1, 16, false>(batch, dim3(gx, n), lds, st, ev);
-        if (R == 16 && C == 1) return launch_variant<16, 1, 16, false>(batch, dim3(gx, n), lds, st, ev);
         if (R == 32 && C == 32) return launch_variant<32, 32, 16, false>(batch, dim3(gx, n), lds, st, ev);
         if (R == 16 && C == 16) return launch_variant<16, 16, 16, false>(batch, dim3(gx, n), lds, st, ev);
     }

@@ -107,33 +107,35 @@ struct LinearUnit {
     };
     __device__ static int offset_in_step() { return (threadIdx.x & 63) / R; }
     __device__ static int feature() { return (threadIdx.x & 63) % R; }
-    // Loads every lane's operands for the unit at p through raw buffer loads based at the
-    // unit: one code path for every unit, no per-lane address arithmetic, and lanes past the
-    // end of the arrays (nnzb blocks) read 0.  Lanes past the unit's row segment read the next
-    // row's blocks; mask() zeroes them before the MFMAs.
+    // Loads every lane's operands for the unit at p through raw buffer loads over the whole
+    // arrays (nnzb blocks): every offset, the unit's included, is in the range-checked vector
+    // offset (constant parts go to the instruction's offset field), so lanes past the end of the
+    // arrays read 0 and touch no memory.  The descriptors do not depend on p, so a loop over
+    // units builds them once.  Lanes past the unit's row segment read the next row's blocks;
+    // mask() zeroes them before the MFMAs.
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int o = offset_in_step(), f = feature();
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices, unsigned(nnzb) * 4u);
+        const int vi = (p + o) * 4;
         if constexpr (BF) {
-            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
-                static_cast<const bf16_t *>(data) + int64_t(p) * R, left * (R * 2u));
+            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data, unsigned(nnzb) * (R * 2u));
+            const int vd = ((p + o) * R + f) * 2;
 #pragma unroll
             for (int m = 0; m < kSteps; ++m) {
-                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
+                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, vi + m * kPer * 4, 0, 0);
                 ops.b[m] = __uint_as_float(unsigned(__builtin_amdgcn_raw_buffer_load_b16(
-                                               rd, (o * R + f) * 2, m * kPer * R * 2, 0))
+                                               rd, vd + m * kPer * R * 2, 0, 0))
                                            << 16);
             }
         } else {
-            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
-                static_cast<const float *>(data) + int64_t(p) * R, left * (R * 4u));
+            const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data, unsigned(nnzb) * (R * 4u));
+            const int vd = ((p + o) * R + f) * 4;
 #pragma unroll
             for (int m = 0; m < kSteps; ++m) {
-                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, o * 4, m * kPer * 4, 0);
+                ops.j[m] = __builtin_amdgcn_raw_buffer_load_b32(ri, vi + m * kPer * 4, 0, 0);
                 ops.b[m] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                         rd, (o * R + f) * 4, m * kPer * R * 4, 0));
+                                                         rd, vd + m * kPer * R * 4, 0, 0));
             }
         }
     }
@@ -264,84 +266,77 @@ __device__ __forceinline__ shortx4 lds_read_tr16(const char *p) {
 }
 
 // 32x1 bf16 blocks on v_mfma_f32_32x32x16_bf16: the contraction index is the block, 16 blocks
-// per instruction, two instructions per unit.  Lane l supplies k-slots 8(l/32) .. +7 for token
-// l%32 (A) and feature l%32 (B); both operands are assembled by transpose reads, four chunks
-// (c = 0..3) per read:
+// per instruction, one instruction per unit.  Lane l supplies k-slots 8(l/32) .. +7 for token
+// l%32 (A) and feature l%32 (B), i.e. blocks 8(l/32) + e, e = 0..7, of the unit; both operands
+// are assembled by transpose reads, four chunks (c = 0..3) per read:
 //   * A from the transposed X tile (each column holds the 32 tokens contiguously, 2 bytes each,
 //     column pitch XP bf16): lane 4c + q of group g addresses tokens 16(g%2) + 4q .. +3 of
-//     column indices[16m + 8(g/2) + 4s + c] for read s of instruction m;
+//     column indices[8(g/2) + 4s + c] for read s = 0, 1;
 //   * B from a per-wave LDS copy of the unit's blocks ([block][32 features]): the same lane
-//     addresses features 16(g%2) + 4q .. +3 of block 16m + 8(g/2) + 4s + c.
+//     addresses features 16(g%2) + 4q .. +3 of block 8(g/2) + 4s + c.
 // Blocks past the segment end read the tile's zero pad column (A) and zero weights (B).
 template <>
 struct Unit<32, 1, true> {
-    static constexpr int KB = 32;
+    static constexpr int KB = 16;
     static constexpr int kPad = 0;
     static constexpr bool kTileBF16 = true;
     static constexpr bool kTransposed = true;
     static constexpr int kRegs = 16;
-    static constexpr int kSlotBytes = 2048;  // LDS per wave for the unit's blocks
+    static constexpr int kSlotBytes = 1024;  // LDS per wave for the unit's blocks
     using Acc = floatx16;
     struct Ops {
-        int j[4];     // index for read (m, s) = 2m + s
-        uintx4 w[2];  // instruction m: block 16m + l/4, features 8(l%4) .. +7
+        int j[2];   // index for read s
+        uintx4 w;   // block l/4, features 8(l%4) .. +7
     };
     __device__ static void zero(Acc &acc) { Unit<32, 1, false>::zero(acc); }
     __device__ static void init(Acc &acc, const float *s_bias, int n0) {
         Unit<32, 1, false>::init(acc, s_bias, n0);
     }
-    __device__ static int read_block(int r) {   // block of read r within the unit, this lane
+    __device__ static int read_block(int s) {   // block of read s within the unit, this lane
         const int l = threadIdx.x & 63;
-        return 16 * (r >> 1) + 8 * (l >> 5) + 4 * (r & 1) + ((l & 15) >> 2);
+        return 8 * (l >> 5) + 4 * s + ((l & 15) >> 2);
     }
+    // Offsets in the range-checked vector offset, descriptors over the whole arrays (as for
+    // the fp32 linear units).
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int l = threadIdx.x & 63;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 32, left * 64u);
-        const int io = (8 * (l >> 5) + ((l & 15) >> 2)) * 4;
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices, unsigned(nnzb) * 4u);
+        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data, unsigned(nnzb) * 64u);
+        const int io = (p + 8 * (l >> 5) + ((l & 15) >> 2)) * 4;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-            ops.j[r] = __builtin_amdgcn_raw_buffer_load_b32(ri, io, (16 * (r >> 1) + 4 * (r & 1)) * 4, 0);
-#pragma unroll
-        for (int m = 0; m < 2; ++m) ops.w[m] = __builtin_amdgcn_raw_buffer_load_b128(rd, l * 16, m * 1024, 0);
+        for (int r = 0; r < 2; ++r)
+            ops.j[r] = __builtin_amdgcn_raw_buffer_load_b32(ri, io + 16 * r, 0, 0);
+        ops.w = __builtin_amdgcn_raw_buffer_load_b128(rd, p * 64 + l * 16, 0, 0);
     }
     __device__ static void mask(Ops &ops, int nvalid) {
         const int l = threadIdx.x & 63;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) ops.j[r] = read_block(r) < nvalid ? ops.j[r] : -1;
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-            const bool in = 16 * m + (l >> 2) < nvalid;
-            ops.w[m] = in ? ops.w[m] : uintx4{0u, 0u, 0u, 0u};
-        }
+        for (int r = 0; r < 2; ++r) ops.j[r] = read_block(r) < nvalid ? ops.j[r] : -1;
+        ops.w = (l >> 2) < nvalid ? ops.w : uintx4{0u, 0u, 0u, 0u};
+    }
+    // A from the transposed tile for the two reads of the unit (cols j0, j1 already clamped).
+    __device__ static shortx8 gather(const void *Xs, int XP, int j0, int j1) {
+        const int l = threadIdx.x & 63, g = l >> 4, q = l & 3;
+        const char *xt = static_cast<const char *>(Xs);
+        const int tok = (16 * (g & 1) + 4 * q) * 2;   // byte offset within a column
+        const shortx4 a0 = lds_read_tr16(xt + j0 * (2 * XP) + tok);
+        const shortx4 a1 = lds_read_tr16(xt + j1 * (2 * XP) + tok);
+        return __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                char *wslot) {
         const int l = threadIdx.x & 63, g = l >> 4, c = (l & 15) >> 2, q = l & 3;
         uintx4 *ws = reinterpret_cast<uintx4 *>(wslot);
-        ws[l] = ops.w[0];
-        ws[64 + l] = ops.w[1];
-        const char *xt = static_cast<const char *>(Xs);
-        const int tok = (16 * (g & 1) + 4 * q) * 2;            // byte offset within a column
+        ws[l] = ops.w;
+        const int tok = (16 * (g & 1) + 4 * q) * 2;
         const int boff = (8 * (g >> 1) + c) * 64 + tok;        // byte offset within the slot
-        shortx4 a[4], b[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            a[r] = lds_read_tr16(xt + clamp_col(ops.j[r], Kb + 1) * (2 * XP) + tok);
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-            b[r] = lds_read_tr16(wslot + (r >> 1) * 1024 + (r & 1) * 256 + boff);
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-            const shortx8 av = __builtin_shufflevector(a[2 * m], a[2 * m + 1], 0, 1, 2, 3, 4, 5, 6, 7);
-            const shortx8 bv = __builtin_shufflevector(b[2 * m], b[2 * m + 1], 0, 1, 2, 3, 4, 5, 6, 7);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
-                                                         __builtin_bit_cast(bf16x8, bv), acc,
-                                                         0, 0, 0);
-        }
+        const shortx8 av = gather(Xs, XP, clamp_col(ops.j[0], Kb + 1), clamp_col(ops.j[1], Kb + 1));
+        const shortx4 b0 = lds_read_tr16(wslot + boff);
+        const shortx4 b1 = lds_read_tr16(wslot + 256 + boff);
+        const shortx8 bv = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
+                                                     __builtin_bit_cast(bf16x8, bv), acc, 0, 0, 0);
     }
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         Unit<32, 1, false>::store(acc, o, n0);
@@ -351,6 +346,93 @@ struct Unit<32, 1, true> {
     }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
+};
+
+// ------------------------------------------------------------------------- planned units
+// A plan (prepared once per matrix) stores, for every unit of KB blocks of one block-row (the
+// last unit of a row padded with zero blocks whose column is the tile's zero pad column), its
+// block columns and its weights already in the lane order of the unit's MFMAs, so that a
+// unit's operands arrive in two 16-byte loads per lane (one for the columns, one for the
+// weights) and no operand is masked or re-arranged at run time.  The sums are those of the
+// unplanned unit of the same shape: the same blocks in the same k-slots of the same
+// instructions.  Loads of a unit at or past `ulim` fetch nothing and return 0 (the unit's
+// offset is in the range-checked vector offset).
+template <int R, int C, bool BF>
+struct PlanUnit;
+
+// fp32 32x1: unit = 8 blocks, four v_mfma_f32_32x32x2_f32 steps; step m of half h = l/32 takes
+// block 2m + h.  Columns: cols[u][h][m] as byte offsets into a row of the X tile, 4 * col with
+// col clamped to [0, Kb] (Kb: the tile's zero pad column), so a gather is one add (32 bytes per
+// unit); weights: vals[u][l][m] = block (2m + l/32), feature l%32 (1 KB per unit).  The unit's
+// offset goes in the scalar offset of the loads (range-checked like the vector offset), so a
+// unit's loads need no per-lane arithmetic.
+template <>
+struct PlanUnit<32, 1, false> {
+    using Base = Unit<32, 1, false>;
+    static constexpr int KB = 8;
+    static constexpr int kColBytes = 32;
+    static constexpr int kValBytes = 1024;
+    static constexpr int kColScale = 4;   // bytes per column in a row of the X tile
+    struct Ops {
+        uintx4 j;
+        floatx4 b;
+    };
+    __device__ static void load(Ops &ops, int u, int ulim, const int32_t *__restrict__ cols,
+                                const void *__restrict__ vals) {
+        const int l = threadIdx.x & 63;
+        const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(cols, unsigned(ulim) * kColBytes);
+        const __amdgpu_buffer_rsrc_t rv = buffer_rsrc(vals, unsigned(ulim) * kValBytes);
+        ops.j = __builtin_amdgcn_raw_buffer_load_b128(rc, (l >> 5) * 16, u * kColBytes, 0);
+        ops.b = __builtin_bit_cast(
+            floatx4, __builtin_amdgcn_raw_buffer_load_b128(rv, l * 16, u * kValBytes, 0));
+    }
+    __device__ static void mma(typename Base::Acc &acc, const Ops &ops, const void *Xs, int XP,
+                               int Kb, char *) {
+        const char *xrow = static_cast<const char *>(Xs) + (threadIdx.x & 31) * XP * 4;
+        float a[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) a[m] = *reinterpret_cast<const float *>(xrow + ops.j[m]);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) acc = mfma32(a[m], ops.b[m], acc);
+    }
+};
+
+// bf16 32x1: unit = 16 blocks, one v_mfma_f32_32x32x16_bf16.  Columns: cols[u][h][c][s] =
+// block 8h + 4s + c as byte offsets of its column in the transposed X tile (column pitch 72
+// bytes: kColScale * col, col clamped to [0, Kb]); lane l reads the pair of (h, c) = (l/32,
+// (l%16)/4) (64 bytes per unit).  Weights: vals[u][l][e] = block 8(l/32) + e, feature l%32, as
+// bf16 (16 bytes per lane, 1 KB per unit) -- exactly the B operand, so no LDS round trip.
+template <>
+struct PlanUnit<32, 1, true> {
+    using Base = Unit<32, 1, true>;
+    static constexpr int KB = 16;
+    static constexpr int kColBytes = 64;
+    static constexpr int kValBytes = 1024;
+    static constexpr int kColScale = 72;  // bytes per column of the transposed tile (pitch 36)
+    struct Ops {
+        uintx2 j;
+        uintx4 b;
+    };
+    __device__ static void load(Ops &ops, int u, int ulim, const int32_t *__restrict__ cols,
+                                const void *__restrict__ vals) {
+        const int l = threadIdx.x & 63;
+        const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(cols, unsigned(ulim) * kColBytes);
+        const __amdgpu_buffer_rsrc_t rv = buffer_rsrc(vals, unsigned(ulim) * kValBytes);
+        ops.j = __builtin_amdgcn_raw_buffer_load_b64(rc, ((l >> 5) * 4 + ((l & 15) >> 2)) * 8,
+                                                     u * kColBytes, 0);
+        ops.b = __builtin_amdgcn_raw_buffer_load_b128(rv, l * 16, u * kValBytes, 0);
+    }
+    __device__ static void mma(typename Base::Acc &acc, const Ops &ops, const void *Xs, int XP,
+                               int Kb, char *) {
+        const int l = threadIdx.x & 63, g = l >> 4, q = l & 3;
+        const char *xt = static_cast<const char *>(Xs) + (16 * (g & 1) + 4 * q) * 2;
+        const shortx4 a0 = lds_read_tr16(xt + ops.j[0]);
+        const shortx4 a1 = lds_read_tr16(xt + ops.j[1]);
+        const shortx8 av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
+                                                     __builtin_bit_cast(bf16x8, ops.b), acc, 0,
+                                                     0, 0);
+    }
 };
 
 // Accumulator, bias and store plumbing shared by the square units (the output layouts of the
@@ -383,15 +465,14 @@ struct Unit<32, 32, false> {
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const float *>(data) + int64_t(p) * 1024, left * 4096u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices, unsigned(nnzb) * 4u);
+        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data, unsigned(nnzb) * 4096u);
+        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, p * 4, 0, 0));
+        const int vd = p * 4096 + (tl * 8 + kh) * 16;
 #pragma unroll
         for (int u = 0; u < 4; ++u)
             ops.d[u] = __builtin_bit_cast(
-                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rd, (tl * 8 + kh) * 16, 32 * u, 0));
+                floatx4, __builtin_amdgcn_raw_buffer_load_b128(rd, vd + 32 * u, 0, 0));
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                     char *) {
@@ -440,14 +521,13 @@ struct Unit<32, 32, true> {
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd =
-            buffer_rsrc(static_cast<const bf16_t *>(data) + int64_t(p) * 1024, left * 2048u);
-        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices, unsigned(nnzb) * 4u);
+        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data, unsigned(nnzb) * 2048u);
+        ops.j = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, p * 4, 0, 0));
+        const int vd = p * 2048 + (tl * 4 + kh) * 16;
 #pragma unroll
         for (int u = 0; u < 2; ++u)
-            ops.d[u] = __builtin_amdgcn_raw_buffer_load_b128(rd, (tl * 4 + kh) * 16, 32 * u, 0);
+            ops.d[u] = __builtin_amdgcn_raw_buffer_load_b128(rd, vd + 32 * u, 0, 0);
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
                                     char *) {
@@ -510,26 +590,24 @@ struct Unit1616 {
     __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
                                 const void *__restrict__ data) {
         const int lane = threadIdx.x & 63;
-        const unsigned left = unsigned(nnzb - p);
-        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices + p, left * 4u);
-        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(
-            static_cast<const char *>(data) + int64_t(p) * kBlockBytes, left * unsigned(kBlockBytes));
+        const __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices, unsigned(nnzb) * 4u);
+        const __amdgpu_buffer_rsrc_t rd = buffer_rsrc(data, unsigned(nnzb) * unsigned(kBlockBytes));
         if constexpr (KB == 1) {
-            ops.j[0] = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, 0, 0, 0));
+            ops.j[0] = uniform(__builtin_amdgcn_raw_buffer_load_b32(ri, p * 4, 0, 0));
         } else {
             static_assert(KB == 4, "one 16-byte load of the unit's indices");
-            const uintx4 jj = __builtin_amdgcn_raw_buffer_load_b128(ri, 0, 0, 0);
+            const uintx4 jj = __builtin_amdgcn_raw_buffer_load_b128(ri, p * 4, 0, 0);
 #pragma unroll
             for (int u = 0; u < KB; ++u) ops.j[u] = uniform(int(jj[u]));
         }
-        const int off = ((lane & 15) * 4 + (lane >> 4)) * (BF ? 8 : 16);
+        const int off = p * kBlockBytes + ((lane & 15) * 4 + (lane >> 4)) * (BF ? 8 : 16);
 #pragma unroll
         for (int u = 0; u < KB; ++u) {
             if constexpr (BF)
-                ops.d[u] = __builtin_amdgcn_raw_buffer_load_b64(rd, off, kBlockBytes * u, 0);
+                ops.d[u] = __builtin_amdgcn_raw_buffer_load_b64(rd, off + kBlockBytes * u, 0, 0);
             else
                 ops.d[u] = __builtin_bit_cast(
-                    floatx4, __builtin_amdgcn_raw_buffer_load_b128(rd, off, kBlockBytes * u, 0));
+                    floatx4, __builtin_amdgcn_raw_buffer_load_b128(rd, off + kBlockBytes * u, 0, 0));
         }
     }
     __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,

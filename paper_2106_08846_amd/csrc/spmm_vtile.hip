@@ -70,14 +70,15 @@ struct VOps {
 };
 
 // Loads the chunk that starts `o` blocks into the row (the row's arrays are the buffer ranges
-// ri / rd, so a chunk past the row end reads 0 and touches no memory).
+// ri / rd and every offset is in the range-checked vector offset, so a chunk past the row end
+// reads 0 and touches no memory).
 template <int R, int C, bool BF>
 __device__ __forceinline__ void vload(VOps<R, C> &ops, __amdgpu_buffer_rsrc_t ri,
                                       __amdgpu_buffer_rsrc_t rd, int o) {
     using S = VShape<R, C>;
     if constexpr (S::U == 8) {
         const uintx4 a = __builtin_amdgcn_raw_buffer_load_b128(ri, o * 4, 0, 0);
-        const uintx4 b = __builtin_amdgcn_raw_buffer_load_b128(ri, o * 4, 16, 0);
+        const uintx4 b = __builtin_amdgcn_raw_buffer_load_b128(ri, o * 4 + 16, 0, 0);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             ops.j[u] = int(a[u]);
@@ -98,7 +99,7 @@ __device__ __forceinline__ void vload(VOps<R, C> &ops, __amdgpu_buffer_rsrc_t ri
         // 8 bf16 weights per 16-byte load, widened exactly to fp32.
 #pragma unroll
         for (int q = 0; q < S::NWORDS / 8; ++q) {
-            const uintx4 v = __builtin_amdgcn_raw_buffer_load_b128(rd, o * (S::RC * 2), 16 * q, 0);
+            const uintx4 v = __builtin_amdgcn_raw_buffer_load_b128(rd, o * (S::RC * 2) + 16 * q, 0, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 ops.w[8 * q + 2 * e] = __uint_as_float(v[e] << 16);
@@ -108,7 +109,7 @@ __device__ __forceinline__ void vload(VOps<R, C> &ops, __amdgpu_buffer_rsrc_t ri
     } else {
 #pragma unroll
         for (int q = 0; q < S::NWORDS / 4; ++q) {
-            const uintx4 v = __builtin_amdgcn_raw_buffer_load_b128(rd, o * (S::RC * 4), 16 * q, 0);
+            const uintx4 v = __builtin_amdgcn_raw_buffer_load_b128(rd, o * (S::RC * 4) + 16 * q, 0, 0);
 #pragma unroll
             for (int e = 0; e < 4; ++e) ops.w[4 * q + e] = __uint_as_float(v[e]);
         }

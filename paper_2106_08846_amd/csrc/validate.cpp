@@ -155,6 +155,35 @@ bsr_status check_spmm_items(const bsr_spmm_item_t *items, int32_t n) {
     return BSR_OK;
 }
 
+bsr_status check_plan_use(const bsr_spmm_item_t &it, const bsr_plan_t *plan,
+                          int64_t layout_bytes) {
+    // The plan must describe this product's matrix (the same arrays and shape) and fit its
+    // recorded layout; its memory must not overlap the product's output.
+    const bsr_matrix_t *W = it.W;
+    if (!plan->mem) return BSR_ERR_NULL;
+    if (plan->n_rows != W->n_rows || plan->n_cols != W->n_cols || plan->nnzb != W->nnzb ||
+        plan->R != W->R || plan->C != W->C || plan->dtype != int(W->dtype) ||
+        plan->indptr != W->indptr || plan->indices != W->indices || plan->data != W->data)
+        return BSR_ERR_ARG;
+    if (layout_bytes <= 0 || int64_t(plan->bytes) < layout_bytes) return BSR_ERR_ARG;
+    if (it.T > 0 && overlaps(it.Y, ((it.T - 1) * it.ldy + W->n_rows) * 4, plan->mem,
+                             int64_t(plan->bytes)))
+        return BSR_ERR_ARG;
+    return BSR_OK;
+}
+
+bsr_status check_plan_prepare(const bsr_matrix_t *W, const void *mem, size_t bytes,
+                              int64_t layout_bytes) {
+    // mem must hold the layout and not overlap the matrix it reads.
+    if (!mem) return BSR_ERR_NULL;
+    if (int64_t(bytes) < layout_bytes) return BSR_ERR_WORKSPACE;
+    if (overlaps(mem, layout_bytes, W->indptr, indptr_bytes(W)) ||
+        overlaps(mem, layout_bytes, W->indices, W->nnzb * 4) ||
+        overlaps(mem, layout_bytes, W->data, data_bytes(W)))
+        return BSR_ERR_ARG;
+    return BSR_OK;
+}
+
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo) {
     if (!W || !out) return BSR_ERR_NULL;
     bsr_status s = check_matrix(W);

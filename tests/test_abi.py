@@ -389,3 +389,38 @@ def test_prune_noalloc_validation(lib):
     assert call(N=1024, K=1025, R=1, C=1, k=10, cap=10, W=None) == 1   # other errors first
     assert call(N=1024, K=1024, R=1, C=1, k=10, cap=10) not in (1, 2, 3, 5, 6)  # fits: past checks
     assert big == 1024 * 1024
+
+
+def test_plan_validation(L, lib):
+    """Plan sizes and preparation are checked on the host before any device work."""
+    n = ctypes.c_size_t(0)
+    assert lib.bsr_plan_bytes(None, ctypes.byref(n)) == 1
+    m = _matrix(L, N=768, K=768, R=32, C=1, nnzb=100)
+    assert lib.bsr_plan_bytes(ctypes.byref(m), ctypes.byref(n)) == 0
+    units = -(-100 // 8) + 24                       # ceil(nnzb / 8) + block-rows
+    assert n.value >= 25 * 4 + units * (32 + 1024)
+    mb = _matrix(L, N=768, K=768, R=32, C=1, nnzb=100, dtype=1)
+    nb16 = ctypes.c_size_t(0)
+    assert lib.bsr_plan_bytes(ctypes.byref(mb), ctypes.byref(nb16)) == 0
+    assert nb16.value >= 25 * 4 + (-(-100 // 16) + 24) * (64 + 1024)
+    sq = _matrix(L, N=64, K=64, R=16, C=16, nnzb=4)
+    assert lib.bsr_plan_bytes(ctypes.byref(sq), ctypes.byref(n)) == 9   # no plan for 16x16
+    assert lib.bsr_plan_bytes(ctypes.byref(_matrix(L, R=7)), ctypes.byref(n)) == 2
+    plan = L.bsr_plan_t()
+    need = lib.bsr_plan_bytes(ctypes.byref(m), ctypes.byref(n)) or n.value
+    assert lib.bsr_plan_prepare(ctypes.byref(m), None, need, ctypes.byref(plan), None) == 1
+    assert lib.bsr_plan_prepare(ctypes.byref(m), 0x900000, need, None, None) == 1
+    assert lib.bsr_plan_prepare(ctypes.byref(m), 0x900000, need - 1, ctypes.byref(plan),
+                                None) == 6
+    # plan memory overlapping the matrix's data (FAKE is its base)
+    assert lib.bsr_plan_prepare(ctypes.byref(m), FAKE - 64, need, ctypes.byref(plan), None) == 3
+    # a planned call whose plan describes another matrix, or NULL memory
+    other = _matrix(L, N=768, K=768, R=32, C=1, nnzb=100, indices=FAKE + 8)
+    plan2 = L.bsr_plan_t(0x900000, need, 768, 768, 100, 32, 1, 0, FAKE, FAKE, FAKE, 8, units,
+                         0, 256, 256 + 256 * ((units * 32 + 255) // 256))
+    arr = (ctypes.POINTER(L.bsr_plan_t) * 1)(ctypes.pointer(plan2))
+    it = _item(L, other, ldx=768, ldy=768)
+    assert lib.bsr_spmm_batched_planned(ctypes.byref(it), arr, 1, None, None) == 3
+    plan2.mem = None
+    it = _item(L, m, ldx=768, ldy=768)
+    assert lib.bsr_spmm_batched_planned(ctypes.byref(it), arr, 1, None, None) == 1
