@@ -12,8 +12,11 @@ by bsr_prune_from_dense, and resident in device memory when timing starts.
 Timing: --warmup untimed steps, then exactly --steps steps between two synchronisations, with an
 event between consecutive steps, so that the JSON line carries the mean step time (the value)
 and the median, p10 and p90 of the per-step times (at least 50 samples; more steps are sampled
-after the timed region when --steps is smaller).  The roofline position comes from HIP events
-that the library records at each product kernel's own start and end (hipExtLaunchKernel).
+after the timed region when --steps is smaller).  The roofline position divides the
+algorithmic bytes or flops of one launch by the timed region's time per launch (the step time
+over the launches of a step, launch gaps included, so an upper bound of the kernel's own time);
+the durations that HIP events recorded at each product kernel's own start and end
+(hipExtLaunchKernel) are reported beside it.
 
 Beside the headline, unless --no-rows, the same line carries the block-shape rows of the other
 configurations, each timed per launch with those kernel events and reported as median, p10, p90:
@@ -80,7 +83,36 @@ def parse(argv=None):
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB --steps times (the reference "
                          "kernel for scaling HBM byte counters) and exit")
+    ap.add_argument("--roof-probe", action="store_true",
+                    help="only time plain device stores, copies and reads (torch kernels) of "
+                         "the product outputs' sizes and of 256 MiB, as the HBM rates a simple "
+                         "kernel reaches here, and exit")
+    ap.add_argument("--trace-summary", metavar="CSV",
+                    help="only summarise a rocprofv3 kernel trace (kernel_trace.csv) per kernel "
+                         "and launch grid, and exit (no GPU needed)")
     return ap.parse_args(argv)
+
+
+def trace_summary(path: str) -> int:
+    """Per (kernel, grid, workgroup, LDS) group of a rocprofv3 kernel trace: dispatches and the
+    mean, median, p10 and p90 duration in microseconds, largest total time first.  Separates
+    the launches of one kernel that differ in grid, such as the headline products (8 per
+    launch: grid y = 8) and single-product rows (grid y = 1)."""
+    import csv
+    groups = {}
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            key = (r["Kernel_Name"], r["Grid_Size_X"], r["Grid_Size_Y"], r["Workgroup_Size_X"],
+                   r["LDS_Block_Size"])
+            us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0
+            groups.setdefault(key, []).append(us)
+    print("| dispatches | mean us | median us | p10 us | p90 us | grid | workgroup | LDS | kernel |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for key, v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        q = pct(v)
+        print(f"| {q['n']} | {q['mean']:.2f} | {q['median']:.2f} | {q['p10']:.2f} | "
+              f"{q['p90']:.2f} | {key[1]} x {key[2]} | {key[3]} | {key[4]} | {key[0]} |")
+    return 0
 
 
 def build_workload(spec: str):
@@ -150,6 +182,47 @@ def pct(samples) -> dict:
     a = np.asarray(samples, dtype=np.float64)
     return {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
             "p90": float(np.percentile(a, 90)), "mean": float(a.mean()), "n": int(a.size)}
+
+
+def roof_probe(args) -> int:
+    """HBM rates of plain torch kernels: a store (fill) of the fused-QKV output (4096 x 2304
+    fp32, 37.7 MB) and of the BERT-large output of one launch (8 x 6144 x 1024 fp32), and a
+    store, a copy and a read (sum) of 256 MiB; median of 20 event-timed runs after 3 warm-up
+    runs each.  The floor a product kernel's own stores and reads can reach on this GPU."""
+    import torch
+    dev = "cuda:0"
+    res = {}
+
+    def time_us(fn, reps=20):
+        for _ in range(3):
+            fn()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return pct([a.elapsed_time(b) * 1e3 for a, b in ev])
+
+    for name, n in (("store_fused_qkv_output", 4096 * 2304),
+                    ("store_bert_large_launch_output", 8 * 6144 * 1024),
+                    ("store_256MiB", (256 << 20) // 4)):
+        t = torch.empty(n, dtype=torch.float32, device=dev)
+        q = time_us(lambda: t.fill_(1.0))
+        res[name] = {"bytes": 4 * n, "us_median": q["median"], "us_p10": q["p10"],
+                     "us_p90": q["p90"], "tbs": 4 * n / q["median"] / 1e6}
+        del t
+    n = (256 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    q = time_us(lambda: dst.copy_(src))
+    res["copy_256MiB"] = {"bytes": 8 * n, "us_median": q["median"], "tbs": 8 * n / q["median"] / 1e6}
+    acc = torch.empty((), dtype=torch.float32, device=dev)
+    q = time_us(lambda: torch.sum(src, dim=0, out=acc))
+    res["read_256MiB"] = {"bytes": 4 * n, "us_median": q["median"], "tbs": 4 * n / q["median"] / 1e6}
+    print(json.dumps({"roof_probe": res, "peak_tbs": HBM_PEAK_GBS / 1e3}), flush=True)
+    return 0
 
 
 def calibrate_copy(args) -> int:
@@ -281,6 +354,7 @@ def step_times_ms(fn, n: int, rotate: int = 1):
 
 
 def roofline(prep, launch_us_mean: float) -> dict:
+    """Roofline position of one launch taking launch_us_mean microseconds."""
     flops = prep.flops_step() / prep.launches_per_step
     nbytes = prep.bytes_step() / prep.launches_per_step
     peak = (BF16_PEAK_TFLOPS if prep.bf16 else FP32_PEAK_TFLOPS) * 1e12
@@ -341,7 +415,8 @@ def dense_times_us(prep, rounds: int) -> dict:
 def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = None,
         plans: bool = True) -> dict:
     """One block-shape row: per-launch kernel-event times (median, p10, p90), effective rates,
-    roof fraction, and the dense GEMM beside it."""
+    roof fraction, the same launches timed back to back (mean per launch, launch gaps
+    included), and the dense GEMM beside it."""
     import torch
     print(f"# row {spec}", file=sys.stderr, flush=True)
     wl = build_workload(spec)
@@ -351,6 +426,7 @@ def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = No
     torch.cuda.synchronize()
     lt = pct(prep.launch_times_us(rounds))
     r = roofline(prep, lt["mean"])
+    loop_ms, _ = step_times_ms(prep.step, rounds, rotate)   # the same launches back to back
     c0 = prep.calls[0]
     out = {"workload": wl.name, "spec": spec, "block": f"{c0['R']}x{c0['C']}",
            "dtype": "bf16" if wl.bf16 else "f32", "tokens": c0["T"], "plans": prep.planned,
@@ -361,6 +437,7 @@ def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = No
                         ("cold by construction: the stack exceeds the last-level cache"
                          if spec.startswith("bert_large") else "warm, launches back to back")),
            "launch_us": {k: lt[k] for k in ("median", "p10", "p90", "mean")},
+           "loop_us_per_launch": loop_ms * 1e3 / (rounds * prep.launches_per_step),
            "effective_tflops": r["achieved_tflops"], "effective_tbs": r["achieved_gbs"] / 1e3,
            "roof": {k: r[k] for k in ("bound", "frac", "arithmetic_intensity")},
            "frac_of_hbm": r["achieved_gbs"] / HBM_PEAK_GBS,
@@ -479,15 +556,19 @@ VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1),
                (4, 4), (8, 8))
 
 
-def kernel_name(c, bf16: bool) -> str:
-    """The kernel libbsr's automatic choice launches for this product: the matrix-core tiled
-    kernel, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
+def kernel_name(c, bf16: bool, planned: bool = False) -> str:
+    """The kernel libbsr's automatic choice launches for this product: the flat-stream kernel
+    for 32x1 and 16x1 (its planned form with a plan), the matrix-core tiled kernel for square
+    blocks, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
     X tile does not fit in LDS, else the generic kernel.  (A label: the library's plan decides,
     and the kernel trace shows what ran.)"""
     shape = (c["R"], c["C"])
     flag = "true" if bf16 else "false"
     xb = 2 if bf16 and shape != (16, 1) else 4
     fits = 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) <= 160 * 1024
+    if shape in ((32, 1), (16, 1)) and fits:
+        pl = "true" if planned and shape == (32, 1) else "false"
+        return f"spmm_flat_kernel<{c['R']}, {flag}, {pl}>"
     if shape in TILED_SHAPES:
         w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
         if fits:
@@ -501,6 +582,8 @@ def kernel_name(c, bf16: bool) -> str:
 
 def main(argv=None) -> int:
     args = parse(argv)
+    if args.trace_summary:
+        return trace_summary(args.trace_summary)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the library has no "
               "multi-GPU path, so run it with --gpus 1.", file=sys.stderr, flush=True)
@@ -513,6 +596,8 @@ def main(argv=None) -> int:
         return 1
     if args.calibrate_copy:
         return calibrate_copy(args)
+    if args.roof_probe:
+        return roof_probe(args)
     if args.workload.startswith("attn_block"):
         return bench_attention_block(args)
     wl = build_workload(args.workload)
@@ -552,16 +637,17 @@ def main(argv=None) -> int:
     print(f"# timed {args.steps} steps: {ms_per_step:.4f} ms per step", file=sys.stderr,
           flush=True)
 
-    # Roofline of the product kernel: the average of the kernel-event durations of every
-    # launch over a few steps (at least 60 launches).
+    # Roofline of the product kernel: the timed region's time per launch.  The kernel-event
+    # durations of every launch over a few more steps (at least 60 launches) go beside it.
     rounds = max(rotate, -(-60 // prep.launches_per_step))
     lt = pct(prep.launch_times_us(rounds))
-    roof = roofline(prep, lt["mean"])
+    roof = roofline(prep, ms_per_step * 1e3 / prep.launches_per_step)
     tr = measured_traffic(wl.name)
     roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
-                 "kernel": " + ".join(dict.fromkeys(kernel_name(c, wl.bf16) for c in prep.calls)),
-                 "launch_us_median": lt["median"], "launch_us_p10": lt["p10"],
-                 "launch_us_p90": lt["p90"], "launches_timed": lt["n"]})
+                 "launch_us_source": "timed region / launches per step",
+                 "kernel": " + ".join(dict.fromkeys(kernel_name(c, wl.bf16, prep.planned)
+                                                    for c in prep.calls)),
+                 "kernel_event_us": {k: lt[k] for k in ("mean", "median", "p10", "p90", "n")}})
 
     value = prep.flops_step() / (ms_per_step * 1e-3) / 1e9
     c0 = prep.calls[0]
