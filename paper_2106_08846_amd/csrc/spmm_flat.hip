@@ -36,6 +36,7 @@ namespace {
 constexpr int kNW = 16;            // waves per workgroup
 constexpr int kDepth = 3;          // units in flight ahead of the one being multiplied
 constexpr int kRing = kDepth + 1;  // operand buffers per wave
+constexpr int kXChunksPersistent = 16;  // 64-column X chunks a persistent workgroup prefetches
 
 // Inclusive prefix sum over the 64 lanes of a wave: row shifts by 1, 2, 4 and 8 lanes sum each
 // row of 16 lanes, then the last lane of row 0 is added to row 1 and of row 2 to row 3, and
@@ -49,6 +50,165 @@ __device__ __forceinline__ int wave_scan_incl(int v) {
     v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15
     v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31
     return v;
+}
+
+// Empty owned rows, the stream and the combine of one (token tile, slice) item, shared by the
+// one-item and the persistent kernel.  `it` holds the wave's share and the LDS layout; the
+// ring holds the operands of the share's first kDepth units; fetch(ops, nvalid, u) loads
+// unit u (nothing past the share).
+struct FlatItem {
+    int lane, wave;
+    int Pw, Pw1;        // the wave's units
+    int rlo, rhi;       // the rows it owns
+    int row, end;       // first row piece: its row and the end of its units
+    bool has_head;      // the share starts inside row rlo - 1
+    int ws, wsn;        // wave starts, one per lane: wave `lane` and wave lane + 1
+    const int *s_up;    // unit row pointer (LDS)
+    const float *s_bias;
+    float *Xs;          // X tile (LDS), reused by the combine
+    int XP, Kb;
+    char *wslot;
+    TileOut out;
+};
+
+template <int R, bool BF, bool PL, class Ops, class Fetch>
+__device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[kRing],
+                                               int (&nvr)[kRing], Fetch &&fetch) {
+    using U = Unit<R, 1, BF>;
+    using Src = std::conditional_t<PL, PlanUnit<R, 1, BF>, U>;
+    constexpr int NW = kNW, KB = U::KB;
+    const int lane = it.lane, wave = it.wave, Pw = it.Pw, Pw1 = it.Pw1, rlo = it.rlo,
+              rhi = it.rhi, XP = it.XP, Kb = it.Kb, ws = it.ws, wsn = it.wsn;
+    const bool has_head = it.has_head;
+    const int *s_up = it.s_up;
+    const float *s_bias = it.s_bias;
+    float *Xs = it.Xs;
+    char *wslot = it.wslot;
+    const TileOut &out = it.out;
+    int r = it.row;
+    int r_end = it.end;
+    // Empty owned rows: Y = bias.
+    for (int rr = rlo; rr < rhi; ++rr) {
+        if (uniform(s_up[rr + 1]) == uniform(s_up[rr])) {
+            typename U::Acc z;
+            U::init(z, s_bias, rr * R);
+            U::store(z, out, rr * R);
+        }
+    }
+
+    // First row after r with units (rhi if none); returns its start and clipped end.
+    auto next_row = [&](int rr, int &start, int &end_) -> int {
+        for (++rr; rr < rhi; ++rr) {
+            start = uniform(s_up[rr]);
+            const int e = uniform(s_up[rr + 1]);
+            if (start < e) {
+                end_ = e < Pw1 ? e : Pw1;
+                return rr;
+            }
+        }
+        start = end_ = 0;
+        return rhi;
+    };
+
+    // The stream.  Unit u is multiplied in ring slot (u - Pw) mod kRing, after the loads of
+    // unit u + kDepth are issued into the slot freed by unit u - 1.  At the last unit of a row
+    // piece the accumulator goes to Y (a complete row), to `head` (a row another wave finishes)
+    // or stays as the tail (a row continuing past Pw1), and the next row starts at its bias.
+    typename U::Acc acc, head;
+    U::zero(head);
+    int tail_row = -1;
+    if (has_head) U::zero(acc);
+    else if (r < rhi) U::init(acc, s_bias, r * R);
+    else U::zero(acc);
+    // Every phase issues its loads (past the wave's range they fetch nothing) and the loop
+    // exits only at its top, so every path through the loop issues the same loads in the same
+    // order: the compiler then counts kDepth units' loads between a unit's loads and its use
+    // and waits for that unit alone.
+    for (int base = Pw; base < Pw1; base += kRing) {
+#pragma unroll
+        for (int ph = 0; ph < kRing; ++ph) {
+            const int u = base + ph;
+            fetch(ring[(ph + kDepth) % kRing], nvr[(ph + kDepth) % kRing], u + kDepth);
+            __builtin_amdgcn_sched_barrier(0);
+            if (u >= Pw1) continue;
+            if constexpr (PL) {
+                Src::mma(acc, ring[ph], Xs, XP, Kb, wslot);
+            } else {
+                if (nvr[ph] < KB) U::mask(ring[ph], nvr[ph]);
+                U::mma(acc, ring[ph], Xs, XP, Kb, wslot);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (u + 1 == r_end) {
+                if (r == rlo - 1) {
+                    head = acc;
+                } else if (uniform(s_up[r + 1]) <= Pw1) {
+                    U::store(acc, out, r * R);
+                } else {
+                    tail_row = r;
+                }
+                int np, nend;
+                r = next_row(r, np, nend);
+                r_end = nend;
+                if (r < rhi) U::init(acc, s_bias, r * R);
+            }
+        }
+    }
+
+    // Combine rows cut by wave boundaries, in wave order (as in the tiled kernel): the owner's
+    // partial (bias and its units), then each later wave's head partial.  The X tile is dead
+    // now; its LDS holds the head partials P[w][v][lane], the partials of wide tails
+    // T[w][v][lane] and one word per wave naming its wide tail row.
+    constexpr int kLocalHeads = 2;
+    constexpr int kSlot = U::kRegs * 64;
+    __syncthreads();
+    float *P = reinterpret_cast<float *>(Xs);
+    float *Tw = P + NW * kSlot;
+    int *s_wide = reinterpret_cast<int *>(Tw + NW * kSlot);
+    unsigned tail_heads = 0;
+    if (tail_row >= 0) {
+        const int e = uniform(s_up[tail_row + 1]);
+        tail_heads = unsigned(__ballot(lane > wave && lane < NW && ws < e && wsn != ws));
+    }
+    const bool wide = __popc(tail_heads) > kLocalHeads;
+    if (has_head) {
+#pragma unroll
+        for (int vv = 0; vv < U::kRegs; ++vv) P[(wave * U::kRegs + vv) * 64 + lane] = U::get(head, vv);
+    }
+    if (wide) {
+#pragma unroll
+        for (int vv = 0; vv < U::kRegs; ++vv) Tw[(wave * U::kRegs + vv) * 64 + lane] = U::get(acc, vv);
+    }
+    s_wide[wave] = wide ? tail_row : -1;
+    s_wide[NW + wave] = int(tail_heads);
+    __syncthreads();
+    if (tail_row >= 0 && !wide) {
+        for (unsigned m = tail_heads; m; m &= m - 1) {
+            const int w2 = __ffs(m) - 1;
+            float h[U::kRegs];
+#pragma unroll
+            for (int vv = 0; vv < U::kRegs; ++vv) h[vv] = P[(w2 * U::kRegs + vv) * 64 + lane];
+#pragma unroll
+            for (int vv = 0; vv < U::kRegs; ++vv) U::add(acc, vv, h[vv]);
+        }
+        U::store(acc, out, tail_row * R);
+    }
+    const int wv = lane < NW ? s_wide[lane] : -1;
+    const int whm = lane < NW ? s_wide[NW + lane] : 0;
+    for (unsigned long long m = __ballot(wv >= 0); m; m &= m - 1) {
+        const int w = __ffsll(static_cast<long long>(m)) - 1;
+        const int trow = __builtin_amdgcn_readlane(wv, w);
+        if (wave < U::kRegs) {
+            const unsigned hm = unsigned(__builtin_amdgcn_readlane(whm, w));
+            const int vv = wave;
+            float x = Tw[(w * U::kRegs + vv) * 64 + lane];
+            float h[NW - 1];
+#pragma unroll
+            for (int i = 0; i < NW - 1; ++i) h[i] = P[((i + 1) * U::kRegs + vv) * 64 + lane];
+#pragma unroll
+            for (int i = 0; i < NW - 1; ++i) x += (hm >> (i + 1)) & 1u ? h[i] : -0.0f;
+            U::store_reg(x, out, trow * R, vv);
+        }
+    }
 }
 
 template <int R, bool BF, bool PL>
@@ -348,9 +508,6 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
     }
     const bool has_head = head_end > Pw;
 
-    // Compute cursor: the row of the unit being multiplied and the end of its piece.
-    int r = row;
-    int r_end = end;
     // Prefetch cursor (unplanned): the row of the next unit to load, its units [pr_u0, pr_u1)
     // and blocks [pr_b0, pr_b1).
     int pr = row, pr_u0 = 0, pr_u1 = 0, pr_b0 = 0, pr_b1 = 0;
@@ -440,140 +597,281 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
     }
     __syncthreads();
 
-    char *wslot = reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048;
-    TileOut out;
-    out.ldy4 = int(ldy) * 4;
-    out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(out.ldy4));
+    FlatItem fi{lane, wave, Pw, Pw1, rlo, rhi, row, end, has_head, ws, wsn, s_up, s_bias, Xs,
+                XP, Kb, reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048, TileOut{}};
+    fi.out.ldy4 = int(ldy) * 4;
+    fi.out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(fi.out.ldy4));
+    flat_item_body<R, BF, PL>(fi, ring, nvr, [&](Ops &o, int &nv, int uu) {
+        fetch(o, nv, uu, read_up_lds, read_ib_lds);
+    });
+}
 
-    // Empty owned rows: Y = bias.
-    for (int rr = rlo; rr < rhi; ++rr) {
-        if (uniform(s_up[rr + 1]) == uniform(s_up[rr])) {
-            typename U::Acc z;
-            U::init(z, s_bias, rr * R);
-            U::store(z, out, rr * R);
-        }
-    }
+// The persistent form: one workgroup per CU, each walking several (token tile, slice) items of
+// its product, used when a launch has more items than the GPU has CUs.  The row pointers and
+// the bias go to LDS once; every item then stores its X tile from registers (loaded under the
+// previous item's stream), computes its wave's share from the LDS row pointers, issues its
+// first units' loads, and after one barrier loads the next item's X rows into registers and
+// runs the shared stream and combine.  Items of one workgroup share an XCD, as in the one-item
+// kernel's mapping.
+template <int R, bool BF, bool PL>
+__global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const TiledBatch batch) {
+    using U = Unit<R, 1, BF>;
+    using Src = std::conditional_t<PL, PlanUnit<R, 1, BF>, U>;
+    using Ops = typename Src::Ops;
+    constexpr int NW = kNW, KB = U::KB, kThreads = NW * 64;
+    extern __shared__ float smem[];
 
-    // First row after r with units (rhi if none); returns its start and clipped end.
-    auto next_row = [&](int rr, int &start, int &end_) -> int {
-        for (++rr; rr < rhi; ++rr) {
-            start = uniform(s_up[rr]);
-            const int e = uniform(s_up[rr + 1]);
-            if (start < e) {
-                end_ = e < Pw1 ? e : Pw1;
-                return rr;
+    const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
+    const int g = blockIdx.x;
+    const TiledItem &I = batch.item[blockIdx.y];
+    const void *__restrict__ X = I.X;
+    const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
+    const int32_t *__restrict__ indptr = I.indptr;
+    const int32_t *__restrict__ indices = I.indices;
+    const void *__restrict__ data = I.data;
+    const int32_t *__restrict__ uptr = I.uptr;
+    const int32_t *__restrict__ ucol = I.ucol;
+    const void *__restrict__ uval = I.uval;
+    const float *__restrict__ bias = I.bias;
+    float *__restrict__ Y = I.Y;
+    const int K = I.K, nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
+              slices = I.slices, XP = I.XP;
+    const int ucap = PL ? I.ucap : nnzb;
+    int *s_up = reinterpret_cast<int *>(smem);
+    int *s_ib = s_up + I.ib_offset;
+    float *s_bias = smem + I.indptr_words;
+    float *Xs = s_bias + I.bias_words;
+
+    // Items: the XCD's range of the product's (tile, slice) pairs, round robin over the
+    // gridDim.x / 8 workgroups of the XCD.
+    const int xcd = g & 7, rank = g >> 3, nrank = int(gridDim.x) >> 3;
+    const int pairs = num_tiles * slices, per_xcd = (pairs + 7) >> 3;
+    const int q_first = xcd * per_xcd + rank;
+    const int q_end = min(xcd * per_xcd + per_xcd, pairs);
+    if (q_first >= q_end) return;
+
+    constexpr int kXBytes = BF ? 2 : 4;
+    constexpr int kRowsPerWave = kTT / NW;
+    constexpr int kXC = kXChunksPersistent;
+    static_assert(kTT % NW == 0, "every wave stages the same number of rows");
+
+    // X rows w + 16 r of a tile in registers, kXC 64-column chunks from column c0.  Rows past
+    // the product's last token, and a tile of no rows (the prefetch after the last item), load
+    // zeros from an empty buffer range.  A guarded load skips chunks that start at or past K;
+    // the prefetch is unguarded, so that every path issues the same loads and the waits in the
+    // stream count them.
+    unsigned v[kRowsPerWave][kXC];
+    auto x_load = [&](int64_t t0_, int rows_, int c0, bool guarded) {
+#pragma unroll
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            const int64_t row = t < rows_ ? t0_ + t : 0;
+            const __amdgpu_buffer_rsrc_t rx =
+                buffer_rsrc(static_cast<const char *>(X) + row * ldx * kXBytes,
+                            t < rows_ ? unsigned(K) * kXBytes : 0u);
+#pragma unroll
+            for (int m = 0; m < kXC; ++m) {
+                if (guarded && c0 + 64 * m >= K) continue;
+                if constexpr (BF)
+                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b16(rx, (c0 + lane) * 2 + 128 * m,
+                                                                   0, 0);
+                else
+                    v[r][m] = __builtin_amdgcn_raw_buffer_load_b32(rx, (c0 + lane) * 4 + 256 * m,
+                                                                   0, 0);
             }
         }
-        start = end_ = 0;
-        return rhi;
     };
-
-    // The stream.  Unit u is multiplied in ring slot (u - Pw) mod kRing, after the loads of
-    // unit u + kDepth are issued into the slot freed by unit u - 1.  At the last unit of a row
-    // piece the accumulator goes to Y (a complete row), to `head` (a row another wave finishes)
-    // or stays as the tail (a row continuing past Pw1), and the next row starts at its bias.
-    typename U::Acc acc, head;
-    U::zero(head);
-    int tail_row = -1;
-    if (has_head) U::zero(acc);
-    else if (r < rhi) U::init(acc, s_bias, r * R);
-    else U::zero(acc);
-    // Every phase issues its loads (past the wave's range they fetch nothing) and the loop
-    // exits only at its top, so every path through the loop issues the same loads in the same
-    // order: the compiler then counts kDepth units' loads between a unit's loads and its use
-    // and waits for that unit alone.
-    for (int base = Pw; base < Pw1; base += kRing) {
+    // Chunks that start at or past K are not stored; a chunk that crosses K sends its columns
+    // past K to column K, the tile's zero pad column.  The lane index and K pass through empty
+    // asm statements at every call, so the compiler computes the addresses here instead of
+    // keeping them in registers across the item loop.
+    auto x_store = [&](int c0) {
+        int ln = lane, Ko = K;
+        asm volatile("" : "+v"(ln));
+        asm volatile("" : "+s"(Ko));
 #pragma unroll
-        for (int ph = 0; ph < kRing; ++ph) {
-            const int u = base + ph;
-            fetch(ring[(ph + kDepth) % kRing], nvr[(ph + kDepth) % kRing], u + kDepth,
-                  read_up_lds, read_ib_lds);
-            __builtin_amdgcn_sched_barrier(0);
-            if (u >= Pw1) continue;
-            if constexpr (PL) {
-                Src::mma(acc, ring[ph], Xs, XP, Kb, wslot);
-            } else {
-                if (nvr[ph] < KB) U::mask(ring[ph], nvr[ph]);
-                U::mma(acc, ring[ph], Xs, XP, Kb, wslot);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            if (u + 1 == r_end) {
-                if (r == rlo - 1) {
-                    head = acc;
-                } else if (uniform(s_up[r + 1]) <= Pw1) {
-                    U::store(acc, out, r * R);
-                } else {
-                    tail_row = r;
+        for (int r = 0; r < kRowsPerWave; ++r) {
+            const int t = wave + NW * r;
+            if constexpr (U::kTransposed) {
+                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs) + t;
+#pragma unroll
+                for (int m = 0; m < kXC; ++m) {
+                    const int cb = c0 + 64 * m;
+                    if (cb < Ko) xt[min(cb + ln, Ko) * XP] = bf16_t(v[r][m]);
                 }
-                int np, nend;
-                r = next_row(r, np, nend);
-                r_end = nend;
-                if (r < rhi) U::init(acc, s_bias, r * R);
+            } else {
+                unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * XP + ln;
+#pragma unroll
+                for (int m = 0; m < kXC; ++m) {
+                    unsigned w = v[r][m];
+                    if constexpr (BF) w <<= 16;   // bf16 -> fp32, exact
+                    const int cb = c0 + 64 * m;
+                    if (cb + 64 <= Ko) dst[cb] = w;
+                    else if (cb < Ko) dst[min(cb + ln, Ko) - ln] = w;
+                }
             }
         }
-    }
+    };
+    auto item_tile = [&](int q, int64_t &t0_, int &rows_, int &s_) {
+        const int tile = q / slices;
+        s_ = q - tile * slices;
+        t0_ = int64_t(tile) * kTT;
+        rows_ = int(T - t0_ < kTT ? T - t0_ : kTT);
+    };
+    int64_t t0;
+    int rows, s;
+    item_tile(q_first, t0, rows, s);
+    x_load(t0, rows, 0, true);
 
-    // Combine rows cut by wave boundaries, in wave order (as in the tiled kernel): the owner's
-    // partial (bias and its units), then each later wave's head partial.  The X tile is dead
-    // now; its LDS holds the head partials P[w][v][lane], the partials of wide tails
-    // T[w][v][lane] and one word per wave naming its wide tail row.
-    constexpr int kLocalHeads = 2;
-    constexpr int kSlot = U::kRegs * 64;
+    // Once: row pointers and bias to LDS (unplanned, wave 0 forms the unit row pointer).
+    if constexpr (PL) {
+        for (int i = threadIdx.x; i <= Nb; i += kThreads) s_up[i] = clampi(uptr[i], 0, ucap);
+    } else {
+        for (int i = threadIdx.x; i <= Nb; i += kThreads) s_ib[i] = clampi(indptr[i], 0, nnzb);
+    }
+    for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
     __syncthreads();
-    float *P = reinterpret_cast<float *>(Xs);
-    float *Tw = P + NW * kSlot;
-    int *s_wide = reinterpret_cast<int *>(Tw + NW * kSlot);
-    unsigned tail_heads = 0;
-    if (tail_row >= 0) {
-        const int e = uniform(s_up[tail_row + 1]);
-        tail_heads = unsigned(__ballot(lane > wave && lane < NW && ws < e && wsn != ws));
-    }
-    const bool wide = __popc(tail_heads) > kLocalHeads;
-    if (has_head) {
-#pragma unroll
-        for (int vv = 0; vv < U::kRegs; ++vv) P[(wave * U::kRegs + vv) * 64 + lane] = U::get(head, vv);
-    }
-    if (wide) {
-#pragma unroll
-        for (int vv = 0; vv < U::kRegs; ++vv) Tw[(wave * U::kRegs + vv) * 64 + lane] = U::get(acc, vv);
-    }
-    s_wide[wave] = wide ? tail_row : -1;
-    s_wide[NW + wave] = int(tail_heads);
-    __syncthreads();
-    if (tail_row >= 0 && !wide) {
-        for (unsigned m = tail_heads; m; m &= m - 1) {
-            const int w2 = __ffs(m) - 1;
-            float h[U::kRegs];
-#pragma unroll
-            for (int vv = 0; vv < U::kRegs; ++vv) h[vv] = P[(w2 * U::kRegs + vv) * 64 + lane];
-#pragma unroll
-            for (int vv = 0; vv < U::kRegs; ++vv) U::add(acc, vv, h[vv]);
+    if constexpr (!PL) {
+        if (wave == 0) {
+            int carry = 0;
+            for (int base = 0; base <= Nb; base += 64) {
+                const int i = base + lane;
+                const int n = i < Nb ? s_ib[i + 1] - s_ib[i] : 0;
+                const int cnt = n > 0 ? (n + KB - 1) / KB : 0;
+                const int incl = wave_scan_incl(cnt) + carry;
+                if (i <= Nb) s_up[i] = incl - cnt;
+                carry = __builtin_amdgcn_readlane(incl, 63);
+            }
         }
-        U::store(acc, out, tail_row * R);
+        __syncthreads();
     }
-    const int wv = lane < NW ? s_wide[lane] : -1;
-    const int whm = lane < NW ? s_wide[NW + lane] : 0;
-    for (unsigned long long m = __ballot(wv >= 0); m; m &= m - 1) {
-        const int w = __ffsll(static_cast<long long>(m)) - 1;
-        const int trow = __builtin_amdgcn_readlane(wv, w);
-        if (wave < U::kRegs) {
-            const unsigned hm = unsigned(__builtin_amdgcn_readlane(whm, w));
-            const int vv = wave;
-            float x = Tw[(w * U::kRegs + vv) * 64 + lane];
-            float h[NW - 1];
-#pragma unroll
-            for (int i = 0; i < NW - 1; ++i) h[i] = P[((i + 1) * U::kRegs + vv) * 64 + lane];
-#pragma unroll
-            for (int i = 0; i < NW - 1; ++i) x += (hm >> (i + 1)) & 1u ? h[i] : -0.0f;
-            U::store_reg(x, out, trow * R, vv);
+    const int64_t k = uniform(s_up[Nb]);
+    auto read_up_lds = [&](int i) { return uniform(s_up[i]); };
+    auto read_ib_lds = [&](int i) { return uniform(s_ib[i]); };
+
+    for (int q = q_first; q < q_end; q += nrank) {
+        if (q != q_first) __syncthreads();   // the previous item's combine reads the X region
+
+        // This item's X tile: chunks [0, kXC) are in registers; wider rows take more passes.
+        x_store(0);
+        for (int c0 = 64 * kXC; c0 < K; c0 += 64 * kXC) {
+            x_load(t0, rows, c0, true);
+            x_store(c0);
         }
+        {
+            int tid = int(threadIdx.x);
+            asm volatile("" : "+v"(tid));
+            if constexpr (U::kPad == 1) {   // the fp32 tile's zero pad column
+                if (tid < kTT) Xs[tid * XP + K] = 0.0f;
+            }
+            if constexpr (U::kTransposed) {   // the transposed tile's zero pad column K
+                if (tid < kTT) reinterpret_cast<bf16_t *>(Xs)[K * XP + tid] = 0;
+            }
+        }
+
+        // The wave's share (as in the one-item kernel's LDS path).
+        const int row_lo =
+            (s == 0) ? 0 : uniform(wave_lower_bound(s_up, Nb, int64_t(s) * k / slices));
+        const int row_hi = (s == slices - 1)
+                               ? Nb
+                               : uniform(wave_lower_bound(s_up, Nb, int64_t(s + 1) * k / slices));
+        const int64_t Q0 = uniform(s_up[row_lo]);
+        int64_t Q1 = uniform(s_up[row_hi]);
+        if (Q1 < Q0) Q1 = Q0;
+        static_assert(NW == 16, "wave starts use a division by 16");
+        const unsigned span = unsigned(Q1 - Q0), hi = span >> 4, lo = span & 15u;
+        const int ws = int(Q0) + int(hi * unsigned(lane) + ((lo * unsigned(lane)) >> 4));
+        const int wsn = int(Q0) + int(hi * unsigned(lane + 1) + ((lo * unsigned(lane + 1)) >> 4));
+        const int Pw = __builtin_amdgcn_readlane(ws, wave);
+        const int Pw1 = __builtin_amdgcn_readlane(wsn, wave);
+        int rlo = (wave == 0) ? row_lo : uniform(wave_lower_bound(s_up, Nb, int64_t(Pw)));
+        rlo = rlo < row_lo ? row_lo : (rlo > row_hi ? row_hi : rlo);
+        int rhi = (wave == NW - 1) ? row_hi : uniform(wave_lower_bound(s_up, Nb, int64_t(Pw1)));
+        rhi = rhi < rlo ? rlo : (rhi > row_hi ? row_hi : rhi);
+        int head_end = (rlo < rhi) ? uniform(s_up[rlo]) : Pw1;
+        head_end = head_end < Pw ? Pw : (head_end > Pw1 ? Pw1 : head_end);
+        int row = rlo - 1, end = head_end;
+        if (head_end <= Pw) {
+            end = 0;
+            for (row = rlo; row < rhi; ++row) {
+                const int p = uniform(s_up[row]);
+                const int e = uniform(s_up[row + 1]);
+                if (p < e) {
+                    end = e < Pw1 ? e : Pw1;
+                    break;
+                }
+            }
+        }
+        const bool has_head = head_end > Pw;
+
+        // Prefetch cursor (unplanned): the row of the next unit to load, its units
+        // [pr_u0, pr_u1) and blocks [pr_b0, pr_b1).
+        int pr = row, pr_u0 = 0, pr_u1 = 0, pr_b0 = 0, pr_b1 = 0;
+        auto fetch = [&](Ops &o, int &nvalid, int uu) {
+            if constexpr (PL) {
+                Src::load(o, uu, Pw1, ucol, uval);
+                nvalid = KB;
+            } else {
+                int p0 = nnzb, nv = KB;
+                if (uu < Pw1) {
+                    while (uu >= pr_u1 && pr < Nb - 1) {
+                        ++pr;
+                        pr_u0 = pr_u1;
+                        pr_u1 = read_up_lds(pr + 1);
+                        pr_b0 = read_ib_lds(pr);
+                        pr_b1 = read_ib_lds(pr + 1);
+                    }
+                    p0 = pr_b0 + KB * (uu - pr_u0);
+                    p0 = p0 < nnzb ? p0 : nnzb;
+                    nv = pr_b1 - p0 < KB ? pr_b1 - p0 : KB;
+                }
+                U::load(o, p0, nnzb, indices, data);
+                nvalid = nv;
+            }
+        };
+        Ops ring[kRing];
+        int nvr[kRing];
+        if constexpr (!PL) {
+            if (row < rhi) {
+                pr_u0 = read_up_lds(row);
+                pr_u1 = read_up_lds(row + 1);
+                pr_b0 = read_ib_lds(row);
+                pr_b1 = read_ib_lds(row + 1);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < kDepth; ++d) fetch(ring[d], nvr[d], Pw + d);
+        __syncthreads();
+
+        FlatItem fi{lane, wave, Pw, Pw1, rlo, rhi, row, end, has_head, ws, wsn, s_up, s_bias,
+                    Xs, XP, Kb, reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048,
+                    TileOut{}};
+        fi.out.ldy4 = int(ldy) * 4;
+        fi.out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(fi.out.ldy4));
+
+        // The next item's X rows, loaded under this item's stream.
+        {
+            const int qn = q + nrank;
+            int64_t t0n = 0;
+            int rowsn = 0, sn = 0;
+            if (qn < q_end) item_tile(qn, t0n, rowsn, sn);
+            x_load(t0n, rowsn, 0, false);
+            t0 = t0n;
+            rows = rowsn;
+            s = sn;
+        }
+        flat_item_body<R, BF, PL>(fi, ring, nvr, fetch);
     }
 }
 
 template <int R, bool BF, bool PL>
-bsr_status launch_flat_variant(const TiledBatch &batch, dim3 grid, size_t lds, hipStream_t st,
-                               const LaunchEvents &ev) {
-    launch_kernel(spmm_flat_kernel<R, BF, PL>, grid, dim3(kNW * 64), lds, st, ev, batch);
+bsr_status launch_flat_variant(const TiledBatch &batch, dim3 grid, size_t lds, bool persistent,
+                               hipStream_t st, const LaunchEvents &ev) {
+    if (persistent)
+        launch_kernel(spmm_flat_persistent_kernel<R, BF, PL>, grid, dim3(kNW * 64), lds, st, ev,
+                      batch);
+    else
+        launch_kernel(spmm_flat_kernel<R, BF, PL>, grid, dim3(kNW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
@@ -638,17 +936,28 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
         if (wgs > gx) gx = wgs;
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
     }
+    // More workgroups than CUs (one per CU fits): the persistent kernel, one workgroup per CU,
+    // each walking several token tiles of its product.
+    const int cus = device_cu_count() > 0 ? device_cu_count() : 256;
+    bool persistent = false;
+    if (int64_t(gx) * n > cus) {
+        const int gp = (cus / n) / 8 * 8;
+        if (gp >= 8 && gp < gx) {
+            gx = gp;
+            persistent = true;
+        }
+    }
     hipStream_t st = as_stream(stream);
     const dim3 grid(gx, n);
     if (R == 32) {
-        if (bf) return planned ? launch_flat_variant<32, true, true>(batch, grid, lds, st, ev)
-                               : launch_flat_variant<32, true, false>(batch, grid, lds, st, ev);
-        return planned ? launch_flat_variant<32, false, true>(batch, grid, lds, st, ev)
-                       : launch_flat_variant<32, false, false>(batch, grid, lds, st, ev);
+        if (bf) return planned ? launch_flat_variant<32, true, true>(batch, grid, lds, persistent, st, ev)
+                               : launch_flat_variant<32, true, false>(batch, grid, lds, persistent, st, ev);
+        return planned ? launch_flat_variant<32, false, true>(batch, grid, lds, persistent, st, ev)
+                       : launch_flat_variant<32, false, false>(batch, grid, lds, persistent, st, ev);
     }
     if (planned) return BSR_ERR_UNSUPPORTED;
-    if (bf) return launch_flat_variant<16, true, false>(batch, grid, lds, st, ev);
-    return launch_flat_variant<16, false, false>(batch, grid, lds, st, ev);
+    if (bf) return launch_flat_variant<16, true, false>(batch, grid, lds, persistent, st, ev);
+    return launch_flat_variant<16, false, false>(batch, grid, lds, persistent, st, ev);
 }
 
 }  // namespace bsr

@@ -179,15 +179,17 @@ struct Unit<32, 1, BF> : LinearUnit<32, BF> {
 #pragma unroll
         for (int m = 0; m < kSteps; ++m) acc = mfma32(a[m], ops.b[m], acc);
     }
-    // Element v of lane l is Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].
+    // Element v of lane l is Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].  The row offset of v
+    // (uniform) goes in the scalar offset, which the hardware range-checks like the vector
+    // offset, so the sixteen stores share one vector offset.
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
         const int vo = 4 * kh * o.ldy4 + tl * 4;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int r = 8 * (v >> 2) + (v & 3);
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), o.rsrc,
-                                                  vo + r * o.ldy4, n0 * 4, kStoreNT);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[v]), o.rsrc, vo,
+                                                  n0 * 4 + r * o.ldy4, kStoreNT);
         }
     }
     // Register v of every lane alone (v uniform).
