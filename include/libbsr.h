@@ -395,6 +395,28 @@ LIBBSR_API bsr_status bsr_to_dense(const bsr_matrix_t *W, float *out, int64_t ld
  */
 LIBBSR_API bsr_status bsr_cast_f32_bf16(const float *src, uint16_t *dst, int64_t n, void *stream);
 
+/*
+ * One gradient step of the iterative projection for Eq. 2 (Sec. 2.1: minimise a loss under a
+ * bound on the number of nonzero blocks).  With the layer-output reconstruction loss on
+ * calibration activations X (T x K), f(W) = 1/2 tr((W - W0) H (W - W0)^T) with
+ * H = X^T X / T, projected gradient descent (iterative hard thresholding) takes
+ *   W <- P_k(W - eta (W - W0) H),
+ * where P_k is the block prune (bsr_prune_from_dense with k blocks).  The two products of the
+ * gradient are bsr_spmm calls with the symmetric H as their X operand: G = H W^T (W the
+ * current BSR iterate) and C0 = H W0^T (W0 stored with all its blocks).  This call forms
+ *   V[n][j] = W[n][j] - eta * (G[j][n] - C0[j][n]),   n < N, j < K,
+ * rounding the subtraction, the product and the final subtraction to fp32 one at a time (no
+ * fused multiply-add).  W: device fp32 N x K (the iterate, dense, row pitch ldw >= K); G, C0:
+ * device fp32 K x N (row pitches ldg, ldc >= N); V: device fp32 N x K (ldv >= K), which may be
+ * W itself (then ldv == ldw) but must not overlap G or C0.  Errors: BSR_ERR_SHAPE (N or K < 0,
+ * a pitch too small), BSR_ERR_ARG (non-finite eta; V overlapping an input other than as W
+ * itself), BSR_ERR_NULL, BSR_ERR_UNSUPPORTED (N >= 2^37, K > 4194240, offsets past 2^53),
+ * BSR_ERR_ARCH, BSR_ERR_HIP.
+ */
+LIBBSR_API bsr_status bsr_iht_update(const float *W, int64_t ldw, const float *G, int64_t ldg,
+                                     const float *C0, int64_t ldc, float eta, int64_t N,
+                                     int64_t K, float *V, int64_t ldv, void *stream);
+
 /* Static, human-readable name of a status code. */
 LIBBSR_API const char *bsr_status_str(bsr_status s);
 

@@ -25,7 +25,7 @@ EXPORTS = ["bsr_prune_count", "bsr_prune_count_ex", "bsr_prune_workspace_bytes",
            "bsr_prune_from_dense", "bsr_prune_from_dense_noalloc", "bsr_prune_from_dense_ex",
            "bsr_spmm", "bsr_spmm_ex",
            "bsr_spmm_batched", "bsr_plan_bytes", "bsr_plan_prepare", "bsr_spmm_batched_planned", "bsr_attention", "bsr_reblock", "bsr_to_dense",
-           "bsr_cast_f32_bf16",
+           "bsr_cast_f32_bf16", "bsr_iht_update",
            "bsr_status_str", "bsr_last_hip_error"]
 NORM_L2, NORM_L1 = 0, 1
 SELECT_GLOBAL, SELECT_PER_ROW = 0, 1
@@ -131,6 +131,9 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_reblock.restype = st
         lib.bsr_cast_f32_bf16.argtypes = [p, p, i64, p]
         lib.bsr_cast_f32_bf16.restype = st
+        lib.bsr_iht_update.argtypes = [p, i64, p, i64, p, i64, ctypes.c_float, i64, i64, p, i64,
+                                       p]
+        lib.bsr_iht_update.restype = st
         lib.bsr_status_str.argtypes = [ctypes.c_int]
         lib.bsr_status_str.restype = ctypes.c_char_p
         lib.bsr_last_hip_error.argtypes = []
@@ -537,6 +540,68 @@ def bsr_to_dense(W: BSRMatrix, out: torch.Tensor | None = None, stream=None) -> 
     _check(_lib().bsr_to_dense(ctypes.byref(m), _ptr(out), _pitch(out, "out"), _stream(stream)),
            "bsr_to_dense")
     return out
+
+
+def bsr_iht_update(W: torch.Tensor, G: torch.Tensor, C0: torch.Tensor, eta: float,
+                   V: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """V = W - eta (G - C0)^T (bsr_iht_update): W [N, K], G and C0 [K, N], fp32 on the device;
+    V may be W itself (in place)."""
+    for t, name in ((W, "W"), (G, "G"), (C0, "C0")):
+        _require_cuda(t, name, torch.float32)
+    if W.dim() != 2:
+        raise ValueError("W must be [N, K]")
+    N, K = W.shape
+    if tuple(G.shape) != (K, N) or tuple(C0.shape) != (K, N):
+        raise ValueError(f"G and C0 must be [{K}, {N}]")
+    if V is None:
+        V = torch.empty((N, K), dtype=torch.float32, device=W.device)
+    _require_cuda(V, "V", torch.float32)
+    if tuple(V.shape) != (N, K):
+        raise ValueError(f"V must be [{N}, {K}]")
+    _check(_lib().bsr_iht_update(_ptr(W), _pitch(W, "W"), _ptr(G), _pitch(G, "G"), _ptr(C0),
+                                 _pitch(C0, "C0"), float(eta), N, K, _ptr(V), _pitch(V, "V"),
+                                 _stream(stream)), "bsr_iht_update")
+    return V
+
+
+def bsr_iht(W0: torch.Tensor, H: torch.Tensor, R: int, C: int, k: int, eta: float, iters: int,
+            stream=None, trace: bool = False):
+    """Iterative projection for Eq. 2 (Sec. 2.1) on the quadratic loss
+    f(W) = 1/2 tr((W - W0) H (W - W0)^T): W_0 = P_k(W0), W_{t+1} = P_k(W_t - eta (W_t - W0) H),
+    P_k the block prune keeping k blocks of R x C.  W0: [N, K] fp32; H: [K, K] fp32, symmetric
+    (for the reconstruction loss, X^T X / T of calibration activations X).
+
+    Each step runs on the library: G = H W_t^T (bsr_spmm with the BSR iterate), the dense
+    iterate (bsr_to_dense), the update (bsr_iht_update, in place) and the prune; C0 = H W0^T is
+    one bsr_spmm with W0 stored with all its blocks.  Returns the BSR iterate W_iters; with
+    trace, also the list of (V_t, W_t) dense pairs of every step (W_t the iterate the step
+    started from, V_t its update before the projection)."""
+    _require_cuda(W0, "W0", torch.float32)
+    _require_cuda(H, "H", torch.float32)
+    if W0.dim() != 2:
+        raise ValueError("W0 must be [N, K]")
+    N, K = W0.shape
+    if tuple(H.shape) != (K, K):
+        raise ValueError(f"H must be [{K}, {K}]")
+    if R <= 0 or C <= 0 or N % R or K % C:
+        raise ValueError("the block shape must divide W0")
+    if iters < 0:
+        raise ValueError("iters must be >= 0")
+    dev = W0.device
+    full = bsr_prune_from_dense(W0, R, C, k=(N // R) * (K // C), stream=stream)
+    C0 = bsr_spmm(H, full, None, torch.empty((K, N), dtype=torch.float32, device=dev), stream)
+    del full
+    M = bsr_prune_from_dense(W0, R, C, k=k, stream=stream)
+    G = torch.empty((K, N), dtype=torch.float32, device=dev)
+    hist = []
+    for _ in range(iters):
+        bsr_spmm(H, M, None, G, stream)
+        Wt = bsr_to_dense(M, stream=stream)
+        V = bsr_iht_update(Wt, G, C0, eta, V=Wt.clone() if trace else Wt, stream=stream)
+        if trace:
+            hist.append((V, Wt))
+        M = bsr_prune_from_dense(V, R, C, k=k, stream=stream)
+    return (M, hist) if trace else M
 
 
 def bsr_reblock(W: BSRMatrix, R2: int, C2: int, stream=None) -> BSRMatrix:

@@ -402,6 +402,16 @@ bsr_status bsr_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2, int32_t *i
     return bsr::launch_reblock(W, R2, C2, indptr_out, indices_out, data_out, stream);
 }
 
+bsr_status bsr_iht_update(const float *W, int64_t ldw, const float *G, int64_t ldg,
+                          const float *C0, int64_t ldc, float eta, int64_t N, int64_t K, float *V,
+                          int64_t ldv, void *stream) {
+    bsr_status s = bsr::check_iht_update(W, ldw, G, ldg, C0, ldc, eta, N, K, V, ldv);
+    if (s != BSR_OK) return s;
+    if (N == 0 || K == 0) return BSR_OK;
+    if ((s = bsr::ensure_device()) != BSR_OK) return s;
+    return bsr::launch_iht_update(W, ldw, G, ldg, C0, ldc, eta, N, K, V, ldv, stream);
+}
+
 bsr_status bsr_cast_f32_bf16(const float *src, uint16_t *dst, int64_t n, void *stream) {
     bsr_status s = bsr::check_cast(src, dst, n);
     if (s != BSR_OK) return s;

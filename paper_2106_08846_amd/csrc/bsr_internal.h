@@ -50,6 +50,9 @@ bsr_status check_plan_prepare(const bsr_matrix_t *W, const void *mem, size_t byt
 bsr_status check_spmm_items(const bsr_spmm_item_t *items, int32_t n);
 bsr_status check_to_dense(const bsr_matrix_t *W, const float *out, int64_t ldo);
 bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n);
+bsr_status check_iht_update(const float *W, int64_t ldw, const float *G, int64_t ldg,
+                            const float *C0, int64_t ldc, float eta, int64_t N, int64_t K,
+                            const float *V, int64_t ldv);
 bsr_status check_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2,
                          const int32_t *indptr_out, const int32_t *indices_out,
                          const void *data_out);
@@ -69,6 +72,9 @@ bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32
                         void *workspace, int norm, int select, void *stream);
 bsr_status launch_to_dense(const bsr_matrix_t *W, float *out, int64_t ldo, void *stream);
 bsr_status launch_cast(const float *src, uint16_t *dst, int64_t n, void *stream);
+bsr_status launch_iht_update(const float *W, int64_t ldw, const float *G, int64_t ldg,
+                             const float *C0, int64_t ldc, float eta, int64_t N, int64_t K,
+                             float *V, int64_t ldv, void *stream);
 bsr_status launch_reblock(const bsr_matrix_t *W, int32_t R2, int32_t C2, int32_t *indptr_out,
                           int32_t *indices_out, void *data_out, void *stream);
 // Optional event pair recorded at a product kernel's start and end (hipExtLaunchKernel).

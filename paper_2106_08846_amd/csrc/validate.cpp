@@ -228,6 +228,27 @@ bsr_status check_cast(const float *src, const uint16_t *dst, int64_t n) {
     return BSR_OK;
 }
 
+bsr_status check_iht_update(const float *W, int64_t ldw, const float *G, int64_t ldg,
+                            const float *C0, int64_t ldc, float eta, int64_t N, int64_t K,
+                            const float *V, int64_t ldv) {
+    if (N < 0 || K < 0) return BSR_ERR_SHAPE;
+    if (ldw < K || ldv < K || ldg < N || ldc < N) return BSR_ERR_SHAPE;
+    if (!std::isfinite(eta)) return BSR_ERR_ARG;
+    if (N == 0 || K == 0) return BSR_OK;
+    if (!W || !G || !C0 || !V) return BSR_ERR_NULL;
+    if (N > kMaxElems / ldw || N > kMaxElems / ldv || K > kMaxElems / ldg ||
+        K > kMaxElems / ldc || N > (int64_t(1) << 37) || K > int64_t(65535) * 64)
+        return BSR_ERR_UNSUPPORTED;
+    // V may be W itself (each element is read before it is written, by the same thread), but
+    // no other overlap of V with an input.
+    const int64_t vb = ((N - 1) * ldv + K) * 4;
+    if (overlaps(V, vb, G, ((K - 1) * ldg + N) * 4) || overlaps(V, vb, C0, ((K - 1) * ldc + N) * 4))
+        return BSR_ERR_ARG;
+    if (V != W && overlaps(V, vb, W, ((N - 1) * ldw + K) * 4)) return BSR_ERR_ARG;
+    if (V == W && ldv != ldw) return BSR_ERR_ARG;
+    return BSR_OK;
+}
+
 bsr_status check_attention(const float *Q, int64_t ldq, const float *K, int64_t ldk,
                            const float *V, int64_t ldv, const float *O, int64_t ldo,
                            int32_t batch, int32_t seq, int32_t heads, int32_t head_dim,

@@ -181,6 +181,27 @@ def test_cast_errors(lib):
     assert lib.bsr_cast_f32_bf16(None, None, 0, None) == 0
 
 
+def test_iht_update_errors(lib):
+    f = ctypes.c_float
+    a = 1 << 20   # three disjoint fake device ranges
+    W, G, C0, V = FAKE, FAKE + a, FAKE + 2 * a, FAKE + 3 * a
+    ok = dict(W=W, ldw=8, G=G, ldg=4, C0=C0, ldc=4, eta=0.5, N=4, K=8, V=V, ldv=8)
+
+    def call(**kw):
+        d = dict(ok, **kw)
+        return lib.bsr_iht_update(d["W"], d["ldw"], d["G"], d["ldg"], d["C0"], d["ldc"],
+                                  f(d["eta"]), d["N"], d["K"], d["V"], d["ldv"], None)
+    assert call(N=-1) == 2 and call(K=-1) == 2
+    assert call(ldw=7) == 2 and call(ldv=7) == 2 and call(ldg=3) == 2 and call(ldc=3) == 2
+    assert call(eta=float("nan")) == 3 and call(eta=float("inf")) == 3
+    assert call(W=None) == 1 and call(G=None) == 1 and call(C0=None) == 1 and call(V=None) == 1
+    assert call(V=G) == 3 and call(V=C0 + 16) == 3          # V overlaps G or C0
+    assert call(V=W + 4) == 3                                # overlaps W without being W
+    assert call(V=W, ldv=9) == 3                             # in place with another pitch
+    assert call(N=0) == 0 and call(K=0) == 0                 # empty: no device needed
+    assert call(K=65535 * 64 + 1, ldw=65535 * 64 + 1, ldv=65535 * 64 + 1) == 9
+
+
 def test_python_binding_rejects_cpu_tensors(L):
     import torch
     with pytest.raises(TypeError):
