@@ -471,7 +471,62 @@ def rows(args) -> dict:
     res["sweep_T128"] = [row(f"sweep:{s}", 1, 100, dense, plans=pl) for s in
                          ("1x1", "8x1", "16x1", "32x1", "1x32", "4x4", "8x8", "16x16", "32x32")]
     res["bert_base_attn_T128"] = [row("bert_base_attn", 1, 100, dense, plans=pl)]
+    res["iht_bert_base"] = [iht_row(32, 1, 0.1), iht_row(1, 32, 0.1)]
     return res
+
+
+def iht_row(R: int, C: int, density: float, iters: int = 20) -> dict:
+    """The iterative projection for Eq. 2 on one BERT-base projection (768 x 768, the Q weight
+    of the BERT-base workload) with the reconstruction loss of 4096 synthetic calibration
+    tokens: GPU time per iteration (product, dense expansion, update, prune), the loss before
+    and after, and the fp64 oracle's time per iteration on this host."""
+    import torch
+    from paper_2106_08846_amd import bsr as B
+    from paper_2106_08846_amd import workloads as G
+    print(f"# row iht {R}x{C}", file=sys.stderr, flush=True)
+    w = G.bert_base_attention()
+    W0 = w.projections[0].W
+    N, K = W0.shape
+    X = G.fused_qkv(R, C, density, tokens=4096).X[0]         # 4096 x 768 activations
+    # H = X^T X by the library's own product (X^T as the input, X^T with all its blocks as the
+    # matrix); the 1/T of the loss is left in the step size (only eta H enters the iteration).
+    XT = torch.from_numpy(np.ascontiguousarray(X.T)).to("cuda:0")
+    full = B.bsr_prune_from_dense(XT, 32, 1, k=(XT.shape[0] // 32) * XT.shape[1])
+    H = B.bsr_spmm(XT, full)
+    del full
+    eta = float(1.0 / torch.linalg.eigvalsh(H.double())[-1])   # the step bound 1/lambda_max
+    k = B.bsr_prune_count(N, K, R, C, density)
+    W0d = torch.from_numpy(W0).to("cuda:0")
+    B.bsr_iht(W0d, H, R, C, k, eta, 2)                       # warm-up
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    M = B.bsr_iht(W0d, H, R, C, k, eta, iters)
+    b.record()
+    torch.cuda.synchronize()
+    total_us = a.elapsed_time(b) * 1e3
+    a.record()
+    B.bsr_iht(W0d, H, R, C, k, eta, 0)
+    b.record()
+    torch.cuda.synchronize()
+    setup_us = a.elapsed_time(b) * 1e3
+    Hd, W064 = H.double(), W0d.double()
+
+    def loss(Wt):
+        E = Wt.double() - W064
+        return float(0.5 * torch.sum((E @ Hd) * E))
+    f0 = loss(B.bsr_to_dense(B.bsr_prune_from_dense(W0d, R, C, k=k)))
+    f1 = loss(B.bsr_to_dense(M))
+    from oracle import iht_oracle as I
+    Hh, W0h = H.double().cpu().numpy(), W0.astype(np.float64)
+    t0 = time.perf_counter()
+    I.iht(W0h, Hh, R, C, k, eta, 2)
+    cpu_ms = (time.perf_counter() - t0) * 1e3 / 3          # three projections, two gradients
+    return {"workload": f"iht_bert_base_768_{R}x{C}_d{int(density * 100)}", "block": f"{R}x{C}",
+            "iterations": iters, "k": k, "eta": eta, "hessian": "X^T X of 4096 tokens",
+            "us_per_iteration": (total_us - setup_us) / iters, "setup_us": setup_us,
+            "loss_one_shot": f0, "loss_after": f1,
+            "cpu_oracle_ms_per_iteration": cpu_ms, "cpu_oracle_threads": "numpy (BLAS) default"}
 
 
 # --------------------------------------------------------------------------- CPU baselines
