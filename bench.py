@@ -611,7 +611,7 @@ VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1),
                (4, 4), (8, 8))
 
 
-def kernel_name(c, bf16: bool, planned: bool = False) -> str:
+def kernel_name(c, bf16: bool, planned: bool = False, persistent: bool = False) -> str:
     """The kernel libbsr's automatic choice launches for this product: the flat-stream kernel
     for 32x1 and 16x1 (its planned form with a plan), the matrix-core tiled kernel for square
     blocks, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
@@ -623,7 +623,8 @@ def kernel_name(c, bf16: bool, planned: bool = False) -> str:
     fits = 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) <= 160 * 1024
     if shape in ((32, 1), (16, 1)) and fits:
         pl = "true" if planned and shape == (32, 1) else "false"
-        return f"spmm_flat_kernel<{c['R']}, {flag}, {pl}>"
+        kern = "spmm_flat_persistent_kernel" if persistent else "spmm_flat_kernel"
+        return f"{kern}<{c['R']}, {flag}, {pl}>"
     if shape in TILED_SHAPES:
         w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
         if fits:
@@ -692,6 +693,11 @@ def main(argv=None) -> int:
     print(f"# timed {args.steps} steps: {ms_per_step:.4f} ms per step", file=sys.stderr,
           flush=True)
 
+    # A launch with more (token tile, slice) items than the GPU's 256 CUs runs the persistent
+    # form of the flat kernel (at least one item per product and tile; the library's automatic
+    # slice count is 1 when tiles alone fill the GPU).
+    per_launch = len(prep.calls) // prep.launches_per_step
+    persistent = per_launch * -(-prep.calls[0]["T"] // 32) > 256
     # Roofline of the product kernel: the timed region's time per launch.  The kernel-event
     # durations of every launch over a few more steps (at least 60 launches) go beside it.
     rounds = max(rotate, -(-60 // prep.launches_per_step))
@@ -700,7 +706,8 @@ def main(argv=None) -> int:
     tr = measured_traffic(wl.name)
     roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
                  "launch_us_source": "timed region / launches per step",
-                 "kernel": " + ".join(dict.fromkeys(kernel_name(c, wl.bf16, prep.planned)
+                 "kernel": " + ".join(dict.fromkeys(kernel_name(c, wl.bf16, prep.planned,
+                                                                persistent)
                                                     for c in prep.calls)),
                  "kernel_event_us": {k: lt[k] for k in ("mean", "median", "p10", "p90", "n")}})
 
