@@ -142,7 +142,8 @@ bsr_status bsr_prune_from_dense_ex(const float *W, int64_t N, int64_t K, int64_t
 bsr_status bsr_spmm_ex(const void *X, bsr_dtype x_dtype, int64_t T, int64_t ldx,
                        const bsr_matrix_t *W, const float *bias, float *Y, int64_t ldy,
                        const bsr_spmm_options_t *opts, void *stream) {
-    bsr_spmm_item_t item{X, x_dtype, T, ldx, W, bias, Y, ldy};
+    bsr_spmm_item_t item{X, BSR_F32, T, ldx, W, bias, Y, ldy};
+    memcpy(&item.x_dtype, &x_dtype, sizeof item.x_dtype);   // any int32 the caller passed
     return bsr_spmm_batched(&item, 1, opts, stream);
 }
 
@@ -200,7 +201,8 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
     for (int32_t i = 0; i < n_items; ++i) {
         const bsr_spmm_item_t &it = items[i];
         bsr_status s =
-            bsr::check_spmm(it.X, int(it.x_dtype), it.T, it.ldx, it.W, it.Y, it.ldy, it.bias);
+            bsr::check_spmm(it.X, bsr::raw_enum(it.x_dtype), it.T, it.ldx, it.W, it.Y, it.ldy,
+                            it.bias);
         if (s != BSR_OK) return s;
         const bsr_plan_t *pl = plans ? plans[i] : nullptr;
         if (pl) {

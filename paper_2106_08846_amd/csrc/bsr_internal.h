@@ -3,10 +3,22 @@
 
 #include <stddef.h>
 #include <stdint.h>
+#include <string.h>
 
 #include "../../include/libbsr.h"
 
 namespace bsr {
+
+// The integer in an enum-typed field or argument a caller passed (a C caller may store any
+// int32 there), read as bytes: loading an enum lvalue that names no enumerator is undefined in
+// C++, so validation reads enums this way before checking them.
+template <class E>
+inline int32_t raw_enum(const E &e) {
+    static_assert(sizeof(E) == sizeof(int32_t), "the ABI's enums are 32-bit");
+    int32_t v;
+    memcpy(&v, &e, sizeof v);
+    return v;
+}
 
 // Workspace layout of the pruning pipeline: fp64 key bits per block, then the source block id
 // of every kept block.  Each region starts on a 256-byte boundary.

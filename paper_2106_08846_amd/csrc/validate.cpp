@@ -80,7 +80,8 @@ bsr_status check_prune_options(const bsr_prune_options_t *opts, int64_t N, int32
 
 bsr_status check_matrix(const bsr_matrix_t *W) {
     if (!W) return BSR_ERR_NULL;
-    if (W->dtype != BSR_F32 && W->dtype != BSR_BF16) return BSR_ERR_ARG;
+    const int32_t dt = raw_enum(W->dtype);
+    if (dt != BSR_F32 && dt != BSR_BF16) return BSR_ERR_ARG;
     if (!tiles(W->n_rows, W->n_cols, W->R, W->C)) return BSR_ERR_SHAPE;
     const int64_t Nb = W->n_rows / W->R, Kb = W->n_cols / W->C;
     if (Nb > kMaxBlocks / Kb) return BSR_ERR_UNSUPPORTED;

@@ -5,10 +5,11 @@ import pytest
 import torch
 
 from oracle import attention_oracle as A
+from oracle import bsr_oracle as O
 from paper_2106_08846_amd import bsr as B
 from paper_2106_08846_amd import workloads as G
 
-from .gpu_common import check_spmm, dev, host, log, prune_on_gpu
+from .gpu_common import check_prune, check_spmm, dev, host, log, oracle_bsr, prune_on_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -114,6 +115,51 @@ def test_attention_block_stage_by_stage(device, R, C, density, batch, seq):
     Qh, Kh, Vh = host(call.Q), host(call.K), host(call.V)
     check_attention(Qh, Kh, Vh, call.ctx, batch, seq, 12)
     check_spmm(host(call.ctx), mats[3], w.projections[3].bias, Y)
+
+
+@pytest.mark.parametrize("R,C,density,batch,seq", [(32, 1, 0.1, 1, 128), (16, 16, 0.2, 2, 64),
+                                                   (32, 1, 0.1, 2, 256)])
+def test_attention_block_end_to_end(device, R, C, density, batch, seq):
+    """The block's output Y against the fp64 oracle's whole block (attention_block) run from X
+    and the pruned weights, with a bound propagated through the stages:
+      * Q, K, V: the product bound dP = 1e-5 S + 1e-6 (A12);
+      * ctx: the kernel's own rounding at its inputs (attention_error_bound at the GPU's Q, K,
+        V), plus the effect of the inputs' error: the scores move by at most
+        D = max_j scale sum_d (dQ |k_jd| + |q_d| dK_jd + dQ dK_jd), so the softmax weights move
+        by a factor within exp(+-2D), and ctx by (e^{2D} - 1) sum_j p_j |v_jd| +
+        e^{2D} sum_j p_j dV_jd;
+      * Y: the product bound at the GPU's ctx plus dctx |Wo|^T."""
+    w, mats, call = _block(R, C, density, batch, seq)
+    Y = call()
+    torch.cuda.synchronize()
+    X = w.X[0].astype(np.float64)
+    for M, prj in zip(mats, w.projections):
+        check_prune(prj.W, R, C, M, M.nnzb)
+    Wd = [O.to_dense(*oracle_bsr(M), 768, 768) for M in mats]
+    bs = [prj.bias for prj in w.projections]
+    Q64, K64, V64, ctx64, Y64 = A.attention_block(X, Wd[0], bs[0], Wd[1], bs[1], Wd[2], bs[2],
+                                                  Wd[3], bs[3], batch, seq, 12)
+    dQ, dK, dV = (1e-5 * O.tolerance_scale(X, Wm) + 1e-6 for Wm in Wd[:3])
+    Qg, Kg, Vg, ctxg = (host(t).astype(np.float64) for t in (call.Q, call.K, call.V, call.ctx))
+    dctx = A.attention_error_bound(Qg, Kg, Vg, batch, seq, 12, 64)
+    scale = 64 ** -0.5
+    for b in range(batch):
+        rows = slice(b * seq, (b + 1) * seq)
+        for h in range(12):
+            cols = slice(h * 64, (h + 1) * 64)
+            q, k, v = Q64[rows, cols], K64[rows, cols], V64[rows, cols]
+            s = scale * (q @ k.T)
+            p = np.exp(s - s.max(axis=1, keepdims=True))
+            p /= p.sum(axis=1, keepdims=True)
+            D = scale * (dQ[rows, cols] @ np.abs(k).T + np.abs(q) @ dK[rows, cols].T
+                         + dQ[rows, cols] @ dK[rows, cols].T)
+            f = np.exp(2 * D.max(axis=1, keepdims=True))
+            dctx[rows, cols] += (f - 1) * (p @ np.abs(v)) + f * (p @ dV[rows, cols])
+    bound = 1e-5 * O.tolerance_scale(ctxg, Wd[3]) + 1e-6 + dctx @ np.abs(Wd[3]).T
+    err = np.abs(host(Y).astype(np.float64) - Y64)
+    log(f"end to end {R}x{C} {batch}x{seq}: worst err/bound {np.max(err / bound):.3g}")
+    assert np.all(np.isfinite(host(Y)))
+    assert np.all(err <= bound)
 
 
 def test_attention_block_graph_replay(device):
