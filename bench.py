@@ -45,6 +45,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+ARITH_SPLIT = 2      # bsr_arith: fp32 data split into three bf16 pieces
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_PEAK_TFLOPS = 157.3       # MI355X fp32 matrix (dense)
 BF16_PEAK_TFLOPS = 2516.6      # MI355X bf16 matrix (dense)
@@ -72,6 +73,9 @@ def parse(argv=None):
                          "workloads that exceed the last-level cache by themselves, else 8)")
     ap.add_argument("--no-plan", action="store_true",
                     help="run the products without per-matrix plans")
+    ap.add_argument("--arith", choices=("native", "split"), default="native",
+                    help="arithmetic of the per-matrix plans: native (fp32 data on fp32 matrix "
+                         "cores) or split (fp32 data as three bf16 pieces on bf16 matrix cores)")
     ap.add_argument("--graph", action="store_true",
                     help="time the step as HIP graph replays instead of direct calls")
     ap.add_argument("--no-rows", action="store_true",
@@ -246,7 +250,7 @@ class Prepared:
     bsr_spmm_batched calls of up to 8 products, `sets` copies of every tensor to rotate through
     (copy s of a launch only touches set s)."""
 
-    def __init__(self, wl, sets: int, slices: int = 0, plans: bool = True):
+    def __init__(self, wl, sets: int, slices: int = 0, plans: bool = True, arith: int = 0):
         import torch
         from paper_2106_08846_amd import bsr as B
         dev = torch.device("cuda:0")
@@ -283,8 +287,9 @@ class Prepared:
                 Y = torch.empty((c["T"], c["N"]), dtype=torch.float32, device=dev)
                 prods.append((xs[c["x_index"]], M, b, Y))
             # Per-matrix plans (prepared once, like the pruning) where the block shape has one.
-            pls = [self._plan(B, p[1]) if plans else None for p in prods]
+            pls = [self._plan(B, p[1], arith) if plans else None for p in prods]
             self.planned = any(pl is not None for pl in pls)
+            self.plan_arith = next((pl.arith for pl in pls if pl is not None), 0)
             groups = [range(i, min(i + 8, len(prods))) for i in range(0, len(prods), 8)]
             self.sets.append([B.SpmmBatchCall([prods[i] for i in g], slices=slices or None,
                                               plans=[pls[i] for i in g]) for g in groups])
@@ -293,10 +298,12 @@ class Prepared:
         torch.cuda.synchronize()
 
     @staticmethod
-    def _plan(B, M):
+    def _plan(B, M, arith: int = 0):
         try:
-            return B.bsr_plan_prepare(M)
+            return B.bsr_plan_prepare(M, arith=arith)
         except B.BSRError as e:
+            if e.status == 9 and arith != 0:   # no split plan for this dtype: the native one
+                return Prepared._plan(B, M, 0)
             if e.status == 9:      # no plan for this block shape
                 return None
             raise
@@ -357,7 +364,10 @@ def roofline(prep, launch_us_mean: float) -> dict:
     """Roofline position of one launch taking launch_us_mean microseconds."""
     flops = prep.flops_step() / prep.launches_per_step
     nbytes = prep.bytes_step() / prep.launches_per_step
-    peak = (BF16_PEAK_TFLOPS if prep.bf16 else FP32_PEAK_TFLOPS) * 1e12
+    # The matrix-core roof of the instructions the products run on: bf16 for bf16 data and
+    # for fp32 data split into bf16 pieces, fp32 otherwise.
+    on_bf16 = prep.bf16 or getattr(prep, "plan_arith", 0) == ARITH_SPLIT
+    peak = (BF16_PEAK_TFLOPS if on_bf16 else FP32_PEAK_TFLOPS) * 1e12
     ai = flops / nbytes
     gbs = nbytes / (launch_us_mean * 1e-6) / 1e9
     tfs = flops / (launch_us_mean * 1e-6) / 1e12
@@ -611,7 +621,8 @@ VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1),
                (4, 4), (8, 8))
 
 
-def kernel_name(c, bf16: bool, planned: bool = False, persistent: bool = False) -> str:
+def kernel_name(c, bf16: bool, planned: bool = False, persistent: bool = False,
+                plan_arith: int = 1) -> str:
     """The kernel libbsr's automatic choice launches for this product: the flat-stream kernel
     for 32x1 and 16x1 (its planned form with a plan), the matrix-core tiled kernel for square
     blocks, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
@@ -622,7 +633,7 @@ def kernel_name(c, bf16: bool, planned: bool = False, persistent: bool = False) 
     xb = 2 if bf16 and shape != (16, 1) else 4
     fits = 32 * (c["K"] + 8) * xb + 4 * c["N"] + 4 * (c["N"] // c["R"] + 8) <= 160 * 1024
     if shape in ((32, 1), (16, 1)) and fits:
-        pl = "true" if planned and shape == (32, 1) else "false"
+        pl = (2 if plan_arith == 2 else 1) if planned and shape == (32, 1) else 0
         kern = "spmm_flat_persistent_kernel" if persistent else "spmm_flat_kernel"
         return f"{kern}<{c['R']}, {flag}, {pl}>"
     if shape in TILED_SHAPES:
@@ -660,7 +671,8 @@ def main(argv=None) -> int:
     rotate = args.rotate or (1 if args.workload.startswith("bert_large") else ROTATE_SETS)
     print(f"# workload {wl.name}: {len(wl.projections)} projections, {rotate} set(s)",
           file=sys.stderr, flush=True)
-    prep = Prepared(wl, rotate, args.slices, plans=not args.no_plan)
+    arith = ARITH_SPLIT if args.arith == "split" else 0
+    prep = Prepared(wl, rotate, args.slices, plans=not args.no_plan, arith=arith)
     for i in range(args.warmup):
         prep.step(i % rotate)
     torch.cuda.synchronize()
@@ -707,7 +719,7 @@ def main(argv=None) -> int:
     roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
                  "launch_us_source": "timed region / launches per step",
                  "kernel": " + ".join(dict.fromkeys(kernel_name(c, wl.bf16, prep.planned,
-                                                                persistent)
+                                                                persistent, prep.plan_arith)
                                                     for c in prep.calls)),
                  "kernel_event_us": {k: lt[k] for k in ("mean", "median", "p10", "p90", "n")}})
 
@@ -726,7 +738,9 @@ def main(argv=None) -> int:
                    "nnz_per_call": [c["k"] * c["R"] * c["C"] for c in prep.calls][:8],
                    "timing": "hip_graph_replay" if args.graph else "direct_calls",
                    "rotating_sets": rotate, "slices": args.slices or "auto",
-                   "plans": prep.planned},
+                   "plans": prep.planned,
+                   "plan_arithmetic": ({1: "native", 2: "bf16x3 split"}[prep.plan_arith]
+                                       if prep.planned else None)},
         "step_ms": {k: st[k] for k in ("median", "p10", "p90", "n")},
         "roofline": roof,
     }

@@ -272,6 +272,28 @@ LIBBSR_API bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_i
                                        const bsr_spmm_options_t *opts, void *stream);
 
 /*
+ * The arithmetic of a planned product (fixed when the plan is prepared).
+ *   BSR_ARITH_AUTO:   BSR_ARITH_NATIVE.
+ *   BSR_ARITH_NATIVE: products in the data's own type on the matrix cores (fp32 data on fp32
+ *                     MFMA, bf16 data on bf16 MFMA), fp32 accumulate; Y is bit-identical to
+ *                     the same product without a plan.
+ *   BSR_ARITH_BF16X3: fp32 data only (32x1 blocks): every fp32 operand x is the sum of three
+ *                     bf16 pieces x0 + x1 + x2 (x0 = x with its low 16 bits cleared, x1 the
+ *                     same of the remainder, x2 what is left; |x1| < 2^-7 |x|,
+ *                     |x2| < 2^-14 |x|), exact for |x| >= 2^-103 (below that the last piece
+ *                     drops bits under 2^-126).  Each product x w is formed from the six
+ *                     cross terms xi wj with i + j <= 2, each exact in fp32, on bf16 MFMA
+ *                     with fp32 accumulate; the three terms left out are below 2^-20 |x w|.
+ *                     Y therefore meets the same accuracy bound as fp32 arithmetic
+ *                     (|err| <= 1e-5 sum |x||w| + 1e-6 in the tests), in a different
+ *                     summation order (not bit-identical to NATIVE).  Integer-valued inputs
+ *                     with |x|, |w| < 256 are their own first pieces, so integer results stay
+ *                     exact.  Non-finite inputs: an infinite x or w gives NaN where fp32
+ *                     arithmetic gives an infinity.
+ */
+typedef enum { BSR_ARITH_AUTO = 0, BSR_ARITH_NATIVE = 1, BSR_ARITH_BF16X3 = 2 } bsr_arith;
+
+/*
  * A per-matrix product plan: the work of a BSR product that depends only on the matrix,
  * prepared once and reused by every product with that matrix (the paper's compiler keeps a
  * buffer of sparse operators and reuses tasks whose sparse structure is identical, Sec. 2.2,
@@ -280,10 +302,11 @@ LIBBSR_API bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_i
  *   - uptr int32[N/R + 1]: the first unit of every block-row (a row pointer over units);
  *   - the units' block columns and weights, packed in the order the matrix cores consume them,
  *     so one 16-byte load per lane fetches a unit's operands;
- * in caller-owned device memory.  A product with a plan computes the same sums in the same
- * order as the product without one (bit-identical Y); it only reads its operands faster.
- * Plans exist for 32x1 blocks (fp32 and bf16 data); bsr_plan_bytes reports
- * BSR_ERR_UNSUPPORTED for other shapes.
+ * in caller-owned device memory.  A plan of BSR_ARITH_NATIVE arithmetic computes the same sums
+ * in the same order as the product without one (bit-identical Y); it only reads its operands
+ * faster.  A plan of BSR_ARITH_BF16X3 stores every weight as its three bf16 pieces and forms
+ * the products as described at bsr_arith.  Plans exist for 32x1 blocks (fp32 and bf16 data);
+ * bsr_plan_bytes reports BSR_ERR_UNSUPPORTED for other shapes.
  * The struct is filled by bsr_plan_prepare and read by the planned products; it records the
  * matrix it was prepared for, and a product whose matrix differs (shape, block shape, dtype,
  * nnzb or array addresses) is rejected with BSR_ERR_ARG.  The plan's memory must stay
@@ -307,12 +330,18 @@ typedef struct {
     int64_t uptr_offset;      /* byte offsets into mem of the three arrays                     */
     int64_t col_offset;
     int64_t val_offset;
+    int32_t arith;            /* the plan's arithmetic, resolved: BSR_ARITH_NATIVE or _BF16X3  */
 } bsr_plan_t;
 
 /* Device bytes a plan for W needs (host only).  Errors: BSR_ERR_NULL, those of a malformed
  * descriptor (BSR_ERR_SHAPE, BSR_ERR_ARG), BSR_ERR_UNSUPPORTED (no planned kernel for the
  * block shape, or sizes past int32 offsets). */
 LIBBSR_API bsr_status bsr_plan_bytes(const bsr_matrix_t *W, size_t *bytes);
+
+/* bsr_plan_bytes for a plan of the given arithmetic (a bsr_arith value; bsr_plan_bytes is
+ * BSR_ARITH_AUTO).  Extra errors: BSR_ERR_ARG (unknown arithmetic), BSR_ERR_UNSUPPORTED
+ * (BSR_ARITH_BF16X3 with bf16 data, or with more than 16383 block columns). */
+LIBBSR_API bsr_status bsr_plan_bytes_ex(const bsr_matrix_t *W, int32_t arith, size_t *bytes);
 
 /*
  * Prepare the plan of W in `mem` (device, caller-owned, at least bsr_plan_bytes(W) bytes, not
@@ -324,11 +353,18 @@ LIBBSR_API bsr_status bsr_plan_bytes(const bsr_matrix_t *W, size_t *bytes);
 LIBBSR_API bsr_status bsr_plan_prepare(const bsr_matrix_t *W, void *mem, size_t bytes,
                                        bsr_plan_t *plan, void *stream);
 
+/* bsr_plan_prepare with the plan's arithmetic (a bsr_arith value; bsr_plan_prepare is
+ * BSR_ARITH_AUTO), recorded in plan->arith.  Errors: those of bsr_plan_bytes_ex and of
+ * bsr_plan_prepare. */
+LIBBSR_API bsr_status bsr_plan_prepare_ex(const bsr_matrix_t *W, int32_t arith, void *mem,
+                                          size_t bytes, bsr_plan_t *plan, void *stream);
+
 /*
  * bsr_spmm_batched with a plan per product (plans may be NULL, or plans[i] NULL for a product
- * without one).  A planned product runs on the planned form of the matrix-core kernel and
- * gives the same Y, bit for bit, as the same call without plans.  Products with and without
- * plans never share a launch.  Errors: those of bsr_spmm_batched, and BSR_ERR_ARG for a plan
+ * without one).  A planned product runs on the planned form of the matrix-core kernel in its
+ * plan's arithmetic: with BSR_ARITH_NATIVE it gives the same Y, bit for bit, as the same call
+ * without plans.  Products with and without plans, or with plans of different arithmetic,
+ * never share a launch.  Errors: those of bsr_spmm_batched, and BSR_ERR_ARG for a plan
  * that does not describe its product's matrix or whose memory overlaps a Y.
  */
 LIBBSR_API bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items,

@@ -24,12 +24,15 @@ STATUS = {0: "BSR_OK", 1: "BSR_ERR_NULL", 2: "BSR_ERR_SHAPE", 3: "BSR_ERR_ARG",
 EXPORTS = ["bsr_prune_count", "bsr_prune_count_ex", "bsr_prune_workspace_bytes",
            "bsr_prune_from_dense", "bsr_prune_from_dense_noalloc", "bsr_prune_from_dense_ex",
            "bsr_spmm", "bsr_spmm_ex",
-           "bsr_spmm_batched", "bsr_plan_bytes", "bsr_plan_prepare", "bsr_spmm_batched_planned", "bsr_attention", "bsr_reblock", "bsr_to_dense",
+           "bsr_spmm_batched", "bsr_plan_bytes", "bsr_plan_bytes_ex", "bsr_plan_prepare",
+           "bsr_plan_prepare_ex", "bsr_spmm_batched_planned", "bsr_attention", "bsr_reblock",
+           "bsr_to_dense",
            "bsr_cast_f32_bf16", "bsr_iht_update",
            "bsr_status_str", "bsr_last_hip_error"]
 NORM_L2, NORM_L1 = 0, 1
 SELECT_GLOBAL, SELECT_PER_ROW = 0, 1
 KERNEL_AUTO, KERNEL_GENERIC, KERNEL_TILED, KERNEL_VALU = 0, 1, 2, 3
+ARITH_AUTO, ARITH_NATIVE, ARITH_BF16X3 = 0, 1, 2
 
 
 class BSRError(RuntimeError):
@@ -71,7 +74,8 @@ class bsr_plan_t(ctypes.Structure):
                 ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p),
                 ("data", ctypes.c_void_p), ("unit_blocks", ctypes.c_int32),
                 ("max_units", ctypes.c_int64), ("uptr_offset", ctypes.c_int64),
-                ("col_offset", ctypes.c_int64), ("val_offset", ctypes.c_int64)]
+                ("col_offset", ctypes.c_int64), ("val_offset", ctypes.c_int64),
+                ("arith", ctypes.c_int32)]
 
 
 _LIB = None
@@ -118,6 +122,11 @@ def _lib() -> ctypes.CDLL:
         lib.bsr_plan_prepare.argtypes = [ctypes.POINTER(bsr_matrix_t), p, sz,
                                          ctypes.POINTER(bsr_plan_t), p]
         lib.bsr_plan_prepare.restype = st
+        lib.bsr_plan_bytes_ex.argtypes = [ctypes.POINTER(bsr_matrix_t), i32, ctypes.POINTER(sz)]
+        lib.bsr_plan_bytes_ex.restype = st
+        lib.bsr_plan_prepare_ex.argtypes = [ctypes.POINTER(bsr_matrix_t), i32, p, sz,
+                                            ctypes.POINTER(bsr_plan_t), p]
+        lib.bsr_plan_prepare_ex.restype = st
         lib.bsr_spmm_batched_planned.argtypes = [ctypes.POINTER(bsr_spmm_item_t),
                                                  ctypes.POINTER(ctypes.POINTER(bsr_plan_t)), i32,
                                                  ctypes.POINTER(bsr_spmm_options_t), p]
@@ -392,6 +401,11 @@ class BSRPlan:
     def unit_blocks(self) -> int:
         return self.struct.unit_blocks
 
+    @property
+    def arith(self) -> int:
+        """The plan's arithmetic: ARITH_NATIVE or ARITH_BF16X3."""
+        return self.struct.arith
+
     def uptr(self) -> torch.Tensor:
         """The unit row pointer (a view into the plan's memory)."""
         nb = self.W.n_rows // self.W.R + 1
@@ -399,18 +413,21 @@ class BSRPlan:
         return self.mem[off:off + 4 * nb].view(torch.int32)
 
 
-def bsr_plan_bytes(W: BSRMatrix) -> int:
-    """Device bytes of W's plan (raises BSRError BSR_ERR_UNSUPPORTED for shapes without one)."""
+def bsr_plan_bytes(W: BSRMatrix, arith: int = ARITH_AUTO) -> int:
+    """Device bytes of W's plan of the given arithmetic (bsr_plan_bytes_ex; raises BSRError
+    BSR_ERR_UNSUPPORTED for shapes without one)."""
     n = ctypes.c_size_t(0)
     m = W.struct()
-    _check(_lib().bsr_plan_bytes(ctypes.byref(m), ctypes.byref(n)), "bsr_plan_bytes")
+    _check(_lib().bsr_plan_bytes_ex(ctypes.byref(m), int(arith), ctypes.byref(n)),
+           "bsr_plan_bytes_ex")
     return int(n.value)
 
 
-def bsr_plan_prepare(W: BSRMatrix, mem: torch.Tensor | None = None, stream=None) -> BSRPlan:
-    """Prepare W's plan in `mem` (a uint8 device tensor of at least bsr_plan_bytes(W) bytes,
-    allocated here when None)."""
-    nbytes = bsr_plan_bytes(W)
+def bsr_plan_prepare(W: BSRMatrix, mem: torch.Tensor | None = None, stream=None,
+                     arith: int = ARITH_AUTO) -> BSRPlan:
+    """Prepare W's plan of the given arithmetic (bsr_plan_prepare_ex) in `mem` (a uint8
+    device tensor of at least bsr_plan_bytes(W, arith) bytes, allocated here when None)."""
+    nbytes = bsr_plan_bytes(W, arith)
     if mem is None:
         mem = torch.empty(nbytes, dtype=torch.uint8, device=W.indptr.device)
     _require_cuda(mem, "mem", torch.uint8)
@@ -418,8 +435,9 @@ def bsr_plan_prepare(W: BSRMatrix, mem: torch.Tensor | None = None, stream=None)
         raise ValueError("mem must be contiguous")
     plan = bsr_plan_t()
     m = W.struct()
-    _check(_lib().bsr_plan_prepare(ctypes.byref(m), _ptr(mem), mem.numel(), ctypes.byref(plan),
-                                   _stream(stream)), "bsr_plan_prepare")
+    _check(_lib().bsr_plan_prepare_ex(ctypes.byref(m), int(arith), _ptr(mem), mem.numel(),
+                                      ctypes.byref(plan), _stream(stream)),
+           "bsr_plan_prepare_ex")
     return BSRPlan(W, mem, plan)
 
 

@@ -152,23 +152,28 @@ bsr_status bsr_spmm_batched(const bsr_spmm_item_t *items, int32_t n_items,
     return bsr_spmm_batched_planned(items, nullptr, n_items, opts, stream);
 }
 
-bsr_status bsr_plan_bytes(const bsr_matrix_t *W, size_t *bytes) {
+bsr_status bsr_plan_bytes_ex(const bsr_matrix_t *W, int32_t arith, size_t *bytes) {
     if (!W || !bytes) return BSR_ERR_NULL;
     bsr_status s = bsr::check_matrix(W);
     if (s != BSR_OK) return s;
-    const bsr::PlanLayout L = bsr::plan_layout(W);
+    if (bsr::resolve_arith(W->dtype, arith) < 0) return BSR_ERR_ARG;
+    const bsr::PlanLayout L = bsr::plan_layout(W, arith);
     if (L.unit_blocks == 0 || L.max_units * 64 >= (int64_t(1) << 31)) return BSR_ERR_UNSUPPORTED;
     *bytes = size_t(L.total);
     return BSR_OK;
 }
 
-bsr_status bsr_plan_prepare(const bsr_matrix_t *W, void *mem, size_t bytes, bsr_plan_t *plan,
-                            void *stream) {
+bsr_status bsr_plan_bytes(const bsr_matrix_t *W, size_t *bytes) {
+    return bsr_plan_bytes_ex(W, BSR_ARITH_AUTO, bytes);
+}
+
+bsr_status bsr_plan_prepare_ex(const bsr_matrix_t *W, int32_t arith, void *mem, size_t bytes,
+                               bsr_plan_t *plan, void *stream) {
     size_t need = 0;
-    bsr_status s = bsr_plan_bytes(W, &need);
+    bsr_status s = bsr_plan_bytes_ex(W, arith, &need);
     if (s != BSR_OK) return s;
     if (!plan) return BSR_ERR_NULL;
-    const bsr::PlanLayout L = bsr::plan_layout(W);
+    const bsr::PlanLayout L = bsr::plan_layout(W, arith);
     if ((s = bsr::check_plan_prepare(W, mem, bytes, L.total)) != BSR_OK) return s;
     if ((s = bsr::ensure_device()) != BSR_OK) return s;
     if ((s = bsr::launch_plan_prepare(W, mem, L, stream)) != BSR_OK) return s;
@@ -189,8 +194,14 @@ bsr_status bsr_plan_prepare(const bsr_matrix_t *W, void *mem, size_t bytes, bsr_
     p.uptr_offset = L.uptr_offset;
     p.col_offset = L.col_offset;
     p.val_offset = L.val_offset;
+    p.arith = L.arith;
     *plan = p;
     return BSR_OK;
+}
+
+bsr_status bsr_plan_prepare(const bsr_matrix_t *W, void *mem, size_t bytes, bsr_plan_t *plan,
+                            void *stream) {
+    return bsr_plan_prepare_ex(W, BSR_ARITH_AUTO, mem, bytes, plan, stream);
 }
 
 bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan_t *const *plans,
@@ -206,7 +217,10 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
         if (s != BSR_OK) return s;
         const bsr_plan_t *pl = plans ? plans[i] : nullptr;
         if (pl) {
-            const bsr::PlanLayout L = bsr::plan_layout(it.W);
+            // The plan's recorded arithmetic must name one (a plan struct filled by hand may
+            // hold anything) and its layout must be the one bsr_plan_prepare_ex writes.
+            if (pl->arith != BSR_ARITH_NATIVE && pl->arith != BSR_ARITH_BF16X3) return BSR_ERR_ARG;
+            const bsr::PlanLayout L = bsr::plan_layout(it.W, pl->arith);
             if (L.unit_blocks == 0 || pl->unit_blocks != L.unit_blocks ||
                 pl->max_units != L.max_units || pl->uptr_offset != L.uptr_offset ||
                 pl->col_offset != L.col_offset || pl->val_offset != L.val_offset)
@@ -291,7 +305,8 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
             if (items[work[v]].W->R != items[work[w]].W->R ||
                 items[work[v]].W->C != items[work[w]].W->C ||
                 items[work[v]].W->dtype != items[work[w]].W->dtype ||
-                (plan_of[v] != nullptr) != (plan_of[w] != nullptr))
+                (plan_of[v] != nullptr) != (plan_of[w] != nullptr) ||
+                (plan_of[v] && plan_of[v]->arith != plan_of[w]->arith))
                 continue;
             l.members.push_back(int(v));
             done[v] = 1;
@@ -335,6 +350,7 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
                 tiled[w].plan_col_offset = pl->col_offset;
                 tiled[w].plan_val_offset = pl->val_offset;
                 tiled[w].plan_max_units = pl->max_units;
+                tiled[w].plan_arith = pl->arith;
             }
         }
     }

@@ -34,9 +34,37 @@ namespace bsr {
 namespace {
 
 constexpr int kNW = 16;            // waves per workgroup
-constexpr int kDepth = 3;          // units in flight ahead of the one being multiplied
-constexpr int kRing = kDepth + 1;  // operand buffers per wave
-constexpr int kXChunksPersistent = 16;  // 64-column X chunks a persistent workgroup prefetches
+// Units in flight ahead of the one being multiplied, per operand source (a split unit holds
+// 16 blocks and six MFMAs, and its operands take 16 registers per lane), and the operand
+// buffers per wave.
+template <int PK>
+constexpr int kDepthOf = PK == 2 ? 2 : 3;
+template <int PK>
+constexpr int kRingOf = kDepthOf<PK> + 1;
+// 64-column X chunks a persistent workgroup prefetches per row (fewer for split units, whose
+// operands need more registers).
+template <int PK>
+constexpr int kXChunksPersistent = PK == 2 ? 8 : 16;
+
+// A slice's units are shared out over the 16 waves by weights that depend on a wave's place
+// among the four waves of its SIMD (wave w runs on SIMD w % 4, after waves w - 4, w - 8, ...).
+// The SIMDs' instruction arbitration favours older waves: with equal shares the first wave of
+// every SIMD finished its stream about 30% before the last (per-wave timestamps on MI355X, the
+// BERT-large 32x1 stack), and the item waits for the last.  Weights 48:38:31:27 made that
+// launch 2% faster than equal shares (same box, A/B).  Start of wave l's units (l = 16: the end
+// of the range).
+constexpr unsigned kShareWeight[4] = {48, 38, 31, 27};
+constexpr unsigned kShareTotal = 4 * (kShareWeight[0] + kShareWeight[1] + kShareWeight[2] +
+                                      kShareWeight[3]);
+__device__ __forceinline__ int wave_start(int64_t Q0, unsigned span, unsigned l) {
+    const unsigned a = l >> 2, b = l & 3;
+    unsigned cum = 0;
+#pragma unroll
+    for (unsigned i = 0; i < 4; ++i) cum += i < a ? 4 * kShareWeight[i] : 0u;
+#pragma unroll
+    for (unsigned i = 0; i < 4; ++i) cum += i == a ? b * kShareWeight[i] : 0u;
+    return int(Q0) + int(uint64_t(span) * cum / kShareTotal);
+}
 
 // Inclusive prefix sum over the 64 lanes of a wave: row shifts by 1, 2, 4 and 8 lanes sum each
 // row of 16 lanes, then the last lane of row 0 is added to row 1 and of row 2 to row 3, and
@@ -71,11 +99,18 @@ struct FlatItem {
     TileOut out;
 };
 
-template <int R, bool BF, bool PL, class Ops, class Fetch>
-__device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[kRing],
-                                               int (&nvr)[kRing], Fetch &&fetch) {
+// The operand source of a unit: the BSR arrays (PK = 0), a native plan (1) or a split plan (2).
+template <int R, bool BF, int PK>
+using SrcOf = std::conditional_t<
+    PK == 2, SplitPlanUnit, std::conditional_t<PK == 1, PlanUnit<R, 1, BF>, Unit<R, 1, BF>>>;
+
+template <int R, bool BF, int PK, class Ops, class Fetch>
+__device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[kRingOf<PK>],
+                                               int (&nvr)[kRingOf<PK>], Fetch &&fetch) {
     using U = Unit<R, 1, BF>;
-    using Src = std::conditional_t<PL, PlanUnit<R, 1, BF>, U>;
+    using Src = SrcOf<R, BF, PK>;
+    constexpr bool PL = PK != 0;
+    constexpr int kDepth = kDepthOf<PK>, kRing = kRingOf<PK>;
     constexpr int NW = kNW, KB = U::KB;
     const int lane = it.lane, wave = it.wave, Pw = it.Pw, Pw1 = it.Pw1, rlo = it.rlo,
               rhi = it.rhi, XP = it.XP, Kb = it.Kb, ws = it.ws, wsn = it.wsn;
@@ -211,10 +246,12 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
     }
 }
 
-template <int R, bool BF, bool PL>
+template <int R, bool BF, int PK>
 __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch batch) {
     using U = Unit<R, 1, BF>;
-    using Src = std::conditional_t<PL, PlanUnit<R, 1, BF>, U>;
+    using Src = SrcOf<R, BF, PK>;
+    constexpr bool PL = PK != 0;
+    constexpr int kDepth = kDepthOf<PK>, kRing = kRingOf<PK>;
     using Ops = typename Src::Ops;
     constexpr int NW = kNW, KB = U::KB, kThreads = NW * 64;
     extern __shared__ float smem[];
@@ -366,11 +403,10 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
     int row_lo, row_hi, Pw, Pw1, rlo, rhi, head_end, row, p, end;
     int ws = 0, wsn = 0;   // wave starts, one per lane: wave `lane` and wave lane + 1
     auto share = [&](auto lower_bound) {
-        static_assert(NW == 16, "wave starts use a division by 16");
-        const unsigned span = unsigned(Q1 - Q0), hi = span >> 4, lo = span & 15u;
-        const unsigned l0 = unsigned(lane), l1 = l0 + 1;
-        ws = int(Q0) + int(hi * l0 + ((lo * l0) >> 4));
-        wsn = int(Q0) + int(hi * l1 + ((lo * l1) >> 4));
+        static_assert(NW == 16, "wave starts are weighted for 16 waves");
+        const unsigned span = unsigned(Q1 - Q0);
+        ws = wave_start(Q0, span, unsigned(lane));
+        wsn = wave_start(Q0, span, unsigned(lane) + 1);
         Pw = __builtin_amdgcn_readlane(ws, wave);
         Pw1 = __builtin_amdgcn_readlane(wsn, wave);
         rlo = (wave == 0) ? row_lo : lower_bound(int64_t(Pw));
@@ -601,7 +637,7 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
                 XP, Kb, reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048, TileOut{}};
     fi.out.ldy4 = int(ldy) * 4;
     fi.out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(fi.out.ldy4));
-    flat_item_body<R, BF, PL>(fi, ring, nvr, [&](Ops &o, int &nv, int uu) {
+    flat_item_body<R, BF, PK>(fi, ring, nvr, [&](Ops &o, int &nv, int uu) {
         fetch(o, nv, uu, read_up_lds, read_ib_lds);
     });
 }
@@ -613,10 +649,12 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
 // first units' loads, and after one barrier loads the next item's X rows into registers and
 // runs the shared stream and combine.  Items of one workgroup share an XCD, as in the one-item
 // kernel's mapping.
-template <int R, bool BF, bool PL>
+template <int R, bool BF, int PK>
 __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const TiledBatch batch) {
     using U = Unit<R, 1, BF>;
-    using Src = std::conditional_t<PL, PlanUnit<R, 1, BF>, U>;
+    using Src = SrcOf<R, BF, PK>;
+    constexpr bool PL = PK != 0;
+    constexpr int kDepth = kDepthOf<PK>, kRing = kRingOf<PK>;
     using Ops = typename Src::Ops;
     constexpr int NW = kNW, KB = U::KB, kThreads = NW * 64;
     extern __shared__ float smem[];
@@ -652,7 +690,7 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
 
     constexpr int kXBytes = BF ? 2 : 4;
     constexpr int kRowsPerWave = kTT / NW;
-    constexpr int kXC = kXChunksPersistent;
+    constexpr int kXC = kXChunksPersistent<PK>;
     static_assert(kTT % NW == 0, "every wave stages the same number of rows");
 
     // X rows w + 16 r of a tile in registers, kXC 64-column chunks from column c0.  Rows past
@@ -778,10 +816,10 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
         const int64_t Q0 = uniform(s_up[row_lo]);
         int64_t Q1 = uniform(s_up[row_hi]);
         if (Q1 < Q0) Q1 = Q0;
-        static_assert(NW == 16, "wave starts use a division by 16");
-        const unsigned span = unsigned(Q1 - Q0), hi = span >> 4, lo = span & 15u;
-        const int ws = int(Q0) + int(hi * unsigned(lane) + ((lo * unsigned(lane)) >> 4));
-        const int wsn = int(Q0) + int(hi * unsigned(lane + 1) + ((lo * unsigned(lane + 1)) >> 4));
+        static_assert(NW == 16, "wave starts are weighted for 16 waves");
+        const unsigned span = unsigned(Q1 - Q0);
+        const int ws = wave_start(Q0, span, unsigned(lane));
+        const int wsn = wave_start(Q0, span, unsigned(lane) + 1);
         const int Pw = __builtin_amdgcn_readlane(ws, wave);
         const int Pw1 = __builtin_amdgcn_readlane(wsn, wave);
         int rlo = (wave == 0) ? row_lo : uniform(wave_lower_bound(s_up, Nb, int64_t(Pw)));
@@ -860,18 +898,18 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
             rows = rowsn;
             s = sn;
         }
-        flat_item_body<R, BF, PL>(fi, ring, nvr, fetch);
+        flat_item_body<R, BF, PK>(fi, ring, nvr, fetch);
     }
 }
 
-template <int R, bool BF, bool PL>
+template <int R, bool BF, int PK>
 bsr_status launch_flat_variant(const TiledBatch &batch, dim3 grid, size_t lds, bool persistent,
                                hipStream_t st, const LaunchEvents &ev) {
     if (persistent)
-        launch_kernel(spmm_flat_persistent_kernel<R, BF, PL>, grid, dim3(kNW * 64), lds, st, ev,
+        launch_kernel(spmm_flat_persistent_kernel<R, BF, PK>, grid, dim3(kNW * 64), lds, st, ev,
                       batch);
     else
-        launch_kernel(spmm_flat_kernel<R, BF, PL>, grid, dim3(kNW * 64), lds, st, ev, batch);
+        launch_kernel(spmm_flat_kernel<R, BF, PK>, grid, dim3(kNW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
@@ -881,8 +919,16 @@ bool flat_supported(int R, int C, int dtype) {
     return (dtype == BSR_F32 || dtype == BSR_BF16) && C == 1 && (R == 32 || R == 16);
 }
 
-bool plan_supported(int R, int C, int dtype) {
-    return (dtype == BSR_F32 || dtype == BSR_BF16) && C == 1 && R == 32;
+int resolve_arith(int dtype, int arith) {
+    if (arith == BSR_ARITH_AUTO) return BSR_ARITH_NATIVE;
+    if (arith == BSR_ARITH_NATIVE || arith == BSR_ARITH_BF16X3) return arith;
+    return -1;
+}
+
+bool plan_supported(int R, int C, int dtype, int arith) {
+    const int a = resolve_arith(dtype, arith);
+    if (a < 0 || (dtype != BSR_F32 && dtype != BSR_BF16) || C != 1 || R != 32) return false;
+    return a == BSR_ARITH_NATIVE || dtype == BSR_F32;
 }
 
 int flat_unit_blocks(int R, int C, int dtype) {
@@ -949,15 +995,22 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
     }
     hipStream_t st = as_stream(stream);
     const dim3 grid(gx, n);
+    const bool split = planned && work[0].plan_arith == BSR_ARITH_BF16X3;
+    for (int i = 0; i < n; ++i)
+        if (planned && (work[i].plan_arith == BSR_ARITH_BF16X3) != split) return BSR_ERR_ARG;
     if (R == 32) {
-        if (bf) return planned ? launch_flat_variant<32, true, true>(batch, grid, lds, persistent, st, ev)
-                               : launch_flat_variant<32, true, false>(batch, grid, lds, persistent, st, ev);
-        return planned ? launch_flat_variant<32, false, true>(batch, grid, lds, persistent, st, ev)
-                       : launch_flat_variant<32, false, false>(batch, grid, lds, persistent, st, ev);
+        if (bf) {
+            if (split) return BSR_ERR_UNSUPPORTED;
+            return planned ? launch_flat_variant<32, true, 1>(batch, grid, lds, persistent, st, ev)
+                           : launch_flat_variant<32, true, 0>(batch, grid, lds, persistent, st, ev);
+        }
+        if (split) return launch_flat_variant<32, false, 2>(batch, grid, lds, persistent, st, ev);
+        return planned ? launch_flat_variant<32, false, 1>(batch, grid, lds, persistent, st, ev)
+                       : launch_flat_variant<32, false, 0>(batch, grid, lds, persistent, st, ev);
     }
     if (planned) return BSR_ERR_UNSUPPORTED;
-    if (bf) return launch_flat_variant<16, true, false>(batch, grid, lds, persistent, st, ev);
-    return launch_flat_variant<16, false, false>(batch, grid, lds, persistent, st, ev);
+    if (bf) return launch_flat_variant<16, true, 0>(batch, grid, lds, persistent, st, ev);
+    return launch_flat_variant<16, false, 0>(batch, grid, lds, persistent, st, ev);
 }
 
 }  // namespace bsr

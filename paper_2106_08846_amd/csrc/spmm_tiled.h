@@ -64,6 +64,7 @@ struct TiledWork {
     int64_t ldy;
     const void *plan_mem = nullptr;
     int64_t plan_uptr_offset = 0, plan_col_offset = 0, plan_val_offset = 0, plan_max_units = 0;
+    int plan_arith = 0;   // with a plan: BSR_ARITH_NATIVE or BSR_ARITH_BF16X3
 };
 
 // The device-side view of one product, passed by value in the kernel arguments.
@@ -101,9 +102,13 @@ bsr_status launch_spmm_tiled(const TiledWork *work, int n, void *stream, const L
 
 // The flat-stream kernel for linear R x 1 blocks (32x1, 16x1): same plan and batch structures
 // as the tiled kernel; `planned` launches read per-matrix plans (32x1 only), and every product
-// of one launch has a plan or none has.
+// of one launch has a plan of the same arithmetic or none has.
 bool flat_supported(int R, int C, int dtype);
-bool plan_supported(int R, int C, int dtype);
+// The resolved arithmetic of a plan request (BSR_ARITH_AUTO -> BSR_ARITH_NATIVE), or -1 for a
+// value that names no arithmetic.
+int resolve_arith(int dtype, int arith);
+// Whether a plan of this arithmetic exists for the block shape and dtype.
+bool plan_supported(int R, int C, int dtype, int arith);
 int flat_unit_blocks(int R, int C, int dtype);   // blocks per unit (0 if unsupported)
 bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *stream,
                             const LaunchEvents &ev);
@@ -111,10 +116,11 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
 // Per-matrix plans: layout and the preparing kernels (plan.hip).
 struct PlanLayout {
     int unit_blocks = 0;
+    int arith = 0;   // resolved
     int64_t max_units = 0;
     int64_t uptr_offset = 0, col_offset = 0, val_offset = 0, total = 0;
 };
-PlanLayout plan_layout(const bsr_matrix_t *W);   // unit_blocks = 0 when unsupported
+PlanLayout plan_layout(const bsr_matrix_t *W, int arith);   // unit_blocks = 0 when unsupported
 bsr_status launch_plan_prepare(const bsr_matrix_t *W, void *mem, const PlanLayout &L,
                                void *stream);
 

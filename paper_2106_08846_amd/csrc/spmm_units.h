@@ -437,6 +437,87 @@ struct PlanUnit<32, 1, true> {
     }
 };
 
+// fp32 32x1 blocks on the bf16 matrix cores, each operand split into three bf16 pieces
+// (a plan of arithmetic BSR_ARITH_BF16X3).  A finite fp32 value v is the exact sum
+// v0 + v1 + v2 of three bf16 values: v0 = v with its low 16 bits cleared, r = v - v0 (exact),
+// v1 = r with its low 16 bits cleared, v2 = r - v1 (exact, at most 8 significant bits), so
+// |v1| < 2^-7 |v| and |v2| < 2^-14 |v|.  Of the nine cross terms of x * w the six with
+// i + j <= 2 are formed (each product of two bf16 values is exact in fp32) and the three left
+// out sum to less than 2^-20 |x w|.  The six v_mfma_f32_32x32x16_bf16 run smallest first into
+// the one fp32 accumulator.
+// Unit = 16 blocks; lane l supplies k-slots 8(l/32) .. +7, i.e. blocks 8(l/32) + e, for token
+// l%32 (A: gathered from the row-major fp32 X tile, split in registers) and feature l%32 (B).
+// Columns: cols[u][h][e] = 4 * column of block 8h + e as uint16 byte offsets into a row of the
+// fp32 tile (column clamped to [0, Kb]; 32 bytes per unit, one 16-byte load per lane).
+// Weights: vals[u][p][l][e] = piece p of block 8(l/32) + e, feature l%32 (three planes of
+// 1 KB per unit, each exactly a B operand).
+struct SplitPlanUnit {
+    using Base = Unit<32, 1, false>;
+    static constexpr int KB = 16;
+    static constexpr int kColBytes = 32;
+    static constexpr int kValBytes = 3072;
+    static constexpr int kPlaneBytes = 1024;
+    static constexpr int kColScale = 4;   // bytes per column in a row of the X tile
+    static constexpr int kMaxColBytes = 65535;
+    struct Ops {
+        uintx4 j;      // byte offsets of blocks 8(l/32) + e, two per word (e even: low half)
+        uintx4 b[3];   // the three weight pieces, bf16 pairs
+    };
+    __device__ static void load(Ops &ops, int u, int ulim, const int32_t *__restrict__ cols,
+                                const void *__restrict__ vals) {
+        const int l = threadIdx.x & 63;
+        const __amdgpu_buffer_rsrc_t rc = buffer_rsrc(cols, unsigned(ulim) * kColBytes);
+        const __amdgpu_buffer_rsrc_t rv = buffer_rsrc(vals, unsigned(ulim) * kValBytes);
+        ops.j = __builtin_amdgcn_raw_buffer_load_b128(rc, (l >> 5) * 16, u * kColBytes, 0);
+#pragma unroll
+        for (int p = 0; p < 3; ++p)
+            ops.b[p] = __builtin_amdgcn_raw_buffer_load_b128(rv, p * kPlaneBytes + l * 16,
+                                                             u * kValBytes, 0);
+    }
+    // The bf16 upper halves of two fp32 words, as one packed pair (a low, b high).
+    __device__ static unsigned hi_pair(unsigned a, unsigned b) {
+        return __builtin_amdgcn_perm(b, a, 0x07060302u);
+    }
+    __device__ static void mma(typename Base::Acc &acc, const Ops &ops, const void *Xs, int XP,
+                               int Kb, char *) {
+        const char *xrow = static_cast<const char *>(Xs) + (threadIdx.x & 31) * XP * 4;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const unsigned w = ops.j[e >> 1];
+            const unsigned off = (e & 1) ? (w >> 16) : (w & 0xffffu);
+            v[e] = *reinterpret_cast<const float *>(xrow + off);
+        }
+        uintx4 x0, x1, x2;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            unsigned r[2], c[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const float a = v[2 * q + i];
+                const float rr = a - __uint_as_float(__float_as_uint(a) & 0xffff0000u);
+                const float cc = rr - __uint_as_float(__float_as_uint(rr) & 0xffff0000u);
+                r[i] = __float_as_uint(rr);
+                c[i] = __float_as_uint(cc);
+            }
+            x0[q] = hi_pair(__float_as_uint(v[2 * q]), __float_as_uint(v[2 * q + 1]));
+            x1[q] = hi_pair(r[0], r[1]);
+            x2[q] = hi_pair(c[0], c[1]);
+        }
+        auto mf = [&](const uintx4 &a, const uintx4 &b) {
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                         __builtin_bit_cast(bf16x8, b), acc, 0,
+                                                         0, 0);
+        };
+        mf(x2, ops.b[0]);
+        mf(x1, ops.b[1]);
+        mf(x0, ops.b[2]);
+        mf(x1, ops.b[0]);
+        mf(x0, ops.b[1]);
+        mf(x0, ops.b[0]);
+    }
+};
+
 // Accumulator, bias and store plumbing shared by the square units (the output layouts of the
 // 32x32 and 16x16 MFMAs do not depend on the input type).
 template <int R>

@@ -438,10 +438,47 @@ def test_plan_validation(L, lib):
     # a planned call whose plan describes another matrix, or NULL memory
     other = _matrix(L, N=768, K=768, R=32, C=1, nnzb=100, indices=FAKE + 8)
     plan2 = L.bsr_plan_t(0x900000, need, 768, 768, 100, 32, 1, 0, FAKE, FAKE, FAKE, 8, units,
-                         0, 256, 256 + 256 * ((units * 32 + 255) // 256))
+                         0, 256, 256 + 256 * ((units * 32 + 255) // 256), L.ARITH_NATIVE)
     arr = (ctypes.POINTER(L.bsr_plan_t) * 1)(ctypes.pointer(plan2))
     it = _item(L, other, ldx=768, ldy=768)
     assert lib.bsr_spmm_batched_planned(ctypes.byref(it), arr, 1, None, None) == 3
     plan2.mem = None
     it = _item(L, m, ldx=768, ldy=768)
     assert lib.bsr_spmm_batched_planned(ctypes.byref(it), arr, 1, None, None) == 1
+    # a plan struct whose recorded arithmetic names none, or whose layout is not that arithmetic's
+    plan2.mem = 0x900000
+    for bad in (L.ARITH_AUTO, 7, -1):
+        plan2.arith = bad
+        assert lib.bsr_spmm_batched_planned(ctypes.byref(it), arr, 1, None, None) == 3
+    plan2.arith = L.ARITH_BF16X3                     # the fp32 layout is not the split one
+    assert lib.bsr_spmm_batched_planned(ctypes.byref(it), arr, 1, None, None) == 3
+
+
+def test_plan_arith_validation(L, lib):
+    """Plan arithmetic: the split layout's size, and the shapes, dtypes and values refused."""
+    n = ctypes.c_size_t(0)
+    m = _matrix(L, N=768, K=768, R=32, C=1, nnzb=100)
+    assert lib.bsr_plan_bytes_ex(None, L.ARITH_BF16X3, ctypes.byref(n)) == 1
+    assert lib.bsr_plan_bytes_ex(ctypes.byref(m), L.ARITH_BF16X3, ctypes.byref(n)) == 0
+    units = -(-100 // 16) + 24                      # 16-block units
+    assert n.value >= 25 * 4 + units * (32 + 3 * 1024)
+    native = ctypes.c_size_t(0)
+    assert lib.bsr_plan_bytes_ex(ctypes.byref(m), L.ARITH_NATIVE, ctypes.byref(native)) == 0
+    auto = ctypes.c_size_t(0)
+    assert lib.bsr_plan_bytes(ctypes.byref(m), ctypes.byref(auto)) == 0
+    assert auto.value == native.value               # AUTO is NATIVE
+    for bad in (3, -1, 1 << 20):
+        assert lib.bsr_plan_bytes_ex(ctypes.byref(m), bad, ctypes.byref(n)) == 3
+    mb = _matrix(L, N=768, K=768, R=32, C=1, nnzb=100, dtype=1)
+    assert lib.bsr_plan_bytes_ex(ctypes.byref(mb), L.ARITH_BF16X3, ctypes.byref(n)) == 9
+    assert lib.bsr_plan_bytes_ex(ctypes.byref(mb), L.ARITH_NATIVE, ctypes.byref(n)) == 0
+    # the split plan's 16-bit column offsets reach 4 * 16383 bytes
+    wide = _matrix(L, N=64, K=16384, R=32, C=1, nnzb=10)
+    assert lib.bsr_plan_bytes_ex(ctypes.byref(wide), L.ARITH_BF16X3, ctypes.byref(n)) == 9
+    ok = _matrix(L, N=64, K=16383, R=32, C=1, nnzb=10)
+    assert lib.bsr_plan_bytes_ex(ctypes.byref(ok), L.ARITH_BF16X3, ctypes.byref(n)) == 0
+    plan = L.bsr_plan_t()
+    assert lib.bsr_plan_prepare_ex(ctypes.byref(mb), L.ARITH_BF16X3, 0x900000, 1 << 20,
+                                   ctypes.byref(plan), None) == 9
+    assert lib.bsr_plan_prepare_ex(ctypes.byref(m), 9, 0x900000, 1 << 20, ctypes.byref(plan),
+                                   None) == 3
