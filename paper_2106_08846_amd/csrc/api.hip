@@ -258,6 +258,7 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
     std::vector<bsr::TiledWork> tiled(work.size());
     std::vector<bsr::KchunkWork> kchunk(work.size());
     std::vector<int> kind(work.size(), kGeneric);
+    std::vector<int> tokens(work.size(), 32);   // tokens per tile of a flat or tiled launch
     for (size_t w = 0; w < work.size(); ++w) {
         const bsr_spmm_item_t &it = items[work[w]];
         const int R = it.W->R, C = it.W->C, dt = it.W->dtype;
@@ -280,8 +281,12 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
             kind[w] = kVchunk;
         if (kind[w] == kGeneric && (kernel == BSR_KERNEL_TILED || kernel == BSR_KERNEL_VALU))
             return BSR_ERR_UNSUPPORTED;
-        // Linear R x 1 blocks run on the flat-stream form of the matrix-core kernel.
-        if (kind[w] == kTiled && bsr::flat_supported(R, C, dt)) kind[w] = kFlat;
+        // Linear R x 1 blocks run on the flat-stream form of the matrix-core kernel, with the
+        // token tile its plan picks (the tiled kernel proper takes 32-token tiles).
+        if (kind[w] == kTiled && bsr::flat_supported(R, C, dt)) {
+            kind[w] = kFlat;
+            tokens[w] = bsr::plan_tiled(it.X, it.T, it.ldx, it.W, it.ldy, 1, lds_limit).tokens;
+        }
     }
     // A plan is used where its product runs on the flat kernel (elsewhere it is not needed:
     // the result is the same without it).
@@ -306,7 +311,8 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
                 items[work[v]].W->C != items[work[w]].W->C ||
                 items[work[v]].W->dtype != items[work[w]].W->dtype ||
                 (plan_of[v] != nullptr) != (plan_of[w] != nullptr) ||
-                (plan_of[v] && plan_of[v]->arith != plan_of[w]->arith))
+                (plan_of[v] && plan_of[v]->arith != plan_of[w]->arith) ||
+                tokens[v] != tokens[w])
                 continue;
             l.members.push_back(int(v));
             done[v] = 1;
@@ -325,7 +331,8 @@ bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items, const bsr_plan
     for (const Launch &l : launches) {
         if (l.kind == kGeneric) continue;
         std::vector<int64_t> tiles;
-        for (int w : l.members) tiles.push_back((items[work[w]].T + 31) / 32);
+        for (int w : l.members)
+            tiles.push_back((items[work[w]].T + tokens[w] - 1) / tokens[w]);
         const int auto_S = bsr::auto_slices(tiles.data(), int(tiles.size()), cus);
         for (int w : l.members) {
             const bsr_spmm_item_t &it = items[work[w]];

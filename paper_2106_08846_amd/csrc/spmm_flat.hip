@@ -99,16 +99,21 @@ struct FlatItem {
     TileOut out;
 };
 
-// The operand source of a unit: the BSR arrays (PK = 0), a native plan (1) or a split plan (2).
-template <int R, bool BF, int PK>
+// The tile and accumulator of a launch (TT tokens per tile: 64 only for bf16 32x1 blocks) and
+// the operand source of a unit: the BSR arrays (PK = 0), a native plan (1) or a split plan (2).
+template <int R, bool BF, int TT>
+using TileOf = std::conditional_t<TT == 64, Unit64BF, Unit<R, 1, BF>>;
+template <int R, bool BF, int PK, int TT>
 using SrcOf = std::conditional_t<
-    PK == 2, SplitPlanUnit, std::conditional_t<PK == 1, PlanUnit<R, 1, BF>, Unit<R, 1, BF>>>;
+    PK == 2, SplitPlanUnit,
+    std::conditional_t<PK == 1, std::conditional_t<TT == 64, PlanUnit64BF, PlanUnit<R, 1, BF>>,
+                       TileOf<R, BF, TT>>>;
 
-template <int R, bool BF, int PK, class Ops, class Fetch>
+template <int R, bool BF, int PK, int TT, class Ops, class Fetch>
 __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[kRingOf<PK>],
                                                int (&nvr)[kRingOf<PK>], Fetch &&fetch) {
-    using U = Unit<R, 1, BF>;
-    using Src = SrcOf<R, BF, PK>;
+    using U = TileOf<R, BF, TT>;
+    using Src = SrcOf<R, BF, PK, TT>;
     constexpr bool PL = PK != 0;
     constexpr int kDepth = kDepthOf<PK>, kRing = kRingOf<PK>;
     constexpr int NW = kNW, KB = U::KB;
@@ -166,12 +171,12 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
             fetch(ring[(ph + kDepth) % kRing], nvr[(ph + kDepth) % kRing], u + kDepth);
             __builtin_amdgcn_sched_barrier(0);
             if (u >= Pw1) continue;
-            if constexpr (PL) {
-                Src::mma(acc, ring[ph], Xs, XP, Kb, wslot);
-            } else {
+            if constexpr (!PL) {
                 if (nvr[ph] < KB) U::mask(ring[ph], nvr[ph]);
-                U::mma(acc, ring[ph], Xs, XP, Kb, wslot);
             }
+            typename Src::A xa;
+            Src::gather(xa, ring[ph], Xs, XP, Kb, wslot);
+            Src::mac(acc, xa, ring[ph]);
             __builtin_amdgcn_sched_barrier(0);
             if (u + 1 == r_end) {
                 if (r == rlo - 1) {
@@ -192,10 +197,11 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
     // Combine rows cut by wave boundaries, in wave order (as in the tiled kernel): the owner's
     // partial (bias and its units), then each later wave's head partial.  The X tile is dead
     // now; its LDS holds the head partials P[w][v][lane], the partials of wide tails
-    // T[w][v][lane] and one word per wave naming its wide tail row.
+    // T[w][v][lane] and one word per wave naming its wide tail row.  An accumulator of two
+    // 32-token halves is combined in two passes, one half (16 registers) per pass.
     constexpr int kLocalHeads = 2;
-    constexpr int kSlot = U::kRegs * 64;
-    __syncthreads();
+    constexpr int kPassRegs = U::kRegs / U::kHalves;
+    constexpr int kSlot = kPassRegs * 64;
     float *P = reinterpret_cast<float *>(Xs);
     float *Tw = P + NW * kSlot;
     int *s_wide = reinterpret_cast<int *>(Tw + NW * kSlot);
@@ -205,51 +211,62 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
         tail_heads = unsigned(__ballot(lane > wave && lane < NW && ws < e && wsn != ws));
     }
     const bool wide = __popc(tail_heads) > kLocalHeads;
-    if (has_head) {
 #pragma unroll
-        for (int vv = 0; vv < U::kRegs; ++vv) P[(wave * U::kRegs + vv) * 64 + lane] = U::get(head, vv);
-    }
-    if (wide) {
+    for (int hh = 0; hh < U::kHalves; ++hh) {
+        const int v0 = hh * kPassRegs;
+        __syncthreads();   // the X tile (first pass) or the previous pass's partials are dead
+        if (has_head) {
 #pragma unroll
-        for (int vv = 0; vv < U::kRegs; ++vv) Tw[(wave * U::kRegs + vv) * 64 + lane] = U::get(acc, vv);
-    }
-    s_wide[wave] = wide ? tail_row : -1;
-    s_wide[NW + wave] = int(tail_heads);
-    __syncthreads();
-    if (tail_row >= 0 && !wide) {
-        for (unsigned m = tail_heads; m; m &= m - 1) {
-            const int w2 = __ffs(m) - 1;
-            float h[U::kRegs];
-#pragma unroll
-            for (int vv = 0; vv < U::kRegs; ++vv) h[vv] = P[(w2 * U::kRegs + vv) * 64 + lane];
-#pragma unroll
-            for (int vv = 0; vv < U::kRegs; ++vv) U::add(acc, vv, h[vv]);
+            for (int vv = 0; vv < kPassRegs; ++vv)
+                P[(wave * kPassRegs + vv) * 64 + lane] = U::get(head, v0 + vv);
         }
-        U::store(acc, out, tail_row * R);
-    }
-    const int wv = lane < NW ? s_wide[lane] : -1;
-    const int whm = lane < NW ? s_wide[NW + lane] : 0;
-    for (unsigned long long m = __ballot(wv >= 0); m; m &= m - 1) {
-        const int w = __ffsll(static_cast<long long>(m)) - 1;
-        const int trow = __builtin_amdgcn_readlane(wv, w);
-        if (wave < U::kRegs) {
-            const unsigned hm = unsigned(__builtin_amdgcn_readlane(whm, w));
-            const int vv = wave;
-            float x = Tw[(w * U::kRegs + vv) * 64 + lane];
-            float h[NW - 1];
+        if (wide) {
 #pragma unroll
-            for (int i = 0; i < NW - 1; ++i) h[i] = P[((i + 1) * U::kRegs + vv) * 64 + lane];
+            for (int vv = 0; vv < kPassRegs; ++vv)
+                Tw[(wave * kPassRegs + vv) * 64 + lane] = U::get(acc, v0 + vv);
+        }
+        if (hh == 0) {
+            s_wide[wave] = wide ? tail_row : -1;
+            s_wide[NW + wave] = int(tail_heads);
+        }
+        __syncthreads();
+        if (tail_row >= 0 && !wide) {
+            for (unsigned m = tail_heads; m; m &= m - 1) {
+                const int w2 = __ffs(m) - 1;
+                float h[kPassRegs];
 #pragma unroll
-            for (int i = 0; i < NW - 1; ++i) x += (hm >> (i + 1)) & 1u ? h[i] : -0.0f;
-            U::store_reg(x, out, trow * R, vv);
+                for (int vv = 0; vv < kPassRegs; ++vv) h[vv] = P[(w2 * kPassRegs + vv) * 64 + lane];
+#pragma unroll
+                for (int vv = 0; vv < kPassRegs; ++vv) U::add(acc, v0 + vv, h[vv]);
+            }
+            if constexpr (U::kHalves == 1) U::store(acc, out, tail_row * R);
+            else U::store_half(acc, out, tail_row * R, hh);
+        }
+        const int wv = lane < NW ? s_wide[lane] : -1;
+        const int whm = lane < NW ? s_wide[NW + lane] : 0;
+        for (unsigned long long m = __ballot(wv >= 0); m; m &= m - 1) {
+            const int w = __ffsll(static_cast<long long>(m)) - 1;
+            const int trow = __builtin_amdgcn_readlane(wv, w);
+            if (wave < kPassRegs) {
+                const unsigned hm = unsigned(__builtin_amdgcn_readlane(whm, w));
+                const int vv = wave;
+                float x = Tw[(w * kPassRegs + vv) * 64 + lane];
+                float h[NW - 1];
+#pragma unroll
+                for (int i = 0; i < NW - 1; ++i) h[i] = P[((i + 1) * kPassRegs + vv) * 64 + lane];
+#pragma unroll
+                for (int i = 0; i < NW - 1; ++i) x += (hm >> (i + 1)) & 1u ? h[i] : -0.0f;
+                U::store_reg(x, out, trow * R, v0 + vv);
+            }
         }
     }
 }
 
-template <int R, bool BF, int PK>
+template <int R, bool BF, int PK, int TT>
 __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch batch) {
-    using U = Unit<R, 1, BF>;
-    using Src = SrcOf<R, BF, PK>;
+    using U = TileOf<R, BF, TT>;
+    using Src = SrcOf<R, BF, PK, TT>;
+    static_assert(U::kTokens == TT, "the unit's tile holds TT tokens");
     constexpr bool PL = PK != 0;
     constexpr int kDepth = kDepthOf<PK>, kRing = kRingOf<PK>;
     using Ops = typename Src::Ops;
@@ -294,12 +311,15 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
     const int q = xcd * per_xcd + rank;
     if (rank >= per_xcd || q >= pairs) return;
     const int tile = q / slices, s = q - tile * slices;
-    const int64_t t0 = int64_t(tile) * kTT;
+    const int64_t t0 = int64_t(tile) * TT;
 
-    const int rows = int(T - t0 < kTT ? T - t0 : kTT);
+    const int rows = int(T - t0 < TT ? T - t0 : TT);
     constexpr int kXBytes = BF ? 2 : 4;
-    constexpr int kRowsPerWave = kTT / NW;
-    static_assert(kTT % NW == 0, "every wave stages the same number of rows");
+    constexpr int kRowsPerWave = TT / NW;
+    static_assert(TT % NW == 0, "every wave stages the same number of rows");
+    // 64-column chunks of an X row staged per pass (the registers of a pass are the same for
+    // both tile sizes).
+    constexpr int kChunks = kStageChunks * 32 / TT;
 
     // Prologue, overlapping the latencies of the row pointers, the X tile and the first units:
     //   (1) every wave loads the row pointers into registers, the bias, then its X-tile rows;
@@ -346,7 +366,7 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
     // X tile staging (as in the tiled kernel): loads into v, then conflict-free LDS stores.
     constexpr int kColsPerLane = 1;
     const int lane_words = K;
-    unsigned v[kRowsPerWave][kStageChunks];
+    unsigned v[kRowsPerWave][kChunks];
     auto x_load = [&](int c0) {
 #pragma unroll
         for (int r = 0; r < kRowsPerWave; ++r) {
@@ -356,7 +376,7 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
                 buffer_rsrc(static_cast<const char *>(X) + (t0 + tr) * ldx * kXBytes,
                             t < rows ? unsigned(K) * kXBytes : 0u);
 #pragma unroll
-            for (int m = 0; m < kStageChunks; ++m) {
+            for (int m = 0; m < kChunks; ++m) {
                 if constexpr (BF)
                     v[r][m] = __builtin_amdgcn_raw_buffer_load_b16(rx, (c0 + lane) * 2 + 128 * m,
                                                                    0, 0);
@@ -371,16 +391,17 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
         for (int r = 0; r < kRowsPerWave; ++r) {
             const int t = wave + NW * r;
             if constexpr (U::kTransposed) {
-                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs) + t;
+                // Tokens 32 h .. 32 h + 31 go to half h of the transposed tile.
+                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs) + (t >> 5) * ((K + 1) * XP) + (t & 31);
 #pragma unroll
-                for (int m = 0; m < kStageChunks; ++m) {
+                for (int m = 0; m < kChunks; ++m) {
                     const int c = c0 + 64 * m + lane;
                     xt[(decltype(clamp)::value ? min(c, K) : c) * XP] = bf16_t(v[r][m]);
                 }
             } else {
                 unsigned *dst = reinterpret_cast<unsigned *>(Xs) + t * XP;
 #pragma unroll
-                for (int m = 0; m < kStageChunks; ++m) {
+                for (int m = 0; m < kChunks; ++m) {
                     unsigned w = v[r][m];
                     if constexpr (BF) w <<= 16;   // bf16 -> fp32, exact
                     const int c = c0 + 64 * m + lane;
@@ -617,19 +638,21 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
     for (int i = threadIdx.x + kBiasPer * kThreads; i < Nb * R; i += kThreads)
         s_bias[i] = bias ? bias[i] : 0.0f;
 
-    if (lane_words >= 64 * kStageChunks)
+    if (lane_words >= 64 * kChunks)
         x_store(0, NoClamp{});
     else
         x_store(0, Clamp{});
-    for (int c0 = 64 * kStageChunks; c0 < lane_words; c0 += 64 * kStageChunks) {
+    for (int c0 = 64 * kChunks; c0 < lane_words; c0 += 64 * kChunks) {
         x_load(c0);
         x_store(c0, Clamp{});
     }
     if constexpr (U::kPad == 1) {   // the fp32 tile's zero pad column
-        if (threadIdx.x < kTT) Xs[threadIdx.x * XP + K] = 0.0f;
+        if (threadIdx.x < TT) Xs[threadIdx.x * XP + K] = 0.0f;
     }
     if constexpr (U::kTransposed) {   // the transposed tile's zero pad column K
-        if (threadIdx.x < kTT) reinterpret_cast<bf16_t *>(Xs)[K * XP + threadIdx.x] = 0;
+        if (threadIdx.x < TT)
+            reinterpret_cast<bf16_t *>(Xs)[(threadIdx.x >> 5) * ((K + 1) * XP) + K * XP +
+                                           (threadIdx.x & 31)] = 0;
     }
     __syncthreads();
 
@@ -637,7 +660,7 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
                 XP, Kb, reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048, TileOut{}};
     fi.out.ldy4 = int(ldy) * 4;
     fi.out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(fi.out.ldy4));
-    flat_item_body<R, BF, PK>(fi, ring, nvr, [&](Ops &o, int &nv, int uu) {
+    flat_item_body<R, BF, PK, TT>(fi, ring, nvr, [&](Ops &o, int &nv, int uu) {
         fetch(o, nv, uu, read_up_lds, read_ib_lds);
     });
 }
@@ -649,10 +672,11 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
 // first units' loads, and after one barrier loads the next item's X rows into registers and
 // runs the shared stream and combine.  Items of one workgroup share an XCD, as in the one-item
 // kernel's mapping.
-template <int R, bool BF, int PK>
+template <int R, bool BF, int PK, int TT>
 __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const TiledBatch batch) {
-    using U = Unit<R, 1, BF>;
-    using Src = SrcOf<R, BF, PK>;
+    using U = TileOf<R, BF, TT>;
+    using Src = SrcOf<R, BF, PK, TT>;
+    static_assert(U::kTokens == TT, "the unit's tile holds TT tokens");
     constexpr bool PL = PK != 0;
     constexpr int kDepth = kDepthOf<PK>, kRing = kRingOf<PK>;
     using Ops = typename Src::Ops;
@@ -689,9 +713,9 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
     if (q_first >= q_end) return;
 
     constexpr int kXBytes = BF ? 2 : 4;
-    constexpr int kRowsPerWave = kTT / NW;
-    constexpr int kXC = kXChunksPersistent<PK>;
-    static_assert(kTT % NW == 0, "every wave stages the same number of rows");
+    constexpr int kRowsPerWave = TT / NW;
+    constexpr int kXC = kXChunksPersistent<PK> * 32 / TT;
+    static_assert(TT % NW == 0, "every wave stages the same number of rows");
 
     // X rows w + 16 r of a tile in registers, kXC 64-column chunks from column c0.  Rows past
     // the product's last token, and a tile of no rows (the prefetch after the last item), load
@@ -731,7 +755,7 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
         for (int r = 0; r < kRowsPerWave; ++r) {
             const int t = wave + NW * r;
             if constexpr (U::kTransposed) {
-                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs) + t;
+                bf16_t *xt = reinterpret_cast<bf16_t *>(Xs) + (t >> 5) * ((Ko + 1) * XP) + (t & 31);
 #pragma unroll
                 for (int m = 0; m < kXC; ++m) {
                     const int cb = c0 + 64 * m;
@@ -753,8 +777,8 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
     auto item_tile = [&](int q, int64_t &t0_, int &rows_, int &s_) {
         const int tile = q / slices;
         s_ = q - tile * slices;
-        t0_ = int64_t(tile) * kTT;
-        rows_ = int(T - t0_ < kTT ? T - t0_ : kTT);
+        t0_ = int64_t(tile) * TT;
+        rows_ = int(T - t0_ < TT ? T - t0_ : TT);
     };
     int64_t t0;
     int rows, s;
@@ -800,10 +824,12 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
             int tid = int(threadIdx.x);
             asm volatile("" : "+v"(tid));
             if constexpr (U::kPad == 1) {   // the fp32 tile's zero pad column
-                if (tid < kTT) Xs[tid * XP + K] = 0.0f;
+                if (tid < TT) Xs[tid * XP + K] = 0.0f;
             }
             if constexpr (U::kTransposed) {   // the transposed tile's zero pad column K
-                if (tid < kTT) reinterpret_cast<bf16_t *>(Xs)[K * XP + tid] = 0;
+                if (tid < TT)
+                    reinterpret_cast<bf16_t *>(Xs)[(tid >> 5) * ((K + 1) * XP) + K * XP +
+                                                   (tid & 31)] = 0;
             }
         }
 
@@ -898,18 +924,18 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
             rows = rowsn;
             s = sn;
         }
-        flat_item_body<R, BF, PK>(fi, ring, nvr, fetch);
+        flat_item_body<R, BF, PK, TT>(fi, ring, nvr, fetch);
     }
 }
 
-template <int R, bool BF, int PK>
+template <int R, bool BF, int PK, int TT = 32>
 bsr_status launch_flat_variant(const TiledBatch &batch, dim3 grid, size_t lds, bool persistent,
                                hipStream_t st, const LaunchEvents &ev) {
     if (persistent)
-        launch_kernel(spmm_flat_persistent_kernel<R, BF, PK>, grid, dim3(kNW * 64), lds, st, ev,
-                      batch);
+        launch_kernel(spmm_flat_persistent_kernel<R, BF, PK, TT>, grid, dim3(kNW * 64), lds, st,
+                      ev, batch);
     else
-        launch_kernel(spmm_flat_kernel<R, BF, PK>, grid, dim3(kNW * 64), lds, st, ev, batch);
+        launch_kernel(spmm_flat_kernel<R, BF, PK, TT>, grid, dim3(kNW * 64), lds, st, ev, batch);
     return launch_status();
 }
 
@@ -996,11 +1022,19 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
     hipStream_t st = as_stream(stream);
     const dim3 grid(gx, n);
     const bool split = planned && work[0].plan_arith == BSR_ARITH_BF16X3;
-    for (int i = 0; i < n; ++i)
+    const int tokens = work[0].plan.tokens;
+    for (int i = 0; i < n; ++i) {
         if (planned && (work[i].plan_arith == BSR_ARITH_BF16X3) != split) return BSR_ERR_ARG;
+        if (work[i].plan.tokens != tokens) return BSR_ERR_ARG;
+    }
+    if (tokens == 64 && !(R == 32 && bf)) return BSR_ERR_ARG;
     if (R == 32) {
         if (bf) {
             if (split) return BSR_ERR_UNSUPPORTED;
+            if (tokens == 64)
+                return planned
+                           ? launch_flat_variant<32, true, 1, 64>(batch, grid, lds, persistent, st, ev)
+                           : launch_flat_variant<32, true, 0, 64>(batch, grid, lds, persistent, st, ev);
             return planned ? launch_flat_variant<32, true, 1>(batch, grid, lds, persistent, st, ev)
                            : launch_flat_variant<32, true, 0>(batch, grid, lds, persistent, st, ev);
         }

@@ -564,20 +564,38 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     p.indptr_words = int((Nb + 1 + 3) & ~int64_t(3)) + p.ib_offset + 4;   // + a spare word
     p.bias_words = int((W->n_rows + 3) & ~int64_t(3));
     size_t tile_bytes;
+    // Partials and wide tails of the combine (an accumulator of two token halves is combined
+    // one half at a time, so `regs` per pass either way).
+    const size_t h_bytes = 2 * size_t(NW) * regs * 64 * 4 + size_t(NW) * 8;
+    const size_t head_bytes = size_t(p.indptr_words + p.bias_words) * 4;
     if (transposed) {
         // K + 1 columns (the last is the zero pad) of 32 tokens, pitch 36 bf16 (72 bytes,
-        // 8-byte aligned for the transpose reads), then 2 KB of block scratch per wave.
+        // 8-byte aligned for the transpose reads), then 2 KB of block scratch per wave.  With
+        // many tokens the tile holds 64 tokens as two such halves one after the other: a unit's
+        // weights then feed two matrix-core instructions (flat kernel only, TiledPlan::tokens).
+        // 64-token tiles are taken when block-rows hold at least kTile64RowBlocks stored blocks
+        // on average, there are at least 32 tiles (with slices they still give every CU an
+        // item), Y's 64-row window stays below 2^31 bytes and LDS holds them.
         p.x_pitch = 36;
-        p.wbuf_offset = int(((K + 1) * 72 + 255) & ~int64_t(255));
-        tile_bytes = size_t(p.wbuf_offset) + size_t(NW) * 2048;
+        const int64_t tiles64 = (T + 63) / 64;
+        const size_t wbuf64 = size_t(((2 * (K + 1)) * 72 + 255) & ~int64_t(255));
+        const size_t t64 = wbuf64 + size_t(NW) * 2048;
+        if (R == 32 && C == 1 && W->nnzb >= kTile64RowBlocks * Nb && tiles64 >= 32 &&
+            ldy < (int64_t(1) << 23) &&
+            head_bytes + (t64 > h_bytes ? t64 : h_bytes) <= lds_limit) {
+            p.tokens = 64;
+            p.wbuf_offset = int(wbuf64);
+            tile_bytes = t64;
+        } else {
+            p.wbuf_offset = int(((K + 1) * 72 + 255) & ~int64_t(255));
+            tile_bytes = size_t(p.wbuf_offset) + size_t(NW) * 2048;
+        }
     } else {
         p.x_pitch = int(tile_pitch(R, C, tile_bf16, K));
         p.wbuf_offset = 0;
         tile_bytes = size_t(kTT) * size_t(p.x_pitch) * (tile_bf16 ? 2 : 4);
     }
-    const size_t h_bytes = 2 * size_t(NW) * regs * 64 * 4 + size_t(NW) * 8;   // partials, wide tails
-    p.lds_bytes = size_t(p.indptr_words + p.bias_words) * 4 +
-                  (tile_bytes > h_bytes ? tile_bytes : h_bytes);
+    p.lds_bytes = head_bytes + (tile_bytes > h_bytes ? tile_bytes : h_bytes);
     if (p.lds_bytes > lds_limit) return TiledPlan{};
     // Buffer ranges are 32-bit: the block data, one X row and a 32-row tile of Y stay below
     // 2^31 bytes.
@@ -590,7 +608,7 @@ TiledPlan plan_tiled(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t *
     // dword loads of the bf16 tile.
     if (bf && C > 1 && ((reinterpret_cast<uintptr_t>(X) & 3) != 0 || (ldx & 1) != 0))
         return TiledPlan{};
-    p.num_tiles = int((T + kTT - 1) / kTT);
+    p.num_tiles = int((T + p.tokens - 1) / p.tokens);
     p.slices = slices > 0 ? slices : 1;
     if (p.slices > Nb) p.slices = int(Nb);
     p.ok = true;

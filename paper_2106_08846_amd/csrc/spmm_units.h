@@ -95,6 +95,8 @@ struct Unit;
 // MFMAs run; the X tile is staged widened to fp32 as well.
 template <int R, bool BF>
 struct LinearUnit {
+    static constexpr int kTokens = 32;      // tokens of the X tile
+    static constexpr int kHalves = 1;       // 32-token halves the accumulator spans
     static constexpr int kPer = 64 / R;     // blocks per MFMA step
     static constexpr int kSteps = 4;
     static constexpr int KB = kPer * kSteps;
@@ -167,17 +169,27 @@ struct Unit<32, 1, BF> : LinearUnit<32, BF> {
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[v] = b;
     }
-    // MFMAs of one unit.  Column indices are clamped to [0, Kb]; column Kb of the X tile is
-    // the zero pad column that masked lanes point at.
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
+    // A unit's X operands, gathered from the LDS tile by gather() and multiplied by mac().
+    // Column indices are clamped to [0, Kb]; column Kb of the X tile is the zero pad column
+    // that masked lanes point at.
+    struct A {
+        float a[LinearUnit<32, BF>::kSteps];
+    };
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int XP, int Kb, char *) {
         constexpr int kSteps = LinearUnit<32, BF>::kSteps;
         const float *xrow = static_cast<const float *>(Xs) + feature() * XP;
-        float a[kSteps];
 #pragma unroll
-        for (int m = 0; m < kSteps; ++m) a[m] = xrow[clamp_col(ops.j[m], Kb + 1)];
+        for (int m = 0; m < kSteps; ++m) x.a[m] = xrow[clamp_col(ops.j[m], Kb + 1)];
+    }
+    __device__ static void mac(Acc &acc, const A &x, const Ops &ops) {
 #pragma unroll
-        for (int m = 0; m < kSteps; ++m) acc = mfma32(a[m], ops.b[m], acc);
+        for (int m = 0; m < LinearUnit<32, BF>::kSteps; ++m) acc = mfma32(x.a[m], ops.b[m], acc);
+    }
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                               char *wslot) {
+        A x;
+        gather(x, ops, Xs, XP, Kb, wslot);
+        mac(acc, x, ops);
     }
     // Element v of lane l is Y[t0 + 8(v/4) + 4(l/32) + v%4][n0 + l%32].  The row offset of v
     // (uniform) goes in the scalar offset, which the hardware range-checks like the vector
@@ -220,23 +232,32 @@ struct Unit<16, 1, BF> : LinearUnit<16, BF> {
 #pragma unroll
         for (int v = 0; v < 4; ++v) acc.h[0][v] = acc.h[1][v] = b;
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                                    char *) {
+    struct A {
+        float a0[LinearUnit<16, BF>::kSteps], a1[LinearUnit<16, BF>::kSteps];
+    };
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int XP, int Kb, char *) {
         constexpr int kSteps = LinearUnit<16, BF>::kSteps;
         const float *x0 = static_cast<const float *>(Xs) + feature() * XP;
         const float *x1 = x0 + 16 * XP;
-        float a0[kSteps], a1[kSteps];
 #pragma unroll
         for (int m = 0; m < kSteps; ++m) {
             const int j = clamp_col(ops.j[m], Kb + 1);
-            a0[m] = x0[j];
-            a1[m] = x1[j];
+            x.a0[m] = x0[j];
+            x.a1[m] = x1[j];
         }
+    }
+    __device__ static void mac(Acc &acc, const A &x, const Ops &ops) {
 #pragma unroll
-        for (int m = 0; m < kSteps; ++m) {
-            acc.h[0] = mfma16(a0[m], ops.b[m], acc.h[0]);
-            acc.h[1] = mfma16(a1[m], ops.b[m], acc.h[1]);
+        for (int m = 0; m < LinearUnit<16, BF>::kSteps; ++m) {
+            acc.h[0] = mfma16(x.a0[m], ops.b[m], acc.h[0]);
+            acc.h[1] = mfma16(x.a1[m], ops.b[m], acc.h[1]);
         }
+    }
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                               char *wslot) {
+        A x;
+        gather(x, ops, Xs, XP, Kb, wslot);
+        mac(acc, x, ops);
     }
     // Element (h, v) of lane l is Y[t0 + 16h + 4(l/16) + v][n0 + l%16].
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
@@ -279,6 +300,8 @@ __device__ __forceinline__ shortx4 lds_read_tr16(const char *p) {
 // Blocks past the segment end read the tile's zero pad column (A) and zero weights (B).
 template <>
 struct Unit<32, 1, true> {
+    static constexpr int kTokens = 32;
+    static constexpr int kHalves = 1;
     static constexpr int KB = 16;
     static constexpr int kPad = 0;
     static constexpr bool kTileBF16 = true;
@@ -326,19 +349,33 @@ struct Unit<32, 1, true> {
         const shortx4 a1 = lds_read_tr16(xt + j1 * (2 * XP) + tok);
         return __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
     }
-    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
-                               char *wslot) {
+    // Both operands pass through LDS (A from the tile, B through the wave's block slot), so
+    // gather() reads both and mac() only multiplies.
+    struct A {
+        shortx8 av, bv;
+    };
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int XP, int Kb,
+                                  char *wslot) {
         const int l = threadIdx.x & 63, g = l >> 4, c = (l & 15) >> 2, q = l & 3;
         uintx4 *ws = reinterpret_cast<uintx4 *>(wslot);
         ws[l] = ops.w;
         const int tok = (16 * (g & 1) + 4 * q) * 2;
         const int boff = (8 * (g >> 1) + c) * 64 + tok;        // byte offset within the slot
-        const shortx8 av = gather(Xs, XP, clamp_col(ops.j[0], Kb + 1), clamp_col(ops.j[1], Kb + 1));
+        x.av = gather(Xs, XP, clamp_col(ops.j[0], Kb + 1), clamp_col(ops.j[1], Kb + 1));
         const shortx4 b0 = lds_read_tr16(wslot + boff);
         const shortx4 b1 = lds_read_tr16(wslot + 256 + boff);
-        const shortx8 bv = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
-                                                     __builtin_bit_cast(bf16x8, bv), acc, 0, 0, 0);
+        x.bv = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    __device__ static void mac(Acc &acc, const A &x, const Ops &) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, x.av),
+                                                     __builtin_bit_cast(bf16x8, x.bv), acc, 0,
+                                                     0, 0);
+    }
+    __device__ static void mma(Acc &acc, const Ops &ops, const void *Xs, int XP, int Kb,
+                               char *wslot) {
+        A x;
+        gather(x, ops, Xs, XP, Kb, wslot);
+        mac(acc, x, ops);
     }
     __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
         Unit<32, 1, false>::store(acc, o, n0);
@@ -348,6 +385,92 @@ struct Unit<32, 1, true> {
     }
     __device__ static float get(const Acc &acc, int v) { return acc[v]; }
     __device__ static void add(Acc &acc, int v, float x) { acc[v] += x; }
+};
+
+// 32x1 bf16 blocks on 64-token tiles: the unit of Unit<32, 1, true> for two 32-token halves of
+// the tile at once.  The halves share the unit's weights (one B operand, loaded once, for two
+// v_mfma_f32_32x32x16_bf16), which halves the weight bytes per matrix-core instruction: with
+// 32-token tiles the stream of 1 KB weight loads per 32-cycle instruction was bound by the rate
+// at which a CU's texture addresser takes vector loads (its busy counter near saturation during
+// the stream, on MI355X).  The transposed tile holds the halves one after the other, each laid
+// out as Unit<32, 1, true>'s tile (K + 1 columns of 32 tokens, column pitch 72 bytes); each
+// half's sums are those of the 32-token unit over the same blocks.
+struct Unit64BF {
+    using Half = Unit<32, 1, true>;
+    static constexpr int KB = 16;
+    static constexpr int kPad = 0;
+    static constexpr bool kTileBF16 = true;
+    static constexpr bool kTransposed = true;
+    static constexpr int kTokens = 64;
+    static constexpr int kHalves = 2;
+    static constexpr int kRegs = 32;
+    using Ops = Half::Ops;
+    struct Acc {
+        floatx16 a[2];
+    };
+    // Bytes from a column of the first half of the tile to the same column of the second.
+    __device__ static int half_bytes(int Kb) { return (Kb + 1) * 72; }
+    __device__ static void zero(Acc &acc) {
+        Half::zero(acc.a[0]);
+        Half::zero(acc.a[1]);
+    }
+    __device__ static void init(Acc &acc, const float *s_bias, int n0) {
+        Half::init(acc.a[0], s_bias, n0);
+        Half::init(acc.a[1], s_bias, n0);
+    }
+    __device__ static void load(Ops &ops, int p, int nnzb, const int *__restrict__ indices,
+                                const void *__restrict__ data) {
+        Half::load(ops, p, nnzb, indices, data);
+    }
+    __device__ static void mask(Ops &ops, int nvalid) { Half::mask(ops, nvalid); }
+    struct A {
+        shortx8 av[2], bv;
+    };
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int XP, int Kb,
+                                  char *wslot) {
+        const int l = threadIdx.x & 63, g = l >> 4, c = (l & 15) >> 2, q = l & 3;
+        uintx4 *ws = reinterpret_cast<uintx4 *>(wslot);
+        ws[l] = ops.w;
+        const int tok = (16 * (g & 1) + 4 * q) * 2;
+        const int boff = (8 * (g >> 1) + c) * 64 + tok;
+        const int j0 = clamp_col(ops.j[0], Kb + 1), j1 = clamp_col(ops.j[1], Kb + 1);
+        x.av[0] = Half::gather(Xs, XP, j0, j1);
+        x.av[1] = Half::gather(static_cast<const char *>(Xs) + half_bytes(Kb), XP, j0, j1);
+        const shortx4 b0 = lds_read_tr16(wslot + boff);
+        const shortx4 b1 = lds_read_tr16(wslot + 256 + boff);
+        x.bv = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    __device__ static void mac(Acc &acc, const A &x, const Ops &) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            acc.a[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, x.av[h]), __builtin_bit_cast(bf16x8, x.bv), acc.a[h],
+                0, 0, 0);
+    }
+    // Half h of the tile: its 32 tokens start 32 h rows into the tile's Y window.
+    __device__ static void store_half(const Acc &acc, const TileOut &o, int n0, int h) {
+        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5;
+        const int vo = 4 * kh * o.ldy4 + tl * 4;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int r = 32 * h + 8 * (v >> 2) + (v & 3);
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc.a[h][v]), o.rsrc, vo,
+                                                  n0 * 4 + r * o.ldy4, kStoreNT);
+        }
+    }
+    __device__ static void store(const Acc &acc, const TileOut &o, int n0) {
+        store_half(acc, o, n0, 0);
+        store_half(acc, o, n0, 1);
+    }
+    // Register v (uniform, 0 .. 31): half v / 16, register v % 16 of the 32-token layout.
+    __device__ static void store_reg(float x, const TileOut &o, int n0, int v) {
+        const int lane = threadIdx.x & 63, tl = lane & 31, kh = lane >> 5, vv = v & 15;
+        const int r = 32 * (v >> 4) + 8 * (vv >> 2) + (vv & 3);
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), o.rsrc,
+                                              (4 * kh + r) * o.ldy4 + tl * 4, n0 * 4, kStoreNT);
+    }
+    __device__ static float get(const Acc &acc, int v) { return acc.a[v >> 4][v & 15]; }
+    __device__ static void add(Acc &acc, int v, float x) { acc.a[v >> 4][v & 15] += x; }
 };
 
 // ------------------------------------------------------------------------- planned units
@@ -388,14 +511,15 @@ struct PlanUnit<32, 1, false> {
         ops.b = __builtin_bit_cast(
             floatx4, __builtin_amdgcn_raw_buffer_load_b128(rv, l * 16, u * kValBytes, 0));
     }
-    __device__ static void mma(typename Base::Acc &acc, const Ops &ops, const void *Xs, int XP,
-                               int Kb, char *) {
+    using A = typename Base::A;
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int XP, int, char *) {
         const char *xrow = static_cast<const char *>(Xs) + (threadIdx.x & 31) * XP * 4;
-        float a[4];
 #pragma unroll
-        for (int m = 0; m < 4; ++m) a[m] = *reinterpret_cast<const float *>(xrow + ops.j[m]);
+        for (int m = 0; m < 4; ++m) x.a[m] = *reinterpret_cast<const float *>(xrow + ops.j[m]);
+    }
+    __device__ static void mac(typename Base::Acc &acc, const A &x, const Ops &ops) {
 #pragma unroll
-        for (int m = 0; m < 4; ++m) acc = mfma32(a[m], ops.b[m], acc);
+        for (int m = 0; m < 4; ++m) acc = mfma32(x.a[m], ops.b[m], acc);
     }
 };
 
@@ -424,44 +548,52 @@ struct PlanUnit<32, 1, true> {
                                                      u * kColBytes, 0);
         ops.b = __builtin_amdgcn_raw_buffer_load_b128(rv, l * 16, u * kValBytes, 0);
     }
-    __device__ static void mma(typename Base::Acc &acc, const Ops &ops, const void *Xs, int XP,
-                               int Kb, char *) {
+    struct A {
+        shortx8 av;
+    };
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int, int, char *) {
         const int l = threadIdx.x & 63, g = l >> 4, q = l & 3;
         const char *xt = static_cast<const char *>(Xs) + (16 * (g & 1) + 4 * q) * 2;
         const shortx4 a0 = lds_read_tr16(xt + ops.j[0]);
         const shortx4 a1 = lds_read_tr16(xt + ops.j[1]);
-        const shortx8 av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
+        x.av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    __device__ static void mac(typename Base::Acc &acc, const A &x, const Ops &ops) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, x.av),
                                                      __builtin_bit_cast(bf16x8, ops.b), acc, 0,
                                                      0, 0);
     }
 };
 
-// fp32 32x1 blocks on the bf16 matrix cores, each operand split into three bf16 pieces
-// (a plan of arithmetic BSR_ARITH_BF16X3).  A finite fp32 value v is the exact sum
-// v0 + v1 + v2 of three bf16 values: v0 = v with its low 16 bits cleared, r = v - v0 (exact),
-// v1 = r with its low 16 bits cleared, v2 = r - v1 (exact, at most 8 significant bits), so
-// |v1| < 2^-7 |v| and |v2| < 2^-14 |v|.  Of the nine cross terms of x * w the six with
-// i + j <= 2 are formed (each product of two bf16 values is exact in fp32) and the three left
-// out sum to less than 2^-20 |x w|.  The six v_mfma_f32_32x32x16_bf16 run smallest first into
-// the one fp32 accumulator.
+// 32x1 blocks on the bf16 matrix cores with the X operand gathered from the row-major fp32 X
+// tile (32 tokens of one column per half-wave: one conflict-free ds_read_b32 per block) and
+// the weights from a plan holding NP bf16 pieces of every weight, each piece an operand plane
+// in MFMA lane order.  NP = 3: fp32 data, a plan of arithmetic BSR_ARITH_BF16X3.  A finite
+// fp32 value v is the sum v0 + v1 + v2 of three bf16 values: v0 = v with its low 16 bits
+// cleared, r = v - v0 (exact), v1 = r with its low 16 bits cleared, v2 = r - v1 (exact, at most
+// 8 significant bits), so |v1| < 2^-7 |v| and |v2| < 2^-14 |v|.  Of the nine cross terms of
+// x * w the six with i + j <= 2 are formed (each product of two bf16 values is exact in fp32)
+// and the three left out sum to less than 2^-20 |x w|.  The six v_mfma_f32_32x32x16_bf16 run
+// smallest first into the one fp32 accumulator.
 // Unit = 16 blocks; lane l supplies k-slots 8(l/32) .. +7, i.e. blocks 8(l/32) + e, for token
-// l%32 (A: gathered from the row-major fp32 X tile, split in registers) and feature l%32 (B).
+// l%32 (A: gathered, then split in registers) and feature l%32 (B).
 // Columns: cols[u][h][e] = 4 * column of block 8h + e as uint16 byte offsets into a row of the
 // fp32 tile (column clamped to [0, Kb]; 32 bytes per unit, one 16-byte load per lane).
-// Weights: vals[u][p][l][e] = piece p of block 8(l/32) + e, feature l%32 (three planes of
-// 1 KB per unit, each exactly a B operand).
-struct SplitPlanUnit {
+// Weights: vals[u][p][l][e] = piece p of block 8(l/32) + e, feature l%32 (NP planes of 1 KB
+// per unit, each exactly a B operand).
+template <int NP>
+struct GatherPlanUnit {
+    static_assert(NP == 3, "three pieces per fp32 weight");
     using Base = Unit<32, 1, false>;
     static constexpr int KB = 16;
     static constexpr int kColBytes = 32;
-    static constexpr int kValBytes = 3072;
     static constexpr int kPlaneBytes = 1024;
+    static constexpr int kValBytes = NP * kPlaneBytes;
     static constexpr int kColScale = 4;   // bytes per column in a row of the X tile
     static constexpr int kMaxColBytes = 65535;
     struct Ops {
-        uintx4 j;      // byte offsets of blocks 8(l/32) + e, two per word (e even: low half)
-        uintx4 b[3];   // the three weight pieces, bf16 pairs
+        uintx4 j;       // byte offsets of blocks 8(l/32) + e, two per word (e even: low half)
+        uintx4 b[NP];   // the weight pieces, bf16 pairs
     };
     __device__ static void load(Ops &ops, int u, int ulim, const int32_t *__restrict__ cols,
                                 const void *__restrict__ vals) {
@@ -470,7 +602,7 @@ struct SplitPlanUnit {
         const __amdgpu_buffer_rsrc_t rv = buffer_rsrc(vals, unsigned(ulim) * kValBytes);
         ops.j = __builtin_amdgcn_raw_buffer_load_b128(rc, (l >> 5) * 16, u * kColBytes, 0);
 #pragma unroll
-        for (int p = 0; p < 3; ++p)
+        for (int p = 0; p < NP; ++p)
             ops.b[p] = __builtin_amdgcn_raw_buffer_load_b128(rv, p * kPlaneBytes + l * 16,
                                                              u * kValBytes, 0);
     }
@@ -478,29 +610,33 @@ struct SplitPlanUnit {
     __device__ static unsigned hi_pair(unsigned a, unsigned b) {
         return __builtin_amdgcn_perm(b, a, 0x07060302u);
     }
-    __device__ static void mma(typename Base::Acc &acc, const Ops &ops, const void *Xs, int XP,
-                               int Kb, char *) {
-        const char *xrow = static_cast<const char *>(Xs) + (threadIdx.x & 31) * XP * 4;
+    // The gathered fp32 values; the split happens in mac().
+    struct A {
         float v[8];
+    };
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int XP, int, char *) {
+        const char *xrow = static_cast<const char *>(Xs) + (threadIdx.x & 31) * XP * 4;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const unsigned w = ops.j[e >> 1];
             const unsigned off = (e & 1) ? (w >> 16) : (w & 0xffffu);
-            v[e] = *reinterpret_cast<const float *>(xrow + off);
+            x.v[e] = *reinterpret_cast<const float *>(xrow + off);
         }
+    }
+    __device__ static void mac(typename Base::Acc &acc, const A &x, const Ops &ops) {
         uintx4 x0, x1, x2;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             unsigned r[2], c[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
-                const float a = v[2 * q + i];
+                const float a = x.v[2 * q + i];
                 const float rr = a - __uint_as_float(__float_as_uint(a) & 0xffff0000u);
                 const float cc = rr - __uint_as_float(__float_as_uint(rr) & 0xffff0000u);
                 r[i] = __float_as_uint(rr);
                 c[i] = __float_as_uint(cc);
             }
-            x0[q] = hi_pair(__float_as_uint(v[2 * q]), __float_as_uint(v[2 * q + 1]));
+            x0[q] = hi_pair(__float_as_uint(x.v[2 * q]), __float_as_uint(x.v[2 * q + 1]));
             x1[q] = hi_pair(r[0], r[1]);
             x2[q] = hi_pair(c[0], c[1]);
         }
@@ -515,6 +651,42 @@ struct SplitPlanUnit {
         mf(x1, ops.b[0]);
         mf(x0, ops.b[1]);
         mf(x0, ops.b[0]);
+    }
+};
+using SplitPlanUnit = GatherPlanUnit<3>;
+
+// Planned 32x1 bf16 blocks on 64-token tiles: PlanUnit<32, 1, true>'s operands (the same plan)
+// multiplied into both halves of Unit64BF's tile.
+struct PlanUnit64BF {
+    using Base = Unit64BF;
+    using One = PlanUnit<32, 1, true>;
+    static constexpr int KB = One::KB;
+    static constexpr int kColBytes = One::kColBytes;
+    static constexpr int kValBytes = One::kValBytes;
+    static constexpr int kColScale = One::kColScale;
+    using Ops = One::Ops;
+    __device__ static void load(Ops &ops, int u, int ulim, const int32_t *__restrict__ cols,
+                                const void *__restrict__ vals) {
+        One::load(ops, u, ulim, cols, vals);
+    }
+    struct A {
+        shortx8 av[2];
+    };
+    __device__ static void gather(A &x, const Ops &ops, const void *Xs, int XP, int Kb,
+                                  char *wslot) {
+        typename One::A h0, h1;
+        One::gather(h0, ops, Xs, XP, Kb, wslot);
+        One::gather(h1, ops, static_cast<const char *>(Xs) + Unit64BF::half_bytes(Kb), XP, Kb,
+                    wslot);
+        x.av[0] = h0.av;
+        x.av[1] = h1.av;
+    }
+    __device__ static void mac(Unit64BF::Acc &acc, const A &x, const Ops &ops) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            acc.a[h] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, x.av[h]), __builtin_bit_cast(bf16x8, ops.b), acc.a[h],
+                0, 0, 0);
     }
 };
 
