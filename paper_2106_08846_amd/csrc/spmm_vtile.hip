@@ -19,6 +19,9 @@
 //   * the weights of a chunk are read from global memory by all 32 lanes of a half (a
 //     broadcast), double-buffered in registers one chunk ahead; X comes from LDS.
 // The summation order depends only on the launch shape, so results are bitwise reproducible.
+#include <type_traits>
+#include <utility>
+
 #include "device_common.h"
 #include "spmm_tiled.h"
 
@@ -63,6 +66,12 @@ struct VecOf<4> {
 };
 
 // Operands of one chunk: U block columns and U * R * C weights (fp32).
+// Waves per workgroup: per-lane weights (bf16) need registers for two chunks, so wide chunks
+// get 8 waves (VShape::NW); broadcast weights (fp32) take at most four registers a chunk, so
+// every shape gets 16.
+template <int R, int C, bool BF>
+constexpr int kWaves = BF ? VShape<R, C>::NW : 16;
+
 template <int R, int C>
 struct VOps {
     int j[VShape<R, C>::U];
@@ -147,10 +156,185 @@ __device__ __forceinline__ void vcompute(float (&acc)[R], const VOps<R, C> &ops,
     }
 }
 
+// fp32 weights through lane broadcasts.  Loading every weight of a chunk into every lane (the
+// loads above) made these kernels bound by the rate at which a CU's texture addresser takes
+// vector loads (about 0.8 of its cycles busy on the 4096-token FFN rows, the vector ALUs under
+// 0.25, MI355X counters).  Instead, each 16-lane row of a half holds 16 words of its half's
+// chunk, one word per lane (both rows of a half the same words), so a chunk of NWORDS weights
+// costs ceil(NWORDS / 16) dword loads, and every multiply-add reads its weight with a DPP row
+// broadcast (v_fmac_f32 with row_newbcast: each row gets the value of one of its lanes).  The
+// chunk's block columns arrive the same way, one per lane, and are broadcast before use.
+template <int R, int C>
+struct DShape {
+    static constexpr int RC = R * C;
+    // Blocks per chunk: up to 16 (one column per lane of a 16-lane row) and 64 weights (four
+    // registers), more multiply-adds per chunk load than the per-lane layout's 32 weights; 1x1
+    // keeps 8 (measured on MI355X, BERT-base FFN at 4096 tokens: 16-block chunks split its rows
+    // of about 77 blocks unevenly between the two halves and ran 1.6 times longer, while 1x32,
+    // 4x4 and 8x1 ran 7-20% faster with the larger chunks).
+    static constexpr int U = RC == 1 ? 8 : (64 / RC >= 16 ? 16 : (64 / RC < 1 ? 1 : 64 / RC));
+    static constexpr int NWORDS = U * RC;
+    static constexpr int NWV = (NWORDS + 15) / 16;   // weight registers
+    static constexpr int VW = VShape<R, C>::VW;
+    static_assert(U <= 16 && NWORDS <= 64, "a chunk's columns fit one 16-lane row");
+};
+
+// Blocks per chunk of the kernels (per-lane or broadcast weights).
 template <int R, int C, bool BF>
-__global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_kernel(const TiledBatch batch) {
+constexpr int kUnits = BF ? VShape<R, C>::U : DShape<R, C>::U;
+
+template <int R, int C>
+struct DOps {
+    int j;                        // column of block (lane % 16) of the half's chunk
+    float w[DShape<R, C>::NWV];   // word 16 k + lane % 16 of the half's chunk
+};
+
+// The chunk that starts `o` blocks into the row (ranges and offsets as in vload: past the
+// row's end a load returns 0 and touches no memory).  Lane l reads word 16 k + l % 16 of the
+// chunk's weights and column l % 16 of its blocks; lanes past the chunk read the next blocks'
+// words, which no broadcast selects.
+template <int R, int C>
+__device__ __forceinline__ void dload(DOps<R, C> &ops, __amdgpu_buffer_rsrc_t ri,
+                                      __amdgpu_buffer_rsrc_t rd, int o) {
+    using S = DShape<R, C>;
+    const int i = threadIdx.x & 15;
+    ops.j = int(__builtin_amdgcn_raw_buffer_load_b32(ri, (o + i) * 4, 0, 0));
+#pragma unroll
+    for (int k = 0; k < DShape<R, C>::NWV; ++k)
+        ops.w[k] = __uint_as_float(
+            __builtin_amdgcn_raw_buffer_load_b32(rd, (o * S::RC + 16 * k + i) * 4, 0, 0));
+}
+
+// acc += w * x with w the value of lane L (0 .. 15, a constant once the caller's loops are
+// unrolled) of acc's 16-lane row in register w.  The s_nop keeps two wait states between any
+// vector-ALU write of w (a register copy the compiler may place just before) and its DPP read,
+// which the compiler's hazard checks do not see inside the asm.
+#define BSR_FMAC_BCAST(N)                                                                    \
+    case N:                                                                                  \
+        if (nop)                                                                             \
+            asm("s_nop 1\n\tv_fmac_f32_dpp %0, %1, %2 row_newbcast:" #N                      \
+                " row_mask:0xf bank_mask:0xf"                                                 \
+                : "+v"(acc)                                                                  \
+                : "v"(w), "v"(x));                                                           \
+        else                                                                                 \
+            asm("v_fmac_f32_dpp %0, %1, %2 row_newbcast:" #N " row_mask:0xf bank_mask:0xf"     \
+                : "+v"(acc)                                                                  \
+                : "v"(w), "v"(x));                                                           \
+        break;
+// `nop`: the first read of w in a chunk (the point after which the compiler has no reason to
+// copy w again) carries the wait states; later reads of the same register follow it.
+__device__ __forceinline__ void fmac_bcast(float &acc, float w, float x, int L, bool nop) {
+    switch (L) {
+        BSR_FMAC_BCAST(0) BSR_FMAC_BCAST(1) BSR_FMAC_BCAST(2) BSR_FMAC_BCAST(3)
+        BSR_FMAC_BCAST(4) BSR_FMAC_BCAST(5) BSR_FMAC_BCAST(6) BSR_FMAC_BCAST(7)
+        BSR_FMAC_BCAST(8) BSR_FMAC_BCAST(9) BSR_FMAC_BCAST(10) BSR_FMAC_BCAST(11)
+        BSR_FMAC_BCAST(12) BSR_FMAC_BCAST(13) BSR_FMAC_BCAST(14) BSR_FMAC_BCAST(15)
+        default: break;
+    }
+}
+#undef BSR_FMAC_BCAST
+
+// Lane L (0 .. 15, constant after unrolling) of v's 16-lane row, in every lane of the row.
+#define BSR_BCAST(N) \
+    case N: return __builtin_amdgcn_update_dpp(0, v, 0x150 + N, 0xf, 0xf, false);
+__device__ __forceinline__ int bcast_lane(int v, int L) {
+    switch (L) {
+        BSR_BCAST(0) BSR_BCAST(1) BSR_BCAST(2) BSR_BCAST(3) BSR_BCAST(4) BSR_BCAST(5)
+        BSR_BCAST(6) BSR_BCAST(7) BSR_BCAST(8) BSR_BCAST(9) BSR_BCAST(10) BSR_BCAST(11)
+        BSR_BCAST(12) BSR_BCAST(13) BSR_BCAST(14) BSR_BCAST(15)
+        default: return v;
+    }
+}
+#undef BSR_BCAST
+
+// base + (lane L of v's 16-lane row), one v_add_u32 with a DPP row broadcast of v (L constant
+// after unrolling; `nop` on the first read of v after the vector-ALU op that wrote it, as for
+// fmac_bcast).
+#define BSR_ADD_BCAST(N)                                                                     \
+    case N:                                                                                  \
+        if (nop)                                                                             \
+            asm("s_nop 1\n\tv_add_u32_dpp %0, %1, %2 row_newbcast:" #N                       \
+                " row_mask:0xf bank_mask:0xf"                                                 \
+                : "=v"(r)                                                                    \
+                : "v"(v), "v"(base));                                                        \
+        else                                                                                 \
+            asm("v_add_u32_dpp %0, %1, %2 row_newbcast:" #N " row_mask:0xf bank_mask:0xf"      \
+                : "=v"(r)                                                                    \
+                : "v"(v), "v"(base));                                                        \
+        break;
+__device__ __forceinline__ unsigned add_bcast(unsigned v, unsigned base, int L, bool nop) {
+    unsigned r = 0;
+    switch (L) {
+        BSR_ADD_BCAST(0) BSR_ADD_BCAST(1) BSR_ADD_BCAST(2) BSR_ADD_BCAST(3) BSR_ADD_BCAST(4)
+        BSR_ADD_BCAST(5) BSR_ADD_BCAST(6) BSR_ADD_BCAST(7) BSR_ADD_BCAST(8) BSR_ADD_BCAST(9)
+        BSR_ADD_BCAST(10) BSR_ADD_BCAST(11) BSR_ADD_BCAST(12) BSR_ADD_BCAST(13)
+        BSR_ADD_BCAST(14) BSR_ADD_BCAST(15)
+        default: break;
+    }
+    return r;
+}
+#undef BSR_ADD_BCAST
+
+typedef __attribute__((address_space(3))) const float lds_cfloat;
+
+// vcompute with broadcast operands: acc[r] += sum over the chunk's first nv blocks (all U when
+// !MASKED) of X[t][j * C + c] * w[r][c], in the same order as vcompute (block, column, output
+// row), so the sums are bitwise those of vcompute.  Each lane clamps and scales the column of
+// its own block of the chunk once; a block's LDS address is then one broadcast add.
+template <int R, int C, bool MASKED>
+__device__ __forceinline__ void dcompute(float (&acc)[R], const DOps<R, C> &ops,
+                                         const float *xrow, int Kb, int nv, int jlo = 0) {
+    using S = DShape<R, C>;
+    using V = typename VecOf<S::VW>::type;
+    typedef __attribute__((address_space(3))) const V lds_cv;
+    const unsigned xbase = unsigned(size_t((lds_cfloat *)xrow));   // its LDS byte address
+    const unsigned cbytes = min(unsigned(ops.j - jlo), unsigned(Kb - 1)) * unsigned(C * 4);
+#pragma unroll
+    for (int u = 0; u < S::U; ++u) {
+        if (MASKED && u >= nv) break;
+        const unsigned a = add_bcast(cbytes, xbase, u, u == 0);
+#pragma unroll
+        for (int c0 = 0; c0 < C; c0 += S::VW) {
+            const V xv = *(lds_cv *)size_t(a + 4 * c0);
+#pragma unroll
+            for (int cc = 0; cc < S::VW; ++cc) {
+                float x;
+                if constexpr (S::VW == 1) x = xv;
+                else x = xv[cc];
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const int word = u * S::RC + r * C + c0 + cc;
+                    fmac_bcast(acc[r], ops.w[word / 16], x, word % 16, word % 16 == 0);
+                }
+            }
+        }
+    }
+}
+
+// A chunk's operands and their use: broadcast operands for fp32 weights, per-lane copies for
+// bf16 weights (widening a bf16 weight is a vector-ALU write, which the broadcast's DPP read
+// must not follow too closely).
+template <int R, int C, bool BF>
+using OpsOf = std::conditional_t<BF, VOps<R, C>, DOps<R, C>>;
+
+template <int R, int C, bool BF>
+__device__ __forceinline__ void oload(OpsOf<R, C, BF> &ops, __amdgpu_buffer_rsrc_t ri,
+                                      __amdgpu_buffer_rsrc_t rd, int o) {
+    if constexpr (BF) vload<R, C, BF>(ops, ri, rd, o);
+    else dload<R, C>(ops, ri, rd, o);
+}
+
+template <int R, int C, bool BF, bool MASKED>
+__device__ __forceinline__ void ocompute(float (&acc)[R], const OpsOf<R, C, BF> &ops,
+                                         const float *xrow, int Kb, int nv, int jlo = 0) {
+    if constexpr (BF) vcompute<R, C, MASKED>(acc, ops, xrow, Kb, nv, jlo);
+    else dcompute<R, C, MASKED>(acc, ops, xrow, Kb, nv, jlo);
+}
+
+template <int R, int C, bool BF>
+__global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_kernel(const TiledBatch batch) {
     using S = VShape<R, C>;
-    constexpr int NW = S::NW, U = S::U;
+    constexpr int NW = kWaves<R, C, BF>, U = kUnits<R, C, BF>;
     extern __shared__ float smem[];
     float *Xs = smem;
 
@@ -248,26 +432,26 @@ __global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_kernel(con
             const int nq = (m + U - 1) / U, iters = (nq + 1) >> 1;
             // Chunk `it` of this half starts (2 it + h) U blocks into the row; every chunk
             // before the last iteration is full.
-            VOps<R, C> A, B;
-            vload<R, C, BF>(A, ri, rd, h * U);
+            OpsOf<R, C, BF> A, B;
+            oload<R, C, BF>(A, ri, rd, h * U);
             int it = 0;
             while (true) {
-                if (it + 1 < iters) vload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
+                if (it + 1 < iters) oload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
-                    vcompute<R, C, true>(acc, A, xrow, Kb, m - (2 * it + h) * U);
+                    ocompute<R, C, BF, true>(acc, A, xrow, Kb, m - (2 * it + h) * U);
                     break;
                 }
-                vcompute<R, C, false>(acc, A, xrow, Kb, U);
+                ocompute<R, C, BF, false>(acc, A, xrow, Kb, U);
                 __builtin_amdgcn_sched_barrier(0);
                 ++it;
-                if (it + 1 < iters) vload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
+                if (it + 1 < iters) oload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
-                    vcompute<R, C, true>(acc, B, xrow, Kb, m - (2 * it + h) * U);
+                    ocompute<R, C, BF, true>(acc, B, xrow, Kb, m - (2 * it + h) * U);
                     break;
                 }
-                vcompute<R, C, false>(acc, B, xrow, Kb, U);
+                ocompute<R, C, BF, false>(acc, B, xrow, Kb, U);
                 __builtin_amdgcn_sched_barrier(0);
                 ++it;
             }
@@ -308,10 +492,10 @@ struct VChunkRows {
 };
 
 template <int R, int C, bool BF>
-__global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_chunk_kernel(
+__global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_chunk_kernel(
     const KchunkBatch batch) {
     using S = VShape<R, C>;
-    constexpr int NW = S::NW, U = S::U, MR = VChunkRows<R>::value;
+    constexpr int NW = kWaves<R, C, BF>, U = kUnits<R, C, BF>, MR = VChunkRows<R>::value;
     extern __shared__ float smem[];
     float *Xs = smem;
 
@@ -434,26 +618,26 @@ __global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_chunk_kern
                 static_cast<const char *>(data) + int64_t(p0) * S::RC * kEs,
                 unsigned(m) * unsigned(S::RC * kEs));
             const int nq = (m + U - 1) / U, iters = (nq + 1) >> 1;
-            VOps<R, C> A, B;
-            vload<R, C, BF>(A, ri, rd, h * U);
+            OpsOf<R, C, BF> A, B;
+            oload<R, C, BF>(A, ri, rd, h * U);
             int it = 0;
             while (true) {
-                if (it + 1 < iters) vload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
+                if (it + 1 < iters) oload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
-                    vcompute<R, C, true>(acc[i], A, xrow, kbw, m - (2 * it + h) * U, jlo);
+                    ocompute<R, C, BF, true>(acc[i], A, xrow, kbw, m - (2 * it + h) * U, jlo);
                     break;
                 }
-                vcompute<R, C, false>(acc[i], A, xrow, kbw, U, jlo);
+                ocompute<R, C, BF, false>(acc[i], A, xrow, kbw, U, jlo);
                 __builtin_amdgcn_sched_barrier(0);
                 ++it;
-                if (it + 1 < iters) vload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
+                if (it + 1 < iters) oload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
-                    vcompute<R, C, true>(acc[i], B, xrow, kbw, m - (2 * it + h) * U, jlo);
+                    ocompute<R, C, BF, true>(acc[i], B, xrow, kbw, m - (2 * it + h) * U, jlo);
                     break;
                 }
-                vcompute<R, C, false>(acc[i], B, xrow, kbw, U, jlo);
+                ocompute<R, C, BF, false>(acc[i], B, xrow, kbw, U, jlo);
                 __builtin_amdgcn_sched_barrier(0);
                 ++it;
             }
@@ -485,7 +669,7 @@ __global__ __launch_bounds__((VShape<R, C>::NW * 64)) void spmm_vtile_chunk_kern
 template <int R, int C, bool BF>
 bsr_status launch_vchunk_variant(const KchunkBatch &batch, dim3 grid, size_t lds, hipStream_t st,
                                  const LaunchEvents &ev) {
-    launch_kernel(spmm_vtile_chunk_kernel<R, C, BF>, grid, dim3(VShape<R, C>::NW * 64), lds, st,
+    launch_kernel(spmm_vtile_chunk_kernel<R, C, BF>, grid, dim3(kWaves<R, C, BF> * 64), lds, st,
                   ev, batch);
     return launch_status();
 }
@@ -516,7 +700,7 @@ bsr_status launch_vchunk_shape(int R, int C, const KchunkBatch &b, dim3 g, size_
 template <int R, int C, bool BF>
 bsr_status launch_vtile_variant(const TiledBatch &batch, dim3 grid, size_t lds, hipStream_t st,
                                 const LaunchEvents &ev) {
-    launch_kernel(spmm_vtile_kernel<R, C, BF>, grid, dim3(VShape<R, C>::NW * 64), lds, st, ev,
+    launch_kernel(spmm_vtile_kernel<R, C, BF>, grid, dim3(kWaves<R, C, BF> * 64), lds, st, ev,
                   batch);
     return launch_status();
 }
@@ -624,7 +808,12 @@ KchunkPlan plan_vchunk(const void *X, int64_t T, int64_t ldx, const bsr_matrix_t
     if (!vtile_supported(R, C, W->dtype)) return kp;
     const int64_t K = W->n_cols, Nb = W->n_rows / R, Kb = K / C;
     const int vw = C % 4 == 0 ? 4 : (C % 2 == 0 ? 2 : 1);
-    const int nw = R * C * (R * C >= 32 ? 1 : (32 / (R * C) > 8 ? 8 : 32 / (R * C))) <= 16 ? 16 : 8;
+    // kWaves: 16 for fp32 weights, else VShape::NW.
+    const int nw = W->dtype == BSR_F32
+                       ? 16
+                       : (R * C * (R * C >= 32 ? 1 : (32 / (R * C) > 8 ? 8 : 32 / (R * C))) <= 16
+                              ? 16
+                              : 8);
     const int mr = R == 1 ? 8 : (R <= 4 ? 4 : 2);   // VChunkRows<R>
     // Slices: at least enough that no wave owns more than mr rows.
     int64_t S = slices > 0 ? slices : 1;
