@@ -423,14 +423,14 @@ def dense_times_us(prep, rounds: int) -> dict:
 
 
 def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = None,
-        plans: bool = True) -> dict:
+        plans: bool = True, arith: int = 0) -> dict:
     """One block-shape row: per-launch kernel-event times (median, p10, p90), effective rates,
     roof fraction, the same launches timed back to back (mean per launch, launch gaps
     included), and the dense GEMM beside it."""
     import torch
     print(f"# row {spec}", file=sys.stderr, flush=True)
     wl = build_workload(spec)
-    prep = Prepared(wl, rotate, plans=plans)
+    prep = Prepared(wl, rotate, plans=plans, arith=arith)
     for s in range(rotate):
         prep.step(s)
     torch.cuda.synchronize()
@@ -440,6 +440,8 @@ def row(spec: str, rotate: int, rounds: int, dense: bool, label: str | None = No
     c0 = prep.calls[0]
     out = {"workload": wl.name, "spec": spec, "block": f"{c0['R']}x{c0['C']}",
            "dtype": "bf16" if wl.bf16 else "f32", "tokens": c0["T"], "plans": prep.planned,
+           "plan_arithmetic": ({1: "native", 2: "bf16x3 split"}[prep.plan_arith]
+                               if prep.planned else None),
            "products_per_launch": len(prep.calls) // prep.launches_per_step,
            "launches": lt["n"],
            "protocol": (f"cold: {rotate} rotating copies of every input and output"
@@ -471,12 +473,21 @@ def rows(args) -> dict:
     pl = not args.no_plan
     other = "bert_large:32x32" if args.workload != "bert_large:32x32" else "bert_large:32x1"
     res["bert_large_zipf"] = [row(other, 1, 5, dense, plans=pl)]
+    if pl:
+        # The headline stack with split-arithmetic plans (fp32 data as bf16 pieces on the bf16
+        # matrix cores), and the fused QKV 32x1 rows the same way.
+        res["bert_large_zipf"].append(row("bert_large:32x1", 1, 5, dense, plans=pl,
+                                          arith=ARITH_SPLIT))
     qkv = []
     for shape in ("32x1", "16x16"):
         for dt in ("", ":bf16"):
             for d in ("0.05", "0.1", "0.2", "0.4"):
                 qkv.append(row(f"fused_qkv:{shape}:{d}{dt}", ROTATE_SETS, 8 * ROTATE_SETS,
                                dense, plans=pl))
+    if pl:
+        for d in ("0.05", "0.1", "0.2", "0.4"):
+            qkv.append(row(f"fused_qkv:32x1:{d}", ROTATE_SETS, 8 * ROTATE_SETS, dense, plans=pl,
+                           arith=ARITH_SPLIT))
     res["fused_qkv"] = qkv
     res["sweep_T128"] = [row(f"sweep:{s}", 1, 100, dense, plans=pl) for s in
                          ("1x1", "8x1", "16x1", "32x1", "1x32", "4x4", "8x8", "16x16", "32x32")]
@@ -635,7 +646,12 @@ def kernel_name(c, bf16: bool, planned: bool = False, persistent: bool = False,
     if shape in ((32, 1), (16, 1)) and fits:
         pl = (2 if plan_arith == 2 else 1) if planned and shape == (32, 1) else 0
         kern = "spmm_flat_persistent_kernel" if persistent else "spmm_flat_kernel"
-        return f"{kern}<{c['R']}, {flag}, {pl}>"
+        # bf16 32x1 with long rows and many tokens takes 64-token tiles when they fit in LDS.
+        nb = c["N"] // 32
+        t64 = (bf16 and shape == (32, 1) and c["k"] >= 128 * nb and -(-c["T"] // 64) >= 32
+               and ((2 * (c["K"] + 1) * 72 + 255) // 256 * 256 + 16 * 2048 + 4 * c["N"]
+                    + 4 * (2 * nb + 10)) <= 160 * 1024)
+        return f"{kern}<{c['R']}, {flag}, {pl}, {64 if t64 else 32}>"
     if shape in TILED_SHAPES:
         w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
         if fits:

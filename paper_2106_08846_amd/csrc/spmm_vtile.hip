@@ -331,6 +331,138 @@ __device__ __forceinline__ void ocompute(float (&acc)[R], const OpsOf<R, C, BF> 
     else dcompute<R, C, MASKED>(acc, ops, xrow, Kb, nv, jlo);
 }
 
+// The rows of a wave (fp32 weights) as one stream.  A wave's rows row0, row0 + step, ... are
+// taken 64 at a time: lane k loads the row pointers and biases of row k of the group, then the
+// wave walks the group's iterations (a row of nq chunks takes max(1, ceil(nq / 2)) of them; in
+// iteration i of a row, half h multiplies chunk 2 i + h) as one sequence, with the operands of
+// the next kDD iterations in flight.  Loads run ahead across row ends, so a row's first chunks
+// arrive under the previous row's work; every phase issues one iteration's loads (past the
+// group's last row they fetch nothing), so the waits count them.  A row's sums are those of
+// the row loop (same chunks, same order).
+constexpr int kDD = 8;
+constexpr int kStreamRowsPerWave = 16;
+
+// Lane k's value of v (k uniform), bit for bit.
+__device__ __forceinline__ float lane_float(float v, int k) {
+    return __uint_as_float(unsigned(__builtin_amdgcn_readlane(int(__float_as_uint(v)), k)));
+}
+
+template <int R, int C>
+__device__ __forceinline__ void stream_rows(int row0, int row_hi, int step,
+                                            const int32_t *__restrict__ indptr,
+                                            const int32_t *__restrict__ indices,
+                                            const void *__restrict__ data, int nnzb,
+                                            const float *xrow, int Kb,
+                                            __amdgpu_buffer_rsrc_t rb, __amdgpu_buffer_rsrc_t ry,
+                                            int vo_row, int h) {
+    using S = DShape<R, C>;
+    constexpr int U = S::U;
+    const int lane = threadIdx.x & 63;
+    const __amdgpu_buffer_rsrc_t rip = buffer_rsrc(indptr, unsigned(row_hi + 1) * 4u);
+#pragma unroll 1
+    for (int g0 = row0; g0 < row_hi; g0 += 64 * step) {
+        // The group: rows g0 + step k, k < nr.
+        const int nr = min(64, (row_hi - g0 + step - 1) / step);
+        int ip0, ip1;
+        float bv[R];
+        {
+            const int row = g0 + step * (lane < nr ? lane : 0);
+            const int a = int(__builtin_amdgcn_raw_buffer_load_b32(rip, row * 4, 0, 0));
+            const int b = int(__builtin_amdgcn_raw_buffer_load_b32(rip, row * 4 + 4, 0, 0));
+            ip0 = clampi(a, 0, nnzb);
+            ip1 = clampi(b, ip0, nnzb);
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                bv[r] = __uint_as_float(
+                    __builtin_amdgcn_raw_buffer_load_b32(rb, (row * R + r) * 4, 0, 0));
+        }
+        // Load cursor: row kl of the group, its iteration il, and the row's operand ranges.
+        int kl = 0, il = 0, lp0 = 0, lm = 0, lits = 0;
+        __amdgpu_buffer_rsrc_t ri = buffer_rsrc(indices, 0u), rd = buffer_rsrc(data, 0u);
+        auto open_row = [&]() {   // kl < nr
+            lp0 = __builtin_amdgcn_readlane(ip0, kl);
+            lm = __builtin_amdgcn_readlane(ip1, kl) - lp0;
+            const int nq = (lm + U - 1) / U;
+            lits = nq > 2 ? (nq + 1) >> 1 : 1;
+            ri = buffer_rsrc(indices + lp0, unsigned(lm) * 4u);
+            rd = buffer_rsrc(static_cast<const float *>(data) + int64_t(lp0) * S::RC,
+                             unsigned(lm) * unsigned(S::RC * 4));
+        };
+        open_row();
+        auto load_next = [&](DOps<R, C> &o) {
+            // Iteration il of row kl (nothing once the group is done), then advance.
+            if (kl < nr) {
+                dload<R, C>(o, ri, rd, (2 * il + h) * U);
+                if (++il == lits) {
+                    il = 0;
+                    if (++kl < nr) open_row();
+                }
+            } else {
+                const __amdgpu_buffer_rsrc_t z = buffer_rsrc(indices, 0u);
+                dload<R, C>(o, z, z, 0);
+            }
+        };
+        DOps<R, C> ring[kDD];
+#pragma unroll
+        for (int d = 0; d < kDD; ++d) load_next(ring[d]);
+        // Compute cursor: row kc, its iteration ic and iteration count.
+        int kc = 0, ic = 0;
+        int cm = __builtin_amdgcn_readlane(ip1, 0) - __builtin_amdgcn_readlane(ip0, 0);
+        int cits;
+        {
+            const int nq = (cm + U - 1) / U;
+            cits = nq > 2 ? (nq + 1) >> 1 : 1;
+        }
+        float acc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] = h == 0 ? lane_float(bv[r], 0) : 0.0f;
+#pragma unroll 1
+        while (kc < nr) {
+#pragma unroll
+            for (int ph = 0; ph < kDD; ++ph) {
+                if (kc < nr) {
+                    const int nv = cm - (2 * ic + h) * U;
+                    if (ic + 1 == cits) {
+                        dcompute<R, C, true>(acc, ring[ph], xrow, Kb, nv);
+                        // Row kc is complete: sum the halves (as in the row loop) and store.
+                        const int n0 = (g0 + step * kc) * R;
+                        const int vo = vo_row + n0 * 4;
+                        constexpr int kHalf = R == 1 ? 1 : R / 2;
+#pragma unroll
+                        for (int r = 0; r < kHalf; ++r) {
+                            const float P = acc[r], Q = acc[R == 1 ? 0 : R / 2 + r];
+                            const auto sw = __builtin_amdgcn_permlane32_swap(
+                                __float_as_uint(P), __float_as_uint(Q), false, false);
+                            const float y = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+                            if (R > 1 || h == 0)
+                                __builtin_amdgcn_raw_buffer_store_b32(
+                                    __float_as_uint(y), ry, vo + (h * kHalf + r) * 4 * (R > 1),
+                                    0, 0);
+                        }
+                        ++kc;
+                        ic = 0;
+                        if (kc < nr) {
+                            const int a = __builtin_amdgcn_readlane(ip0, kc);
+                            cm = __builtin_amdgcn_readlane(ip1, kc) - a;
+                            const int nq = (cm + U - 1) / U;
+                            cits = nq > 2 ? (nq + 1) >> 1 : 1;
+#pragma unroll
+                            for (int r = 0; r < R; ++r)
+                                acc[r] = h == 0 ? lane_float(bv[r], kc) : 0.0f;
+                        }
+                    } else {
+                        dcompute<R, C, false>(acc, ring[ph], xrow, Kb, U);
+                        ++ic;
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                load_next(ring[ph]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+}
+
 template <int R, int C, bool BF>
 __global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_kernel(const TiledBatch batch) {
     using S = VShape<R, C>;
@@ -409,6 +541,16 @@ __global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_kernel(con
         buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(ldy4));
     const __amdgpu_buffer_rsrc_t rb = buffer_rsrc(bias, bias ? unsigned(Nb * R) * 4u : 0u);
     constexpr int kEs = BF ? 2 : 4;   // bytes per stored weight
+
+    if constexpr (!BF) {
+        // Many rows per wave: the streamed loop (its prologue per 64 rows costs more than it
+        // saves on short slices: measured slower at 2 and 12 rows per wave, faster at 24+).
+        if (row_hi - row_lo >= kStreamRowsPerWave * NW) {
+            stream_rows<R, C>(row_lo + wave, row_hi, NW, indptr, indices, data, nnzb, xrow, Kb,
+                              rb, ry, t * ldy4, h);
+            return;
+        }
+    }
 
 #pragma unroll 1
     for (int row = row_lo + wave; row < row_hi; row += NW) {
