@@ -668,14 +668,27 @@ def bsr_attention(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, batch: int,
     return O
 
 
+def _plan_or_none(W: "BSRMatrix") -> "BSRPlan | None":
+    """W's native plan, or None for a block shape or dtype without plans."""
+    try:
+        return bsr_plan_prepare(W)
+    except BSRError as e:
+        if e.status == 9:   # BSR_ERR_UNSUPPORTED
+            return None
+        raise
+
+
 class AttentionBlockCall:
     """The BERT attention block on pruned weights, prepared once and re-issued:
     Q, K, V = three BSR products of X (one bsr_spmm_batched launch), ctx = bsr_attention,
-    Y = the O BSR product of ctx.  Buffers are allocated here, on construction."""
+    Y = the O BSR product of ctx.  Buffers are allocated here, on construction; with
+    `plans` (the default) every weight whose block shape has per-matrix plans gets its native
+    plan here too (same Y, bit for bit, as without; the kernel choice `kernel` must then be
+    automatic)."""
 
     def __init__(self, X: torch.Tensor, Wq: "BSRMatrix", bq, Wk: "BSRMatrix", bk,
                  Wv: "BSRMatrix", bv, Wo: "BSRMatrix", bo, batch: int, seq: int, heads: int,
-                 kernel: int | None = None):
+                 kernel: int | None = None, plans: bool = True):
         T = batch * seq
         dev = X.device
         self.batch, self.seq, self.heads = batch, seq, heads
@@ -684,9 +697,12 @@ class AttentionBlockCall:
         self.V = torch.empty((T, Wv.n_rows), dtype=torch.float32, device=dev)
         self.ctx = torch.empty((T, heads * 64), dtype=torch.float32, device=dev)
         self.Y = torch.empty((T, Wo.n_rows), dtype=torch.float32, device=dev)
+        use = plans and not kernel
+        self.plans = [_plan_or_none(W) if use else None for W in (Wq, Wk, Wv, Wo)]
+        qkv_plans = self.plans[:3] if any(p is not None for p in self.plans[:3]) else None
         self.qkv = SpmmBatchCall([(X, Wq, bq, self.Q), (X, Wk, bk, self.K), (X, Wv, bv, self.V)],
-                                 kernel=kernel)
-        self.out = SpmmCall(self.ctx, Wo, bo, self.Y, kernel=kernel)
+                                 kernel=kernel, plans=qkv_plans)
+        self.out = SpmmCall(self.ctx, Wo, bo, self.Y, kernel=kernel, plan=self.plans[3])
         bsr_attention(self.Q, self.K, self.V, batch, seq, heads, O=self.ctx)   # checks once
         lib = _lib()
         args = (_ptr(self.Q), _pitch(self.Q, "Q"), _ptr(self.K), _pitch(self.K, "K"),

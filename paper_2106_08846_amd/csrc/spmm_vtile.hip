@@ -289,22 +289,27 @@ __device__ __forceinline__ void dcompute(float (&acc)[R], const DOps<R, C> &ops,
     typedef __attribute__((address_space(3))) const V lds_cv;
     const unsigned xbase = unsigned(size_t((lds_cfloat *)xrow));   // its LDS byte address
     const unsigned cbytes = min(unsigned(ops.j - jlo), unsigned(Kb - 1)) * unsigned(C * 4);
+    // A guard rather than a break: the loop keeps a constant trip count, so it unrolls fully
+    // and every broadcast lane and weight register is a constant (with a break, chunks of 16
+    // blocks were left rolled, with the weights in scratch memory and a switch per broadcast).
+    // The guard is uniform over each 16-lane row (both rows of a half share nv).
 #pragma unroll
     for (int u = 0; u < S::U; ++u) {
-        if (MASKED && u >= nv) break;
-        const unsigned a = add_bcast(cbytes, xbase, u, u == 0);
+        if (!MASKED || u < nv) {
+            const unsigned a = add_bcast(cbytes, xbase, u, u == 0);
 #pragma unroll
-        for (int c0 = 0; c0 < C; c0 += S::VW) {
-            const V xv = *(lds_cv *)size_t(a + 4 * c0);
+            for (int c0 = 0; c0 < C; c0 += S::VW) {
+                const V xv = *(lds_cv *)size_t(a + 4 * c0);
 #pragma unroll
-            for (int cc = 0; cc < S::VW; ++cc) {
-                float x;
-                if constexpr (S::VW == 1) x = xv;
-                else x = xv[cc];
+                for (int cc = 0; cc < S::VW; ++cc) {
+                    float x;
+                    if constexpr (S::VW == 1) x = xv;
+                    else x = xv[cc];
 #pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const int word = u * S::RC + r * C + c0 + cc;
-                    fmac_bcast(acc[r], ops.w[word / 16], x, word % 16, word % 16 == 0);
+                    for (int r = 0; r < R; ++r) {
+                        const int word = u * S::RC + r * C + c0 + cc;
+                        fmac_bcast(acc[r], ops.w[word / 16], x, word % 16, word % 16 == 0);
+                    }
                 }
             }
         }

@@ -183,3 +183,21 @@ def test_attention_block_graph_replay(device):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(call.Y.view(torch.int32), ref.view(torch.int32)), f"replay {rep}"
+
+
+def test_attention_block_plans_bit_identical(device):
+    """The block with per-matrix plans (the default for 32x1 weights) gives the same Y, bit for
+    bit, as the block without them; shapes without plans run unplanned."""
+    w, mats, call = _block(32, 1, 0.1, 2, 128)
+    assert all(p is not None for p in call.plans)
+    X = dev(w.X[0])
+    biases = [dev(prj.bias) for prj in w.projections]
+    plain = B.AttentionBlockCall(X, mats[0], biases[0], mats[1], biases[1], mats[2], biases[2],
+                                 mats[3], biases[3], 2, 128, 12, plans=False)
+    assert all(p is None for p in plain.plans)
+    Y1, Y0 = call(), plain()
+    torch.cuda.synchronize()
+    for a, b in ((call.Q, plain.Q), (call.K, plain.K), (call.V, plain.V), (Y1, Y0)):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    _, _, sq = _block(16, 16, 0.2, 1, 64)
+    assert all(p is None for p in sq.plans)
