@@ -9,7 +9,8 @@
 //   1. prune_keys_kernel: one thread per block, fp64 key summed sequentially (row r outer,
 //      column c inner).  Each fp32 square and each |x| is exact in fp64, so fma(x, x, s) and
 //      s + |x| round exactly like the CPU's sequential loop: the key is bit-identical.
-//   2. prune_select_kernel: one workgroup.  Radix select over the 64-bit key patterns (keys
+//   2. prune_select_kernel (prune_select_reg_kernel when the keys fit in the workgroup's
+//      registers): one workgroup.  Radix select over the 64-bit key patterns (keys
 //      are >= +0.0, so bit order is value order; NaN is canonicalised above +inf) finds the
 //      k-th largest key tau and how many keys equal to tau are kept.  A second sweep in block
 //      id order uses workgroup prefix sums to decide each block (key > tau, or key == tau among
@@ -85,6 +86,57 @@ __device__ __forceinline__ void wg_scan(bool pred, unsigned &excl, unsigned &tot
     total = tot;
 }
 
+// One radix step of the selection, by the first wave, lane l holding the counts c of bins
+// 4 l .. 4 l + 3 (the bins of this digit of the keys that match the prefix so far): the digit
+// of the key with rank `remaining` (1-based, descending), i.e. the largest v whose bins
+// v .. 255 hold at least `remaining` keys.  Suffix sums over the lanes give each bin's count
+// of keys at or above it.  Writes the extended prefix and the rank within bin v.
+__device__ __forceinline__ void pick_digit_counts(const unsigned (&c)[4], long long remaining,
+                                                  unsigned long long prefix, int shift,
+                                                  unsigned long long *s_prefix,
+                                                  long long *s_remaining) {
+    const int lane = threadIdx.x & 63;
+    const unsigned t = c[0] + c[1] + c[2] + c[3];
+    unsigned sfx = t;   // keys in the bins of lanes >= lane
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const unsigned y = __shfl_down(sfx, d);
+        sfx += lane + d < 64 ? y : 0u;
+    }
+    long long at[4];    // keys in bins >= 4 lane + q
+    at[3] = static_cast<long long>(sfx - t) + c[3];
+    at[2] = at[3] + c[2];
+    at[1] = at[2] + c[1];
+    at[0] = at[1] + c[0];
+    const int qb = at[3] >= remaining ? 3 : at[2] >= remaining ? 2
+                 : at[1] >= remaining ? 1 : at[0] >= remaining ? 0 : -1;
+    const unsigned long long m = __ballot(qb >= 0);
+    if (m == 0ull) {   // fewer keys than the rank (not reached for 1 <= k <= nb)
+        if (lane == 0) {
+            *s_prefix = prefix;
+            *s_remaining = remaining - static_cast<long long>(sfx);
+        }
+        return;
+    }
+    const int L = 63 - __clzll(static_cast<long long>(m));
+    if (lane == L) {
+        const int digit = 4 * lane + qb;
+        *s_prefix = prefix | (static_cast<unsigned long long>(digit) << shift);
+        *s_remaining = remaining - (at[qb] - static_cast<long long>(c[qb]));
+    }
+}
+
+__device__ __forceinline__ void pick_digit(const unsigned *hist, long long remaining,
+                                           unsigned long long prefix, int shift,
+                                           unsigned long long *s_prefix,
+                                           long long *s_remaining) {
+    const int lane = threadIdx.x & 63;
+    unsigned c[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) c[q] = hist[4 * lane + q];
+    pick_digit_counts(c, remaining, prefix, shift, s_prefix, s_remaining);
+}
+
 __global__ __launch_bounds__(kSelThreads) void prune_select_kernel(
     const unsigned long long *__restrict__ keybits, int64_t nb, int64_t Kb, int64_t Nb,
     int64_t k, int32_t *__restrict__ indptr, int32_t *__restrict__ indices,
@@ -112,20 +164,7 @@ __global__ __launch_bounds__(kSelThreads) void prune_select_kernel(
             if ((u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & 255ull], 1u);
         }
         __syncthreads();
-        if (tid == 0) {
-            long long cum = 0;
-            int digit = 0;
-            for (int v = 255; v >= 0; --v) {
-                const long long h = hist[v];
-                if (cum + h >= remaining) {
-                    digit = v;
-                    break;
-                }
-                cum += h;
-            }
-            s_prefix = prefix | (static_cast<unsigned long long>(digit) << shift);
-            s_remaining = remaining - cum;
-        }
+        if (tid < 64) pick_digit(hist, remaining, prefix, shift, &s_prefix, &s_remaining);
         __syncthreads();
         prefix = s_prefix;
         remaining = s_remaining;
@@ -164,6 +203,189 @@ __global__ __launch_bounds__(kSelThreads) void prune_select_kernel(
     if (tid == 0) indptr[Nb] = static_cast<int32_t>(k);
 }
 
+// prune_select_kernel for nb <= kSelThreads * kRegKeys (e.g. a 1024 x 1024 weight in 32 x 1
+// blocks): the same selection (radix select of tau, then the keys > tau and the first need_eq
+// keys == tau in id order) with every key read once, coalesced, into registers: thread t holds
+// ids t + kSelThreads e, e < kRegKeys ("round" e).
+//   * The high bytes that every key shares (min and max agree on them) are not radix passes.
+//   * Histogram bins are spread over kHistCopies copies (lane mod kHistCopies), kHistPitch =
+//     257 words apart, because the keys of one matrix crowd into few bins: one bin's copies then
+//     sit in different LDS banks.  The first wave sums the copies (and clears them for the next
+//     pass) and picks the digit, so a pass costs two barriers.
+//   * Placement: per round and wave, the counts of equal keys and then of kept keys go to a
+//     table of kRegKeys x kSelWaves entries whose exclusive prefix, in (round, wave) order, is id
+//     order; a key's rank is its table entry plus the lanes below it in its wave.
+constexpr int kRegKeys = 32;
+constexpr int kHistCopies = 16;
+constexpr int kHistPitch = 257;
+constexpr int kTab = kRegKeys * kSelWaves;   // 512
+
+// Exclusive prefix, in place, of tab[kTab] by the first wave (8 entries per lane).
+__device__ __forceinline__ void tab_excl_scan(unsigned *tab) {
+    const int lane = threadIdx.x & 63;
+    unsigned v[8], t = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        v[q] = tab[8 * lane + q];
+        t += v[q];
+    }
+    unsigned incl = t;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const unsigned y = __shfl_up(incl, d);
+        incl += lane >= d ? y : 0u;
+    }
+    unsigned run = incl - t;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        tab[8 * lane + q] = run;
+        run += v[q];
+    }
+}
+
+__global__ __launch_bounds__(kSelThreads) void prune_select_reg_kernel(
+    const unsigned long long *__restrict__ keybits, int64_t nb, int64_t Kb, int64_t Nb,
+    int64_t k, int32_t *__restrict__ indptr, int32_t *__restrict__ indices,
+    int32_t *__restrict__ src) {
+    __shared__ unsigned hist[kHistCopies * kHistPitch];
+    __shared__ unsigned tab[kTab];
+    __shared__ unsigned long long s_min[kSelWaves], s_max[kSelWaves];
+    __shared__ unsigned long long s_prefix;
+    __shared__ long long s_remaining;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+    if (k <= 0) {
+        for (int64_t i = tid; i <= Nb; i += kSelThreads) indptr[i] = 0;
+        return;
+    }
+    const int n = int(nb);
+    // All loads are issued before any is used: range-checked buffer loads (ids past nb read
+    // 0 and touch no memory) need no branch per key.
+    unsigned long long key[kRegKeys];
+    {
+        const __amdgpu_buffer_rsrc_t rk = buffer_rsrc(keybits, unsigned(n) * 8u);
+#pragma unroll
+        for (int e = 0; e < kRegKeys; ++e) {
+            const auto w = __builtin_amdgcn_raw_buffer_load_b64(rk, (tid + kSelThreads * e) * 8,
+                                                                0, 0);
+            key[e] = (static_cast<unsigned long long>(w[1]) << 32) | w[0];
+        }
+    }
+    for (int i = tid; i < kHistCopies * kHistPitch; i += kSelThreads) hist[i] = 0;
+    unsigned long long kmin = ~0ull, kmax = 0ull;
+#pragma unroll
+    for (int e = 0; e < kRegKeys; ++e) {
+        if (tid + kSelThreads * e < n) {
+            kmin = key[e] < kmin ? key[e] : kmin;
+            kmax = key[e] > kmax ? key[e] : kmax;
+        }
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        const unsigned long long x = __shfl_xor(kmin, d), y = __shfl_xor(kmax, d);
+        kmin = x < kmin ? x : kmin;
+        kmax = y > kmax ? y : kmax;
+    }
+    if (lane == 0) {
+        s_min[wave] = kmin;
+        s_max[wave] = kmax;
+    }
+    __syncthreads();
+    kmin = ~0ull;
+    kmax = 0ull;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+        kmin = s_min[w] < kmin ? s_min[w] : kmin;
+        kmax = s_max[w] > kmax ? s_max[w] : kmax;
+    }
+    // Leading bytes shared by every key: all keys match them, so the select's prefix there is
+    // that of any key and the rank is unchanged.
+    int pass0 = 0;
+    while (pass0 < 8 && ((kmin ^ kmax) >> (56 - 8 * pass0)) == 0) ++pass0;
+    const unsigned long long shared_mask = pass0 == 0 ? 0ull : ~0ull << (64 - 8 * pass0);
+    unsigned long long prefix = kmin & shared_mask, pmask = shared_mask;
+    long long remaining = k;
+    unsigned *h = hist + (lane % kHistCopies) * kHistPitch;
+    for (int pass = pass0; pass < 8; ++pass) {
+        const int shift = 56 - 8 * pass;
+#pragma unroll
+        for (int e = 0; e < kRegKeys; ++e)
+            if (tid + kSelThreads * e < n && (key[e] & pmask) == prefix)
+                atomicAdd(&h[(key[e] >> shift) & 255ull], 1u);
+        __syncthreads();
+        if (wave == 0) {
+            unsigned c[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int cp = 0; cp < kHistCopies; ++cp) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    c[q] += hist[cp * kHistPitch + 4 * lane + q];
+                    hist[cp * kHistPitch + 4 * lane + q] = 0;
+                }
+            }
+            pick_digit_counts(c, remaining, prefix, shift, &s_prefix, &s_remaining);
+        }
+        __syncthreads();
+        prefix = s_prefix;
+        remaining = s_remaining;
+        pmask |= 0xFFull << shift;
+    }
+    const unsigned long long tau = prefix;
+    const long long need_eq = remaining;   // keys == tau to keep, lowest ids first
+
+    const unsigned long long below = (1ull << lane) - 1ull;   // lanes under this one
+    unsigned eqm = 0, gtm = 0;
+#pragma unroll
+    for (int e = 0; e < kRegKeys; ++e) {
+        const bool v = tid + kSelThreads * e < n;
+        eqm |= (v && key[e] == tau) ? 1u << e : 0u;
+        gtm |= (v && key[e] > tau) ? 1u << e : 0u;
+    }
+    // Ranks of the equal keys in id order.
+#pragma unroll
+    for (int e = 0; e < kRegKeys; ++e) {
+        const unsigned long long b = __ballot((eqm >> e) & 1u);
+        if (lane == 0) tab[e * kSelWaves + wave] = unsigned(__popcll(b));
+    }
+    __syncthreads();
+    if (wave == 0) tab_excl_scan(tab);
+    __syncthreads();
+    unsigned keepm = gtm;
+#pragma unroll
+    for (int e = 0; e < kRegKeys; ++e) {
+        const unsigned long long b = __ballot((eqm >> e) & 1u);
+        const long long rank = static_cast<long long>(tab[e * kSelWaves + wave]) +
+                               __popcll(b & below);
+        keepm |= ((eqm >> e) & 1u) && rank < need_eq ? 1u << e : 0u;
+    }
+    __syncthreads();   // every wave has read the equal-key ranks
+    // Positions of the kept keys in id order.
+#pragma unroll
+    for (int e = 0; e < kRegKeys; ++e) {
+        const unsigned long long b = __ballot((keepm >> e) & 1u);
+        if (lane == 0) tab[e * kSelWaves + wave] = unsigned(__popcll(b));
+    }
+    __syncthreads();
+    if (wave == 0) tab_excl_scan(tab);
+    __syncthreads();
+    const unsigned kb = unsigned(Kb);
+#pragma unroll
+    for (int e = 0; e < kRegKeys; ++e) {
+        const unsigned id = unsigned(tid + kSelThreads * e);
+        const unsigned long long b = __ballot((keepm >> e) & 1u);
+        if (id < unsigned(n)) {
+            const int pos = int(tab[e * kSelWaves + wave]) + __popcll(b & below);
+            const unsigned i = id / kb, j = id - i * kb;
+            if (j == 0) indptr[i] = pos;
+            if ((keepm >> e) & 1u) {
+                indices[pos] = int32_t(j);
+                src[pos] = int32_t(id);
+            }
+        }
+    }
+    if (tid == 0) indptr[Nb] = static_cast<int32_t>(k);
+}
+
 constexpr int kRowThreads = 256;
 constexpr int kRowWaves = kRowThreads / 64;
 
@@ -198,20 +420,7 @@ __global__ __launch_bounds__(kRowThreads) void prune_select_rows_kernel(
             if ((u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & 255ull], 1u);
         }
         __syncthreads();
-        if (tid == 0) {
-            long long cum = 0;
-            int digit = 0;
-            for (int v = 255; v >= 0; --v) {
-                const long long h = hist[v];
-                if (cum + h >= remaining) {
-                    digit = v;
-                    break;
-                }
-                cum += h;
-            }
-            s_prefix = prefix | (static_cast<unsigned long long>(digit) << shift);
-            s_remaining = remaining - cum;
-        }
+        if (tid < 64) pick_digit(hist, remaining, prefix, shift, &s_prefix, &s_remaining);
         __syncthreads();
         prefix = s_prefix;
         remaining = s_remaining;
@@ -307,6 +516,9 @@ bsr_status launch_prune(const float *W, int64_t N, int64_t K, int64_t ldw, int32
         hipLaunchKernelGGL(prune_select_rows_kernel, dim3(static_cast<unsigned>(Nb)),
                            dim3(kRowThreads), 0, st, keybits, Kb, Nb, k / Nb, indptr, indices,
                            src);
+    else if (nb <= int64_t(kSelThreads) * kRegKeys)
+        hipLaunchKernelGGL(prune_select_reg_kernel, dim3(1), dim3(kSelThreads), 0, st, keybits,
+                           nb, Kb, Nb, k, indptr, indices, src);
     else
         hipLaunchKernelGGL(prune_select_kernel, dim3(1), dim3(kSelThreads), 0, st, keybits, nb,
                            Kb, Nb, k, indptr, indices, src);
