@@ -23,6 +23,7 @@
 //     plan.
 // The X tile staging, the bias, the combine of block-rows cut by wave boundaries (in wave
 // order, in LDS) and the stores are those of the tiled kernel.
+#include <climits>
 #include <type_traits>
 
 #include "device_common.h"
@@ -97,6 +98,10 @@ struct FlatItem {
     int XP, Kb;
     char *wslot;
     TileOut out;
+    // Paired products: rows from rsplit on belong to the second product, whose Y tile is out2
+    // (its rows counted from rsplit); rsplit = INT_MAX without a pair.
+    TileOut out2;
+    int rsplit;
 };
 
 // The tile and accumulator of a launch (TT tokens per tile: 64 only for bf16 32x1 blocks) and
@@ -109,7 +114,7 @@ using SrcOf = std::conditional_t<
     std::conditional_t<PK == 1, std::conditional_t<TT == 64, PlanUnit64BF, PlanUnit<R, 1, BF>>,
                        TileOf<R, BF, TT>>>;
 
-template <int R, bool BF, int PK, int TT, class Ops, class Fetch>
+template <int R, bool BF, int PK, int TT, bool PAIR = false, class Ops, class Fetch>
 __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[kRingOf<PK>],
                                                int (&nvr)[kRingOf<PK>], Fetch &&fetch) {
     using U = TileOf<R, BF, TT>;
@@ -127,12 +132,25 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
     const TileOut &out = it.out;
     int r = it.row;
     int r_end = it.end;
+    // The Y tile of row rr and the row's first output column in it.
+    auto out_of = [&](int rr, int &n0) -> const TileOut & {
+        if constexpr (PAIR) {
+            if (rr >= it.rsplit) {
+                n0 = (rr - it.rsplit) * R;
+                return it.out2;
+            }
+        }
+        n0 = rr * R;
+        return out;
+    };
     // Empty owned rows: Y = bias.
     for (int rr = rlo; rr < rhi; ++rr) {
         if (uniform(s_up[rr + 1]) == uniform(s_up[rr])) {
             typename U::Acc z;
             U::init(z, s_bias, rr * R);
-            U::store(z, out, rr * R);
+            int n0;
+            const TileOut &o = out_of(rr, n0);
+            U::store(z, o, n0);
         }
     }
 
@@ -182,7 +200,9 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
                 if (r == rlo - 1) {
                     head = acc;
                 } else if (uniform(s_up[r + 1]) <= Pw1) {
-                    U::store(acc, out, r * R);
+                    int n0;
+                    const TileOut &o = out_of(r, n0);
+                    U::store(acc, o, n0);
                 } else {
                     tail_row = r;
                 }
@@ -239,8 +259,10 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
 #pragma unroll
                 for (int vv = 0; vv < kPassRegs; ++vv) U::add(acc, v0 + vv, h[vv]);
             }
-            if constexpr (U::kHalves == 1) U::store(acc, out, tail_row * R);
-            else U::store_half(acc, out, tail_row * R, hh);
+            int n0;
+            const TileOut &o = out_of(tail_row, n0);
+            if constexpr (U::kHalves == 1) U::store(acc, o, n0);
+            else U::store_half(acc, o, n0, hh);
         }
         const int wv = lane < NW ? s_wide[lane] : -1;
         const int whm = lane < NW ? s_wide[NW + lane] : 0;
@@ -256,7 +278,9 @@ __device__ __forceinline__ void flat_item_body(const FlatItem &it, Ops (&ring)[k
                 for (int i = 0; i < NW - 1; ++i) h[i] = P[((i + 1) * kPassRegs + vv) * 64 + lane];
 #pragma unroll
                 for (int i = 0; i < NW - 1; ++i) x += (hm >> (i + 1)) & 1u ? h[i] : -0.0f;
-                U::store_reg(x, out, trow * R, v0 + vv);
+                int n0;
+                const TileOut &o = out_of(trow, n0);
+                U::store_reg(x, o, n0, v0 + vv);
             }
         }
     }
@@ -657,7 +681,8 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
     __syncthreads();
 
     FlatItem fi{lane, wave, Pw, Pw1, rlo, rhi, row, end, has_head, ws, wsn, s_up, s_bias, Xs,
-                XP, Kb, reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048, TileOut{}};
+                XP, Kb, reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048, TileOut{},
+                TileOut{}, INT_MAX};
     fi.out.ldy4 = int(ldy) * 4;
     fi.out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(fi.out.ldy4));
     flat_item_body<R, BF, PK, TT>(fi, ring, nvr, [&](Ops &o, int &nv, int uu) {
@@ -672,7 +697,13 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_kernel(const TiledBatch ba
 // first units' loads, and after one barrier loads the next item's X rows into registers and
 // runs the shared stream and combine.  Items of one workgroup share an XCD, as in the one-item
 // kernel's mapping.
-template <int R, bool BF, int PK, int TT>
+//
+// PAIR (planned products only): the workgroups of group blockIdx.y serve two products that share
+// X (the same token tiles), item.partner naming the second.  An item then covers both
+// products' block-rows for one X tile: the rows of the second follow those of the first (its
+// units after the first's), so one X store, one share computation and one combine serve twice
+// the work, and the waves' shares run across the boundary.
+template <int R, bool BF, int PK, int TT, bool PAIR = false>
 __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const TiledBatch batch) {
     using U = TileOf<R, BF, TT>;
     using Src = SrcOf<R, BF, PK, TT>;
@@ -686,6 +717,8 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
     const int lane = threadIdx.x & 63, wave = uniform(threadIdx.x >> 6);
     const int g = blockIdx.x;
     const TiledItem &I = batch.item[blockIdx.y];
+    static_assert(!PAIR || PK != 0, "paired products are planned");
+    const TiledItem &IB = batch.item[PAIR ? I.partner : blockIdx.y];   // the second product
     const void *__restrict__ X = I.X;
     const int64_t T = I.T, ldx = I.ldx, ldy = I.ldy;
     const int32_t *__restrict__ indptr = I.indptr;
@@ -696,8 +729,10 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
     const void *__restrict__ uval = I.uval;
     const float *__restrict__ bias = I.bias;
     float *__restrict__ Y = I.Y;
-    const int K = I.K, nnzb = I.nnzb, Nb = I.Nb, Kb = I.Kb, num_tiles = I.num_tiles,
-              slices = I.slices, XP = I.XP;
+    // Nb: the item's block-rows (both products' when paired; the second's follow NbA).
+    const int NbA = I.Nb;
+    const int K = I.K, nnzb = I.nnzb, Nb = PAIR ? I.Nb + IB.Nb : I.Nb, Kb = I.Kb,
+              num_tiles = I.num_tiles, slices = I.slices, XP = I.XP;
     const int ucap = PL ? I.ucap : nnzb;
     int *s_up = reinterpret_cast<int *>(smem);
     int *s_ib = s_up + I.ib_offset;
@@ -785,13 +820,25 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
     item_tile(q_first, t0, rows, s);
     x_load(t0, rows, 0, true);
 
-    // Once: row pointers and bias to LDS (unplanned, wave 0 forms the unit row pointer).
-    if constexpr (PL) {
+    // Once: row pointers and bias to LDS (unplanned, wave 0 forms the unit row pointer).  A
+    // pair's second product continues the first's unit row pointer (offset by the first's
+    // units UA) and bias.
+    [[maybe_unused]] int UA = 0;
+    if constexpr (PAIR) {
+        UA = uniform(clampi(uptr[NbA], 0, ucap));
+        for (int i = threadIdx.x; i <= NbA; i += kThreads) s_up[i] = clampi(uptr[i], 0, ucap);
+        for (int i = threadIdx.x; i < IB.Nb; i += kThreads)
+            s_up[NbA + 1 + i] = UA + clampi(IB.uptr[i + 1], 0, IB.ucap);
+        for (int i = threadIdx.x; i < NbA * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
+        for (int i = threadIdx.x; i < IB.Nb * R; i += kThreads)
+            s_bias[NbA * R + i] = IB.bias ? IB.bias[i] : 0.0f;
+    } else if constexpr (PL) {
         for (int i = threadIdx.x; i <= Nb; i += kThreads) s_up[i] = clampi(uptr[i], 0, ucap);
     } else {
         for (int i = threadIdx.x; i <= Nb; i += kThreads) s_ib[i] = clampi(indptr[i], 0, nnzb);
     }
-    for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
+    if constexpr (!PAIR)
+        for (int i = threadIdx.x; i < Nb * R; i += kThreads) s_bias[i] = bias ? bias[i] : 0.0f;
     __syncthreads();
     if constexpr (!PL) {
         if (wave == 0) {
@@ -872,7 +919,17 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
         // [pr_u0, pr_u1) and blocks [pr_b0, pr_b1).
         int pr = row, pr_u0 = 0, pr_u1 = 0, pr_b0 = 0, pr_b1 = 0;
         auto fetch = [&](Ops &o, int &nvalid, int uu) {
-            if constexpr (PL) {
+            if constexpr (PAIR) {
+                // Units from UA on are the second product's (its unit uu - UA); each range
+                // ends at the wave's share, so past it nothing is read.
+                const bool second = uu >= UA;
+                const int32_t *cols = second ? IB.ucol : ucol;
+                const void *vals = second ? IB.uval : uval;
+                const int u2 = second ? uu - UA : uu;
+                const int lim = second ? (Pw1 > UA ? Pw1 - UA : 0) : (Pw1 < UA ? Pw1 : UA);
+                Src::load(o, u2, lim, cols, vals);
+                nvalid = KB;
+            } else if constexpr (PL) {
                 Src::load(o, uu, Pw1, ucol, uval);
                 nvalid = KB;
             } else {
@@ -909,9 +966,13 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
 
         FlatItem fi{lane, wave, Pw, Pw1, rlo, rhi, row, end, has_head, ws, wsn, s_up, s_bias,
                     Xs, XP, Kb, reinterpret_cast<char *>(Xs) + I.wbuf_offset + wave * 2048,
-                    TileOut{}};
+                    TileOut{}, TileOut{}, PAIR ? NbA : INT_MAX};
         fi.out.ldy4 = int(ldy) * 4;
         fi.out.rsrc = buffer_rsrc(Y + t0 * ldy, unsigned(rows) * unsigned(fi.out.ldy4));
+        if constexpr (PAIR) {
+            fi.out2.ldy4 = int(IB.ldy) * 4;
+            fi.out2.rsrc = buffer_rsrc(IB.Y + t0 * IB.ldy, unsigned(rows) * unsigned(fi.out2.ldy4));
+        }
 
         // The next item's X rows, loaded under this item's stream.
         {
@@ -924,13 +985,20 @@ __global__ __launch_bounds__(kNW * 64) void spmm_flat_persistent_kernel(const Ti
             rows = rowsn;
             s = sn;
         }
-        flat_item_body<R, BF, PK, TT>(fi, ring, nvr, fetch);
+        flat_item_body<R, BF, PK, TT, PAIR>(fi, ring, nvr, fetch);
     }
 }
 
 template <int R, bool BF, int PK, int TT = 32>
 bsr_status launch_flat_variant(const TiledBatch &batch, dim3 grid, size_t lds, bool persistent,
-                               hipStream_t st, const LaunchEvents &ev) {
+                               hipStream_t st, const LaunchEvents &ev, bool paired = false) {
+    if constexpr (PK != 0) {
+        if (paired) {
+            launch_kernel(spmm_flat_persistent_kernel<R, BF, PK, TT, true>, grid,
+                          dim3(kNW * 64), lds, st, ev, batch);
+            return launch_status();
+        }
+    }
     if (persistent)
         launch_kernel(spmm_flat_persistent_kernel<R, BF, PK, TT>, grid, dim3(kNW * 64), lds, st,
                       ev, batch);
@@ -1004,6 +1072,7 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
             it.uval = base + w.plan_val_offset;
             it.ucap = int(w.plan_max_units);
         }
+        it.partner = -1;
         const int wgs = ((w.plan.num_tiles * w.plan.slices + 7) / 8) * 8;
         if (wgs > gx) gx = wgs;
         if (w.plan.lds_bytes > lds) lds = w.plan.lds_bytes;
@@ -1011,8 +1080,58 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
     // More workgroups than CUs (one per CU fits): the persistent kernel, one workgroup per CU,
     // each walking several token tiles of its product.
     const int cus = device_cu_count() > 0 ? device_cu_count() : 256;
+    // Paired products: a planned launch of an even number of products where products 2i and
+    // 2i + 1 share X (same tensor, tokens, pitch and tile layout) and the persistent form is
+    // taken runs n / 2 groups, each item covering one X tile of both products: the X store,
+    // share computation and combine of an item are paid once for two products' work.  The LDS
+    // head then holds both products' unit row pointers and biases.
+    int pair_ipw[kMaxItems / 2] = {}, pair_bw[kMaxItems / 2] = {};
+    size_t pair_lds = 0;
+    bool paired = planned && n >= 2 && n % 2 == 0;
+    for (int i = 0; paired && i + 1 < n; i += 2) {
+        const TiledWork &a = work[i], &b = work[i + 1];
+        paired = a.X == b.X && a.T == b.T && a.ldx == b.ldx && a.W->n_cols == b.W->n_cols &&
+                 a.plan.x_pitch == b.plan.x_pitch && a.plan.num_tiles == b.plan.num_tiles &&
+                 a.plan.slices == b.plan.slices && a.plan.tokens == b.plan.tokens &&
+                 a.plan.wbuf_offset == b.plan.wbuf_offset && a.plan_arith == b.plan_arith;
+        if (!paired) break;
+        const int64_t nb2 = a.W->n_rows / R + b.W->n_rows / R;
+        const int ipw = int((nb2 + 1 + 3) & ~int64_t(3)) + 4;   // + a spare word
+        const int bw = int((a.W->n_rows + b.W->n_rows + 3) & ~int64_t(3));
+        size_t rest = 0;   // the tile region (X tile, combine partials), as for one product
+        for (const TiledWork *w : {&a, &b}) {
+            const size_t r =
+                w->plan.lds_bytes - size_t(w->plan.indptr_words + w->plan.bias_words) * 4;
+            rest = r > rest ? r : rest;
+        }
+        const size_t need = size_t(ipw + bw) * 4 + rest;
+        if (need > device_lds_per_block() || nb2 > INT_MAX / 64) paired = false;
+        pair_ipw[i / 2] = ipw;
+        pair_bw[i / 2] = bw;
+        pair_lds = need > pair_lds ? need : pair_lds;
+    }
     bool persistent = false;
-    if (int64_t(gx) * n > cus) {
+    if (paired) {
+        const int groups = n / 2;
+        const int gp = (cus / groups) / 8 * 8;
+        paired = int64_t(gx) * groups > cus && gp >= 8 && gp < gx;
+        if (paired) {
+            TiledBatch pb{};
+            pb.n = n;
+            for (int g = 0; g < groups; ++g) {
+                pb.item[g] = batch.item[2 * g];
+                pb.item[g].indptr_words = pair_ipw[g];
+                pb.item[g].bias_words = pair_bw[g];
+                pb.item[g].partner = groups + g;
+                pb.item[groups + g] = batch.item[2 * g + 1];
+            }
+            batch = pb;
+            gx = gp;
+            lds = pair_lds;
+            persistent = true;
+        }
+    }
+    if (!paired && int64_t(gx) * n > cus) {
         const int gp = (cus / n) / 8 * 8;
         if (gp >= 8 && gp < gx) {
             gx = gp;
@@ -1020,7 +1139,7 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
         }
     }
     hipStream_t st = as_stream(stream);
-    const dim3 grid(gx, n);
+    const dim3 grid(gx, paired ? n / 2 : n);
     const bool split = planned && work[0].plan_arith == BSR_ARITH_BF16X3;
     const int tokens = work[0].plan.tokens;
     for (int i = 0; i < n; ++i) {
@@ -1032,15 +1151,20 @@ bsr_status launch_spmm_flat(const TiledWork *work, int n, bool planned, void *st
         if (bf) {
             if (split) return BSR_ERR_UNSUPPORTED;
             if (tokens == 64)
-                return planned
-                           ? launch_flat_variant<32, true, 1, 64>(batch, grid, lds, persistent, st, ev)
-                           : launch_flat_variant<32, true, 0, 64>(batch, grid, lds, persistent, st, ev);
-            return planned ? launch_flat_variant<32, true, 1>(batch, grid, lds, persistent, st, ev)
-                           : launch_flat_variant<32, true, 0>(batch, grid, lds, persistent, st, ev);
+                return planned ? launch_flat_variant<32, true, 1, 64>(batch, grid, lds,
+                                                                      persistent, st, ev, paired)
+                               : launch_flat_variant<32, true, 0, 64>(batch, grid, lds,
+                                                                      persistent, st, ev);
+            return planned
+                       ? launch_flat_variant<32, true, 1>(batch, grid, lds, persistent, st, ev,
+                                                          paired)
+                       : launch_flat_variant<32, true, 0>(batch, grid, lds, persistent, st, ev);
         }
-        if (split) return launch_flat_variant<32, false, 2>(batch, grid, lds, persistent, st, ev);
-        return planned ? launch_flat_variant<32, false, 1>(batch, grid, lds, persistent, st, ev)
-                       : launch_flat_variant<32, false, 0>(batch, grid, lds, persistent, st, ev);
+        if (split)
+            return launch_flat_variant<32, false, 2>(batch, grid, lds, persistent, st, ev, paired);
+        return planned
+                   ? launch_flat_variant<32, false, 1>(batch, grid, lds, persistent, st, ev, paired)
+                   : launch_flat_variant<32, false, 0>(batch, grid, lds, persistent, st, ev);
     }
     if (planned) return BSR_ERR_UNSUPPORTED;
     if (bf) return launch_flat_variant<16, true, 0>(batch, grid, lds, persistent, st, ev);

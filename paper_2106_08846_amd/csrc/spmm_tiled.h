@@ -86,6 +86,9 @@ struct TiledItem {
     const int32_t *uptr;
     const int32_t *ucol;
     const void *uval;
+    // Planned flat launches of paired products (see launch_spmm_flat): the batch index of the
+    // product that shares this one's workgroups and X tiles, or -1.
+    int partner;
 };
 
 struct TiledBatch {
