@@ -633,7 +633,7 @@ VALU_SHAPES = ((1, 1), (1, 2), (1, 4), (1, 8), (1, 16), (1, 32), (2, 1), (4, 1),
 
 
 def kernel_name(c, bf16: bool, planned: bool = False, persistent: bool = False,
-                plan_arith: int = 1) -> str:
+                plan_arith: int = 1, paired: bool = False) -> str:
     """The kernel libbsr's automatic choice launches for this product: the flat-stream kernel
     for 32x1 and 16x1 (its planned form with a plan), the matrix-core tiled kernel for square
     blocks, else the vector-ALU tile kernel, each in its column-chunked form when the 32-token
@@ -651,7 +651,8 @@ def kernel_name(c, bf16: bool, planned: bool = False, persistent: bool = False,
         t64 = (bf16 and shape == (32, 1) and c["k"] >= 128 * nb and -(-c["T"] // 64) >= 32
                and ((2 * (c["K"] + 1) * 72 + 255) // 256 * 256 + 16 * 2048 + 4 * c["N"]
                     + 4 * (2 * nb + 10)) <= 160 * 1024)
-        return f"{kern}<{c['R']}, {flag}, {pl}, {64 if t64 else 32}>"
+        pair = ", true" if paired and persistent and pl else ""
+        return f"{kern}<{c['R']}, {flag}, {pl}, {64 if t64 else 32}{pair}>"
     if shape in TILED_SHAPES:
         w = 4 if shape == (16, 16) and c["k"] >= 8 * (c["N"] // 16) else 1
         if fits:
@@ -726,6 +727,11 @@ def main(argv=None) -> int:
     # slice count is 1 when tiles alone fill the GPU).
     per_launch = len(prep.calls) // prep.launches_per_step
     persistent = per_launch * -(-prep.calls[0]["T"] // 32) > 256
+    # Planned products 2i and 2i + 1 of a launch that share X run paired in the persistent
+    # kernel (one item per X tile for both).
+    paired = (persistent and prep.planned and per_launch % 2 == 0 and
+              all(prep.calls[i]["x_index"] == prep.calls[i + 1]["x_index"]
+                  for i in range(0, len(prep.calls) - 1, 2)))
     # Roofline of the product kernel: the timed region's time per launch.  The kernel-event
     # durations of every launch over a few more steps (at least 60 launches) go beside it.
     rounds = max(rotate, -(-60 // prep.launches_per_step))
@@ -735,7 +741,8 @@ def main(argv=None) -> int:
     roof.update({"traffic": tr["bytes_per_launch"] if tr else None,
                  "launch_us_source": "timed region / launches per step",
                  "kernel": " + ".join(dict.fromkeys(kernel_name(c, wl.bf16, prep.planned,
-                                                                persistent, prep.plan_arith)
+                                                                persistent, prep.plan_arith,
+                                                                paired)
                                                     for c in prep.calls)),
                  "kernel_event_us": {k: lt[k] for k in ("mean", "median", "p10", "p90", "n")}})
 
