@@ -363,9 +363,14 @@ LIBBSR_API bsr_status bsr_plan_prepare_ex(const bsr_matrix_t *W, int32_t arith, 
  * bsr_spmm_batched with a plan per product (plans may be NULL, or plans[i] NULL for a product
  * without one).  A planned product runs on the planned form of the matrix-core kernel in its
  * plan's arithmetic: with BSR_ARITH_NATIVE it gives the same Y, bit for bit, as the same call
- * without plans.  Products with and without plans, or with plans of different arithmetic,
- * never share a launch.  Errors: those of bsr_spmm_batched, and BSR_ERR_ARG for a plan
- * that does not describe its product's matrix or whose memory overlaps a Y.
+ * without plans, with one exception: when a launch has more token tiles than the GPU has CUs
+ * and holds an even number of planned products in which items 2i and 2i + 1 read the same X
+ * (same pointer, T, ldx and column count), those two run paired, one workgroup serving a token
+ * tile of both, and sum their rows in another order (same accuracy; integer-valued results
+ * stay exact).  A paired product's Y is still bitwise reproducible for the same call.  Products
+ * with and without plans, or with plans of different arithmetic, never share a launch.
+ * Errors: those of bsr_spmm_batched, and BSR_ERR_ARG for a plan that does not describe its
+ * product's matrix or whose memory overlaps a Y.
  */
 LIBBSR_API bsr_status bsr_spmm_batched_planned(const bsr_spmm_item_t *items,
                                                const bsr_plan_t *const *plans, int32_t n_items,
