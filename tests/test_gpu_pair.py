@@ -6,7 +6,8 @@ products of a pair in one set of workgroups: each item covers one X tile of both
 second product's block-rows following the first's.  The waves' shares then run across the
 boundary between the products, so the partial sums differ from those of the products launched
 alone: both must meet the oracle's tolerance, and on integer-valued inputs (where every order
-is exact) equal the exact product bit for bit.
+is exact) equal the exact product bit for bit.  Calls of 16 products run as two launches of 8,
+each paired; 4 products of 32768 tokens run as two pairs of 128 workgroups each.
 """
 import zlib
 
@@ -49,6 +50,14 @@ CASES = [
     ("bf16 32-token tiles", [1024, 1024, 768, 768], 768, 9000, 0.05, True, B.ARITH_NATIVE, 1),
     ("bf16 64-token tiles", [1536, 1536], 768, 20000, 0.3, True, B.ARITH_NATIVE, None),
     ("split arithmetic", [1024, 1024, 1024, 1024], 1024, 6144, 0.1, False, B.ARITH_BF16X3, 1),
+    # calls of 16 products (two launches), long token counts
+    ("fp32 16 products", [1024] * 16, 1024, 6144, 0.1, False, B.ARITH_NATIVE, 1),
+    ("fp32 4 products long T", [1024, 768, 1024, 2304], 1024, 32768 + 3, 0.1, False,
+     B.ARITH_NATIVE, 1),
+    ("bf16 32-token tiles 16 products", [1024, 768, 2304, 768] * 4, 768, 6144 - 7, 0.05, True,
+     B.ARITH_NATIVE, 1),
+    ("bf16 64-token tiles 16 products", [1536] * 16, 768, 20000, 0.3, True, B.ARITH_NATIVE, None),
+    ("split arithmetic 16 products", [1024] * 16, 1024, 6144, 0.1, False, B.ARITH_BF16X3, 1),
 ]
 
 
@@ -81,13 +90,21 @@ def test_paired_launch_within_tolerance(device, case):
         check_spmm(Xh, M, b, Y1, rows=rows, bf16=bf16)
 
 
+INT_CASES = [
+    # name, [N per product], T
+    ("pairs", [1024, 768, 1024, 1024], 8192 + 9),
+    ("16 products", [1024, 768, 1024, 1024] * 4, 6144 + 9),
+]
+
+
+@pytest.mark.parametrize("case", INT_CASES, ids=[c[0] for c in INT_CASES])
 @pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
-def test_paired_launch_integers_exact(device, bf16):
+def test_paired_launch_integers_exact(device, bf16, case):
     """Integer-valued inputs: every summation order is exact, so the paired launch equals the
     exact product bit for bit, and equals the products launched alone."""
     g = rng(77)
-    T, K = 8192 + 9, 768
-    Ns = [1024, 768, 1024, 1024]
+    _, Ns, T = case
+    K = 768
     Xh = g.integers(-8, 9, (T, K)).astype(np.float32)
     X = bf16_tensor(Xh) if bf16 else dev(Xh)
     mats, exact, Ys, biases = [], [], [], []
