@@ -289,6 +289,25 @@ __device__ __forceinline__ void dcompute(float (&acc)[R], const DOps<R, C> &ops,
     typedef __attribute__((address_space(3))) const V lds_cv;
     const unsigned xbase = unsigned(size_t((lds_cfloat *)xrow));   // its LDS byte address
     const unsigned cbytes = min(unsigned(ops.j - jlo), unsigned(Kb - 1)) * unsigned(C * 4);
+    if constexpr (!MASKED && C == 1) {
+        // One LDS read per block: issue the chunk's U reads before its first multiply-add, so
+        // all of them are in flight at once (left to the scheduler, the reads and multiply-adds
+        // interleaved with two or three reads outstanding, and the waves waited on LDS latency).
+        float xs[S::U];
+#pragma unroll
+        for (int u = 0; u < S::U; ++u)
+            xs[u] = *(lds_cfloat *)size_t(add_bcast(cbytes, xbase, u, u == 0));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < S::U; ++u) {
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int word = u * S::RC + r;
+                fmac_bcast(acc[r], ops.w[word / 16], xs[u], word % 16, word % 16 == 0);
+            }
+        }
+        return;
+    }
     // A guard rather than a break: the loop keeps a constant trip count, so it unrolls fully
     // and every broadcast lane and weight register is a constant (with a break, chunks of 16
     // blocks were left rolled, with the weights in scratch memory and a switch per broadcast).
@@ -578,12 +597,15 @@ __global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_kernel(con
                 unsigned(m) * unsigned(S::RC * kEs));
             const int nq = (m + U - 1) / U, iters = (nq + 1) >> 1;
             // Chunk `it` of this half starts (2 it + h) U blocks into the row; every chunk
-            // before the last iteration is full.
+            // before the last iteration is full.  The next chunk is loaded in every iteration,
+            // also past the row's end (those loads return 0 and touch no memory), so the wait
+            // for the current chunk always leaves the next one's loads in flight (a conditional
+            // load left the compiler's wait at zero outstanding loads).
             OpsOf<R, C, BF> A, B;
             oload<R, C, BF>(A, ri, rd, h * U);
             int it = 0;
             while (true) {
-                if (it + 1 < iters) oload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
+                oload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
                     ocompute<R, C, BF, true>(acc, A, xrow, Kb, m - (2 * it + h) * U);
@@ -592,7 +614,7 @@ __global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_kernel(con
                 ocompute<R, C, BF, false>(acc, A, xrow, Kb, U);
                 __builtin_amdgcn_sched_barrier(0);
                 ++it;
-                if (it + 1 < iters) oload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
+                oload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
                     ocompute<R, C, BF, true>(acc, B, xrow, Kb, m - (2 * it + h) * U);
@@ -769,7 +791,7 @@ __global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_chunk_kern
             oload<R, C, BF>(A, ri, rd, h * U);
             int it = 0;
             while (true) {
-                if (it + 1 < iters) oload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
+                oload<R, C, BF>(B, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
                     ocompute<R, C, BF, true>(acc[i], A, xrow, kbw, m - (2 * it + h) * U, jlo);
@@ -778,7 +800,7 @@ __global__ __launch_bounds__((kWaves<R, C, BF> * 64)) void spmm_vtile_chunk_kern
                 ocompute<R, C, BF, false>(acc[i], A, xrow, kbw, U, jlo);
                 __builtin_amdgcn_sched_barrier(0);
                 ++it;
-                if (it + 1 < iters) oload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
+                oload<R, C, BF>(A, ri, rd, (2 * (it + 1) + h) * U);
                 __builtin_amdgcn_sched_barrier(0);
                 if (it + 1 >= iters) {
                     ocompute<R, C, BF, true>(acc[i], B, xrow, kbw, m - (2 * it + h) * U, jlo);
