@@ -74,7 +74,13 @@ def check_spmm(X: np.ndarray, M: B.BSRMatrix, bias: np.ndarray | None, Y: torch.
 
 
 def prune_on_gpu(W: np.ndarray, R: int, C: int, k: int) -> B.BSRMatrix:
-    return B.bsr_prune_from_dense(dev(W), R, C, k=k)
+    """W pruned to its k largest R x C blocks on the GPU, checked bit for bit against the
+    oracle's prune before it is returned, so that every product test whose oracle input is
+    built from the device's BSR arrays (oracle_bsr) multiplies the matrix the paper's pruning
+    defines."""
+    M = B.bsr_prune_from_dense(dev(W), R, C, k=k)
+    check_prune(W, R, C, M, k)
+    return M
 
 
 def bf16_tensor(x: np.ndarray) -> torch.Tensor:

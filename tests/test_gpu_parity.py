@@ -93,8 +93,8 @@ def test_bert_large_zipf(device, R, C):
     (every one checked bit for bit against the oracle's prune, with its Zipf row counts), then
     12 batched launches of 8 products with per-matrix plans where the block shape has them (the
     persistent flat kernel for 32x1, products that share X paired in its workgroups); every
-    product meets the oracle's tolerance on 48 sampled token rows.  One-product launches of the
-    first launch's products meet it too; unpaired square blocks equal them bit for bit (paired
+    product meets the oracle's tolerance on every one of its 6144 x 1024 outputs.  One-product
+    launches of the first launch's products meet it on 48 sampled token rows; unpaired square blocks equal them bit for bit (paired
     products sum in another order: tests/test_gpu_pair.py checks those on integer inputs)."""
     w = G.bert_large_zipf(R, C, B.bsr_prune_count(1024, 1024, R, C, 0.1))
     Xs = [dev(x) for x in w.X]
@@ -119,7 +119,7 @@ def test_bert_large_zipf(device, R, C):
                         plans=plans if planned else None)()
         torch.cuda.synchronize()
         for p, M, Y in zip(group, mats, Ys):
-            check_spmm(w.X[p.x_index], M, p.bias, Y, rows=sample)
+            check_spmm(w.X[p.x_index], M, p.bias, Y)
         if g0 == 0:
             for p, M, b, Y in zip(group, mats, biases, Ys):
                 Y1 = B.bsr_spmm(Xs[p.x_index], M, b)
