@@ -94,12 +94,10 @@ def test_bert_large_zipf(device, R, C):
     12 batched launches of 8 products with per-matrix plans where the block shape has them (the
     persistent flat kernel for 32x1, products that share X paired in its workgroups); every
     product meets the oracle's tolerance on every one of its 6144 x 1024 outputs.  One-product
-    launches of the first launch's products meet it on 48 sampled token rows; unpaired square blocks equal them bit for bit (paired
+    launches of the first launch's products meet it too; unpaired square blocks equal them bit for bit (paired
     products sum in another order: tests/test_gpu_pair.py checks those on integer inputs)."""
     w = G.bert_large_zipf(R, C, B.bsr_prune_count(1024, 1024, R, C, 0.1))
     Xs = [dev(x) for x in w.X]
-    sample = rng(5).choice(w.tokens, size=48, replace=False)
-    sample.sort()
     planned = (R, C) == (32, 1)
     projs = w.projections
     for g0 in range(0, len(projs), 8):
@@ -124,7 +122,7 @@ def test_bert_large_zipf(device, R, C):
             for p, M, b, Y in zip(group, mats, biases, Ys):
                 Y1 = B.bsr_spmm(Xs[p.x_index], M, b)
                 torch.cuda.synchronize()
-                check_spmm(w.X[p.x_index], M, p.bias, Y1, rows=sample)
+                check_spmm(w.X[p.x_index], M, p.bias, Y1)
                 if not planned:
                     assert np.array_equal(host(Y).view(np.uint32), host(Y1).view(np.uint32))
 
